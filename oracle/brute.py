@@ -1,0 +1,104 @@
+"""Brute-force numpy twin of the oracle, float64, for tiny inputs.  Test infrastructure.
+
+Written independently of solref.c: the rotary embedding is complex
+multiplication by exp(j*phi) over explicit per-token positions, attention
+materialises the full score matrix and normalises it with scipy's softmax.
+"""
+import numpy as np
+from scipy.special import softmax
+
+
+def grid_positions(N, T, Hl, Wl):
+    """Per-token (t, h, w) positions, int64 [N, 3]; -1 marks prefix (text) tokens.
+
+    Packing is text first, then the video latent in t-major raster order
+    (Sec. 3.4 "Safety rails": prefix tokens precede the target video).
+    """
+    nv = T * Hl * Wl
+    nt = N - nv
+    if nt < 0:
+        raise ValueError("grid larger than the sequence")
+    pos = -np.ones((N, 3), dtype=np.int64)
+    tt, hh, ww = np.meshgrid(np.arange(T), np.arange(Hl), np.arange(Wl), indexing="ij")
+    pos[nt:, 0] = tt.reshape(-1)
+    pos[nt:, 1] = hh.reshape(-1)
+    pos[nt:, 2] = ww.reshape(-1)
+    return pos
+
+
+def rope_angles(pos, D=128, split=(32, 48, 48), base=10000.0):
+    """Rotation angle of every interleaved pair, float64 [N, D/2].
+
+    Pair i of the chunk owned by axis a (width d_a) turns by
+    pos_a * base**(-2 i / d_a); prefix tokens (pos < 0) and pairs beyond the
+    three chunks do not turn.
+    """
+    N = pos.shape[0]
+    ang = np.zeros((N, D // 2), dtype=np.float64)
+    off = 0
+    for a, d in enumerate(split):
+        freq = base ** (-2.0 * np.arange(d // 2) / d)
+        p = np.where(pos[:, a] >= 0, pos[:, a], 0).astype(np.float64)
+        ang[:, off // 2: off // 2 + d // 2] = p[:, None] * freq[None, :]
+        off += d
+    return ang
+
+
+def rope_np(x, ang):
+    """Rotate x[..., N, D] (float64): (x_2i + j x_2i+1) * exp(j ang_i)."""
+    z = x[..., 0::2] + 1j * x[..., 1::2]
+    z = z * np.exp(1j * ang)
+    y = np.empty_like(x, dtype=np.float64)
+    y[..., 0::2] = z.real
+    y[..., 1::2] = z.imag
+    return y
+
+
+def bf16_bits_to_f64(bits):
+    """uint16 bf16 bit patterns -> float64 (exact)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def nearest_bf16(x):
+    """Round float64 to the nearest bf16 (ties to even mantissa) by comparing the
+    two bf16 neighbours, found by truncating the float32 bit pattern.  Finite,
+    in-range inputs only.  Returns float64 values."""
+    x = np.asarray(x, dtype=np.float64)
+    f = x.astype(np.float32)  # may round; fix below with exact neighbour search
+    bits = f.view(np.uint32) & np.uint32(0xFFFF0000)
+    lo = bits.view(np.float32).astype(np.float64)
+    # neighbours of the truncated value one bf16 step either side
+    up = (bits + np.uint32(0x10000)).view(np.float32).astype(np.float64)
+    dn = (bits - np.uint32(0x10000)).view(np.float32).astype(np.float64)
+    cands = np.stack([dn, lo, up], axis=-1)
+    dist = np.abs(cands - x[..., None])
+    best = dist.min(axis=-1, keepdims=True)
+    tie = dist == best
+    cbits = np.stack([bits - np.uint32(0x10000), bits, bits + np.uint32(0x10000)], axis=-1)
+    even = ((cbits >> np.uint32(16)) & np.uint32(1)) == 0
+    pick = np.where(tie.sum(-1, keepdims=True) > 1, tie & even, tie)
+    idx = np.argmax(pick, axis=-1)
+    return np.take_along_axis(cands, idx[..., None], axis=-1)[..., 0]
+
+
+def attention_np(qh, kh, v):
+    """softmax(qh kh^T / sqrt(D)) v over the last two axes, float64, materialised."""
+    D = qh.shape[-1]
+    s = np.matmul(qh, np.swapaxes(kh, -1, -2)) / np.sqrt(D)
+    p = softmax(s, axis=-1)
+    return np.matmul(p, v), p
+
+
+def fused_reference(q_bits, k_bits, v_bits, T, Hl, Wl, contract=True,
+                    split=(32, 48, 48), base=10000.0):
+    """The whole path on [B, H, N, D] bf16 bits: rotate q, k (rounding once to
+    bf16 in contract mode), then exact attention.  Returns (out, probs)."""
+    q = bf16_bits_to_f64(q_bits)
+    k = bf16_bits_to_f64(k_bits)
+    v = bf16_bits_to_f64(v_bits)
+    N, D = q.shape[-2], q.shape[-1]
+    ang = rope_angles(grid_positions(N, T, Hl, Wl), D, split, base)
+    qh, kh = rope_np(q, ang), rope_np(k, ang)
+    if contract:
+        qh, kh = nearest_bf16(qh), nearest_bf16(kh)
+    return attention_np(qh, kh, v)

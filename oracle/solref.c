@@ -1,0 +1,294 @@
+/*
+ * solref.c -- CPU oracle for 3D-RoPE + full softmax attention.
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check
+ * and the benchmark's CPU-baseline leg may load this library.  It shares no
+ * code, header, table or constant generator with the HIP library: its own
+ * trigonometry, its own token indexing, its own bf16 rounding.
+ *
+ * What it computes (all arithmetic in IEEE double):
+ *
+ *   The video DiT's spatio-temporal self-attention (Sec. 3.2 "Optimized
+ *   attention collectives": the SDPA term that dominates the denoising step;
+ *   Sec. 3.4: its cost grows with the square of the token count) applied to
+ *   queries and keys that first pass through the partial/3D rotary embedding
+ *   of Sec. 3.5 (fusion group 2, "QK normalization with partial RoPE"; the
+ *   normalization half is not part of this path).
+ *
+ *   Sequence packing (Sec. 3.4 "Safety rails"): the Nt = N - T*Hl*Wl leading
+ *   tokens are a prefix (text) that is not rotated; token n >= Nt is the
+ *   video latent at r = n - Nt, raster order t-major: t = r / (Hl*Wl),
+ *   h = (r / Wl) mod Hl, w = r mod Wl.
+ *
+ *   Rotary embedding: head dims [0,dt) carry t, [dt,dt+dh) carry h,
+ *   [dt+dh,dt+dh+dw) carry w, the rest pass through.  Inside an axis chunk of
+ *   width d, the pair (2i, 2i+1) is the complex number x_{2i} + j x_{2i+1},
+ *   multiplied by exp(j * pos * base^(-2i/d)).
+ *
+ *   Rounding point ("contract" mode, the default): the rotated q and k are
+ *   rounded to bf16 (round to nearest, ties to even) once, as any bf16 matrix
+ *   unit must consume them.  contract = 0 keeps them in double (diagnostic).
+ *
+ *   Attention per (b, h, query i), the plain two-pass definition:
+ *     s_j = <q_i, k_j> / sqrt(D)               for every key j < N
+ *     m   = max_j s_j
+ *     p_j = exp(s_j - m),  l = sum_j p_j
+ *     o_i = (sum_j p_j v_j) / l
+ *
+ * Tensors: bf16 bit patterns (uint16), contiguous [B][H][N][D].
+ */
+#define _GNU_SOURCE
+#include <math.h>
+#include <pthread.h>
+#include <sched.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* bf16 bit pattern -> double (exact). */
+static double bf16_to_double(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* double -> bf16 bit pattern, round to nearest, ties to even, computed from
+ * the double directly (no intermediate float rounding).  NaN -> quiet NaN. */
+static uint16_t double_to_bf16(double x) {
+  if (isnan(x)) return 0x7fc0;
+  uint16_t sign = signbit(x) ? 0x8000 : 0;
+  double a = fabs(x);
+  if (a == 0.0) return sign;
+  if (isinf(a)) return sign | 0x7f80;
+  /* bf16: 8 significant bits.  Find e with 2^e <= a < 2^(e+1). */
+  int e;
+  (void)frexp(a, &e); /* a = f * 2^e with f in [0.5, 1) */
+  e -= 1;             /* now 2^e <= a < 2^(e+1) */
+  if (e < -126) e = -126;   /* subnormal range: fixed quantum 2^-133 */
+  double quantum = ldexp(1.0, e - 7);
+  double n = a / quantum;   /* exact: power-of-two division */
+  double fl = floor(n);
+  double rem = n - fl;
+  if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;
+  double r = fl * quantum;
+  if (r >= ldexp(1.0, 128)) return sign | 0x7f80; /* overflow to inf */
+  float rf = (float)r; /* exact: r has at most 8 significant bits */
+  uint32_t u;
+  memcpy(&u, &rf, sizeof u);
+  return sign | (uint16_t)(u >> 16);
+}
+
+void solref_round_bf16(const double* x, uint16_t* y, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) y[i] = double_to_bf16(x[i]);
+}
+
+/* Position of token n on each axis; returns 0 for a prefix (unrotated) token. */
+static int token_position(int64_t n, int N, int T, int Hl, int Wl, int* pt, int* ph, int* pw) {
+  int64_t nv = (int64_t)T * Hl * Wl;
+  int64_t nt = (int64_t)N - nv;
+  if (n < nt) return 0;
+  int64_t r = n - nt;
+  *pt = (int)(r / ((int64_t)Hl * Wl));
+  *ph = (int)((r / Wl) % Hl);
+  *pw = (int)(r % Wl);
+  (void)T;
+  return 1;
+}
+
+/* Rotate one D-vector (in place, double) by the 3D rotary embedding at
+ * (pt, ph, pw).  Axis chunks are [0,dt), [dt,dt+dh), [dt+dh,dt+dh+dw). */
+static void rotate_vector(double* x, int D, int dt, int dh, int dw, double base,
+                          int pt, int ph, int pw) {
+  const int widths[3] = {dt, dh, dw};
+  const int pos[3] = {pt, ph, pw};
+  int off = 0;
+  for (int a = 0; a < 3; ++a) {
+    int d = widths[a];
+    for (int i = 0; i < d / 2; ++i) {
+      double theta = pow(base, -2.0 * i / (double)d);
+      double phi = (double)pos[a] * theta;
+      double c = cos(phi), s = sin(phi);
+      double re = x[off + 2 * i], im = x[off + 2 * i + 1];
+      x[off + 2 * i] = re * c - im * s;
+      x[off + 2 * i + 1] = re * s + im * c;
+    }
+    off += d;
+  }
+  (void)D;
+}
+
+/* Rotate rows of a bf16 tensor [BH][N][D] and write doubles.  If contract,
+ * the rotated values are rounded to bf16 (then widened back, exactly). */
+static void rotate_row(const uint16_t* src, double* dst, int64_t n, int N, int D,
+                       int T, int Hl, int Wl, int dt, int dh, int dw, double base,
+                       int use_rope, int contract) {
+  for (int d = 0; d < D; ++d) dst[d] = bf16_to_double(src[d]);
+  int pt, ph, pw;
+  if (use_rope && token_position(n, N, T, Hl, Wl, &pt, &ph, &pw)) {
+    rotate_vector(dst, D, dt, dh, dw, base, pt, ph, pw);
+    if (contract)
+      for (int d = 0; d < D; ++d) dst[d] = bf16_to_double(double_to_bf16(dst[d]));
+  }
+}
+
+/* Rotation in double, no rounding: x, y are double [rows][D]; row r is token r mod N. */
+void solref_rope3d_f64(const double* x, double* y, int64_t rows, int N, int D,
+                       int T, int Hl, int Wl, int dt, int dh, int dw, double base) {
+  for (int64_t r = 0; r < rows; ++r) {
+    int64_t n = r % N;
+    for (int d = 0; d < D; ++d) y[r * D + d] = x[r * D + d];
+    int pt, ph, pw;
+    if (token_position(n, N, T, Hl, Wl, &pt, &ph, &pw))
+      rotate_vector(y + r * D, D, dt, dh, dw, base, pt, ph, pw);
+  }
+}
+
+/* Contract-mode rotation of a bf16 tensor: rotate in double, round once to bf16. */
+void solref_rope3d(const uint16_t* x, uint16_t* y, int64_t rows, int N, int D,
+                   int T, int Hl, int Wl, int dt, int dh, int dw, double base) {
+  double* buf = (double*)malloc(sizeof(double) * (size_t)D);
+  for (int64_t r = 0; r < rows; ++r) {
+    int64_t n = r % N;
+    rotate_row(x + r * D, buf, n, N, D, T, Hl, Wl, dt, dh, dw, base, 1, 0);
+    for (int d = 0; d < D; ++d) y[r * D + d] = double_to_bf16(buf[d]);
+  }
+  free(buf);
+}
+
+/* ------------------------------------------------------------------ attention */
+
+typedef struct {
+  /* one (b,h) slab */
+  const uint16_t* q;      /* [N][D] */
+  const double* khat;     /* [N][D] rotated keys */
+  const double* vd;       /* [N][D] */
+  int N, D, T, Hl, Wl, dt, dh, dw, use_rope, contract;
+  double base;
+  const int64_t* qrows;   /* query indices within the slab */
+  float* out;             /* [nq][D] */
+  int64_t nq;
+  int64_t next;           /* shared work counter */
+  pthread_mutex_t lock;
+} slab_job;
+
+static void attend_one(slab_job* J, int64_t idx, double* s, double* qhat, double* acc) {
+  const int N = J->N, D = J->D;
+  int64_t i = J->qrows[idx];
+  rotate_row(J->q + i * D, qhat, i, N, D, J->T, J->Hl, J->Wl, J->dt, J->dh, J->dw, J->base,
+             J->use_rope, J->contract);
+  const double scale = 1.0 / sqrt((double)D);
+  /* pass 1: logits and their maximum */
+  double m = -INFINITY;
+  for (int j = 0; j < N; ++j) {
+    const double* kj = J->khat + (int64_t)j * D;
+    double dot = 0.0;
+    for (int d = 0; d < D; ++d) dot += qhat[d] * kj[d];
+    s[j] = dot * scale;
+    if (s[j] > m) m = s[j];
+  }
+  /* pass 2: exponentials, normaliser, weighted sum of values */
+  double l = 0.0;
+  for (int d = 0; d < D; ++d) acc[d] = 0.0;
+  for (int j = 0; j < N; ++j) {
+    double p = exp(s[j] - m);
+    l += p;
+    const double* vj = J->vd + (int64_t)j * D;
+    for (int d = 0; d < D; ++d) acc[d] += p * vj[d];
+  }
+  for (int d = 0; d < D; ++d) J->out[idx * D + d] = (float)(acc[d] / l);
+}
+
+static void* slab_worker(void* arg) {
+  slab_job* J = (slab_job*)arg;
+  double* s = (double*)malloc(sizeof(double) * (size_t)J->N);
+  double* qhat = (double*)malloc(sizeof(double) * (size_t)J->D);
+  double* acc = (double*)malloc(sizeof(double) * (size_t)J->D);
+  for (;;) {
+    pthread_mutex_lock(&J->lock);
+    int64_t idx = J->next++;
+    pthread_mutex_unlock(&J->lock);
+    if (idx >= J->nq) break;
+    attend_one(J, idx, s, qhat, acc);
+  }
+  free(s);
+  free(qhat);
+  free(acc);
+  return NULL;
+}
+
+int solref_num_threads(void) {
+  cpu_set_t set;
+  if (sched_getaffinity(0, sizeof set, &set) == 0) return CPU_COUNT(&set);
+  return 1;
+}
+
+/*
+ * Attention output for selected query rows.
+ *   q,k,v    : bf16 bits [B][H][N][D]
+ *   rows     : global row ids r = (b*H + h)*N + i, grouped by (b,h) in any order
+ *   out      : float [nrows][D], row k is the output for rows[k]
+ *   use_rope : 0 = plain attention (no rotation anywhere)
+ *   nthreads : <= 0 means every CPU in the affinity mask
+ * Returns 0, or -1 on bad arguments / allocation failure.
+ */
+int solref_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                     int B, int H, int N, int D, int T, int Hl, int Wl,
+                     int dt, int dh, int dw, double base, int use_rope, int contract,
+                     const int64_t* rows, int64_t nrows, float* out, int nthreads) {
+  if (B < 1 || H < 1 || N < 1 || D < 2 || !q || !k || !v || !out || (nrows > 0 && !rows)) return -1;
+  if (use_rope && ((int64_t)T * Hl * Wl > N || dt + dh + dw > D || T < 0 || Hl < 0 || Wl < 0)) return -1;
+  if (nthreads <= 0) nthreads = solref_num_threads();
+  const int64_t slab = (int64_t)N * D;
+  int64_t* qrows = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nrows > 0 ? nrows : 1));
+  int64_t* where = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nrows > 0 ? nrows : 1));
+  float* obuf = (float*)malloc(sizeof(float) * (size_t)(nrows > 0 ? nrows : 1) * D);
+  double* khat = (double*)malloc(sizeof(double) * (size_t)slab);
+  double* vd = (double*)malloc(sizeof(double) * (size_t)slab);
+  pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
+  if (!qrows || !where || !obuf || !khat || !vd || !th) {
+    free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
+    return -1;
+  }
+  for (int64_t bh = 0; bh < (int64_t)B * H; ++bh) {
+    /* collect the requested rows of this slab */
+    int64_t nq = 0;
+    for (int64_t r = 0; r < nrows; ++r) {
+      if (rows[r] < 0 || rows[r] >= (int64_t)B * H * N) {
+        free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
+        return -1;
+      }
+      if (rows[r] / N == bh) {
+        qrows[nq] = rows[r] % N;
+        where[nq] = r;
+        ++nq;
+      }
+    }
+    if (nq == 0) continue;
+    const uint16_t* ks = k + bh * slab;
+    const uint16_t* vs = v + bh * slab;
+    for (int64_t j = 0; j < N; ++j) {
+      rotate_row(ks + j * D, khat + j * D, j, N, D, T, Hl, Wl, dt, dh, dw, base, use_rope, contract);
+      for (int d = 0; d < D; ++d) vd[j * D + d] = bf16_to_double(vs[j * D + d]);
+    }
+    slab_job J;
+    J.q = q + bh * slab;
+    J.khat = khat;
+    J.vd = vd;
+    J.N = N; J.D = D; J.T = T; J.Hl = Hl; J.Wl = Wl;
+    J.dt = dt; J.dh = dh; J.dw = dw; J.base = base;
+    J.use_rope = use_rope; J.contract = contract;
+    J.qrows = qrows;
+    J.out = obuf;
+    J.nq = nq;
+    J.next = 0;
+    pthread_mutex_init(&J.lock, NULL);
+    int nt = nthreads < nq ? nthreads : (int)nq;
+    for (int t = 0; t < nt; ++t) pthread_create(&th[t], NULL, slab_worker, &J);
+    for (int t = 0; t < nt; ++t) pthread_join(th[t], NULL);
+    pthread_mutex_destroy(&J.lock);
+    for (int64_t r = 0; r < nq; ++r) memcpy(out + where[r] * D, obuf + r * D, sizeof(float) * D);
+  }
+  free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
+  return 0;
+}

@@ -1,0 +1,377 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each ``pin_*`` takes an ``oracle.Oracle`` and raises AssertionError when the
+oracle disagrees with a closed form, an invariant, a library routine
+(torch SDPA, torch's float->bf16 conversion, scipy rotations) or the
+independent numpy brute force.  ``test_oracle.py`` runs them on the real
+oracle and on deliberately broken copies of it (each copy must fail one).
+
+Nothing the paper prints pins these values numerically: it gives no worked
+example of the rotary embedding or of attention.  The paper fixes *what* is
+computed (3D rotary embedding on q and k, then exact softmax attention, with
+the text prefix unrotated); the pins below check that meaning.
+"""
+import math
+
+import numpy as np
+import torch
+from scipy.spatial.transform import Rotation
+
+from oracle import brute
+
+SPLIT = (32, 48, 48)
+BASE = 10000.0
+D = 128
+
+
+def _bits(x):
+    """float array -> bf16 bit patterns via torch's own conversion."""
+    t = torch.as_tensor(np.asarray(x, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def _rand_bits(rng, shape, std=1.0):
+    return _bits(rng.standard_normal(shape) * std)
+
+
+def _f(bits):
+    return brute.bf16_bits_to_f64(bits)
+
+
+# --------------------------------------------------------------- bf16 rounding
+
+def pin_round_bf16_vs_torch(o):
+    """RNE to bf16 equals torch's float32->bfloat16 conversion (library routine),
+    including exact ties, subnormals, zeros and overflow to infinity."""
+    rng = np.random.default_rng(1)
+    x = (rng.standard_normal(20000) * np.exp2(rng.integers(-140, 120, 20000))).astype(np.float32)
+    # exact ties: a bf16 value plus half of its quantum
+    base = _f(_bits(rng.standard_normal(2000)))
+    quantum = np.exp2(np.floor(np.log2(np.abs(base))) - 7)
+    ties = (base + 0.5 * quantum * np.sign(base)).astype(np.float32)
+    specials = np.array([0.0, -0.0, 1e-45, -1e-45, 3.0e38, -3.4e38, 1.0, 1.00390625,
+                         1.01171875, 2.0 ** -133, 2.0 ** -134, 3 * 2.0 ** -134], dtype=np.float32)
+    for xs in (x, ties, specials):
+        got = o.round_bf16(xs.astype(np.float64))
+        want = torch.from_numpy(xs).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(got, want), "bf16 rounding differs from torch"
+
+
+def pin_round_bf16_double_nearest(o):
+    """For doubles that float32 cannot hold, the result is the nearest bf16
+    (ties to even), found by brute-force neighbour comparison."""
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal(20000) * np.exp2(rng.integers(-30, 30, 20000))
+    got = _f(o.round_bf16(x))
+    want = brute.nearest_bf16(x)
+    assert np.array_equal(got, want), "bf16 rounding of doubles is not nearest-even"
+
+
+# ----------------------------------------------------------- rotary embedding
+
+def _extract_angles(o, N, T, Hl, Wl):
+    """Rotate the unit vectors e_0 and e_1 of every pair at every token; return
+    the per-pair 2x2 matrices [N, D/2, 2, 2] (columns = images of e_0, e_1)."""
+    e0 = np.zeros((N, D))
+    e0[:, 0::2] = 1.0
+    e1 = np.zeros((N, D))
+    e1[:, 1::2] = 1.0
+    y0 = o.rope3d_f64(e0, T, Hl, Wl, SPLIT, BASE)
+    y1 = o.rope3d_f64(e1, T, Hl, Wl, SPLIT, BASE)
+    M = np.empty((N, D // 2, 2, 2))
+    M[..., 0, 0] = y0[:, 0::2]
+    M[..., 1, 0] = y0[:, 1::2]
+    M[..., 0, 1] = y1[:, 0::2]
+    M[..., 1, 1] = y1[:, 1::2]
+    return M
+
+
+def pin_rope_pairs_are_rotations(o):
+    """Every interleaved pair is turned by a proper, counter-clockwise planar
+    rotation (scipy's z-axis rotation by the extracted angle), and the map is
+    linear in the input."""
+    T, Hl, Wl = 2, 3, 4
+    N = T * Hl * Wl + 3
+    M = _extract_angles(o, N, T, Hl, Wl)
+    phi = np.arctan2(M[..., 1, 0], M[..., 0, 0])
+    R = Rotation.from_rotvec(np.stack([np.zeros(phi.size), np.zeros(phi.size), phi.ravel()], -1))
+    want = R.as_matrix()[:, :2, :2].reshape(M.shape)
+    assert np.allclose(M, want, atol=1e-13), "a pair is not rotated by a proper rotation"
+    rng = np.random.default_rng(3)
+    a, b = rng.standard_normal((2, N, D))
+    lhs = o.rope3d_f64(2.0 * a - 3.0 * b, T, Hl, Wl, SPLIT, BASE)
+    rhs = 2.0 * o.rope3d_f64(a, T, Hl, Wl, SPLIT, BASE) - 3.0 * o.rope3d_f64(b, T, Hl, Wl, SPLIT, BASE)
+    assert np.allclose(lhs, rhs, atol=1e-12), "rotation is not linear"
+
+
+def pin_rope_axis_chunks(o):
+    """A grid that varies along one axis only changes only that axis's head dims:
+    t -> [0,32), h -> [32,80), w -> [80,128)."""
+    rng = np.random.default_rng(4)
+    chunks = {0: (0, 32), 1: (32, 80), 2: (80, 128)}
+    for axis in range(3):
+        dims = [1, 1, 1]
+        dims[axis] = 5
+        N = 5
+        x = rng.standard_normal((N, D))
+        y = o.rope3d_f64(x, *dims, SPLIT, BASE)
+        lo, hi = chunks[axis]
+        keep = np.ones(D, bool)
+        keep[lo:hi] = False
+        assert np.array_equal(y[:, keep], x[:, keep]), "dims outside the axis chunk changed"
+        assert np.abs(y[1:, lo:hi] - x[1:, lo:hi]).max() > 1e-3, "axis chunk did not rotate"
+
+
+def pin_rope_frequency_schedule(o):
+    """At position 1 along an axis of width d, pair i turns by theta_i with
+    theta_0 = 1 rad and theta_{i+1}/theta_i = base^(-2/d) (a geometric
+    progression with the stated base over the axis's own width)."""
+    for axis, (lo, d) in enumerate([(0, 32), (32, 48), (80, 48)]):
+        dims = [1, 1, 1]
+        dims[axis] = 2
+        M = _extract_angles(o, 2, *dims)
+        phi = np.arctan2(M[1, :, 1, 0], M[1, :, 0, 0])
+        sect = phi[lo // 2: (lo + d) // 2]
+        assert abs(sect[0] - 1.0) < 1e-14, "lowest pair must turn by pos * 1 rad"
+        ratio = sect[1:] / sect[:-1]
+        assert np.allclose(ratio, BASE ** (-2.0 / d), rtol=1e-12), "frequencies not geometric in base^(-2/d)"
+        others = np.ones(D // 2, bool)
+        others[lo // 2: (lo + d) // 2] = False
+        assert np.all(phi[others] == 0.0)
+
+
+def pin_rope_token_order(o):
+    """Tokens are a text prefix (unrotated) then the latent in t-major raster
+    order; read back through the lowest pair of each axis, which turns by
+    exactly the position (positions < pi, no wrap)."""
+    T, Hl, Wl, nt = 2, 3, 3, 4
+    N = nt + T * Hl * Wl
+    M = _extract_angles(o, N, T, Hl, Wl)
+    got = np.stack([np.arctan2(M[:, c, 1, 0], M[:, c, 0, 0]) for c in (0, 16, 40)], -1)
+    want = np.zeros((N, 3))
+    n = 0
+    for t in range(T):
+        for h in range(Hl):
+            for w in range(Wl):
+                want[nt + n] = (t, h, w)
+                n += 1
+    assert np.allclose(got, want, atol=1e-13), "token -> (t, h, w) order is not t-major raster"
+
+
+def pin_rope_prefix_identity_and_origin(o):
+    """Prefix tokens and the latent at (0, 0, 0) come back bit-identical."""
+    rng = np.random.default_rng(5)
+    T, Hl, Wl, nt = 2, 2, 2, 3
+    x_bits = _rand_bits(rng, (1, 2, nt + T * Hl * Wl, D))
+    y_bits = o.rope3d_bf16(x_bits, T, Hl, Wl, SPLIT, BASE)
+    assert np.array_equal(y_bits[..., : nt + 1, :], x_bits[..., : nt + 1, :])
+    assert not np.array_equal(y_bits[..., nt + 1:, :], x_bits[..., nt + 1:, :])
+
+
+def pin_rope_group_law(o):
+    """R(p1) R(p2) = R(p1 + p2) and norms of pairs are preserved, using tokens
+    of one grid whose positions add up."""
+    rng = np.random.default_rng(6)
+    T, Hl, Wl = 4, 4, 4
+    N = T * Hl * Wl
+
+    def tok(t, h, w):
+        return (t * Hl + h) * Wl + w
+
+    x = rng.standard_normal(D)
+    for p1, p2 in [((1, 0, 2), (2, 3, 1)), ((0, 1, 1), (3, 2, 2)), ((1, 1, 1), (1, 1, 1))]:
+        p3 = tuple(a + b for a, b in zip(p1, p2))
+        buf = np.zeros((N, D))
+        buf[tok(*p1)] = x
+        y = o.rope3d_f64(buf, T, Hl, Wl, SPLIT, BASE)[tok(*p1)]
+        buf[:] = 0
+        buf[tok(*p2)] = y
+        y2 = o.rope3d_f64(buf, T, Hl, Wl, SPLIT, BASE)[tok(*p2)]
+        buf[:] = 0
+        buf[tok(*p3)] = x
+        y3 = o.rope3d_f64(buf, T, Hl, Wl, SPLIT, BASE)[tok(*p3)]
+        assert np.allclose(y2, y3, atol=1e-12), "rotations do not compose additively"
+        assert np.allclose(np.hypot(y[0::2], y[1::2]), np.hypot(x[0::2], x[1::2]), atol=1e-13)
+
+
+def pin_rope_relative_position(o):
+    """<R(p) q, R(p') k> depends on p - p' only: shifting both tokens by the
+    same offset along any axis leaves the score unchanged."""
+    rng = np.random.default_rng(7)
+    T, Hl, Wl = 5, 5, 5
+    N = T * Hl * Wl
+
+    def tok(t, h, w):
+        return (t * Hl + h) * Wl + w
+
+    q, k = rng.standard_normal((2, D))
+    qs = np.broadcast_to(q, (N, D))
+    ks = np.broadcast_to(k, (N, D))
+    rq = o.rope3d_f64(qs, T, Hl, Wl, SPLIT, BASE)
+    rk = o.rope3d_f64(ks, T, Hl, Wl, SPLIT, BASE)
+    ref = rq[tok(1, 0, 2)] @ rk[tok(0, 2, 1)]
+    for c in [(1, 0, 0), (0, 2, 0), (0, 0, 2), (3, 2, 1)]:
+        a = tok(1 + c[0], 0 + c[1], 2 + c[2])
+        b = tok(0 + c[0], 2 + c[1], 1 + c[2])
+        assert abs(rq[a] @ rk[b] - ref) < 1e-10, "score is not a function of relative position"
+
+
+def pin_rope_numpy_twin(o):
+    """The C rotation equals the numpy complex-multiplication twin (with a prefix)."""
+    rng = np.random.default_rng(8)
+    T, Hl, Wl, nt = 3, 4, 5, 7
+    N = nt + T * Hl * Wl
+    x = rng.standard_normal((2, 3, N, D))
+    ang = brute.rope_angles(brute.grid_positions(N, T, Hl, Wl), D, SPLIT, BASE)
+    assert np.allclose(o.rope3d_f64(x, T, Hl, Wl, SPLIT, BASE), brute.rope_np(x, ang), atol=1e-12)
+
+
+def pin_rope_contract_rounding(o):
+    """Contract mode is exactly: rotate in double, round once to nearest bf16."""
+    rng = np.random.default_rng(9)
+    T, Hl, Wl = 3, 8, 8
+    x_bits = _rand_bits(rng, (1, 2, T * Hl * Wl, D))
+    got = _f(o.rope3d_bf16(x_bits, T, Hl, Wl, SPLIT, BASE))
+    want = brute.nearest_bf16(o.rope3d_f64(_f(x_bits), T, Hl, Wl, SPLIT, BASE))
+    assert np.array_equal(got, want)
+
+
+# ------------------------------------------------------------------ attention
+
+def _sdpa64(q, k, v):
+    return torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v)).numpy()
+
+
+def pin_attention_vs_torch_sdpa(o):
+    """Without rotation the oracle is torch's scaled_dot_product_attention
+    (float64, default 1/sqrt(D) scale) on the same values."""
+    rng = np.random.default_rng(10)
+    for N, std in [(37, 1.0), (130, 3.0), (1, 1.0)]:
+        q, k, v = (_rand_bits(rng, (1, 3, N, D), std) for _ in range(3))
+        got = o.attn_rows(q, k, v, 0, 0, 0, rope=False)
+        want = _sdpa64(_f(q), _f(k), _f(v))
+        assert np.allclose(got, want, atol=2e-6, rtol=1e-6), "plain attention differs from SDPA"
+
+
+def pin_attention_unit_grid_is_sdpa(o):
+    """A 1x1x1 grid (the lone latent token sits at the origin) plus a text
+    prefix rotates nothing, so the RoPE path also equals SDPA."""
+    rng = np.random.default_rng(11)
+    N = 9
+    q, k, v = (_rand_bits(rng, (2, 2, N, D)) for _ in range(3))
+    got = o.attn_rows(q, k, v, 1, 1, 1, rope=True)
+    assert np.allclose(got, _sdpa64(_f(q), _f(k), _f(v)), atol=2e-6, rtol=1e-6)
+
+
+def pin_attention_vs_brute(o):
+    """Rotated attention equals the numpy brute force (materialised scores,
+    scipy softmax) on tiny grids, with and without a text prefix, in contract
+    and pure-double modes."""
+    rng = np.random.default_rng(12)
+    for (T, Hl, Wl, nt) in [(2, 2, 3, 0), (2, 2, 3, 5), (3, 8, 8, 0)]:
+        N = nt + T * Hl * Wl
+        q, k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(3))
+        for contract in (True, False):
+            got = o.attn_rows(q, k, v, T, Hl, Wl, contract=contract)
+            want, _ = brute.fused_reference(q, k, v, T, Hl, Wl, contract=contract)
+            assert np.allclose(got, want, atol=2e-6, rtol=1e-6), "rotated attention differs from brute force"
+
+
+def pin_attention_weights_sum_to_one(o):
+    """With one value column all ones the output in that column is the softmax
+    row sum, 1."""
+    rng = np.random.default_rng(13)
+    T, Hl, Wl = 2, 3, 4
+    N = T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D), 2.0) for _ in range(3))
+    v = v.copy()
+    v[..., 5] = _bits(np.ones(1))[0]
+    out = o.attn_rows(q, k, v, T, Hl, Wl)
+    assert np.allclose(out[..., 5], 1.0, atol=1e-6)
+
+
+def pin_attention_constant_v(o):
+    """Every v_j = c gives o_i = c exactly (up to float32 output rounding)."""
+    rng = np.random.default_rng(14)
+    T, Hl, Wl = 2, 3, 4
+    N = T * Hl * Wl + 2
+    q, k = (_rand_bits(rng, (1, 2, N, D), 3.0) for _ in range(2))
+    c = _bits(rng.standard_normal(D))
+    v = np.broadcast_to(c, (1, 2, N, D)).copy()
+    out = o.attn_rows(q, k, v, T, Hl, Wl)
+    assert np.allclose(out, np.broadcast_to(_f(c), out.shape), atol=1e-6, rtol=1e-6)
+
+
+def pin_attention_joint_permutation(o):
+    """Permuting the (rotated key, value) pairs together leaves every output
+    unchanged; the fused call equals rotate-then-attend."""
+    rng = np.random.default_rng(15)
+    T, Hl, Wl, nt = 2, 3, 4, 3
+    N = nt + T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(3))
+    ref = o.attn_rows(q, k, v, T, Hl, Wl)
+    qh = o.rope3d_bf16(q, T, Hl, Wl, SPLIT, BASE)
+    kh = o.rope3d_bf16(k, T, Hl, Wl, SPLIT, BASE)
+    perm = rng.permutation(N)
+    out = o.attn_rows(qh, np.ascontiguousarray(kh[:, :, perm]), np.ascontiguousarray(v[:, :, perm]),
+                      0, 0, 0, rope=False)
+    assert np.allclose(out, ref, atol=1e-6, rtol=1e-6)
+
+
+def pin_attention_one_hot(o):
+    """A key aligned with the query and a logit gap >= 40 takes all the weight:
+    o_i = v_{j*}."""
+    rng = np.random.default_rng(16)
+    N = 50
+    q = _rand_bits(rng, (1, 1, N, D), 0.05)
+    k = _rand_bits(rng, (1, 1, N, D), 0.05)
+    v = _rand_bits(rng, (1, 1, N, D))
+    i, j = 7, 31
+    q[0, 0, i] = _bits(np.full(D, 2.0))
+    k[0, 0, j] = _bits(np.full(D, 2.0))  # logit 4*128/sqrt(128) = 45 against ~0
+    out = o.attn_rows(q, k, v, 0, 0, 0, rope=False)
+    assert np.allclose(out[0, 0, i], _f(v[0, 0, j]), atol=1e-12 + 1e-12)
+
+
+def pin_attention_zero_query(o):
+    """q = 0 gives uniform weights: o_i = mean_j v_j."""
+    rng = np.random.default_rng(17)
+    T, Hl, Wl = 2, 2, 5
+    N = T * Hl * Wl
+    k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(2))
+    q = np.zeros_like(k)
+    out = o.attn_rows(q, k, v, T, Hl, Wl)
+    want = _f(v).mean(axis=2, keepdims=True)
+    assert np.allclose(out, np.broadcast_to(want, out.shape), atol=1e-6)
+
+
+def pin_attention_two_key_closed_form(o):
+    """Two keys with logits a and 0 weigh their values by e^a : 1."""
+    q = np.zeros((1, 1, 2, D), np.uint16)
+    k = np.zeros((1, 1, 2, D), np.uint16)
+    v = np.zeros((1, 1, 2, D), np.uint16)
+    q[0, 0, :, 0] = _bits([1.5, 1.5])
+    k[0, 0, 0, 0] = _bits([3.0])[0]
+    v[0, 0, 0, 1] = _bits([1.0])[0]
+    v[0, 0, 1, 2] = _bits([1.0])[0]
+    a = 1.5 * 3.0 / math.sqrt(D)
+    out = o.attn_rows(q, k, v, 0, 0, 0, rope=False)
+    w = math.exp(a) / (math.exp(a) + 1.0)
+    assert abs(out[0, 0, 0, 1] - w) < 1e-7 and abs(out[0, 0, 0, 2] - (1 - w)) < 1e-7
+
+
+def pin_attention_rows_and_threads(o):
+    """A row subset (any order) reproduces the full computation bit for bit,
+    for one thread and many."""
+    rng = np.random.default_rng(18)
+    T, Hl, Wl = 2, 3, 5
+    N = T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (2, 2, N, D)) for _ in range(3))
+    full = o.attn_rows(q, k, v, T, Hl, Wl, threads=1)
+    rows = rng.permutation(2 * 2 * N)[:17]
+    sub = o.attn_rows(q, k, v, T, Hl, Wl, rows=rows, threads=4)
+    assert np.array_equal(sub, full.reshape(-1, D)[rows])
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

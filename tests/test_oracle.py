@@ -1,0 +1,106 @@
+"""The CPU oracle, pinned (CPU only).
+
+See ``oracle_pins.py`` for what each pin checks.  The mutation test below
+plants plausible mistakes in copies of the oracle's C source (sign, index,
+operand, scale, rounding, packing) and requires each copy to fail a pin, so
+the pins are shown to have teeth.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import brute
+
+import oracle_pins as P
+
+
+@pytest.mark.parametrize("pin", P.ALL_PINS, ids=lambda f: f.__name__)
+def test_pin(orc, pin):
+    pin(orc)
+
+
+# ---------------------------------------------------- the numpy twin, pinned
+
+def test_brute_attention_is_sdpa():
+    rng = np.random.default_rng(20)
+    q, k, v = rng.standard_normal((3, 2, 3, 21, 128))
+    out, p = brute.attention_np(q, k, v)
+    want = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v)).numpy()
+    assert np.allclose(out, want, atol=1e-12)
+    assert np.allclose(p.sum(-1), 1.0, atol=1e-14)
+
+
+def test_brute_nearest_bf16_is_torch_on_float32():
+    rng = np.random.default_rng(21)
+    x = (rng.standard_normal(5000) * np.exp2(rng.integers(-60, 60, 5000))).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(brute.nearest_bf16(x.astype(np.float64)), want)
+
+
+def test_brute_positions_grid():
+    pos = brute.grid_positions(2 + 2 * 3 * 4, 2, 3, 4)
+    assert (pos[:2] == -1).all()
+    assert tuple(pos[2]) == (0, 0, 0) and tuple(pos[3]) == (0, 0, 1)
+    assert tuple(pos[2 + 4]) == (0, 1, 0) and tuple(pos[2 + 12]) == (1, 0, 0)
+    assert tuple(pos[-1]) == (1, 2, 3)
+
+
+def test_oracle_rejects_bad_arguments(orc):
+    q = np.zeros((1, 1, 4, 128), np.uint16)
+    with pytest.raises(ValueError):
+        orc.attn_rows(q, q, q, 2, 2, 2)            # grid larger than the sequence
+    with pytest.raises(ValueError):
+        orc.attn_rows(q, q, q, 1, 1, 1, rows=np.array([4]))   # row out of range
+    with pytest.raises(TypeError):
+        orc.attn_rows(q.astype(np.float32), q, q, 1, 1, 1)
+
+
+# ------------------------------------------------------------ mutation test
+
+MUTANTS = [
+    ("rotation turns the wrong way",
+     "x[off + 2 * i] = re * c - im * s;\n      x[off + 2 * i + 1] = re * s + im * c;",
+     "x[off + 2 * i] = re * c + im * s;\n      x[off + 2 * i + 1] = -re * s + im * c;"),
+    ("frequency exponent over the whole head dim",
+     "pow(base, -2.0 * i / (double)d)", "pow(base, -2.0 * i / (double)D)"),
+    ("frequency index off by one",
+     "pow(base, -2.0 * i / (double)d)", "pow(base, -2.0 * (i + 1) / (double)d)"),
+    ("axis chunks not advanced", "    off += d;\n", "\n"),
+    ("h/w raster swapped", "*ph = (int)((r / Wl) % Hl);", "*ph = (int)(r % Hl);"),
+    ("prefix tokens rotated", "if (n < nt) return 0;", "if (n < 0) return 0;"),
+    ("softmax scale dropped", "s[j] = dot * scale;", "s[j] = dot;"),
+    ("exponent sign flipped", "double p = exp(s[j] - m);", "double p = exp(m - s[j]);"),
+    ("normaliser dropped", "(float)(acc[d] / l)", "(float)(acc[d])"),
+    ("keys used as values", "const double* vj = J->vd + (int64_t)j * D;",
+     "const double* vj = J->khat + (int64_t)j * D;"),
+    ("ties rounded away from zero",
+     "if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;",
+     "if (rem >= 0.5) fl += 1.0;"),
+    ("rotated q/k not rounded to bf16", "    if (contract)\n", "    if (0)\n"),
+    ("dot product skips the last dim", "for (int d = 0; d < D; ++d) dot += qhat[d] * kj[d];",
+     "for (int d = 0; d < D - 1; ++d) dot += qhat[d] * kj[d];"),
+]
+
+
+@pytest.mark.parametrize("name,find,repl", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(tmp_path, name, find, repl):
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "solref.c")).read()
+    assert src.count(find) == 1, "mutation anchor not found: %s" % name
+    path = tmp_path / "solref_mut.c"
+    path.write_text(src.replace(find, repl))
+    lib = tmp_path / "libsolref_mut.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", str(path), "-o",
+                    str(lib), "-lm"], check=True)
+    mutant = oracle.Oracle(str(lib))
+    failed = []
+    for pin in P.ALL_PINS:
+        try:
+            pin(mutant)
+        except AssertionError:
+            failed.append(pin.__name__)
+    assert failed, "no pin caught: %s" % name
