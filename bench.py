@@ -1,0 +1,192 @@
+"""Benchmark of the fused 3D-RoPE + softmax attention layer on one MI355X.
+
+A step is one call of sol_attn_fwd over the whole workload (every batch and
+head of one attention layer): 3D rotary embedding of q and k fused into the
+tile loads, softmax(q^ k^T / sqrt(D)) v, bf16 out.  Inputs are resident in
+HBM before the timed region starts.
+
+Prints ONE JSON line: throughput in TFLOP/s (4 N^2 D H B algorithmic flops
+per layer), ms per layer, the fraction of the dense bf16 MFMA peak measured
+with HIP events on the kernel's stream, the CPU oracle timed on a bounded
+row sample of the same workload, and the parity of those rows.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+METRIC = "attention TFLOP/s + % of bf16 MFMA peak and ms/layer at 111,600 tokens"
+# MI355X dense bf16 MFMA peak: 256 CUs x 4 SIMDs x 1024 flop/clk x 2.4 GHz.
+PEAK_BF16_TFLOPS = 2516.6
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_fwd_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_35110_amd", "csrc", "sol_kernels.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, if they
+    were taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = rec.get(workload_name)
+    if not entry or entry.get("kernel_sha") != kernel_source_hash():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread):
+    """Time the oracle on a bounded, seeded sample of query rows of slab (0, 0)
+    against all keys; check those rows of the GPU output against it."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from parity import compare
+    from paper_2609_35110_amd import workloads as W
+
+    threads = oracle.num_threads()
+    n_rows = min(w.N, rows_per_thread * threads)
+    gen = torch.Generator().manual_seed(w.seed + 31337)
+    rows = np.sort(torch.randperm(w.N, generator=gen)[:n_rows].numpy()).astype(np.int64)
+    # the oracle needs slab (0, 0) only
+    qb, kb, vb = (W.as_bits(t[:1, :1].contiguous()) for t in (q, k, v))
+    t0 = time.perf_counter()
+    ref = oracle.attn_rows(qb, kb, vb, w.T, w.Hl, w.Wl, rows=rows, threads=threads)
+    dt = time.perf_counter() - t0
+    flops = 4.0 * w.N * w.D * n_rows
+    got = W.as_bits(out_gpu[0, 0].cpu()).reshape(w.N, w.D)[rows]
+    par = compare(got, ref, np.zeros(n_rows, np.int64))
+    cpu = {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "%d query rows (seeded) of head (0,0) against all %d keys, fp64 C oracle, %.1f s; "
+                  "full layer extrapolates to %.0f s" % (n_rows, w.N, dt, dt * w.B * w.H * w.N / n_rows),
+    }
+    return cpu, par
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="p720", help="tiny | low | p480 | p720 | share")
+    ap.add_argument("--cpu-rows-per-thread", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the attention layer shards by heads; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_35110_amd import sol
+    from paper_2609_35110_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("no HIP device visible", file=sys.stderr)
+        sys.exit(1)
+    w = W.WORKLOADS[args.workload]
+    dev = "cuda:0"
+    log("workload %s: %s" % (w.name, w.describe()))
+    t0 = time.perf_counter()
+    q, k, v = W.make_inputs(w)
+    log("inputs generated in %.1f s" % (time.perf_counter() - t0))
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    out = torch.empty_like(qd)
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=dev)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    total_ms = ev[0].elapsed_time(ev[-1])
+    ms_step = total_ms / args.steps
+    ms_launch = sum(per) / len(per)
+    per_sorted = sorted(per)
+    ms_median = per_sorted[len(per) // 2]
+    tflops = w.flops / (ms_step * 1e-3) / 1e12
+    achieved = w.flops / (ms_launch * 1e-3) / 1e12
+    log("timed %d steps: %.3f ms/step (median launch %.3f ms, min %.3f, max %.3f) -> %.1f TFLOP/s"
+        % (args.steps, ms_step, ms_median, per_sorted[0], per_sorted[-1], tflops))
+
+    traffic = measured_traffic(w.name)
+    result = {
+        "metric": METRIC,
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/k/v of the layer's shape)",
+        "config": {
+            "workload": "%s: %s" % (w.name, w.describe()),
+            "B": w.B, "H": w.H, "N": w.N, "D": w.D, "grid": [w.T, w.Hl, w.Wl], "n_text": w.n_text,
+            "rope": "3d (32/48/48, base 1e4) fused into the q/k tile loads",
+        },
+        "ms_per_layer": ms_step,
+        "ms_per_layer_median": ms_median,
+        "pct_peak_bf16": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "roofline": {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        cpu, par = cpu_baseline(w, q, k, v, out, args.cpu_rows_per_thread)
+        result["cpu_baseline"] = cpu
+        result["parity"] = par
+        from parity import passes
+        if not passes(par):
+            # fail closed: no throughput for a kernel that disagrees with the oracle
+            result["value"] = None
+            result["error"] = "parity failed on the sampled rows"
+        log("cpu baseline: %s; parity %s" % (cpu, par))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,117 @@
+/*
+ * sol.h -- C ABI of libsol.so: fused 3D rotary embedding + softmax attention
+ * for the video DiT self-attention, on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (the attention that dominates a denoising step, Sec. 3.2
+ * "Optimized attention collectives"; its cost grows with the square of the
+ * token count, Sec. 3.4): for every batch b and head h,
+ *
+ *     q^ = bf16(R(pos) q),  k^ = bf16(R(pos) k)      (3D rotary embedding)
+ *     out = softmax(q^ k^T / sqrt(D)) v               (no mask, bidirectional)
+ *
+ * R is the rotary embedding of Sec. 3.5 (fusion group 2, "partial RoPE"),
+ * extended to three axes: head dims [0, D/4) rotate with the latent frame t,
+ * [D/4, 5D/8) with the latent row h, [5D/8, D) with the latent column w (the
+ * 32/48/48 split at D = 128).  Within an axis chunk of width d, the
+ * interleaved pair (2i, 2i+1) is turned by the angle pos * base^(-2i/d).
+ *
+ * Sequence packing follows Sec. 3.4 "Safety rails" (prefix before the target
+ * video): of the N tokens, the first Nt = N - T*Hl*Wl form an unrotated
+ * prefix (text); token n >= Nt is the latent at r = n - Nt in t-major raster
+ * order: t = r / (Hl*Wl), h = (r / Wl) mod Hl, w = r mod Wl.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are bf16, contiguous [B][H][N][D] (row-major, D fastest), base
+ *    pointers 16-byte aligned, device memory.  Offsets are 64-bit.
+ *  - Only D = 128 is implemented (SOL_ERR_UNSUPPORTED otherwise).
+ *  - The caller owns every buffer (tensors and the rotary table) and keeps
+ *    them alive until the work on `stream` completes.  The library never
+ *    allocates, frees or synchronises, and keeps no state across calls except
+ *    a thread-local error message.
+ *  - Arguments are validated on the host before any HIP call; a rejected call
+ *    returns a negative status and launches nothing.  Launch failures return
+ *    SOL_ERR_HIP.  Work is asynchronous on `stream` (NULL = the null stream);
+ *    device-side faults surface at the caller's next synchronisation.
+ *  - Every function is thread-safe.
+ */
+#ifndef SOL_H
+#define SOL_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t. */
+typedef struct ihipStream_t* sol_stream_t;
+
+enum {
+  SOL_OK = 0,
+  SOL_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad size, aliasing */
+  SOL_ERR_UNSUPPORTED = -2, /* valid but not implemented (D != 128, huge N) */
+  SOL_ERR_HIP = -3          /* the HIP runtime reported an error */
+};
+
+/* Largest N the kernels accept (token indices stay exact in float32 arithmetic). */
+#define SOL_MAX_TOKENS (1 << 23)
+
+/*
+ * Number of floats in the rotary table for head dim D and latent grid
+ * T x Hl x Wl: 2 * (T*D/8 + Hl*3D/16 + Wl*3D/16).  Returns 0 for invalid
+ * arguments (D not a positive multiple of 16, a negative extent).
+ */
+size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl);
+
+/*
+ * Fill a HOST buffer with the rotary table (caller copies it to the device).
+ * Layout (float pairs (cos, sin), computed in double and rounded to float):
+ *   [T  rows x D/8  pairs]  frame axis:  angle t * base^(-2i/(D/4))
+ *   [Hl rows x 3D/16 pairs] row axis:    angle h * base^(-2i/(3D/8))
+ *   [Wl rows x 3D/16 pairs] column axis: angle w * base^(-2i/(3D/8))
+ * host_tab must hold n_floats >= sol_rope3d_table_floats(D, T, Hl, Wl).
+ * base > 1 (10000 for the workloads here).  Host-only: no HIP call.
+ */
+int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, double base);
+
+/*
+ * y = bf16(R(pos) x) for every token (prefix tokens copied unchanged).
+ * Same rounding as the rotation fused into sol_attn_fwd, bit for bit.
+ * x, y: [B][H][N][D] bf16; y == x (in place) is allowed, any other overlap
+ * is rejected.  0 <= T*Hl*Wl <= N.  rope_tab_dev: device copy of
+ * sol_rope3d_table(D, T, Hl, Wl), 16-byte aligned; it may be NULL only when
+ * the grid is empty (then every token is prefix and y = x).
+ */
+int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
+               const float* rope_tab_dev, sol_stream_t stream);
+
+/*
+ * out = softmax(q^ k^T / sqrt(D)) v with q^, k^ rotated and rounded to bf16
+ * inside the kernel (fused into the tile loads).  fp32 logits, softmax
+ * statistics and accumulators.  The second product takes the probabilities
+ * rounded to fp16 and v converted to fp16 (exact for |v| < 65504; larger
+ * values overflow to inf), so the output error stays at the bf16 rounding of
+ * out (round to nearest even).
+ * q, k, v, out: [B][H][N][D] bf16, 16-byte aligned; out must not overlap
+ * q, k or v.  0 <= T*Hl*Wl <= N.  rope_tab_dev = NULL or T*Hl*Wl = 0 means
+ * plain attention (nothing rotated); otherwise it is the device copy of
+ * sol_rope3d_table(D, T, Hl, Wl), 16-byte aligned.
+ */
+int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
+                 int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
+
+/* Static description of a status code. */
+const char* sol_status_string(int status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* sol_last_error(void);
+
+/* ABI version, major * 100 + minor. */
+int sol_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOL_H */

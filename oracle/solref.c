@@ -199,6 +199,37 @@ static void attend_one(slab_job* J, int64_t idx, double* s, double* qhat, double
   for (int d = 0; d < D; ++d) J->out[idx * D + d] = (float)(acc[d] / l);
 }
 
+/* Rotation of one slab's keys (and widening of its values), split over threads. */
+typedef struct {
+  const uint16_t* ks;
+  const uint16_t* vs;
+  double* khat;
+  double* vd;
+  int N, D, T, Hl, Wl, dt, dh, dw, use_rope, contract;
+  double base;
+  int64_t next;
+  pthread_mutex_t lock;
+} keys_job;
+
+static void* keys_worker(void* arg) {
+  keys_job* J = (keys_job*)arg;
+  const int D = J->D;
+  for (;;) {
+    pthread_mutex_lock(&J->lock);
+    int64_t j0 = J->next;
+    J->next += 256;
+    pthread_mutex_unlock(&J->lock);
+    if (j0 >= J->N) break;
+    int64_t j1 = j0 + 256 < J->N ? j0 + 256 : J->N;
+    for (int64_t j = j0; j < j1; ++j) {
+      rotate_row(J->ks + j * D, J->khat + j * D, j, J->N, D, J->T, J->Hl, J->Wl, J->dt, J->dh,
+                 J->dw, J->base, J->use_rope, J->contract);
+      for (int d = 0; d < D; ++d) J->vd[j * D + d] = bf16_to_double(J->vs[j * D + d]);
+    }
+  }
+  return NULL;
+}
+
 static void* slab_worker(void* arg) {
   slab_job* J = (slab_job*)arg;
   double* s = (double*)malloc(sizeof(double) * (size_t)J->N);
@@ -265,12 +296,19 @@ int solref_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
       }
     }
     if (nq == 0) continue;
-    const uint16_t* ks = k + bh * slab;
-    const uint16_t* vs = v + bh * slab;
-    for (int64_t j = 0; j < N; ++j) {
-      rotate_row(ks + j * D, khat + j * D, j, N, D, T, Hl, Wl, dt, dh, dw, base, use_rope, contract);
-      for (int d = 0; d < D; ++d) vd[j * D + d] = bf16_to_double(vs[j * D + d]);
-    }
+    keys_job K;
+    K.ks = k + bh * slab;
+    K.vs = v + bh * slab;
+    K.khat = khat;
+    K.vd = vd;
+    K.N = N; K.D = D; K.T = T; K.Hl = Hl; K.Wl = Wl;
+    K.dt = dt; K.dh = dh; K.dw = dw; K.base = base;
+    K.use_rope = use_rope; K.contract = contract;
+    K.next = 0;
+    pthread_mutex_init(&K.lock, NULL);
+    for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, keys_worker, &K);
+    for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+    pthread_mutex_destroy(&K.lock);
     slab_job J;
     J.q = q + bh * slab;
     J.khat = khat;

@@ -1,0 +1,153 @@
+// C ABI front end of libsol.so: argument validation (before any HIP call),
+// the host-side rotary table builder, launch and error mapping.
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include <cmath>
+
+#include "sol.h"
+#include "sol_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_last_error[0] = '\0';
+  return SOL_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Common shape checks of the tensor entry points.
+int check_shape(int B, int H, int N, int D, int T, int Hl, int Wl) {
+  if (B < 1 || H < 1 || N < 1) return fail(SOL_ERR_INVALID_ARG, "B, H, N must be >= 1 (got %d, %d, %d)", B, H, N);
+  if (T < 0 || Hl < 0 || Wl < 0) return fail(SOL_ERR_INVALID_ARG, "negative latent grid %dx%dx%d", T, Hl, Wl);
+  if ((int64_t)T * Hl * Wl > N)
+    return fail(SOL_ERR_INVALID_ARG, "latent grid %dx%dx%d holds more tokens than N=%d", T, Hl, Wl, N);
+  if (D != sol::kHeadDim) return fail(SOL_ERR_UNSUPPORTED, "head dim %d not supported (only 128)", D);
+  if (N > SOL_MAX_TOKENS) return fail(SOL_ERR_UNSUPPORTED, "N=%d exceeds %d", N, SOL_MAX_TOKENS);
+  if ((int64_t)B * H > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "B*H too large");
+  return SOL_OK;
+}
+
+}  // namespace
+
+sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl) {
+  SeqGrid g;
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  g.n = N;
+  g.nt = (int)(N - nv);
+  // An empty grid rotates nothing: every token is prefix; keep divisors valid.
+  g.T = nv ? T : 1;
+  g.Hl = nv ? Hl : 1;
+  g.Wl = nv ? Wl : 1;
+  g.hw = g.Hl * g.Wl;
+  g.inv_hw = 1.0f / (float)g.hw;
+  g.inv_wl = 1.0f / (float)g.Wl;
+  g.tab_h = g.T * (kHeadDim / 8);
+  g.tab_w = g.tab_h + g.Hl * (3 * kHeadDim / 16);
+  return g;
+}
+
+extern "C" {
+
+size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl) {
+  if (D <= 0 || D % 16 != 0 || T < 0 || Hl < 0 || Wl < 0) return 0;
+  return 2 * ((size_t)T * (D / 8) + (size_t)Hl * (3 * D / 16) + (size_t)Wl * (3 * D / 16));
+}
+
+int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, double base) {
+  const size_t need = sol_rope3d_table_floats(D, T, Hl, Wl);
+  if (need == 0 && (D <= 0 || D % 16 != 0 || T < 0 || Hl < 0 || Wl < 0))
+    return fail(SOL_ERR_INVALID_ARG, "bad table shape D=%d grid %dx%dx%d", D, T, Hl, Wl);
+  if (!host_tab && need) return fail(SOL_ERR_INVALID_ARG, "host_tab is NULL");
+  if (n_floats < need) return fail(SOL_ERR_INVALID_ARG, "table needs %zu floats, got %zu", need, n_floats);
+  if (!(base > 1.0) || !std::isfinite(base)) return fail(SOL_ERR_INVALID_ARG, "base must be finite and > 1");
+  // Section for one axis of extent `len` whose chunk is `width` head dims wide:
+  // row pos, pair i holds (cos, sin) of pos * base^(-2i/width).
+  float* dst = host_tab;
+  auto section = [&](int len, int width) {
+    for (int pos = 0; pos < len; ++pos)
+      for (int i = 0; i < width / 2; ++i) {
+        const double phi = (double)pos * std::pow(base, -2.0 * i / (double)width);
+        *dst++ = (float)std::cos(phi);
+        *dst++ = (float)std::sin(phi);
+      }
+  };
+  section(T, D / 4);
+  section(Hl, 3 * D / 8);
+  section(Wl, 3 * D / 8);
+  return ok();
+}
+
+int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
+               const float* rope_tab_dev, sol_stream_t stream) {
+  if (!x || !y) return fail(SOL_ERR_INVALID_ARG, "x and y must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  if (!aligned16(x) || !aligned16(y)) return fail(SOL_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  if (nv > 0 && !rope_tab_dev) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev is NULL for a non-empty grid");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (x != y && overlaps(x, bytes, y, bytes)) return fail(SOL_ERR_INVALID_ARG, "x and y partially overlap");
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  hipError_t e = sol::launch_rope3d(static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y),
+                                    (int64_t)B * H * N, g, reinterpret_cast<const float2*>(rope_tab_dev),
+                                    reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "rope3d launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int D,
+                 int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
+  if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must be 16-byte aligned");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k, bytes) || overlaps(out, bytes, v, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k or v");
+  if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  hipError_t e = sol::launch_attn_fwd(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                      static_cast<const uint16_t*>(v), static_cast<uint16_t*>(out), B * H,
+                                      g, tab, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+const char* sol_status_string(int status) {
+  switch (status) {
+    case SOL_OK: return "ok";
+    case SOL_ERR_INVALID_ARG: return "invalid argument";
+    case SOL_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SOL_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* sol_last_error(void) { return g_last_error; }
+
+int sol_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,37 @@
+// Internal interface between the C ABI front end (sol_api.cpp) and the HIP
+// launchers (sol_kernels.hip).  Arguments reaching these functions have been
+// validated already.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sol {
+
+constexpr int kHeadDim = 128;
+
+// Latent grid and packing of one sequence.  Derived on the host.
+struct SeqGrid {
+  int n;        // tokens per sequence N
+  int nt;       // prefix (unrotated) tokens: N - T*Hl*Wl
+  int T, Hl, Wl;
+  int hw;       // Hl * Wl
+  float inv_hw; // 1 / (Hl*Wl), for exact-after-correction division
+  float inv_wl; // 1 / Wl
+  int tab_h;    // first pair of the row-axis section of the table  (T * D/8)
+  int tab_w;    // first pair of the column-axis section  (T*D/8 + Hl*3D/16)
+};
+
+SeqGrid make_grid(int N, int T, int Hl, int Wl);
+
+hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int64_t rows, const SeqGrid& g,
+                         const float2* tab, hipStream_t stream);
+
+hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                           uint16_t* out, int BH, const SeqGrid& g, const float2* tab,
+                           hipStream_t stream);
+
+// Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
+int64_t attn_max_workgroups(int N, int BH);
+
+}  // namespace sol

@@ -1,0 +1,160 @@
+"""Python binding of libsol.so (include/sol.h): argument marshalling only.
+
+The ``sol_*`` functions mirror the C ABI one to one (device pointers and
+streams as integers).  ``rope3d_table``, ``rope3d`` and ``attn_fwd`` take torch
+tensors and pass their device pointers and the current HIP stream.  Every
+step of the computation runs in the HIP library; there is no fallback: if
+libsol.so is missing or fails to load, every call raises.
+"""
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsol.so")
+
+SOL_OK = 0
+SOL_ERR_INVALID_ARG = -1
+SOL_ERR_UNSUPPORTED = -2
+SOL_ERR_HIP = -3
+HEAD_DIM = 128
+ROPE_BASE = 10000.0
+
+_lib = None
+
+
+class SolError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(msg)
+        self.status = status
+
+
+def lib():
+    """Load libsol.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libsol.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, sz, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_double
+        L.sol_rope3d_table_floats.argtypes = [i32, i32, i32, i32]
+        L.sol_rope3d_table_floats.restype = sz
+        L.sol_rope3d_table.argtypes = [P, sz, i32, i32, i32, i32, f64]
+        L.sol_rope3d_table.restype = i32
+        L.sol_rope3d.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
+        L.sol_rope3d.restype = i32
+        L.sol_attn_fwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
+        L.sol_attn_fwd.restype = i32
+        L.sol_status_string.argtypes = [i32]
+        L.sol_status_string.restype = ctypes.c_char_p
+        L.sol_last_error.argtypes = []
+        L.sol_last_error.restype = ctypes.c_char_p
+        L.sol_version.argtypes = []
+        L.sol_version.restype = i32
+        _lib = L
+    return _lib
+
+
+# ---------------------------------------------------------------- raw C ABI
+
+def sol_rope3d_table_floats(D, T, Hl, Wl):
+    return lib().sol_rope3d_table_floats(D, T, Hl, Wl)
+
+
+def sol_rope3d_table(host_tab, n_floats, D, T, Hl, Wl, base):
+    return lib().sol_rope3d_table(host_tab, n_floats, D, T, Hl, Wl, base)
+
+
+def sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_status_string(status):
+    return lib().sol_status_string(status).decode()
+
+
+def sol_last_error():
+    return lib().sol_last_error().decode()
+
+
+def sol_version():
+    return lib().sol_version()
+
+
+def check(status):
+    """Raise SolError for a non-zero status, with the library's message."""
+    if status != SOL_OK:
+        raise SolError(status, "%s: %s" % (sol_status_string(status), sol_last_error()))
+
+
+# ------------------------------------------------------- torch marshalling
+
+def rope3d_table_host(T, Hl, Wl, D=HEAD_DIM, base=ROPE_BASE) -> np.ndarray:
+    """The rotary table as a host float32 array (built by the library)."""
+    n = sol_rope3d_table_floats(D, T, Hl, Wl)
+    tab = np.zeros(max(n, 4), dtype=np.float32)
+    check(sol_rope3d_table(tab.ctypes.data_as(ctypes.c_void_p), n, D, T, Hl, Wl, base))
+    return tab
+
+
+def rope3d_table(T, Hl, Wl, D=HEAD_DIM, base=ROPE_BASE, device="cuda") -> torch.Tensor:
+    """The rotary table, copied to `device` (float32)."""
+    return torch.from_numpy(rope3d_table_host(T, Hl, Wl, D, base)).to(device)
+
+
+def _stream(t):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _check_tensor(name, t, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != torch.bfloat16:
+        raise TypeError("%s must be bfloat16, got %s" % (name, t.dtype))
+    if not t.is_cuda:
+        raise ValueError("%s must be on a HIP device" % name)
+    if t.dim() != 4 or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous [B, H, N, D] tensor" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+
+
+def _table_ptr(table, dev):
+    if table is None:
+        return None
+    if table.dtype != torch.float32 or table.device != dev or not table.is_contiguous():
+        raise ValueError("rope table must be a contiguous float32 tensor on %s" % dev)
+    return ctypes.c_void_p(table.data_ptr())
+
+
+def rope3d(x, T, Hl, Wl, table, out=None):
+    """out = bf16(R(pos) x) for x [B, H, N, D] bf16 (out may be x)."""
+    _check_tensor("x", x)
+    B, H, N, D = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    _check_tensor("out", out, x.shape)
+    check(sol_rope3d(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N, D,
+                     T, Hl, Wl, _table_ptr(table, x.device), _stream(x)))
+    return out
+
+
+def attn_fwd(q, k, v, T, Hl, Wl, table=None, out=None):
+    """softmax(q^ k^T / sqrt(D)) v with the 3D rotary embedding fused (table=None: none)."""
+    _check_tensor("q", q)
+    _check_tensor("k", k, q.shape)
+    _check_tensor("v", v, q.shape)
+    B, H, N, D = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensor("out", out, q.shape)
+    check(sol_attn_fwd(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                       ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N, D,
+                       T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
+    return out

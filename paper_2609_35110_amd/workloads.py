@@ -15,10 +15,17 @@ public dataset; every tensor here is synthetic:
 * ``share`` : B=2, H=5,  grid 31x45x80 + 512 text tokens first (N=112,112);
               video N(0,1), text q N(0,1), text k/v N(0, 0.5^2)
 
-Recipe: a torch CPU ``Generator`` seeded with 20260903 + config index; draws in
-the order q, k, v (video part), then text q, k, v, then the boosted-key
-indices; float32 ``randn`` -> (scale in float32) -> bf16 round-to-nearest-even.
+Recipe: every (tensor, b, h) slab has its own torch CPU ``Generator``, seeded
+with ``slab_seed(seed, tensor, b*H + h)`` where seed = 20260903 + config index
+and tensor is 0/1/2 for q/k/v; it draws the text prefix rows (if any), then the
+video rows, as float32 ``randn`` -> (times the std, in float32) -> bf16 round to
+nearest even.  The boosted keys are ``randperm(N)[:N//100]`` from a generator
+seeded with ``slab_seed(seed, 3, 0)``, the same tokens in every head, multiplied
+by 8 after the bf16 cast (exact).  Slabs are independent, so they are drawn in
+parallel and any single slab can be regenerated alone.
 """
+from concurrent.futures import ThreadPoolExecutor
+import os
 from dataclasses import dataclass
 
 import torch
@@ -81,37 +88,51 @@ def custom(B, H, T, Hl, Wl, n_text=0, seed_index=100, **kw) -> Workload:
     return Workload("custom", seed_index, B, H, T, Hl, Wl, n_text=n_text, **kw)
 
 
-def _draw(gen, shape, std):
-    x = torch.randn(shape, generator=gen, dtype=torch.float32)
-    if std != 1.0:
-        x.mul_(torch.tensor(std, dtype=torch.float32))
-    return x.to(torch.bfloat16)
+def slab_seed(seed: int, tensor: int, slab: int) -> int:
+    """Seed of one (tensor, slab) stream; tensor 0/1/2 = q/k/v, 3 = boost indices."""
+    return (seed * 1000003 + tensor * 7919 + slab * 104729) % (2 ** 63)
 
 
-def make_inputs(w: Workload, seed: int = None):
-    """Return (q, k, v): bf16 CPU tensors [B, H, N, D], contiguous."""
-    gen = torch.Generator().manual_seed(w.seed if seed is None else seed)
-    shp_v = (w.B, w.H, w.n_video, w.D)
-    qv = _draw(gen, shp_v, w.scale)
-    kv = _draw(gen, shp_v, w.scale)
-    vv = _draw(gen, shp_v, w.scale)
+def _fill_slab(dst, seed, tensor, slab, w: Workload):
+    gen = torch.Generator().manual_seed(slab_seed(seed, tensor, slab))
     if w.n_text:
-        shp_t = (w.B, w.H, w.n_text, w.D)
-        qt = _draw(gen, shp_t, 1.0)
-        kt = _draw(gen, shp_t, w.text_kv_std)
-        vt = _draw(gen, shp_t, w.text_kv_std)
-        q = torch.cat([qt, qv], dim=2)
-        k = torch.cat([kt, kv], dim=2)
-        v = torch.cat([vt, vv], dim=2)
-        del qt, kt, vt
-    else:
-        q, k, v = qv, kv, vv
-    if w.boost_frac > 0:
-        n_boost = int(w.N * w.boost_frac)
-        idx = torch.randperm(w.N, generator=gen)[:n_boost]
-        # exact in bf16: the boost is a power of two
-        k[:, :, idx, :] *= torch.tensor(w.boost, dtype=torch.bfloat16)
-    return q.contiguous(), k.contiguous(), v.contiguous()
+        std = 1.0 if tensor == 0 else w.text_kv_std
+        x = torch.randn((w.n_text, w.D), generator=gen, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(torch.tensor(std, dtype=torch.float32))
+        dst[: w.n_text].copy_(x)
+    x = torch.randn((w.n_video, w.D), generator=gen, dtype=torch.float32)
+    if w.scale != 1.0:
+        x.mul_(torch.tensor(w.scale, dtype=torch.float32))
+    dst[w.n_text:].copy_(x)  # float32 -> bf16, round to nearest even
+
+
+def boosted_tokens(w: Workload, seed: int = None):
+    """Token indices whose keys are boosted (empty when the workload has none)."""
+    if w.boost_frac <= 0:
+        return torch.zeros(0, dtype=torch.int64)
+    gen = torch.Generator().manual_seed(slab_seed(w.seed if seed is None else seed, 3, 0))
+    return torch.randperm(w.N, generator=gen)[: int(w.N * w.boost_frac)]
+
+
+def make_inputs(w: Workload, seed: int = None, threads: int = None):
+    """Return (q, k, v): bf16 CPU tensors [B, H, N, D], contiguous."""
+    seed = w.seed if seed is None else seed
+    out = [torch.empty((w.B, w.H, w.N, w.D), dtype=torch.bfloat16) for _ in range(3)]
+    jobs = [(t, bh) for t in range(3) for bh in range(w.B * w.H)]
+    if threads is None:
+        threads = min(16, len(os.sched_getaffinity(0)))
+
+    def run(job):
+        t, bh = job
+        _fill_slab(out[t].view(w.B * w.H, w.N, w.D)[bh], seed, t, bh, w)
+
+    with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
+        list(ex.map(run, jobs))
+    idx = boosted_tokens(w, seed)
+    if idx.numel():
+        out[1][:, :, idx, :] *= torch.tensor(w.boost, dtype=torch.bfloat16)
+    return tuple(out)
 
 
 def as_bits(t: torch.Tensor):
@@ -120,17 +141,17 @@ def as_bits(t: torch.Tensor):
     return t.contiguous().view(torch.int16).numpy().view(np.uint16)
 
 
-def sample_rows(w: Workload, per_slab: int, bm: int = 256, seed: int = None):
+def sample_rows(w: Workload, per_slab: int, head: int = 64, tail: int = 512, seed: int = None):
     """Seeded query rows to check at full size, as global ids (b*H + h)*N + i.
 
-    Per (b, h): the first 64 rows, the last two row tiles of ``bm`` (the ragged
-    one included), the text/video boundary when there is a prefix, and
+    Per (b, h): the first ``head`` rows, the last ``tail`` rows (which hold the
+    ragged row tile), the text/video boundary when there is a prefix, and
     ``per_slab`` uniformly drawn rows.
     """
     gen = torch.Generator().manual_seed((w.seed if seed is None else seed) + 7777)
     N = w.N
-    fixed = set(range(min(64, N)))
-    fixed.update(range(max(0, N - (N % bm or bm) - bm), N))
+    fixed = set(range(min(head, N)))
+    fixed.update(range(max(0, N - tail), N))
     if w.n_text:
         fixed.update({w.n_text - 1, w.n_text})
     rows = []

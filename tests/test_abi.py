@@ -1,0 +1,127 @@
+"""The C ABI without a GPU: exported symbols, host-side validation (which
+returns before any HIP call) and the host rotary-table builder."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import brute
+from paper_2609_35110_amd import sol
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+P = ctypes.c_void_p
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(sol.LIB_PATH):
+        from paper_2609_35110_amd import build
+        build.build()
+    return sol.lib()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "sol.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sol_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(L):
+    names = declared_functions()
+    assert {"sol_attn_fwd", "sol_rope3d", "sol_rope3d_table", "sol_rope3d_table_floats"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), "libsol.so does not export %s" % n
+
+
+def test_status_strings(L):
+    assert sol.sol_status_string(0) == "ok"
+    for s in (-1, -2, -3):
+        assert sol.sol_status_string(s) not in ("ok", "unknown status")
+    assert sol.sol_version() == 100
+
+
+# Fake, 16-byte aligned device addresses: every call below is rejected on the
+# host before anything would dereference them.
+A, Bp, C, Dp, TAB = (P(0x100000 * i) for i in range(1, 6))
+
+
+def attn(q=A, k=Bp, v=C, out=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB):
+    return sol.sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, tab, None)
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(q=None), -1, "NULL"),
+    (dict(out=None), -1, "NULL"),
+    (dict(D=64), -2, "head dim"),
+    (dict(N=0), -1, ">= 1"),
+    (dict(B=0), -1, ">= 1"),
+    (dict(T=-1), -1, "negative"),
+    (dict(T=4), -1, "more tokens"),
+    (dict(N=(1 << 23) + 1, T=1, Hl=1, Wl=1), -2, "exceeds"),
+    (dict(q=P(0x100008)), -1, "aligned"),
+    (dict(out=P(0x500004)), -1, "aligned"),
+    (dict(tab=P(0x500008)), -1, "aligned"),
+    (dict(out=A), -1, "overlaps"),
+    (dict(out=P(0x100000 + 1024)), -1, "overlaps"),
+])
+def test_attn_fwd_rejects_before_any_hip_call(L, kw, status, fragment):
+    st = attn(**kw)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), -1),
+    (dict(D=96), -2),
+    (dict(T=5), -1),
+    (dict(tab=None), -1),
+    (dict(y=P(0x100000 + 4096)), -1),   # partial overlap (in place is allowed)
+])
+def test_rope3d_rejects_before_any_hip_call(L, kw, status):
+    args = dict(x=A, y=Bp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
+    args.update(kw)
+    st = sol.sol_rope3d(args["x"], args["y"], args["B"], args["H"], args["N"], args["D"],
+                        args["T"], args["Hl"], args["Wl"], args["tab"], None)
+    assert st == status, sol.sol_last_error()
+
+
+def test_binding_rejects_wrong_dtype_and_device():
+    import torch
+    x = torch.zeros(1, 1, 4, 128, dtype=torch.float32)
+    with pytest.raises(TypeError):
+        sol.attn_fwd(x, x, x, 1, 1, 1)
+    xb = x.to(torch.bfloat16)
+    with pytest.raises(ValueError):
+        sol.attn_fwd(xb, xb, xb, 1, 1, 1)  # CPU tensors are not device memory
+
+
+# ------------------------------------------------------------ rotary table
+
+def test_table_size(L):
+    assert sol.sol_rope3d_table_floats(128, 31, 45, 80) == 2 * (31 * 16 + 45 * 24 + 80 * 24)
+    assert sol.sol_rope3d_table_floats(100, 1, 1, 1) == 0
+    tab = np.zeros(10, np.float32)
+    st = sol.sol_rope3d_table(tab.ctypes.data_as(P), 10, 128, 3, 8, 8, 10000.0)
+    assert st == -1 and "needs" in sol.sol_last_error()
+
+
+def test_table_matches_oracle_angles(L):
+    """Each (cos, sin) entry is the float32 rounding of the oracle's angle for
+    that axis position and pair (within 1 float32 ulp: libm vs numpy)."""
+    T, Hl, Wl = 5, 7, 9
+    tab = sol.rope3d_table_host(T, Hl, Wl).reshape(-1, 2)
+    # the oracle's angle of every pair at every position of each axis alone
+    sections = []
+    for axis, (ext, lo, width) in enumerate([(T, 0, 32), (Hl, 32, 48), (Wl, 80, 48)]):
+        pos = np.zeros((ext, 3), np.int64)
+        pos[:, axis] = np.arange(ext)
+        ang = brute.rope_angles(pos)[:, lo // 2:(lo + width) // 2]
+        sections.append(ang.reshape(-1))
+    ang = np.concatenate(sections)
+    want = np.stack([np.cos(ang), np.sin(ang)], -1).astype(np.float32)
+    assert tab.shape == want.shape
+    ulps = np.abs(tab.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
+    close = np.abs(tab - want) <= 1e-7
+    assert np.all((ulps <= 1) | close)

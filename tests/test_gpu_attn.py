@@ -1,0 +1,280 @@
+"""GPU parity of the HIP path (libsol.so, through the C ABI) against the oracle.
+
+Full-tensor comparisons at sizes the oracle finishes in seconds (several row
+and key tiles, ragged tails, text prefixes, degenerate N); seeded row samples
+at the full workload sizes, in the launch configuration the benchmark times.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_35110_amd import sol
+from paper_2609_35110_amd import workloads as W
+
+from parity import assert_parity, bits_to_f32, compare
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    sol.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _bits(t):
+    return W.as_bits(t.cpu())
+
+
+def _run(q, k, v, w, rope=True):
+    """HIP path on device copies; returns the bf16 output on the CPU."""
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV) if rope and w.n_video else None
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    out = sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab)
+    torch.cuda.synchronize()
+    return out.cpu()
+
+
+def _full_parity(w, q, k, v, label, rope=True):
+    out = _run(q, k, v, w, rope)
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rope=rope)
+    R = w.B * w.H * w.N
+    slab = np.repeat(np.arange(w.B * w.H), w.N)
+    st = compare(_bits(out).reshape(R, w.D), ref.reshape(R, w.D), slab)
+    _log("%s %s: %s" % (label, w.describe(), st))
+    assert_parity(st, label)
+    return out, ref
+
+
+def test_library_is_the_in_tree_build():
+    assert os.path.dirname(sol.lib()._name) == os.path.dirname(sol.__file__)
+    assert sol.sol_version() == 100
+
+
+def test_tiny_full_parity():
+    w = W.WORKLOADS["tiny"]
+    q, k, v = W.make_inputs(w)
+    _full_parity(w, q, k, v, "tiny")
+
+
+EDGE = [
+    # (B, H, T, Hl, Wl, n_text): ragged row and key tiles, prefixes, degenerate N
+    (1, 3, 3, 11, 13, 37),    # N=466: 2 row tiles, 8 key tiles, ragged, text prefix
+    (2, 2, 2, 5, 7, 0),       # N=70: fewer rows than one tile
+    (1, 1, 1, 1, 1, 0),       # N=1: o = v
+    (1, 1, 4, 8, 8, 0),       # N=256: exact row tile, exact key tiles
+    (1, 2, 1, 1, 1, 256),     # N=257: one token past a tile
+    (1, 2, 2, 16, 16, 1),     # N=513
+    (2, 1, 5, 7, 9, 64),      # N=379, B=2
+]
+
+
+@pytest.mark.parametrize("shape", EDGE, ids=[str(s) for s in EDGE])
+def test_edge_shapes_full_parity(shape):
+    B, H, T, Hl, Wl, nt = shape
+    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=200 + sum(shape))
+    q, k, v = W.make_inputs(w)
+    out, _ = _full_parity(w, q, k, v, "edge")
+    if w.N == 1:
+        assert torch.equal(out, v), "N=1 must return v exactly"
+
+
+def test_text_only_no_rotation():
+    """An empty latent grid: nothing is rotated (plain attention, table NULL)."""
+    w = W.custom(1, 2, 0, 0, 0, n_text=300, seed_index=301)
+    q, k, v = W.make_inputs(w)
+    _full_parity(w, q, k, v, "text-only", rope=False)
+
+
+@pytest.mark.parametrize("name", ["low", "p480", "p720", "share"])
+def test_workload_sampled_parity(name):
+    w = W.WORKLOADS[name]
+    _log("generating %s" % w.describe())
+    q, k, v = W.make_inputs(w)
+    out = _run(q, k, v, w)
+    rows = W.sample_rows(w, per_slab=16, head=32, tail=80).numpy()
+    _log("oracle on %d rows" % len(rows))
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rows=rows)
+    got = _bits(out).reshape(-1, w.D)[rows]
+    st = compare(got, ref, rows // w.N)
+    _log("%s: %s" % (name, st))
+    assert_parity(st, name)
+
+
+# ------------------------------------------------------------ rotary kernel
+
+@pytest.mark.parametrize("shape", [(1, 2, 3, 8, 8, 0), (2, 3, 3, 11, 13, 37), (1, 2, 31, 45, 80, 512)])
+def test_rope3d_matches_oracle(shape):
+    """Standalone rotation vs the oracle's contract rotation (double, one
+    rounding).  The kernel rotates in fp32 with fp32 (cos, sin), an absolute
+    error of a few 2^-24 |pair|, so each element lies within one bf16 ulp of
+    the oracle's plus 4 * 2^-24 |pair| (the second term matters only where
+    a cos - b sin nearly cancels); >= 99.9 % are bit-identical."""
+    B, H, T, Hl, Wl, nt = shape
+    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=400 + sum(shape))
+    q, _, _ = W.make_inputs(w)
+    tab = sol.rope3d_table(T, Hl, Wl, device=DEV)
+    y = sol.rope3d(q.to(DEV), T, Hl, Wl, tab)
+    torch.cuda.synchronize()
+    got_bits, want_bits, x_bits = _bits(y), oracle.rope3d_bf16(_bits(q), T, Hl, Wl), _bits(q)
+    got, want, x = bits_to_f32(got_bits), bits_to_f32(want_bits), bits_to_f32(x_bits)
+    pair = np.sqrt(x[..., 0::2].astype(np.float64) ** 2 + x[..., 1::2].astype(np.float64) ** 2)
+    pair = np.repeat(pair, 2, axis=-1)
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(want), 1e-38))) - 7)
+    bound = ulp + 4.0 * 2.0 ** -24 * pair
+    diff = np.abs(got.astype(np.float64) - want)
+    exact = float((got_bits == want_bits).mean())
+    _log("rope3d %s: max diff/bound %.3f, exact %.6f" % (shape, (diff / bound).max(), exact))
+    assert (diff <= bound).all() and exact >= 0.999
+    assert np.array_equal(got_bits[..., :nt, :], x_bits[..., :nt, :]), "prefix must be copied"
+
+
+def test_rope3d_in_place():
+    w = W.custom(1, 2, 2, 6, 6, n_text=5, seed_index=410)
+    q, _, _ = W.make_inputs(w)
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    a = sol.rope3d(q.to(DEV), w.T, w.Hl, w.Wl, tab)
+    b = q.to(DEV)
+    sol.rope3d(b, w.T, w.Hl, w.Wl, tab, out=b)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 3, 8, 8, 0), (1, 3, 3, 11, 13, 37), (2, 1, 5, 7, 9, 64)])
+def test_fused_rotation_equals_prerotated(shape):
+    """Rotating q and k with sol_rope3d, then attending without rotation, is
+    bit-identical to the fused kernel (same fp32 rotation, same rounding)."""
+    B, H, T, Hl, Wl, nt = shape
+    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=500 + sum(shape))
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(T, Hl, Wl, device=DEV)
+    fused = sol.attn_fwd(q, k, v, T, Hl, Wl, tab)
+    qh, kh = sol.rope3d(q, T, Hl, Wl, tab), sol.rope3d(k, T, Hl, Wl, tab)
+    pre = sol.attn_fwd(qh, kh, v, T, Hl, Wl, None)
+    torch.cuda.synchronize()
+    assert torch.equal(fused, pre)
+
+
+# ------------------------------------------------------------ closed forms
+
+def test_constant_values_give_constant_output():
+    w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=600)
+    q, k, _ = W.make_inputs(w)
+    c = torch.randn(w.D, generator=torch.Generator().manual_seed(5)).to(torch.bfloat16)
+    v = c.expand(w.B, w.H, w.N, w.D).contiguous()
+    out = _run(q, k, v, w).float()
+    err = (out - c.float()).abs() / c.float().abs().clamp_min(1e-3)
+    assert err.max().item() <= 2.0 ** -7, "constant V must give V back within one bf16 ulp"
+
+
+def test_zero_query_gives_mean_of_values():
+    w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=601)
+    _, k, v = W.make_inputs(w)
+    q = torch.zeros_like(k)
+    out = _run(q, k, v, w).float()
+    want = v.float().mean(dim=2, keepdim=True).expand_as(out)
+    rms = want.pow(2).mean().sqrt()
+    assert ((out - want).abs() / rms).max().item() < 2e-2
+
+
+def test_one_hot_attention_returns_the_value():
+    """A key equal to the (unrotated) query with a logit gap of ~45 takes all
+    the weight: the output row is that value row, exactly."""
+    w = W.custom(1, 1, 0, 0, 0, n_text=200, seed_index=602)
+    q, k, v = W.make_inputs(w)
+    q.mul_(0.05)
+    k.mul_(0.05)
+    i, j = 17, 133
+    q[0, 0, i] = 2.0
+    k[0, 0, j] = 2.0
+    out = _run(q, k, v, w, rope=False)
+    assert torch.equal(out[0, 0, i], v[0, 0, j])
+
+
+# ------------------------------------------------------------ guards
+
+def test_no_out_of_bounds_reads_or_writes():
+    """Inputs live inside NaN-filled buffers and the output inside a sentinel
+    buffer: nothing past N may be read (NaN would leak) or written."""
+    w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=700)
+    q, k, v = W.make_inputs(w)
+    numel = q.numel()
+    pad = 4096 * w.D
+
+    def nan_padded(t):
+        buf = torch.full((numel + pad,), float("nan"), dtype=torch.bfloat16, device=DEV)
+        buf[:numel].copy_(t.reshape(-1))
+        return buf[:numel].view(t.shape)
+
+    qd, kd, vd = nan_padded(q), nan_padded(k), nan_padded(v)
+    sentinel = torch.full((numel + pad,), 123.0, dtype=torch.bfloat16, device=DEV)
+    out = sentinel[:numel].view(q.shape)
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()
+    assert (sentinel[numel:] == 123.0).all(), "write past the end of out"
+    clean = _run(q, k, v, w)
+    assert torch.equal(out.cpu(), clean)
+
+
+def test_repeated_runs_are_bitwise_identical():
+    w = W.custom(1, 4, 4, 16, 24, n_text=11, seed_index=701)
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    a = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
+    b = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_heads_and_batches_are_independent():
+    w = W.custom(2, 3, 3, 11, 13, n_text=5, seed_index=702)
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    full = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
+    b, h = 1, 2
+    one = sol.attn_fwd(q[b:b + 1, h:h + 1].contiguous(), k[b:b + 1, h:h + 1].contiguous(),
+                       v[b:b + 1, h:h + 1].contiguous(), w.T, w.Hl, w.Wl, tab)
+    torch.cuda.synchronize()
+    assert torch.equal(full[b:b + 1, h:h + 1], one)
+
+
+def test_offsets_beyond_2_pow_31_elements():
+    """B=1, H=160 heads of the 111,600-token layer: 2.29e9 elements per tensor.
+    Only the last two heads and the first one carry data; the rest are zero."""
+    base = W.WORKLOADS["p720"]
+    H = 160
+    w1 = W.custom(1, 2, base.T, base.Hl, base.Wl, seed_index=800)
+    qs, ks, vs = W.make_inputs(w1)
+    shape = (1, H, base.N, base.D)
+    assert np.prod(shape) > 2 ** 31
+    q = torch.zeros(shape, dtype=torch.bfloat16, device=DEV)
+    k = torch.zeros_like(q)
+    v = torch.zeros_like(q)
+    q[:, H - 2:].copy_(qs)
+    k[:, H - 2:].copy_(ks)
+    v[:, H - 2:].copy_(vs)
+    tab = sol.rope3d_table(base.T, base.Hl, base.Wl, device=DEV)
+    out = sol.attn_fwd(q, k, v, base.T, base.Hl, base.Wl, tab)
+    torch.cuda.synchronize()
+    tail = out[:, H - 2:].cpu()
+    del q, k, v, out
+    torch.cuda.empty_cache()
+    rows = W.sample_rows(w1, per_slab=16, head=8, tail=80).numpy()
+    ref = oracle.attn_rows(_bits(qs), _bits(ks), _bits(vs), w1.T, w1.Hl, w1.Wl, rows=rows)
+    st = compare(_bits(tail).reshape(-1, w1.D)[rows], ref, rows // w1.N)
+    _log("2^31 offsets: %s" % st)
+    assert_parity(st, "large offsets")
