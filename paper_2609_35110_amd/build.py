@@ -17,6 +17,9 @@ HIPCC_FLAGS = [
     "--offload-arch=" + ARCH,
     # every multiply/add in the kernels is written out; no silent contraction
     "-ffp-contract=off",
+    # no NaN arises in the kernels' own arithmetic (masking uses -inf): lets
+    # max reductions compile to v_max3 without NaN canonicalisation
+    "-fno-honor-nans",
     # no packed fp32 VALU instructions (v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-command-line-argument",

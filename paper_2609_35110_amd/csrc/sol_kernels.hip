@@ -101,9 +101,7 @@ __device__ __forceinline__ uint4 bf16x8_to_f16x8(uint4 x) {
 //   (a, b) -> (a cos - b sin, a sin + b cos), fp32, then bf16 RNE.
 // The one function every rotation in this library goes through, so the
 // standalone rotation and the fused tile loads agree bit for bit.
-__device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ tab, int pair0) {
-  const float4 cs01 = *reinterpret_cast<const float4*>(tab + pair0);
-  const float4 cs23 = *reinterpret_cast<const float4*>(tab + pair0 + 2);
+__device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) {
   const float c[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
   const float s[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
   uint32_t w[4] = {x.x, x.y, x.z, x.w};
@@ -116,6 +114,11 @@ __device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ 
     w[u] = pack_bf16x2(ar, br);
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ tab, int pair0) {
+  return rope_rotate(x, *reinterpret_cast<const float4*>(tab + pair0),
+                     *reinterpret_cast<const float4*>(tab + pair0 + 2));
 }
 
 // --------------------------------------------------------- standalone rotary
@@ -146,17 +149,43 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int BM = 32 * kWaves;  // query rows per workgroup (32 per wave)
 constexpr int BN = 64;           // keys per tile
 constexpr int KS = D + 8;        // K tile row stride in LDS (elements): 272 B
-constexpr int VS = D + 16;       // V tile row stride in LDS (elements): 288 B
+constexpr int VS = D + 32;       // V tile row stride in LDS (elements): 320 B
+constexpr int kTabLdsPairs = 6144;  // rotary tables up to 48 KB are staged in LDS
 constexpr float kLazyRescaleLog2 = 8.0f;
-static_assert(2 * kThreads == BN * kChunks, "staging: two 16-byte chunks of K and V per thread per tile");
+static_assert(kThreads == 8 * BN, "staging: one tile row per 8 threads, two 16-byte chunks each");
 
-template <bool kRope>
+// Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSgMfma = 0x008, kSgValu = 0x002, kSgDsRead = 0x100, kSgDsWrite = 0x200;
+
+// First table pair of chunk c (< 8: frame or row axis) and c + 8 (row or column axis).
+__device__ __forceinline__ int tab_pair_lo(int c, const Pos& p, const SeqGrid& g) {
+  return c < 4 ? p.t * 16 + 4 * c : g.tab_h + p.h * 24 + 4 * (c - 4);
+}
+__device__ __forceinline__ int tab_pair_hi(int c, const Pos& p, const SeqGrid& g) {
+  return c < 2 ? g.tab_h + p.h * 24 + 4 * (c + 4) : g.tab_w + p.w * 24 + 4 * (c - 2);
+}
+
+// Software pipeline, per wave, one barrier per 64-key tile.  Iteration i:
+//   phase A (one scheduling region): S(i+1) = K^(i+1) Q^^T on the matrix
+//     cores, interleaved with P(i) = exp2(S(i) c - m c) and its row sums on
+//     the VALU -- independent work, so the two pipes overlap;
+//   phase B (one region): O^T += V(i)^T P(i)^T on the matrix cores,
+//     interleaved with staging K(i+2) (rotated, bf16) and V(i+1) (fp16) from
+//     registers into LDS;
+//   then the mask, row max and (rare) lazy rescale for tile i+1.
+// K runs one tile ahead of V.  LDS: K(i+1) is read while K(i+2) is written
+// over K(i) (last read in iteration i-1); V(i) is read while V(i+1) is
+// written over V(i-1); the barrier ending each iteration orders every reuse.
+// Loads past the last tile re-read row N-1 and land in buffers nobody reads,
+// so phases A and B are branch-free.
+template <bool kRope, bool kTabLds>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
-    const float2* __restrict__ tab, int n_qtiles, float c_log2) {
+    const float2* __restrict__ tab_g, int tab_pairs, int n_qtiles, float c_log2) {
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][BN * KS];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][BN * VS];
+  __shared__ __attribute__((aligned(16))) float2 tab_lds[kTabLds ? kTabLdsPairs : 2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -171,92 +200,99 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   const uint16_t* __restrict__ ks = k + slab;
   const uint16_t* __restrict__ vs = v + slab;
 
+  const float2* tab = tab_g;
+  if (kRope && kTabLds) {
+    for (int i = tid * 2; i < tab_pairs; i += 2 * kThreads)  // tab_pairs is a multiple of 4
+      *reinterpret_cast<float4*>(&tab_lds[i]) = *reinterpret_cast<const float4*>(&tab_g[i]);
+    tab = tab_lds;
+  }
+
   // ---- Q^ fragment (B operand of S^T = K^ Q^^T): dims [16kk + 8hh, +8) of one row.
   const int qrow = qt * BM + wave * 32 + l32;
   bf16x8 qf[8];
-  if (qrow < N) {
-    const uint4* src = reinterpret_cast<const uint4*>(qs + (size_t)qrow * D);
+  {
+    const uint4* src = reinterpret_cast<const uint4*>(qs + (size_t)min(qrow, N - 1) * D);
     Pos p{0, 0, 0, false};
-    if (kRope) p = token_pos(qrow, g);
+    if (kRope) p = token_pos(min(qrow, N - 1), g);
+    if (kRope && kTabLds) __syncthreads();  // table staged
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       const int cc = 2 * kk + hh;
       uint4 x = src[cc];
-      if (kRope && p.rot) x = rope_chunk(x, tab, tab_pair(cc, p, g));
+      // prefix tokens sit at (0, 0, 0): cos 0 = 1, sin 0 = 0, an exact identity
+      if (kRope) x = rope_chunk(x, tab, tab_pair(cc, p, g));
       qf[kk] = __builtin_bit_cast(bf16x8, x);
     }
-  } else {
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) qf[kk] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
   }
 
-  // ---- K/V staging: this thread moves chunk column cc_s of tile rows rs0 and rs0 + 32.
-  const int cc_s = tid & (kChunks - 1);
-  const int rs0 = tid >> 4;
+  // ---- staging: thread moves chunks c0 and c0 + 8 of tile row rr.
+  const int rr = tid >> 3;
+  const int c0 = tid & 7;
   uint4 kreg[2], vreg[2];
-  auto load_tile = [&](int kv0) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int j = kv0 + rs0 + 32 * i;
-      if (j < N) {
-        kreg[i] = reinterpret_cast<const uint4*>(ks + (size_t)j * D)[cc_s];
-        vreg[i] = reinterpret_cast<const uint4*>(vs + (size_t)j * D)[cc_s];
-      } else {
-        kreg[i] = make_uint4(0, 0, 0, 0);  // keys past N are masked, values must be finite
-        vreg[i] = make_uint4(0, 0, 0, 0);
-      }
+  float4 kcs[4];  // (cos, sin) of the 8 rotary pairs of the two staged K chunks
+  auto load_kv = [&](int kv0k, int kv0v) {
+    const uint4* sk = reinterpret_cast<const uint4*>(ks + (size_t)min(kv0k + rr, N - 1) * D);
+    const uint4* sv = reinterpret_cast<const uint4*>(vs + (size_t)min(kv0v + rr, N - 1) * D);
+    kreg[0] = sk[c0];
+    kreg[1] = sk[c0 + 8];
+    vreg[0] = sv[c0];
+    vreg[1] = sv[c0 + 8];
+  };
+  auto fetch_k_rotation = [&](int kv0) {
+    if (kRope) {
+      const Pos p = token_pos(min(kv0 + rr, N - 1), g);
+      const int a0 = tab_pair_lo(c0, p, g), a1 = tab_pair_hi(c0, p, g);
+      kcs[0] = *reinterpret_cast<const float4*>(tab + a0);
+      kcs[1] = *reinterpret_cast<const float4*>(tab + a0 + 2);
+      kcs[2] = *reinterpret_cast<const float4*>(tab + a1);
+      kcs[3] = *reinterpret_cast<const float4*>(tab + a1 + 2);
     }
   };
-  auto store_tile = [&](int kv0, int buf) {
+  auto store_k = [&](int buf) {
+    uint4 x0 = kreg[0], x1 = kreg[1];
+    if (kRope) {
+      x0 = rope_rotate(x0, kcs[0], kcs[1]);
+      x1 = rope_rotate(x1, kcs[2], kcs[3]);
+    }
+    *reinterpret_cast<uint4*>(&k_lds[buf][rr * KS + c0 * 8]) = x0;
+    *reinterpret_cast<uint4*>(&k_lds[buf][rr * KS + c0 * 8 + 64]) = x1;
+  };
+  auto store_v = [&](int buf) {
+    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8]) = bf16x8_to_f16x8(vreg[0]);
+    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8 + 64]) = bf16x8_to_f16x8(vreg[1]);
+  };
+
+  // K fragment (A operand) of key block kb (0/1), dims [16kk + 8hh, +8).
+  auto kfrag = [&](const uint16_t* kbuf, int kb, int kk) {
+    return *reinterpret_cast<const bf16x8*>(kbuf + (32 * kb + l32) * KS + kk * 16 + hh * 8);
+  };
+  auto scores = [&](int buf, f32x16& s0, f32x16& s1) {
+    const uint16_t* kb = k_lds[buf];
+    s0 = f32x16{};
+    s1 = f32x16{};
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int r = rs0 + 32 * i;
-      uint4 kx = kreg[i];
-      if (kRope) {
-        const int j = kv0 + r;
-        if (j < N) {
-          const Pos p = token_pos(j, g);
-          if (p.rot) kx = rope_chunk(kx, tab, tab_pair(cc_s, p, g));
-        }
-      }
-      *reinterpret_cast<uint4*>(&k_lds[buf][r * KS + cc_s * 8]) = kx;
-      *reinterpret_cast<uint4*>(&v_lds[buf][r * VS + cc_s * 8]) = bf16x8_to_f16x8(vreg[i]);
+    for (int kk = 0; kk < 8; ++kk) {
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, 0, kk), qf[kk], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, 1, kk), qf[kk], s1, 0, 0, 0);
     }
   };
 
   // V^T operand addressing for the transpose read: within each 16-lane group,
   // lane 4s + c supplies row s (of 4) and 4 columns starting at 4c.
   const int g16 = lane >> 4, i16 = lane & 15;
-  const int v_row = 4 * (g16 >> 1) + (i16 >> 2);
-  const int v_col = 16 * (g16 & 1) + 4 * (i16 & 3);
-
-  const int n_kv = (N + BN - 1) / BN;
-  load_tile(0);
-  store_tile(0, 0);
-  __syncthreads();
+  const int v_off = (4 * (g16 >> 1) + (i16 >> 2)) * VS + 16 * (g16 & 1) + 4 * (i16 & 3);
 
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
   float m_run = -__builtin_inff();
   float l_run = 0.0f;
+  const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 
-  for (int it = 0; it < n_kv; ++it) {
-    const int buf = it & 1;
+  // Mask keys >= N (tile `it` is the ragged last one) and fold the tile's row
+  // max into the running max (lazy rescale of o and l).
+  auto row_max = [&](int it, f32x16& s0, f32x16& s1) {
     const int kv0 = it * BN;
-    const bool has_next = it + 1 < n_kv;
-    if (has_next) load_tile(kv0 + BN);
-
-    // S^T for key blocks [kv0, kv0+32) and [kv0+32, kv0+64).
-    const uint16_t* kb = k_lds[buf];
-    f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(kb + l32 * KS + kk * 16 + hh * 8);
-      const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(kb + (32 + l32) * KS + kk * 16 + hh * 8);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[kk], s1, 0, 0, 0);
-    }
     // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of that block.
     if (kv0 + BN > N) {
 #pragma unroll
@@ -266,7 +302,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
         if (key + 32 >= N) s1[j] = -__builtin_inff();
       }
     }
-
     float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
     for (int j = 1; j < 16; ++j) mx = fmaxf(mx, fmaxf(s0[j], s1[j]));
@@ -279,37 +314,93 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
 #pragma unroll
       for (int db = 0; db < 4; ++db) o[db] *= alpha;
     }
-    const float mc = m_run * c_log2;
+  };
 
-    // P = exp2(S c - m c), rounded to fp16: the B operand of O^T += V^T P^T.
-    f16x8 pb[4];
+  const int n_kv = (N + BN - 1) / BN;
+  auto iteration = [&](int it, f32x16& cs0, f32x16& cs1, f32x16& ns0, f32x16& ns1) {
+    load_kv((it + 2) * BN, (it + 1) * BN);
+    fetch_k_rotation((it + 2) * BN);
+    __builtin_amdgcn_sched_barrier(0);  // issue the loads first: phase B consumes them
+    // ---- phase A: S(it+1) on MFMA; P(it) and its row sums on VALU.
+    {
+      const uint16_t* kb = k_lds[(it + 1) & 1];
+      ns0 = f32x16{};
+      ns1 = f32x16{};
+      const float mc = m_run * c_log2;
+      f16x8 pb[4];
+      float la = 0.0f, lb = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s0[j], c_log2, -mc));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s1[j], c_log2, -mc));
-      l_run += p0 + p1;
-      pb[j >> 3][j & 7] = (_Float16)p0;
-      pb[2 + (j >> 3)][j & 7] = (_Float16)p1;
-    }
-
-    // O^T[d, q] += sum over 16-key steps of V^T[d, key] P^T[key, q].
-    const uint16_t* vb = v_lds[buf];
+      for (int kk = 0; kk < 8; ++kk) {
+        ns0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, 0, kk), qf[kk], ns0, 0, 0, 0);
+        ns1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, 1, kk), qf[kk], ns1, 0, 0, 0);
+        // logits 4kk .. 4kk+3 of this lane: s0[0..15] then s1[0..15]
 #pragma unroll
-    for (int kst = 0; kst < 4; ++kst) {
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const uint16_t* p0 = vb + (16 * kst + v_row) * VS + 32 * db + v_col;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 8 * VS));
-        const f16x8 a = __builtin_bit_cast(
-            f16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb[kst], o[db], 0, 0, 0);
+        for (int u = 0; u < 4; ++u) {
+          const int idx = 4 * kk + u;
+          const float sv = idx < 16 ? cs0[idx] : cs1[idx - 16];
+          pb[idx >> 3][idx & 7] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(sv, c_log2, -mc));
+        }
+        // row sums of the rounded probabilities (exact fp32 sums of fp16
+        // values), so numerator and denominator weigh keys identically
+        const int t = kk >> 1, e = 4 * (kk & 1);
+        la = __builtin_amdgcn_fdot2(f16x2{pb[t][e], pb[t][e + 1]}, ones, la, false);
+        lb = __builtin_amdgcn_fdot2(f16x2{pb[t][e + 2], pb[t][e + 3]}, ones, lb, false);
       }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSgValu, 12, 0);
+      }
+      l_run += la + lb;
+      // ---- phase B: O^T += V(it)^T P(it)^T on MFMA; staging on VALU.
+      const uint16_t* vb = v_lds[it & 1] + v_off;
+#pragma unroll
+      for (int kst = 0; kst < 4; ++kst) {
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const uint16_t* p0 = vb + 16 * kst * VS + 32 * db;
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 8 * VS));
+          const f16x8 a = __builtin_bit_cast(
+              f16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pb[kst], o[db], 0, 0, 0);
+        }
+      }
+      store_k(it & 1);
+      store_v((it + 1) & 1);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 1);
+        __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(kSgValu, 6, 1);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSgDsWrite, 4, 1);
     }
-
-    if (has_next) store_tile(kv0 + BN, buf ^ 1);
+    if (it + 1 < n_kv) row_max(it + 1, ns0, ns1);
     __syncthreads();
+  };
+
+  // ---- prologue: K(0), V(0), K(1) into LDS; S(0) and its row max.
+  load_kv(0, 0);
+  fetch_k_rotation(0);
+  store_k(0);
+  store_v(0);
+  load_kv(BN, BN);
+  fetch_k_rotation(BN);
+  store_k(1);
+  __syncthreads();
+  f32x16 sa0, sa1, sb0, sb1;
+  scores(0, sa0, sa1);
+  row_max(0, sa0, sa1);
+  __syncthreads();  // K(2) will overwrite K(0)
+
+  int it = 0;
+  for (; it + 1 < n_kv; it += 2) {
+    iteration(it, sa0, sa1, sb0, sb1);
+    iteration(it + 1, sb0, sb1, sa0, sa1);
   }
+  if (it < n_kv) iteration(it, sa0, sa1, sb0, sb1);
 
   // ---- epilogue: out = O / l in bf16; register j of block db is dim 32db + 8(j/4) + 4hh + j%4.
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -349,12 +440,16 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
-  if (tab != nullptr)
-    hipLaunchKernelGGL(attn_fwd_kernel<true>, grid, dim3(kThreads), 0, stream, q, k, v, out, g,
-                       tab, n_qtiles, c_log2);
+  const int tab_pairs = g.tab_w + g.Wl * (3 * D / 16);
+  if (tab == nullptr)
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false>), grid, dim3(kThreads), 0, stream, q, k, v,
+                       out, g, tab, 0, n_qtiles, c_log2);
+  else if (tab_pairs <= kTabLdsPairs)
+    hipLaunchKernelGGL((attn_fwd_kernel<true, true>), grid, dim3(kThreads), 0, stream, q, k, v,
+                       out, g, tab, tab_pairs, n_qtiles, c_log2);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<false>, grid, dim3(kThreads), 0, stream, q, k, v, out, g,
-                       tab, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_fwd_kernel<true, false>), grid, dim3(kThreads), 0, stream, q, k, v,
+                       out, g, tab, tab_pairs, n_qtiles, c_log2);
   return hipGetLastError();
 }
 
