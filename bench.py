@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="p720", help="tiny | low | p480 | p720 | share")
+    ap.add_argument("--path", default="fused", choices=["fused", "ws"],
+                    help="fused: sol_attn_fwd (K rotated in every tile load); ws: sol_attn_fwd_ws "
+                         "(K rotated and V converted once into a workspace, then tile copies)")
     ap.add_argument("--cpu-rows-per-thread", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -137,8 +140,17 @@ def main():
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=dev)
     torch.cuda.synchronize()
 
+    if args.path == "ws":
+        ws = sol.attn_workspace(qd)
+
+        def step():
+            sol.attn_fwd_ws(qd, kd, vd, w.T, w.Hl, w.Wl, tab, workspace=ws, out=out)
+    else:
+        def step():
+            sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+
     for _ in range(args.warmup):
-        sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+        step()
     torch.cuda.synchronize()
     log("warmup done")
 
@@ -147,7 +159,7 @@ def main():
     torch.cuda.synchronize()
     ev[0].record(stream)
     for i in range(args.steps):
-        sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+        step()
         ev[i + 1].record(stream)
     torch.cuda.synchronize()
     per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
@@ -178,7 +190,9 @@ def main():
         "config": {
             "workload": "%s: %s" % (w.name, w.describe()),
             "B": w.B, "H": w.H, "N": w.N, "D": w.D, "grid": [w.T, w.Hl, w.Wl], "n_text": w.n_text,
-            "rope": "3d (32/48/48, base 1e4) fused into the q/k tile loads",
+            "rope": ("3d (32/48/48, base 1e4) fused into the q/k tile loads" if args.path == "fused"
+                     else "3d (32/48/48, base 1e4): q in the tile load, k in a one-pass prologue"),
+            "path": "sol_attn_fwd" if args.path == "fused" else "sol_attn_fwd_ws",
         },
         "ms_per_layer": ms_step,
         "ms_per_layer_median": ms_median,

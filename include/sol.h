@@ -101,6 +101,26 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
 int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
                  int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
 
+/*
+ * Bytes of device workspace sol_attn_fwd_ws needs: room for the rotated K
+ * (bf16) and V converted to fp16, 2 * B*H*N*D * 2 bytes.  0 for invalid sizes.
+ */
+size_t sol_attn_workspace_bytes(int B, int H, int N, int D);
+
+/*
+ * Same result as sol_attn_fwd, bit for bit, computed in two launches on
+ * `stream`: one HBM pass writes k^ = bf16(R(pos) k) and fp16(v) into the
+ * caller's workspace (the rotation of K done once per token instead of once
+ * per query tile), then the attention kernel rotates q in its tile load and
+ * streams the prepared K and V tiles unchanged.  workspace: device memory of
+ * at least sol_attn_workspace_bytes(B, H, N, D) bytes, 16-byte aligned, not
+ * overlapping q, k, v or out; its contents on entry are ignored and on exit
+ * hold the prepared K and V.  Other arguments and errors as sol_attn_fwd.
+ */
+int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
+                    int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,
+                    size_t workspace_bytes, sol_stream_t stream);
+
 /* Static description of a status code. */
 const char* sol_status_string(int status);
 

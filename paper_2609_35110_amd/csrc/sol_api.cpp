@@ -136,6 +136,44 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
   return ok();
 }
 
+size_t sol_attn_workspace_bytes(int B, int H, int N, int D) {
+  if (B < 1 || H < 1 || N < 1 || D < 1) return 0;
+  return 2 * (size_t)B * H * N * D * 2;
+}
+
+int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
+                    int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,
+                    size_t workspace_bytes, sol_stream_t stream) {
+  if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must be 16-byte aligned");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k, bytes) || overlaps(out, bytes, v, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k or v");
+  const size_t need = sol_attn_workspace_bytes(B, H, N, D);
+  if (!workspace) return fail(SOL_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SOL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  if (workspace_bytes < need)
+    return fail(SOL_ERR_INVALID_ARG, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (overlaps(workspace, need, q, bytes) || overlaps(workspace, need, k, bytes) ||
+      overlaps(workspace, need, v, bytes) || overlaps(workspace, need, out, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "workspace overlaps q, k, v or out");
+  if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  uint16_t* k_rot = static_cast<uint16_t*>(workspace);
+  uint16_t* v_f16 = k_rot + (size_t)B * H * N * D;
+  hipError_t e = sol::launch_attn_fwd_pre(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                          static_cast<const uint16_t*>(v), static_cast<uint16_t*>(out),
+                                          k_rot, v_f16, B * H, g, tab, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_ws launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 const char* sol_status_string(int status) {
   switch (status) {
     case SOL_OK: return "ok";

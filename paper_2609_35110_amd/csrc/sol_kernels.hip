@@ -142,6 +142,31 @@ __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x
   }
 }
 
+// One pass over K and V for the workspace path: K^ = rotated K (bf16, the same
+// rounding as the fused tile load), V converted to fp16.  One thread per
+// 16-byte chunk of one (b, h) slab; grid.y walks the slabs.
+template <bool kRope>
+__global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ k,
+                                                      const uint4* __restrict__ v,
+                                                      uint4* __restrict__ kh, uint4* __restrict__ v16,
+                                                      int64_t bh_count, SeqGrid g,
+                                                      const float2* __restrict__ tab) {
+  const int64_t per_slab = (int64_t)g.n * kChunks;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= per_slab) return;
+  const int n = (int)(i / kChunks);
+  const int cc = (int)(i % kChunks);
+  const Pos p = kRope ? token_pos(n, g) : Pos{0, 0, 0, false};
+  const int pair0 = (kRope && p.rot) ? tab_pair(cc, p, g) : 0;
+  for (int64_t bh = blockIdx.y; bh < bh_count; bh += gridDim.y) {
+    const int64_t idx = bh * per_slab + i;
+    uint4 x = k[idx];
+    if (kRope && p.rot) x = rope_chunk(x, tab, pair0);
+    kh[idx] = x;
+    v16[idx] = bf16x8_to_f16x8(v[idx]);
+  }
+}
+
 // ------------------------------------------------------------ fused attention
 
 constexpr int kWaves = 8;
@@ -178,7 +203,10 @@ __device__ __forceinline__ int tab_pair_hi(int c, const Pos& p, const SeqGrid& g
 // written over V(i-1); the barrier ending each iteration orders every reuse.
 // Loads past the last tile re-read row N-1 and land in buffers nobody reads,
 // so phases A and B are branch-free.
-template <bool kRope, bool kTabLds>
+// kRope: rotate Q (and K unless kPre) with the table; kTabLds: the table is
+// staged in LDS; kPre: k is already rotated and v already fp16 (workspace
+// path), so staging is a plain copy.
+template <bool kRope, bool kTabLds, bool kPre>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
@@ -239,7 +267,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     vreg[1] = sv[c0 + 8];
   };
   auto fetch_k_rotation = [&](int kv0) {
-    if (kRope) {
+    if (kRope && !kPre) {
       const Pos p = token_pos(min(kv0 + rr, N - 1), g);
       const int a0 = tab_pair_lo(c0, p, g), a1 = tab_pair_hi(c0, p, g);
       kcs[0] = *reinterpret_cast<const float4*>(tab + a0);
@@ -250,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   };
   auto store_k = [&](int buf) {
     uint4 x0 = kreg[0], x1 = kreg[1];
-    if (kRope) {
+    if (kRope && !kPre) {
       x0 = rope_rotate(x0, kcs[0], kcs[1]);
       x1 = rope_rotate(x1, kcs[2], kcs[3]);
     }
@@ -258,8 +286,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     *reinterpret_cast<uint4*>(&k_lds[buf][rr * KS + c0 * 8 + 64]) = x1;
   };
   auto store_v = [&](int buf) {
-    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8]) = bf16x8_to_f16x8(vreg[0]);
-    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8 + 64]) = bf16x8_to_f16x8(vreg[1]);
+    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8]) = kPre ? vreg[0] : bf16x8_to_f16x8(vreg[0]);
+    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8 + 64]) = kPre ? vreg[1] : bf16x8_to_f16x8(vreg[1]);
   };
 
   // K fragment (A operand) of key block kb (0/1), dims [16kk + 8hh, +8).
@@ -442,14 +470,43 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   const int tab_pairs = g.tab_w + g.Wl * (3 * D / 16);
   if (tab == nullptr)
-    hipLaunchKernelGGL((attn_fwd_kernel<false, false>), grid, dim3(kThreads), 0, stream, q, k, v,
-                       out, g, tab, 0, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false, false>), grid, dim3(kThreads), 0, stream, q,
+                       k, v, out, g, tab, 0, n_qtiles, c_log2);
   else if (tab_pairs <= kTabLdsPairs)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, true>), grid, dim3(kThreads), 0, stream, q, k, v,
-                       out, g, tab, tab_pairs, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_fwd_kernel<true, true, false>), grid, dim3(kThreads), 0, stream, q,
+                       k, v, out, g, tab, tab_pairs, n_qtiles, c_log2);
   else
-    hipLaunchKernelGGL((attn_fwd_kernel<true, false>), grid, dim3(kThreads), 0, stream, q, k, v,
-                       out, g, tab, tab_pairs, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_fwd_kernel<true, false, false>), grid, dim3(kThreads), 0, stream, q,
+                       k, v, out, g, tab, tab_pairs, n_qtiles, c_log2);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_fwd_pre(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                               uint16_t* out, uint16_t* k_rot, uint16_t* v_f16, int BH,
+                               const SeqGrid& g, const float2* tab, hipStream_t stream) {
+  const int64_t per_slab = (int64_t)g.n * kChunks;
+  const dim3 pgrid((unsigned)((per_slab + 255) / 256), (unsigned)(BH < 65535 ? BH : 65535));
+  if (tab != nullptr)
+    hipLaunchKernelGGL(prep_kv_kernel<true>, pgrid, dim3(256), 0, stream,
+                       reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
+                       reinterpret_cast<uint4*>(k_rot), reinterpret_cast<uint4*>(v_f16),
+                       (int64_t)BH, g, tab);
+  else
+    hipLaunchKernelGGL(prep_kv_kernel<false>, pgrid, dim3(256), 0, stream,
+                       reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
+                       reinterpret_cast<uint4*>(k_rot), reinterpret_cast<uint4*>(v_f16),
+                       (int64_t)BH, g, tab);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n_qtiles = (g.n + BM - 1) / BM;
+  const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
+  const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
+  if (tab != nullptr)
+    hipLaunchKernelGGL((attn_fwd_kernel<true, false, true>), grid, dim3(kThreads), 0, stream, q,
+                       k_rot, v_f16, out, g, tab, 0, n_qtiles, c_log2);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false, true>), grid, dim3(kThreads), 0, stream, q,
+                       k_rot, v_f16, out, g, tab, 0, n_qtiles, c_log2);
   return hipGetLastError();
 }
 

@@ -47,6 +47,10 @@ def lib():
         L.sol_rope3d.restype = i32
         L.sol_attn_fwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_attn_fwd.restype = i32
+        L.sol_attn_workspace_bytes.argtypes = [i32, i32, i32, i32]
+        L.sol_attn_workspace_bytes.restype = sz
+        L.sol_attn_fwd_ws.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, sz, P]
+        L.sol_attn_fwd_ws.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
         L.sol_last_error.argtypes = []
@@ -73,6 +77,15 @@ def sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream):
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
     return lib().sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_attn_workspace_bytes(B, H, N, D):
+    return lib().sol_attn_workspace_bytes(B, H, N, D)
+
+
+def sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, workspace, workspace_bytes, stream):
+    return lib().sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, workspace,
+                                 workspace_bytes, stream)
 
 
 def sol_status_string(status):
@@ -157,4 +170,32 @@ def attn_fwd(q, k, v, T, Hl, Wl, table=None, out=None):
     check(sol_attn_fwd(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
                        ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N, D,
                        T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
+    return out
+
+
+def attn_workspace(q):
+    """A device workspace of the size attn_fwd_ws needs for q's shape (uint8)."""
+    B, H, N, D = q.shape
+    return torch.empty(sol_attn_workspace_bytes(B, H, N, D), dtype=torch.uint8, device=q.device)
+
+
+def attn_fwd_ws(q, k, v, T, Hl, Wl, table=None, workspace=None, out=None):
+    """attn_fwd through the workspace path (K rotated and V converted in one
+    pass, then tile copies); bitwise the same result."""
+    _check_tensor("q", q)
+    _check_tensor("k", k, q.shape)
+    _check_tensor("v", v, q.shape)
+    B, H, N, D = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensor("out", out, q.shape)
+    if workspace is None:
+        workspace = attn_workspace(q)
+    if not workspace.is_cuda or workspace.device != q.device or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor on %s" % q.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    check(sol_attn_fwd_ws(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                          ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N,
+                          D, T, Hl, Wl, _table_ptr(table, q.device),
+                          ctypes.c_void_p(workspace.data_ptr()), nbytes, _stream(q)))
     return out

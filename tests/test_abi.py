@@ -72,6 +72,36 @@ def test_attn_fwd_rejects_before_any_hip_call(L, kw, status, fragment):
     assert fragment in sol.sol_last_error()
 
 
+WS = P(0x10000000)
+
+
+def attn_ws(q=A, k=Bp, v=C, out=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB, ws=WS,
+            ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = sol.sol_attn_workspace_bytes(B, H, N, D)
+    return sol.sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, tab, ws, ws_bytes, None)
+
+
+def test_workspace_size(L):
+    assert sol.sol_attn_workspace_bytes(1, 40, 111600, 128) == 2 * 40 * 111600 * 128 * 2
+    assert sol.sol_attn_workspace_bytes(0, 1, 1, 128) == 0
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(ws=None), -1, "workspace is NULL"),
+    (dict(ws=P(0x10000008)), -1, "aligned"),
+    (dict(ws_bytes=1000), -1, "workspace needs"),
+    (dict(ws=P(0x100000 - 4096)), -1, "workspace overlaps"),
+    (dict(D=64), -2, "head dim"),
+    (dict(out=Bp), -1, "overlaps"),
+    (dict(T=9), -1, "more tokens"),
+])
+def test_attn_fwd_ws_rejects_before_any_hip_call(L, kw, status, fragment):
+    st = attn_ws(**kw)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(x=None), -1),
     (dict(D=96), -2),

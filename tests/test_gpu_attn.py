@@ -167,6 +167,41 @@ def test_fused_rotation_equals_prerotated(shape):
     assert torch.equal(fused, pre)
 
 
+@pytest.mark.parametrize("shape", [(1, 2, 3, 8, 8, 0), (1, 3, 3, 11, 13, 37), (2, 1, 5, 7, 9, 64),
+                                   (1, 1, 1, 1, 1, 0), (1, 2, 0, 0, 0, 300)])
+def test_workspace_path_is_bitwise_the_fused_path(shape):
+    """sol_attn_fwd_ws (K rotated and V converted once into the workspace)
+    returns exactly the bytes of sol_attn_fwd, and leaves the prepared K and V
+    in the workspace."""
+    B, H, T, Hl, Wl, nt = shape
+    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=550 + sum(shape))
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(T, Hl, Wl, device=DEV) if w.n_video else None
+    fused = sol.attn_fwd(q, k, v, T, Hl, Wl, tab)
+    ws = sol.attn_workspace(q)
+    ws.fill_(0xFF)  # contents on entry are ignored
+    pre = sol.attn_fwd_ws(q, k, v, T, Hl, Wl, tab, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(fused, pre)
+    n = q.numel()
+    k_rot = ws[: 2 * n].view(torch.bfloat16).view(q.shape)
+    want_k = sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k
+    torch.cuda.synchronize()
+    assert torch.equal(k_rot, want_k)
+    assert torch.equal(ws[2 * n: 4 * n].view(torch.float16).view(q.shape), v.to(torch.float16))
+
+
+@pytest.mark.parametrize("name", ["p480", "share"])
+def test_workspace_path_full_size_matches_fused(name):
+    w = W.WORKLOADS[name]
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    a = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
+    b = sol.attn_fwd_ws(q, k, v, w.T, w.Hl, w.Wl, tab)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
 # ------------------------------------------------------------ closed forms
 
 def test_constant_values_give_constant_output():
