@@ -330,9 +330,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
         if (key + 32 >= N) s1[j] = -__builtin_inff();
       }
     }
+    // a chain of three-input maxima (v_max3_f32): one instruction per two scores
     float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
-    for (int j = 1; j < 16; ++j) mx = fmaxf(mx, fmaxf(s0[j], s1[j]));
+    for (int j = 1; j < 16; ++j) mx = fmaxf(fmaxf(mx, s0[j]), s1[j]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
     if (__any((m_new - m_run) * c_log2 > kLazyRescaleLog2)) {
@@ -355,25 +356,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
       ns0 = f32x16{};
       ns1 = f32x16{};
       const float mc = m_run * c_log2;
-      f16x8 pb[4];
+      // P in fp16 pairs: word w holds logits 2w and 2w+1 (s0[0..15] then s1[0..15])
+      uint32_t pw[16];
       float la = 0.0f, lb = 0.0f;
 #pragma unroll
       for (int kk = 0; kk < 8; ++kk) {
         ns0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, 0, kk), qf[kk], ns0, 0, 0, 0);
         ns1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kfrag(kb, 1, kk), qf[kk], ns1, 0, 0, 0);
-        // logits 4kk .. 4kk+3 of this lane: s0[0..15] then s1[0..15]
+        // logits 4kk .. 4kk+3 of this lane
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int idx = 4 * kk + u;
-          const float sv = idx < 16 ? cs0[idx] : cs1[idx - 16];
-          pb[idx >> 3][idx & 7] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(sv, c_log2, -mc));
+        for (int u = 0; u < 2; ++u) {
+          const int idx = 4 * kk + 2 * u;
+          const float a = idx < 16 ? cs0[idx] : cs1[idx - 16];
+          const float b = idx < 16 ? cs0[idx + 1] : cs1[idx - 15];
+          f16x2 h;
+          h[0] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(a, c_log2, -mc));
+          h[1] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(b, c_log2, -mc));
+          pw[2 * kk + u] = __builtin_bit_cast(uint32_t, h);
         }
         // row sums of the rounded probabilities (exact fp32 sums of fp16
         // values), so numerator and denominator weigh keys identically
-        const int t = kk >> 1, e = 4 * (kk & 1);
-        la = __builtin_amdgcn_fdot2(f16x2{pb[t][e], pb[t][e + 1]}, ones, la, false);
-        lb = __builtin_amdgcn_fdot2(f16x2{pb[t][e + 2], pb[t][e + 3]}, ones, lb, false);
+        la = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, pw[2 * kk]), ones, la, false);
+        lb = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, pw[2 * kk + 1]), ones, lb, false);
       }
+      f16x8 pb[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        pb[t] = __builtin_bit_cast(f16x8, make_uint4(pw[4 * t], pw[4 * t + 1], pw[4 * t + 2], pw[4 * t + 3]));
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
