@@ -37,15 +37,15 @@ def kernel_source_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload_name):
-    """HBM bytes per launch from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel source; else None."""
+def measured_traffic(workload_name, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    runs, if they were taken on the current kernel source; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    entry = rec.get(workload_name)
+    entry = rec.get("%s/%s" % (workload_name, kernel))
     if not entry or entry.get("kernel_sha") != kernel_source_hash():
         return None
     return entry.get("bytes_per_launch")
@@ -102,9 +102,10 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="p720", help="tiny | low | p480 | p720 | share")
-    ap.add_argument("--path", default="fused", choices=["fused", "ws"],
-                    help="fused: sol_attn_fwd (K rotated in every tile load); ws: sol_attn_fwd_ws "
-                         "(K rotated and V converted once into a workspace, then tile copies)")
+    ap.add_argument("--path", default="prepared", choices=["fused", "prepared"],
+                    help="prepared: sol_prepare_kv (K rotated, V to fp16, one pass) then "
+                         "sol_attn_fwd_prepared (q rotated in its tile load); fused: sol_attn_fwd "
+                         "(q and k rotated in every tile load)")
     ap.add_argument("--cpu-rows-per-thread", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -140,40 +141,60 @@ def main():
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=dev)
     torch.cuda.synchronize()
 
-    if args.path == "ws":
-        ws = sol.attn_workspace(qd)
+    ws = sol.attn_workspace(qd)
+    n_el = qd.numel()
+    k_rot = ws[: 2 * n_el].view(torch.bfloat16).view(qd.shape)
+    v_f16 = ws[2 * n_el: 4 * n_el].view(torch.float16).view(qd.shape)
 
-        def step():
-            sol.attn_fwd_ws(qd, kd, vd, w.T, w.Hl, w.Wl, tab, workspace=ws, out=out)
-    else:
-        def step():
-            sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+    def launches(path):
+        """The launches of one step, in order: [(name, fn)]."""
+        if path == "prepared":
+            return [("prepare_kv", lambda: sol.prepare_kv(kd, vd, w.T, w.Hl, w.Wl, tab, k_rot, v_f16)),
+                    ("attn_fwd_prepared", lambda: sol.attn_fwd_prepared(qd, k_rot, v_f16, w.T, w.Hl, w.Wl,
+                                                                        tab, out=out))]
+        return [("attn_fwd", lambda: sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out))]
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log("warmup done")
+    def timed(path, steps, warmup):
+        """HIP events around every launch on the launch stream: per-step ms and
+        per-launch ms lists."""
+        ls = launches(path)
+        for _ in range(warmup):
+            for _, fn in ls:
+                fn()
+        stream = torch.cuda.current_stream()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps * len(ls) + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        e = 1
+        for _ in range(steps):
+            for _, fn in ls:
+                fn()
+                ev[e].record(stream)
+                e += 1
+        torch.cuda.synchronize()
+        per = {name: [] for name, _ in ls}
+        for i in range(steps):
+            for j, (name, _) in enumerate(ls):
+                a = i * len(ls) + j
+                per[name].append(ev[a].elapsed_time(ev[a + 1]))
+        total = ev[0].elapsed_time(ev[-1])
+        return total / steps, per
 
-    stream = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        step()
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
-    total_ms = ev[0].elapsed_time(ev[-1])
-    ms_step = total_ms / args.steps
-    ms_launch = sum(per) / len(per)
-    per_sorted = sorted(per)
-    ms_median = per_sorted[len(per) // 2]
+    ms_step, per = timed(args.path, args.steps, args.warmup)
+    main_kernel = "attn_fwd" if args.path == "fused" else "attn_fwd_prepared"
+    kern = per[main_kernel]
+    ms_launch = sum(kern) / len(kern)
+    ks = sorted(kern)
+    ms_median = ks[len(ks) // 2]
     tflops = w.flops / (ms_step * 1e-3) / 1e12
     achieved = w.flops / (ms_launch * 1e-3) / 1e12
-    log("timed %d steps: %.3f ms/step (median launch %.3f ms, min %.3f, max %.3f) -> %.1f TFLOP/s"
-        % (args.steps, ms_step, ms_median, per_sorted[0], per_sorted[-1], tflops))
+    log("timed %d steps (%s): %.3f ms/step, %s %.3f ms avg (median %.3f) -> %.1f TFLOP/s"
+        % (args.steps, args.path, ms_step, main_kernel, ms_launch, ms_median, tflops))
+    other = "fused" if args.path == "prepared" else "prepared"
+    ms_other, per_other = timed(other, min(3, args.steps), 1)
+    log("other path (%s): %.3f ms/step" % (other, ms_other))
 
-    traffic = measured_traffic(w.name)
+    traffic = measured_traffic(w.name, main_kernel)
     result = {
         "metric": METRIC,
         "value": tflops,
@@ -190,14 +211,19 @@ def main():
         "config": {
             "workload": "%s: %s" % (w.name, w.describe()),
             "B": w.B, "H": w.H, "N": w.N, "D": w.D, "grid": [w.T, w.Hl, w.Wl], "n_text": w.n_text,
-            "rope": ("3d (32/48/48, base 1e4) fused into the q/k tile loads" if args.path == "fused"
+            "rope": ("3d (32/48/48, base 1e4) fused into the q and k tile loads" if args.path == "fused"
                      else "3d (32/48/48, base 1e4): q in the tile load, k in a one-pass prologue"),
-            "path": "sol_attn_fwd" if args.path == "fused" else "sol_attn_fwd_ws",
+            "path": ("sol_attn_fwd" if args.path == "fused"
+                     else "sol_prepare_kv + sol_attn_fwd_prepared"),
         },
         "ms_per_layer": ms_step,
-        "ms_per_layer_median": ms_median,
+        "kernel_ms_median": ms_median,
         "pct_peak_bf16": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "kernel_ms": {name: sum(v) / len(v) for name, v in per.items()},
+        "other_path": {"path": other, "ms_per_step": ms_other,
+                       "tflops": w.flops / (ms_other * 1e-3) / 1e12},
         "roofline": {
+            "kernel": main_kernel,
             "bound": "mfma",
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,

@@ -102,20 +102,40 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
                  int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
 
 /*
- * Bytes of device workspace sol_attn_fwd_ws needs: room for the rotated K
- * (bf16) and V converted to fp16, 2 * B*H*N*D * 2 bytes.  0 for invalid sizes.
+ * The attention in two stages, for callers that keep prepared K/V (the
+ * paper's reference-KV cache, Sec. 5, reuses one key/value set across
+ * denoising steps) or that time the stages apart.
+ *
+ * sol_prepare_kv: one HBM pass, k_rot = bf16(R(pos) k) (the same rounding as
+ * the rotation fused into sol_attn_fwd) and v_f16 = fp16(v) (exact for
+ * |v| < 65504).  k_rot, v_f16: [B][H][N][D] 16-bit, 16-byte aligned, not
+ * overlapping each other, k or v.  rope_tab_dev as in sol_attn_fwd.
+ *
+ * sol_attn_fwd_prepared: the attention kernel on prepared K/V; q is rotated
+ * in its tile load.  out must not overlap q, k_rot or v_f16.
+ *
+ * sol_prepare_kv followed by sol_attn_fwd_prepared returns exactly the bytes
+ * of sol_attn_fwd on the same inputs.
+ */
+int sol_prepare_kv(const void* k, const void* v, void* k_rot, void* v_f16, int B, int H, int N,
+                   int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
+int sol_attn_fwd_prepared(const void* q, const void* k_rot, const void* v_f16, void* out, int B,
+                          int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                          sol_stream_t stream);
+
+/*
+ * Bytes of device workspace sol_attn_fwd_ws needs: room for k_rot then
+ * v_f16, 2 * B*H*N*D * 2 bytes.  0 for invalid sizes.
  */
 size_t sol_attn_workspace_bytes(int B, int H, int N, int D);
 
 /*
- * Same result as sol_attn_fwd, bit for bit, computed in two launches on
- * `stream`: one HBM pass writes k^ = bf16(R(pos) k) and fp16(v) into the
- * caller's workspace (the rotation of K done once per token instead of once
- * per query tile), then the attention kernel rotates q in its tile load and
- * streams the prepared K and V tiles unchanged.  workspace: device memory of
- * at least sol_attn_workspace_bytes(B, H, N, D) bytes, 16-byte aligned, not
+ * sol_prepare_kv into the caller's workspace, then sol_attn_fwd_prepared:
+ * the rotation of K done once per token instead of once per query tile.
+ * Same result as sol_attn_fwd, bit for bit.  workspace: device memory of at
+ * least sol_attn_workspace_bytes(B, H, N, D) bytes, 16-byte aligned, not
  * overlapping q, k, v or out; its contents on entry are ignored and on exit
- * hold the prepared K and V.  Other arguments and errors as sol_attn_fwd.
+ * hold k_rot then v_f16.  Other arguments and errors as sol_attn_fwd.
  */
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
                     int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,

@@ -141,18 +141,59 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int D) {
   return 2 * (size_t)B * H * N * D * 2;
 }
 
+int sol_prepare_kv(const void* k, const void* v, void* k_rot, void* v_f16, int B, int H, int N,
+                   int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
+  if (!k || !v || !k_rot || !v_f16) return fail(SOL_ERR_INVALID_ARG, "k, v, k_rot, v_f16 must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_rot) || !aligned16(v_f16))
+    return fail(SOL_ERR_INVALID_ARG, "k, v, k_rot, v_f16 must be 16-byte aligned");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(k_rot, bytes, k, bytes) || overlaps(k_rot, bytes, v, bytes) ||
+      overlaps(v_f16, bytes, k, bytes) || overlaps(v_f16, bytes, v, bytes) ||
+      overlaps(k_rot, bytes, v_f16, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "k_rot / v_f16 overlap each other or k, v");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  hipError_t e = sol::launch_prepare_kv(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                                        static_cast<uint16_t*>(k_rot), static_cast<uint16_t*>(v_f16), B * H,
+                                        g, tab, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "prepare_kv launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int sol_attn_fwd_prepared(const void* q, const void* k_rot, const void* v_f16, void* out, int B,
+                          int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                          sol_stream_t stream) {
+  if (!q || !k_rot || !v_f16 || !out) return fail(SOL_ERR_INVALID_ARG, "q, k_rot, v_f16, out must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  if (!aligned16(q) || !aligned16(k_rot) || !aligned16(v_f16) || !aligned16(out))
+    return fail(SOL_ERR_INVALID_ARG, "q, k_rot, v_f16, out must be 16-byte aligned");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k_rot, bytes) || overlaps(out, bytes, v_f16, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_rot or v_f16");
+  if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_rot),
+                                               static_cast<const uint16_t*>(v_f16), static_cast<uint16_t*>(out),
+                                               B * H, g, tab, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_prepared launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
                     int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,
                     size_t workspace_bytes, sol_stream_t stream) {
   if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
-    return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must be 16-byte aligned");
-  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   const size_t bytes = (size_t)B * H * N * D * 2;
-  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k, bytes) || overlaps(out, bytes, v, bytes))
-    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k or v");
   const size_t need = sol_attn_workspace_bytes(B, H, N, D);
   if (!workspace) return fail(SOL_ERR_INVALID_ARG, "workspace is NULL");
   if (!aligned16(workspace)) return fail(SOL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
@@ -161,17 +202,13 @@ int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int 
   if (overlaps(workspace, need, q, bytes) || overlaps(workspace, need, k, bytes) ||
       overlaps(workspace, need, v, bytes) || overlaps(workspace, need, out, bytes))
     return fail(SOL_ERR_INVALID_ARG, "workspace overlaps q, k, v or out");
-  if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
-  const int64_t nv = (int64_t)T * Hl * Wl;
-  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
-  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k, bytes) || overlaps(out, bytes, v, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k or v");
   uint16_t* k_rot = static_cast<uint16_t*>(workspace);
   uint16_t* v_f16 = k_rot + (size_t)B * H * N * D;
-  hipError_t e = sol::launch_attn_fwd_pre(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                                          static_cast<const uint16_t*>(v), static_cast<uint16_t*>(out),
-                                          k_rot, v_f16, B * H, g, tab, reinterpret_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_ws launch: %s", hipGetErrorString(e));
-  return ok();
+  st = sol_prepare_kv(k, v, k_rot, v_f16, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
+  if (st != SOL_OK) return st;
+  return sol_attn_fwd_prepared(q, k_rot, v_f16, out, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
 }
 
 const char* sol_status_string(int status) {

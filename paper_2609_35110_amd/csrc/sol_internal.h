@@ -31,11 +31,15 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
                            uint16_t* out, int BH, const SeqGrid& g, const float2* tab,
                            hipStream_t stream);
 
-// Workspace path: k_rot / v_f16 (each BH * N * D 16-bit elements) receive the
-// rotated K and the fp16 V in one pass, then the attention kernel copies tiles.
-hipError_t launch_attn_fwd_pre(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                               uint16_t* out, uint16_t* k_rot, uint16_t* v_f16, int BH,
-                               const SeqGrid& g, const float2* tab, hipStream_t stream);
+// Prepared path: k_rot / v_f16 (each BH * N * D 16-bit elements) receive the
+// rotated K and the fp16 V in one pass; the attention kernel then rotates only
+// q and copies prepared tiles.
+hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_rot,
+                             uint16_t* v_f16, int BH, const SeqGrid& g, const float2* tab,
+                             hipStream_t stream);
+hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_rot,
+                                    const uint16_t* v_f16, uint16_t* out, int BH,
+                                    const SeqGrid& g, const float2* tab, hipStream_t stream);
 
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
 int64_t attn_max_workgroups(int N, int BH);

@@ -490,9 +490,9 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   return hipGetLastError();
 }
 
-hipError_t launch_attn_fwd_pre(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                               uint16_t* out, uint16_t* k_rot, uint16_t* v_f16, int BH,
-                               const SeqGrid& g, const float2* tab, hipStream_t stream) {
+hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_rot,
+                             uint16_t* v_f16, int BH, const SeqGrid& g, const float2* tab,
+                             hipStream_t stream) {
   const int64_t per_slab = (int64_t)g.n * kChunks;
   const dim3 pgrid((unsigned)((per_slab + 255) / 256), (unsigned)(BH < 65535 ? BH : 65535));
   if (tab != nullptr)
@@ -505,8 +505,12 @@ hipError_t launch_attn_fwd_pre(const uint16_t* q, const uint16_t* k, const uint1
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
                        reinterpret_cast<uint4*>(k_rot), reinterpret_cast<uint4*>(v_f16),
                        (int64_t)BH, g, tab);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_rot,
+                                    const uint16_t* v_f16, uint16_t* out, int BH,
+                                    const SeqGrid& g, const float2* tab, hipStream_t stream) {
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));

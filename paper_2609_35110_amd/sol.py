@@ -47,6 +47,10 @@ def lib():
         L.sol_rope3d.restype = i32
         L.sol_attn_fwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_attn_fwd.restype = i32
+        L.sol_prepare_kv.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
+        L.sol_prepare_kv.restype = i32
+        L.sol_attn_fwd_prepared.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
+        L.sol_attn_fwd_prepared.restype = i32
         L.sol_attn_workspace_bytes.argtypes = [i32, i32, i32, i32]
         L.sol_attn_workspace_bytes.restype = sz
         L.sol_attn_fwd_ws.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, sz, P]
@@ -77,6 +81,14 @@ def sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream):
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
     return lib().sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_prepare_kv(k, v, k_rot, v_f16, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_prepare_kv(k, v, k_rot, v_f16, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_attn_fwd_prepared(q, k_rot, v_f16, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_attn_fwd_prepared(q, k_rot, v_f16, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
 
 
 def sol_attn_workspace_bytes(B, H, N, D):
@@ -198,4 +210,41 @@ def attn_fwd_ws(q, k, v, T, Hl, Wl, table=None, workspace=None, out=None):
                           ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N,
                           D, T, Hl, Wl, _table_ptr(table, q.device),
                           ctypes.c_void_p(workspace.data_ptr()), nbytes, _stream(q)))
+    return out
+
+
+def _check_16bit(name, t, shape):
+    if not isinstance(t, torch.Tensor) or t.dtype not in (torch.bfloat16, torch.float16):
+        raise TypeError("%s must be a bfloat16 or float16 tensor" % name)
+    if not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must be a contiguous device tensor of shape %s" % (name, tuple(shape)))
+
+
+def prepare_kv(k, v, T, Hl, Wl, table=None, k_rot=None, v_f16=None):
+    """(k_rot bf16, v_f16 float16): K rotated and V converted, one pass."""
+    _check_tensor("k", k)
+    _check_tensor("v", v, k.shape)
+    B, H, N, D = k.shape
+    k_rot = torch.empty_like(k) if k_rot is None else k_rot
+    v_f16 = torch.empty(k.shape, dtype=torch.float16, device=k.device) if v_f16 is None else v_f16
+    _check_16bit("k_rot", k_rot, k.shape)
+    _check_16bit("v_f16", v_f16, k.shape)
+    check(sol_prepare_kv(ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
+                         ctypes.c_void_p(k_rot.data_ptr()), ctypes.c_void_p(v_f16.data_ptr()),
+                         B, H, N, D, T, Hl, Wl, _table_ptr(table, k.device), _stream(k)))
+    return k_rot, v_f16
+
+
+def attn_fwd_prepared(q, k_rot, v_f16, T, Hl, Wl, table=None, out=None):
+    """Attention on prepare_kv's outputs; q rotated in the tile load."""
+    _check_tensor("q", q)
+    _check_16bit("k_rot", k_rot, q.shape)
+    _check_16bit("v_f16", v_f16, q.shape)
+    B, H, N, D = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensor("out", out, q.shape)
+    check(sol_attn_fwd_prepared(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_rot.data_ptr()),
+                                ctypes.c_void_p(v_f16.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                B, H, N, D, T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
     return out

@@ -102,6 +102,38 @@ def test_attn_fwd_ws_rejects_before_any_hip_call(L, kw, status, fragment):
     assert fragment in sol.sol_last_error()
 
 
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(k=None), -1, "NULL"),
+    (dict(k_rot=P(0x100008)), -1, "aligned"),
+    (dict(k_rot=Bp), -1, "overlap"),
+    (dict(v_f16=P(0x300000 + 4096)), -1, "overlap"),
+    (dict(D=32), -2, "head dim"),
+])
+def test_prepare_kv_rejects_before_any_hip_call(L, kw, status, fragment):
+    args = dict(k=A, v=Bp, k_rot=C, v_f16=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
+    args.update(kw)
+    st = sol.sol_prepare_kv(args["k"], args["v"], args["k_rot"], args["v_f16"], args["B"], args["H"],
+                            args["N"], args["D"], args["T"], args["Hl"], args["Wl"], args["tab"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(q=None), -1, "NULL"),
+    (dict(out=C), -1, "overlaps"),
+    (dict(v_f16=P(0x300008)), -1, "aligned"),
+    (dict(N=100, T=9), -1, "more tokens"),
+])
+def test_attn_fwd_prepared_rejects_before_any_hip_call(L, kw, status, fragment):
+    args = dict(q=A, k_rot=Bp, v_f16=C, out=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
+    args.update(kw)
+    st = sol.sol_attn_fwd_prepared(args["q"], args["k_rot"], args["v_f16"], args["out"], args["B"],
+                                   args["H"], args["N"], args["D"], args["T"], args["Hl"], args["Wl"],
+                                   args["tab"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(x=None), -1),
     (dict(D=96), -2),

@@ -191,6 +191,24 @@ def test_workspace_path_is_bitwise_the_fused_path(shape):
     assert torch.equal(ws[2 * n: 4 * n].view(torch.float16).view(q.shape), v.to(torch.float16))
 
 
+@pytest.mark.parametrize("shape", [(1, 3, 3, 11, 13, 37), (1, 2, 0, 0, 0, 300)])
+def test_prepared_path_is_bitwise_the_fused_path(shape):
+    """sol_prepare_kv then sol_attn_fwd_prepared == sol_attn_fwd, and the
+    prepared K equals sol_rope3d's output, V the exact fp16 conversion."""
+    B, H, T, Hl, Wl, nt = shape
+    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=560 + sum(shape))
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(T, Hl, Wl, device=DEV) if w.n_video else None
+    k_rot, v_f16 = sol.prepare_kv(k, v, T, Hl, Wl, tab)
+    pre = sol.attn_fwd_prepared(q, k_rot, v_f16, T, Hl, Wl, tab)
+    fused = sol.attn_fwd(q, k, v, T, Hl, Wl, tab)
+    want_k = sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k
+    torch.cuda.synchronize()
+    assert torch.equal(pre, fused)
+    assert torch.equal(k_rot, want_k)
+    assert torch.equal(v_f16, v.to(torch.float16))
+
+
 @pytest.mark.parametrize("name", ["p480", "share"])
 def test_workspace_path_full_size_matches_fused(name):
     w = W.WORKLOADS[name]
