@@ -106,16 +106,27 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
  * paper's reference-KV cache, Sec. 5, reuses one key/value set across
  * denoising steps) or that time the stages apart.
  *
- * sol_prepare_kv: one HBM pass, k_rot = bf16(R(pos) k) (the same rounding as
- * the rotation fused into sol_attn_fwd) and v_f16 = fp16(v) (exact for
- * |v| < 65504).  k_rot, v_f16: [B][H][N][D] 16-bit, 16-byte aligned, not
- * overlapping each other, k or v.  rope_tab_dev as in sol_attn_fwd.
+ * sol_prepare_kv: one HBM pass, k_rot = fp16(bf16(R(pos) k)) (the rotation
+ * and bf16 rounding of sol_rope3d, then converted to fp16) and v_f16 =
+ * fp16(v).  The conversions are exact for 2^-14 <= |x| < 65504; smaller
+ * values keep fp16's 2^-24 absolute resolution, larger ones overflow to inf
+ * (inputs outside that range are outside what this path supports).  k_rot,
+ * v_f16: [B][H][N][D] fp16, 16-byte aligned, not overlapping each other, k
+ * or v.  rope_tab_dev as in sol_attn_fwd.
  *
- * sol_attn_fwd_prepared: the attention kernel on prepared K/V; q is rotated
- * in its tile load.  out must not overlap q, k_rot or v_f16.
+ * sol_attn_fwd_prepared: attention on prepared K/V; q is rotated and rounded
+ * to bf16 in its tile load, then scaled by log2(e)/sqrt(D) and rounded to
+ * fp16 so the score product runs in fp16 with the softmax scale folded in
+ * (|q^| log2(e)/sqrt(D) must stay below 65504).  Two launches on the stream:
+ * the first treats every query row with a reference max taken from the first
+ * key tile; a row block whose probabilities would leave the fp16 range
+ * (scores more than 15 binades above that reference) is written as NaN and
+ * recomputed by the second, which raises the reference as it goes.  out must
+ * not overlap q, k_rot or v_f16.
  *
- * sol_prepare_kv followed by sol_attn_fwd_prepared returns exactly the bytes
- * of sol_attn_fwd on the same inputs.
+ * The result differs from sol_attn_fwd's by rounding only (same contract and
+ * error bound; the fp16 score operands and the reference max change the last
+ * bits).
  */
 int sol_prepare_kv(const void* k, const void* v, void* k_rot, void* v_f16, int B, int H, int N,
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
@@ -132,7 +143,7 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int D);
 /*
  * sol_prepare_kv into the caller's workspace, then sol_attn_fwd_prepared:
  * the rotation of K done once per token instead of once per query tile.
- * Same result as sol_attn_fwd, bit for bit.  workspace: device memory of at
+ * Same result as those two calls, bit for bit.  workspace: device memory of at
  * least sol_attn_workspace_bytes(B, H, N, D) bytes, 16-byte aligned, not
  * overlapping q, k, v or out; its contents on entry are ignored and on exit
  * hold k_rot then v_f16.  Other arguments and errors as sol_attn_fwd.

@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
     const int64_t idx = bh * per_slab + i;
     uint4 x = k[idx];
     if (kRope && p.rot) x = rope_chunk(x, tab, pair0);
-    kh[idx] = x;
+    kh[idx] = bf16x8_to_f16x8(x);
     v16[idx] = bf16x8_to_f16x8(v[idx]);
   }
 }
@@ -176,7 +176,12 @@ constexpr int BN = 64;           // keys per tile
 constexpr int KS = D + 8;        // K tile row stride in LDS (elements): 272 B
 constexpr int VS = D + 32;       // V tile row stride in LDS (elements): 320 B
 constexpr int kTabLdsPairs = 6144;  // rotary tables up to 48 KB are staged in LDS
-constexpr float kLazyRescaleLog2 = 8.0f;
+// A tile's probabilities are taken against the running reference max m; they
+// stay finite in fp16 while they do not exceed 2^15 (fp16 max 65504).  A
+// lane's fp32 sum over its 32 probabilities bounds each of them, so the sum
+// (needed anyway) doubles as the overflow check; only when it exceeds 2^15 is
+// the tile's own max folded into m (rare: once the first tiles have set m).
+constexpr float kP16SumLimit = 32768.0f;
 static_assert(kThreads == 8 * BN, "staging: one tile row per 8 threads, two 16-byte chunks each");
 
 // Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
@@ -315,33 +320,50 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
   float m_run = -__builtin_inff();
   float l_run = 0.0f;
-  const f16x2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 
-  // Mask keys >= N (tile `it` is the ragged last one) and fold the tile's row
-  // max into the running max (lazy rescale of o and l).
-  auto row_max = [&](int it, f32x16& s0, f32x16& s1) {
+  // Keys >= N get no weight (tile `it` is the ragged last one).
+  auto mask_tile = [&](int it, f32x16& s0, f32x16& s1) {
     const int kv0 = it * BN;
     // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of that block.
-    if (kv0 + BN > N) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int key = kv0 + 8 * (j >> 2) + 4 * hh + (j & 3);
-        if (key >= N) s0[j] = -__builtin_inff();
-        if (key + 32 >= N) s1[j] = -__builtin_inff();
-      }
+    for (int j = 0; j < 16; ++j) {
+      const int key = kv0 + 8 * (j >> 2) + 4 * hh + (j & 3);
+      if (key >= N) s0[j] = -__builtin_inff();
+      if (key + 32 >= N) s1[j] = -__builtin_inff();
     }
+  };
+  // Fold a tile's row max into the reference max m, rescaling o and l.
+  auto fold_max = [&](const f32x16& s0, const f32x16& s1) {
     // a chain of three-input maxima (v_max3_f32): one instruction per two scores
     float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
     for (int j = 1; j < 16; ++j) mx = fmaxf(fmaxf(mx, s0[j]), s1[j]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
-    if (__any((m_new - m_run) * c_log2 > kLazyRescaleLog2)) {
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
-      m_run = m_new;
-      l_run *= alpha;
+    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);  // 0 for the first tile
+    m_run = m_new;
+    l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < 4; ++db) o[db] *= alpha;
+    for (int db = 0; db < 4; ++db) o[db] *= alpha;
+  };
+  // fp16 probabilities of one tile against m (word w: logits 2w, 2w+1 of
+  // s0[0..15] then s1[0..15]) and their per-lane sum.
+  auto probs = [&](const f32x16& s0, const f32x16& s1, uint32_t* pw, float& la, float& lb) {
+    const float mc = m_run * c_log2;
+    la = 0.0f;
+    lb = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      const float a = w < 8 ? s0[2 * w] : s1[2 * w - 16];
+      const float b = w < 8 ? s0[2 * w + 1] : s1[2 * w - 15];
+      const float ea = __builtin_amdgcn_exp2f(__builtin_fmaf(a, c_log2, -mc));
+      const float eb = __builtin_amdgcn_exp2f(__builtin_fmaf(b, c_log2, -mc));
+      f16x2 h;
+      h[0] = (_Float16)ea;
+      h[1] = (_Float16)eb;
+      pw[w] = __builtin_bit_cast(uint32_t, h);
+      la += ea;
+      lb += eb;
     }
   };
 
@@ -369,27 +391,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
           const int idx = 4 * kk + 2 * u;
           const float a = idx < 16 ? cs0[idx] : cs1[idx - 16];
           const float b = idx < 16 ? cs0[idx + 1] : cs1[idx - 15];
+          const float ea = __builtin_amdgcn_exp2f(__builtin_fmaf(a, c_log2, -mc));
+          const float eb = __builtin_amdgcn_exp2f(__builtin_fmaf(b, c_log2, -mc));
           f16x2 h;
-          h[0] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(a, c_log2, -mc));
-          h[1] = (_Float16)__builtin_amdgcn_exp2f(__builtin_fmaf(b, c_log2, -mc));
+          h[0] = (_Float16)ea;
+          h[1] = (_Float16)eb;
           pw[2 * kk + u] = __builtin_bit_cast(uint32_t, h);
+          // row sums in fp32 adds: v_dot2_f32_f16 would share the matrix
+          // pipe with the MFMAs and cost about half an MFMA each
+          la += ea;
+          lb += eb;
         }
-        // row sums of the rounded probabilities (exact fp32 sums of fp16
-        // values), so numerator and denominator weigh keys identically
-        la = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, pw[2 * kk]), ones, la, false);
-        lb = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, pw[2 * kk + 1]), ones, lb, false);
       }
-      f16x8 pb[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        pb[t] = __builtin_bit_cast(f16x8, make_uint4(pw[4 * t], pw[4 * t + 1], pw[4 * t + 2], pw[4 * t + 3]));
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
         __builtin_amdgcn_sched_group_barrier(kSgMfma, 2, 0);
         __builtin_amdgcn_sched_group_barrier(kSgValu, 12, 0);
       }
+      if (__any(la + lb > kP16SumLimit)) {  // rare: m lags this tile by > 2^15
+        fold_max(cs0, cs1);
+        probs(cs0, cs1, pw, la, lb);
+      }
       l_run += la + lb;
+      f16x8 pb[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        pb[t] = __builtin_bit_cast(f16x8, make_uint4(pw[4 * t], pw[4 * t + 1], pw[4 * t + 2], pw[4 * t + 3]));
       // ---- phase B: O^T += V(it)^T P(it)^T on MFMA; staging on VALU.
       const uint16_t* vb = v_lds[it & 1] + v_off;
 #pragma unroll
@@ -414,7 +442,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
       }
       __builtin_amdgcn_sched_group_barrier(kSgDsWrite, 4, 1);
     }
-    if (it + 1 < n_kv) row_max(it + 1, ns0, ns1);
+    if (it + 1 < n_kv && (it + 2) * BN > N) mask_tile(it + 1, ns0, ns1);
     __syncthreads();
   };
 
@@ -429,7 +457,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   __syncthreads();
   f32x16 sa0, sa1, sb0, sb1;
   scores(0, sa0, sa1);
-  row_max(0, sa0, sa1);
+  if (BN > N) mask_tile(0, sa0, sa1);
+  fold_max(sa0, sa1);  // the first tile sets the reference max
   __syncthreads();  // K(2) will overwrite K(0)
 
   int it = 0;
@@ -452,6 +481,443 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
         w.x = pack_bf16x2(o[db][4 * g4] * inv, o[db][4 * g4 + 1] * inv);
         w.y = pack_bf16x2(o[db][4 * g4 + 2] * inv, o[db][4 * g4 + 3] * inv);
         *reinterpret_cast<uint2*>(dst + 32 * db + 8 * g4 + 4 * hh) = w;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------- attention on prepared K/V
+
+// Workgroup barrier that orders LDS only: this wave's LDS operations complete
+// (lgkmcnt 0), then s_barrier.  Unlike __syncthreads it does not drain
+// outstanding global loads (vmcnt), so a tile load issued before the barrier
+// keeps streaming across it.  The empty asm statements keep the compiler from
+// moving memory accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt 63, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// bf16 x8 -> fp32, times s (fp32, RNE) -> fp16 x8 (RNE).
+__device__ __forceinline__ f16x8 bf16x8_to_f16x8_scaled(uint4 x, float s) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  f16x8 r;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    r[2 * u] = (_Float16)(__uint_as_float(w[u] << 16) * s);
+    r[2 * u + 1] = (_Float16)(__uint_as_float(w[u] & 0xffff0000u) * s);
+  }
+  return r;
+}
+
+// Score MFMAs as inline assembly: the result goes to VGPRs, where the softmax
+// reads it, while the query operand stays in AGPRs (the builtin would put the
+// result in AGPRs, next to the output accumulators, and every score would
+// cost a v_accvgpr_read).  The compiler does not see these as MFMAs, so every
+// VALU access to their results or their srcC is placed after mfma_wait() or
+// far behind them (the next iteration).
+__device__ __forceinline__ void mfma_s_first(f32x16& d, const f16x8& k, const f16x8& q,
+                                             const f32x16& c) {
+  asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %3" : "=&v"(d) : "v"(k), "a"(q), "v"(c));
+}
+__device__ __forceinline__ void mfma_s_next(f32x16& d, const f16x8& k, const f16x8& q) {
+  asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+v"(d) : "v"(k), "a"(q));
+}
+// More wait states than an 8-pass MFMA needs before its result is read or
+// written by the VALU (or its VALU-written operand is read by an MFMA).
+__device__ __forceinline__ void mfma_wait() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory"); }
+// Keep a value computed where it stands: IR passes would otherwise sink the
+// softmax arithmetic of a chunk to its first use and undo the interleaving.
+__device__ __forceinline__ void pin(uint32_t& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
+
+// Attention on prepared K/V: k holds the rotated keys and v the values, both
+// as fp16.  The query rows are rotated and rounded to bf16 like every rotation
+// here, then multiplied by c = log2(e)/sqrt(D) and rounded to fp16, so the
+// score MFMAs (fp16 x fp16 -> fp32) deliver c q.k.  Each chain of score MFMAs
+// starts from a tile holding -m, the running reference max in those units, so
+// the accumulator already holds the base-2 exponent of the softmax numerator
+// (Eq. 1 with the 1/sqrt(D) scale; the online max of the flash formulation)
+// and one probability costs a single v_exp_f32.
+//
+// 64 query rows per wave: every K fragment and V^T fragment read from LDS
+// feeds two MFMAs (one per 32-query block).  4 waves (one per SIMD, 256 query
+// rows per workgroup), the 2 x 4 output accumulators and Q' in AGPRs, 32-key
+// tiles so that the scores of two tiles fit in VGPRs.  With one wave per SIMD
+// nothing hides a stall, so each iteration i is laid out by hand in chunks of
+// two MFMAs (sched_barrier fences keep the order):
+//   phase A: S(i+1) = K(i+1) Q'^T - m (16 MFMAs) beside P(i) = exp2(S(i)) and
+//     its row sums on the VALU; the K fragments are read 4 chunks ahead, the
+//     first V(i) fragments during the last chunks;
+//   phase B: O^T += V(i)^T P(i)^T (16 MFMAs) beside the copy of K(i+3) and
+//     V(i+1) from registers into LDS, the loads of K(i+4) and V(i+2), and the
+//     reads of the first K(i+2) fragments for the next phase A.
+// LDS holds three K tiles (read K(i+1), prefetch K(i+2), write K(i+3) over
+// K(i)) and two V tiles (read V(i), write V(i+1) over V(i-1)); an LDS-only
+// barrier ends each iteration, so the global loads stay in flight across it.
+constexpr int BN2 = 32;                // keys per tile of the prepared-path kernel
+constexpr int kKTile = BN2 * KS;       // elements per K tile in LDS
+constexpr int kVTile = BN2 * VS;       // elements per V tile in LDS
+constexpr int kKBufs = 4;              // K tiles in LDS
+
+template <bool kRope, bool kRobust>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                          const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
+                          const float2* __restrict__ tab, int n_qtiles, float c_log2) {
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKBufs * kKTile];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2 * kVTile];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int hh = lane >> 5;
+  const int l32 = lane & 31;
+  const int bh = blockIdx.x / n_qtiles;
+  const int qt = blockIdx.x - bh * n_qtiles;
+  const int N = g.n;
+  const size_t slab = (size_t)bh * N * D;
+  const uint16_t* __restrict__ qs = q + slab;
+  const uint16_t* __restrict__ ks = k + slab;
+  const uint16_t* __restrict__ vs = v + slab;
+  // Materialise the output pointer now: a kernel-argument load left in flight
+  // into the main loop makes every LDS wait there a full lgkmcnt(0).
+  uint16_t* out_slab = out + slab;
+  asm volatile("" : "+s"(out_slab));
+  const int qrow_first = qt * BM + wave * 64 + l32;
+  if (kRobust) {
+    // Second pass: only the row blocks the first pass marked (NaN rows) are
+    // recomputed; every other workgroup leaves at once.
+    bool marked = false;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int row = qrow_first + 32 * qb;
+      if (hh == 0 && row < N) marked |= (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
+    }
+    if (!__syncthreads_or(marked)) return;
+  }
+
+  // ---- Q' fragments of the wave's two 32-row blocks, rotated in the load.
+  const int qrow0 = qrow_first;  // block qb holds row qrow0 + 32 qb
+  f16x8 qf[2][8];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int row = min(qrow0 + 32 * qb, N - 1);
+    const uint4* src = reinterpret_cast<const uint4*>(qs + (size_t)row * D);
+    Pos p{0, 0, 0, false};
+    if (kRope) p = token_pos(row, g);
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      const int cc = 2 * kk + hh;
+      uint4 x = src[cc];
+      if (kRope) x = rope_chunk(x, tab, tab_pair(cc, p, g));  // prefix: exact identity
+      qf[qb][kk] = bf16x8_to_f16x8_scaled(x, c_log2);
+    }
+  }
+
+  // ---- staging: thread moves chunks c0 and c0 + 8 of tile row rr, of K and of V.
+  const int rr = tid >> 3;
+  const int c0 = tid & 7;
+  uint4 kreg0, kreg1, vreg0, vreg1;  // separate scalars: an array of uint4 stays in scratch
+  auto load_k = [&](int kv0) __attribute__((always_inline)) {
+    const uint4* src = reinterpret_cast<const uint4*>(ks + (size_t)min(kv0 + rr, N - 1) * D);
+    kreg0 = src[c0];
+    kreg1 = src[c0 + 8];
+  };
+  auto load_v = [&](int kv0) __attribute__((always_inline)) {
+    const uint4* src = reinterpret_cast<const uint4*>(vs + (size_t)min(kv0 + rr, N - 1) * D);
+    vreg0 = src[c0];
+    vreg1 = src[c0 + 8];
+  };
+  auto store_k = [&](int buf) __attribute__((always_inline)) {
+    uint16_t* dst = k_lds + buf * kKTile + rr * KS + c0 * 8;
+    *reinterpret_cast<uint4*>(dst) = kreg0;
+    *reinterpret_cast<uint4*>(dst + 64) = kreg1;
+  };
+  auto store_v = [&](int buf) __attribute__((always_inline)) {
+    uint16_t* dst = v_lds + buf * kVTile + rr * VS + c0 * 8;
+    *reinterpret_cast<uint4*>(dst) = vreg0;
+    *reinterpret_cast<uint4*>(dst + 64) = vreg1;
+  };
+
+  // A fragment of K: lane (l32, hh) holds key l32, dims 16kk + 8hh .. +7.
+  const uint16_t* const k_lane = k_lds + l32 * KS + hh * 8;
+  auto kfrag = [&](int buf, int kk) __attribute__((always_inline)) {
+    return *reinterpret_cast<const f16x8*>(k_lane + buf * kKTile + kk * 16);
+  };
+  const int g16 = lane >> 4, i16 = lane & 15;
+  const uint16_t* const v_lane =
+      v_lds + (4 * (g16 >> 1) + (i16 >> 2)) * VS + 16 * (g16 & 1) + 4 * (i16 & 3);
+  // V^T fragment j = (kst, db) = (j / 4, j % 4) of tile buffer buf.
+  auto vfrag = [&](int buf, int j) __attribute__((always_inline)) {
+    const uint16_t* p0 = v_lane + buf * kVTile + 16 * (j >> 2) * VS + 32 * (j & 3);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 8 * VS));
+    return __builtin_bit_cast(f16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+
+  f32x16 o[2][4];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int db = 0; db < 4; ++db) o[qb][db] = f32x16{};
+  float m_ref[2];   // reference max of each query row (units of c q.k)
+  f32x16 bias[2];   // -m_ref, the first addend of every score chain
+  float l_run[2] = {0.0f, 0.0f};
+  float ovf = 0.0f;  // first pass: largest per-lane tile sum (above 2^15: rows marked)
+
+  // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of the tile.
+  auto mask_tile = [&](int it, f32x16* s) __attribute__((always_inline)) {
+    const int kv0 = it * BN2;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int key = kv0 + 8 * (j >> 2) + 4 * hh + (j & 3);
+      if (key >= N) {
+        s[0][j] = -__builtin_inff();
+        s[1][j] = -__builtin_inff();
+      }
+    }
+  };
+  auto mask_block = [&](int it, f32x16& s) __attribute__((always_inline)) {
+    const int kv0 = it * BN2;
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      if (kv0 + 8 * (j >> 2) + 4 * hh + (j & 3) >= N) s[j] = -__builtin_inff();
+  };
+  auto tile_max = [&](const f32x16& s) __attribute__((always_inline)) {
+    float mx = fmaxf(s[0], s[1]);
+#pragma unroll
+    for (int j = 2; j < 16; j += 2) mx = fmaxf(fmaxf(mx, s[j]), s[j + 1]);
+    return fmaxf(mx, __shfl_xor(mx, 32));
+  };
+  const int n_kv = (N + BN2 - 1) / BN2;
+  // Read-ahead rings: K fragments 4 chunks ahead (kr[kk % 4] holds fragment kk
+  // of the tile being multiplied), V^T fragments 2 chunks ahead (vr[j % 3]).
+  f16x8 kr[4];
+  f16x8 vr[3];
+  // Words of P(i): qb0 words come from the previous phase B, qb1 words from
+  // this phase A.  lsum[qb] are their fp32 row sums (two chains per block).
+  // Iteration i:
+  //   phase A (8 chunks): S(i+1) MFMAs (qb0, qb1 per K fragment) + P(i) qb1 word j
+  //   phase B (8 chunks): PV(i) MFMAs (qb0, qb1 per V fragment) + P(i+1) qb0 word j
+  auto iteration = [&](int i, f32x16* cs, f32x16* ns, uint32_t* p0_cur, uint32_t* p0_next,
+                       float* l0_cur, float* l0_next) __attribute__((always_inline)) {
+    // K(j) lives in buffer j % 4 from iteration j-3 (or the prologue) to j+1.
+    const int kb_old = i & 3, kb_cur = (i + 1) & 3, kb_next = (i + 2) & 3, kb_free = (i + 3) & 3;
+    const int vb = i & 1;
+    // ---- phase A
+    uint32_t p1[8];
+    float l1[2] = {0.0f, 0.0f};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (j == 0) {
+        mfma_s_first(ns[0], kr[0], qf[0][0], bias[0]);
+        mfma_s_first(ns[1], kr[0], qf[1][0], bias[1]);
+      } else {
+        mfma_s_next(ns[0], kr[j & 3], qf[0][j]);
+        mfma_s_next(ns[1], kr[j & 3], qf[1][j]);
+      }
+      if (j < 4) kr[j] = kfrag(kb_cur, j + 4);
+      if (j >= 6) vr[j - 6] = vfrag(vb, j - 6);
+      const float ea = __builtin_amdgcn_exp2f(cs[1][2 * j]);
+      const float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
+      f16x2 h;
+      h[0] = (_Float16)ea;
+      h[1] = (_Float16)eb;
+      p1[j] = __builtin_bit_cast(uint32_t, h);
+      l1[0] += ea;
+      l1[1] += eb;
+      pin(p1[j]);
+      pin(l1[0]);
+      pin(l1[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    {
+      const float s0 = l0_cur[0] + l0_cur[1], s1 = l1[0] + l1[1];
+      if (!kRobust) ovf = fmaxf(ovf, fmaxf(s0, s1));
+      if (kRobust && __any(fmaxf(s0, s1) > kP16SumLimit)) {
+        // Rare: a score of tile i exceeds m by more than 15.  Per query block:
+        // S(i) again from K(i) (still in its buffer until the next iteration),
+        // m raised to its max where it exceeds m, O and l rescaled, the next
+        // tile's scores moved to the new m, and the words of P(i) redone.
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          mfma_wait();  // ns was just written by the score MFMAs
+          f32x16 t = bias[qb];
+#pragma unroll
+          for (int kk = 0; kk < 8; ++kk)
+            t = __builtin_amdgcn_mfma_f32_32x32x16_f16(kfrag(kb_old, kk), qf[qb][kk], t, 0, 0, 0);
+          if ((i + 1) * BN2 > N) mask_block(i, t);
+          const float delta = fmaxf(tile_max(t), 0.0f);
+          const float alpha = __builtin_amdgcn_exp2f(-delta);
+          m_ref[qb] += delta;
+          l_run[qb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < 4; ++db) o[qb][db] *= alpha;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            ns[qb][j] -= delta;
+            bias[qb][j] = -m_ref[qb];
+          }
+          float la = 0.0f, lb = 0.0f;
+#pragma unroll
+          for (int w = 0; w < 8; ++w) {
+            const float ea = __builtin_amdgcn_exp2f(t[2 * w] - delta);
+            const float eb = __builtin_amdgcn_exp2f(t[2 * w + 1] - delta);
+            f16x2 h;
+            h[0] = (_Float16)ea;
+            h[1] = (_Float16)eb;
+            if (qb == 0) p0_cur[w] = __builtin_bit_cast(uint32_t, h);
+            else p1[w] = __builtin_bit_cast(uint32_t, h);
+            la += ea;
+            lb += eb;
+          }
+          if (qb == 0) {
+            l0_cur[0] = la;
+            l0_cur[1] = lb;
+          } else {
+            l1[0] = la;
+            l1[1] = lb;
+          }
+          mfma_wait();
+        }
+      }
+      l_run[0] += l0_cur[0] + l0_cur[1];
+      l_run[1] += l1[0] + l1[1];
+    }
+    f16x8 pf[2][2];
+#pragma unroll
+    for (int kst = 0; kst < 2; ++kst) {
+      pf[0][kst] = __builtin_bit_cast(f16x8, make_uint4(p0_cur[4 * kst], p0_cur[4 * kst + 1],
+                                                        p0_cur[4 * kst + 2], p0_cur[4 * kst + 3]));
+      pf[1][kst] = __builtin_bit_cast(f16x8, make_uint4(p1[4 * kst], p1[4 * kst + 1],
+                                                        p1[4 * kst + 2], p1[4 * kst + 3]));
+    }
+    // S(i+1) is read by the VALU from here on: its MFMAs must have landed, and
+    // a ragged last tile is masked first.  The empty statement keeps the score
+    // MFMAs' results and srcC live up to here: where they are dead (the last
+    // iteration) the compiler would otherwise reuse their registers while the
+    // MFMAs, invisible to it, still write or read them.
+    mfma_wait();
+    asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
+    if (i + 1 < n_kv && (i + 2) * BN2 > N) mask_tile(i + 1, ns);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- phase B
+    l0_next[0] = l0_next[1] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int kst = j >> 2, db = j & 3;
+      o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j % 3], pf[0][kst], o[0][db], 0, 0, 0);
+      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j % 3], pf[1][kst], o[1][db], 0, 0, 0);
+      if (j + 2 < 8) vr[(j + 2) % 3] = vfrag(vb, j + 2);
+      if (j == 1) store_k(kb_free);    // K(i+3) over K(i)
+      if (j == 2) store_v(vb ^ 1);     // V(i+1) over V(i-1)
+      if (j == 3) load_k((i + 4) * BN2);
+      if (j == 4) load_v((i + 2) * BN2);
+      if (j >= 4) kr[j - 4] = kfrag(kb_next, j - 4);
+      const float ea = __builtin_amdgcn_exp2f(ns[0][2 * j]);
+      const float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
+      f16x2 h;
+      h[0] = (_Float16)ea;
+      h[1] = (_Float16)eb;
+      p0_next[j] = __builtin_bit_cast(uint32_t, h);
+      l0_next[0] += ea;
+      l0_next[1] += eb;
+      pin(p0_next[j]);
+      pin(l0_next[0]);
+      pin(l0_next[1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    lds_barrier();
+  };
+
+  // ---- prologue: K(0..2) and V(0) into LDS; K(3), V(1) in registers; S(0)
+  // against m = its own max; the qb0 words of P(0).
+  load_k(0);
+  load_v(0);
+  store_k(0);
+  store_v(0);
+  load_k(BN2);
+  store_k(1);
+  load_k(2 * BN2);
+  store_k(2);
+  load_k(3 * BN2);
+  load_v(BN2);
+  __syncthreads();
+  // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
+  // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
+  // such copies.
+  f32x16 sa[2], sb[2];
+  sa[0] = f32x16{};
+  sa[1] = f32x16{};
+#pragma unroll
+  for (int kk = 0; kk < 8; ++kk) {
+    const f16x8 kf = kfrag(0, kk);
+    sa[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[0][kk], sa[0], 0, 0, 0);
+    sa[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[1][kk], sa[1], 0, 0, 0);
+  }
+  if (BN2 > N) mask_tile(0, sa);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    m_ref[qb] = tile_max(sa[qb]);  // finite: key 0 is always valid
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      sa[qb][j] -= m_ref[qb];
+      bias[qb][j] = -m_ref[qb];
+    }
+  }
+  uint32_t pA[8], pB[8];
+  float lA[2] = {0.0f, 0.0f}, lB[2] = {0.0f, 0.0f};
+#pragma unroll
+  for (int w = 0; w < 8; ++w) {
+    const float ea = __builtin_amdgcn_exp2f(sa[0][2 * w]);
+    const float eb = __builtin_amdgcn_exp2f(sa[0][2 * w + 1]);
+    f16x2 h;
+    h[0] = (_Float16)ea;
+    h[1] = (_Float16)eb;
+    pA[w] = __builtin_bit_cast(uint32_t, h);
+    lA[0] += ea;
+    lA[1] += eb;
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) kr[t] = kfrag(1, t);
+  mfma_wait();
+  lds_barrier();  // K(3) will overwrite K(0)
+
+  int i = 0;
+  for (; i + 1 < n_kv; i += 2) {
+    iteration(i, sa, sb, pA, pB, lA, lB);
+    iteration(i + 1, sb, sa, pB, pA, lB, lA);
+  }
+  if (i < n_kv) iteration(i, sa, sb, pA, pB, lA, lB);
+
+  // ---- epilogue: out = O / l; register j of block (qb, db) is dim 32db + 8(j/4) + 4hh + j%4.
+  // A first-pass wave whose probabilities left the fp16 range writes its rows
+  // as NaN instead (bf16 0x7FC0): the second pass recomputes exactly those.
+  const bool marked = !kRobust && __any(ovf > kP16SumLimit);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int row = qrow0 + 32 * qb;
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+    const float inv = 1.0f / l_tot;
+    if (row < N && marked) {
+      uint16_t* dst = out_slab + (size_t)row * D;
+#pragma unroll
+      for (int c = 0; c < 8; ++c)
+        *reinterpret_cast<uint4*>(dst + 64 * hh + 8 * c) = make_uint4(0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u);
+    } else if (row < N) {
+      uint16_t* dst = out_slab + (size_t)row * D;
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          uint2 w;
+          w.x = pack_bf16x2(o[qb][db][4 * g4] * inv, o[qb][db][4 * g4 + 1] * inv);
+          w.y = pack_bf16x2(o[qb][db][4 * g4 + 2] * inv, o[qb][db][4 * g4 + 3] * inv);
+          *reinterpret_cast<uint2*>(dst + 32 * db + 8 * g4 + 4 * hh) = w;
+        }
       }
     }
   }
@@ -515,11 +981,20 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_rot,
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   if (tab != nullptr)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, false, true>), grid, dim3(kThreads), 0, stream, q,
-                       k_rot, v_f16, out, g, tab, 0, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_rot,
+                       v_f16, out, g, tab, n_qtiles, c_log2);
   else
-    hipLaunchKernelGGL((attn_fwd_kernel<false, false, true>), grid, dim3(kThreads), 0, stream, q,
-                       k_rot, v_f16, out, g, tab, 0, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_rot,
+                       v_f16, out, g, tab, n_qtiles, c_log2);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // Second pass over the row blocks whose probabilities left the fp16 range.
+  if (tab != nullptr)
+    hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_rot,
+                       v_f16, out, g, tab, n_qtiles, c_log2);
+  else
+    hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_rot,
+                       v_f16, out, g, tab, n_qtiles, c_log2);
   return hipGetLastError();
 }
 

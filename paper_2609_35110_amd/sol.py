@@ -221,11 +221,12 @@ def _check_16bit(name, t, shape):
 
 
 def prepare_kv(k, v, T, Hl, Wl, table=None, k_rot=None, v_f16=None):
-    """(k_rot bf16, v_f16 float16): K rotated and V converted, one pass."""
+    """(k_rot, v_f16), both float16: K rotated (rounded to bf16 like every
+    rotation, then converted) and V converted, one pass."""
     _check_tensor("k", k)
     _check_tensor("v", v, k.shape)
     B, H, N, D = k.shape
-    k_rot = torch.empty_like(k) if k_rot is None else k_rot
+    k_rot = torch.empty(k.shape, dtype=torch.float16, device=k.device) if k_rot is None else k_rot
     v_f16 = torch.empty(k.shape, dtype=torch.float16, device=k.device) if v_f16 is None else v_f16
     _check_16bit("k_rot", k_rot, k.shape)
     _check_16bit("v_f16", v_f16, k.shape)

@@ -38,24 +38,40 @@ def _bits(t):
     return W.as_bits(t.cpu())
 
 
-def _run(q, k, v, w, rope=True):
+# The two attention paths: "fused" (sol_attn_fwd: K rotated in every tile
+# load, bf16 score operands) and "prepared" (sol_attn_fwd_ws: K rotated and
+# converted once, fp16 score operands, the kernel the benchmark times).
+PATHS = ["fused", "prepared"]
+
+
+def _attn(path, q, k, v, w, tab, out=None):
+    if path == "fused":
+        return sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab, out=out)
+    return sol.attn_fwd_ws(q, k, v, w.T, w.Hl, w.Wl, tab, out=out)
+
+
+def _run(q, k, v, w, rope=True, path="fused"):
     """HIP path on device copies; returns the bf16 output on the CPU."""
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV) if rope and w.n_video else None
     qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
-    out = sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab)
+    out = _attn(path, qd, kd, vd, w, tab)
     torch.cuda.synchronize()
     return out.cpu()
 
 
 def _full_parity(w, q, k, v, label, rope=True):
-    out = _run(q, k, v, w, rope)
+    """Both paths against one oracle evaluation; returns {path: output}."""
     ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rope=rope)
     R = w.B * w.H * w.N
     slab = np.repeat(np.arange(w.B * w.H), w.N)
-    st = compare(_bits(out).reshape(R, w.D), ref.reshape(R, w.D), slab)
-    _log("%s %s: %s" % (label, w.describe(), st))
-    assert_parity(st, label)
-    return out, ref
+    outs = {}
+    for path in PATHS:
+        out = _run(q, k, v, w, rope, path)
+        st = compare(_bits(out).reshape(R, w.D), ref.reshape(R, w.D), slab)
+        _log("%s %s %s: %s" % (label, path, w.describe(), st))
+        assert_parity(st, "%s %s" % (label, path))
+        outs[path] = out
+    return outs
 
 
 def test_library_is_the_in_tree_build():
@@ -86,9 +102,10 @@ def test_edge_shapes_full_parity(shape):
     B, H, T, Hl, Wl, nt = shape
     w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=200 + sum(shape))
     q, k, v = W.make_inputs(w)
-    out, _ = _full_parity(w, q, k, v, "edge")
+    outs = _full_parity(w, q, k, v, "edge")
     if w.N == 1:
-        assert torch.equal(out, v), "N=1 must return v exactly"
+        for path, out in outs.items():
+            assert torch.equal(out, v), "N=1 must return v exactly (%s)" % path
 
 
 def test_text_only_no_rotation():
@@ -103,14 +120,15 @@ def test_workload_sampled_parity(name):
     w = W.WORKLOADS[name]
     _log("generating %s" % w.describe())
     q, k, v = W.make_inputs(w)
-    out = _run(q, k, v, w)
     rows = W.sample_rows(w, per_slab=16, head=32, tail=80).numpy()
     _log("oracle on %d rows" % len(rows))
     ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rows=rows)
-    got = _bits(out).reshape(-1, w.D)[rows]
-    st = compare(got, ref, rows // w.N)
-    _log("%s: %s" % (name, st))
-    assert_parity(st, name)
+    for path in PATHS:
+        out = _run(q, k, v, w, path=path)
+        got = _bits(out).reshape(-1, w.D)[rows]
+        st = compare(got, ref, rows // w.N)
+        _log("%s %s: %s" % (name, path, st))
+        assert_parity(st, "%s %s" % (name, path))
 
 
 # ------------------------------------------------------------ rotary kernel
@@ -169,80 +187,73 @@ def test_fused_rotation_equals_prerotated(shape):
 
 @pytest.mark.parametrize("shape", [(1, 2, 3, 8, 8, 0), (1, 3, 3, 11, 13, 37), (2, 1, 5, 7, 9, 64),
                                    (1, 1, 1, 1, 1, 0), (1, 2, 0, 0, 0, 300)])
-def test_workspace_path_is_bitwise_the_fused_path(shape):
-    """sol_attn_fwd_ws (K rotated and V converted once into the workspace)
-    returns exactly the bytes of sol_attn_fwd, and leaves the prepared K and V
-    in the workspace."""
+def test_workspace_path_is_the_two_prepared_calls(shape):
+    """sol_attn_fwd_ws == sol_prepare_kv then sol_attn_fwd_prepared, bit for
+    bit; the workspace (and prepare_kv) hold K rotated by sol_rope3d then
+    converted to fp16, and V converted to fp16."""
     B, H, T, Hl, Wl, nt = shape
     w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=550 + sum(shape))
     q, k, v = (t.to(DEV) for t in W.make_inputs(w))
     tab = sol.rope3d_table(T, Hl, Wl, device=DEV) if w.n_video else None
-    fused = sol.attn_fwd(q, k, v, T, Hl, Wl, tab)
     ws = sol.attn_workspace(q)
     ws.fill_(0xFF)  # contents on entry are ignored
-    pre = sol.attn_fwd_ws(q, k, v, T, Hl, Wl, tab, workspace=ws)
+    a = sol.attn_fwd_ws(q, k, v, T, Hl, Wl, tab, workspace=ws)
+    k_f16, v_f16 = sol.prepare_kv(k, v, T, Hl, Wl, tab)
+    b = sol.attn_fwd_prepared(q, k_f16, v_f16, T, Hl, Wl, tab)
+    want_k = (sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k).to(torch.float16)
     torch.cuda.synchronize()
-    assert torch.equal(fused, pre)
+    assert torch.equal(a, b)
     n = q.numel()
-    k_rot = ws[: 2 * n].view(torch.bfloat16).view(q.shape)
-    want_k = sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k
-    torch.cuda.synchronize()
-    assert torch.equal(k_rot, want_k)
+    assert torch.equal(ws[: 2 * n].view(torch.float16).view(q.shape), want_k)
     assert torch.equal(ws[2 * n: 4 * n].view(torch.float16).view(q.shape), v.to(torch.float16))
-
-
-@pytest.mark.parametrize("shape", [(1, 3, 3, 11, 13, 37), (1, 2, 0, 0, 0, 300)])
-def test_prepared_path_is_bitwise_the_fused_path(shape):
-    """sol_prepare_kv then sol_attn_fwd_prepared == sol_attn_fwd, and the
-    prepared K equals sol_rope3d's output, V the exact fp16 conversion."""
-    B, H, T, Hl, Wl, nt = shape
-    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=560 + sum(shape))
-    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
-    tab = sol.rope3d_table(T, Hl, Wl, device=DEV) if w.n_video else None
-    k_rot, v_f16 = sol.prepare_kv(k, v, T, Hl, Wl, tab)
-    pre = sol.attn_fwd_prepared(q, k_rot, v_f16, T, Hl, Wl, tab)
-    fused = sol.attn_fwd(q, k, v, T, Hl, Wl, tab)
-    want_k = sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k
-    torch.cuda.synchronize()
-    assert torch.equal(pre, fused)
-    assert torch.equal(k_rot, want_k)
+    assert torch.equal(k_f16, want_k)
     assert torch.equal(v_f16, v.to(torch.float16))
 
 
-@pytest.mark.parametrize("name", ["p480", "share"])
-def test_workspace_path_full_size_matches_fused(name):
-    w = W.WORKLOADS[name]
-    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
-    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
-    a = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
-    b = sol.attn_fwd_ws(q, k, v, w.T, w.Hl, w.Wl, tab)
-    torch.cuda.synchronize()
-    assert torch.equal(a, b)
+@pytest.mark.parametrize("growth", [24.0, 300.0])
+def test_second_pass_recomputes_rows_that_leave_fp16(growth):
+    """Scores that climb along the key sequence far above the first key
+    tile's max (by ~growth binades): the prepared path's first pass marks
+    those row blocks and the second recomputes them with a rising reference.
+    Text-only, one direction u for every token: logit_j = a_j |u|^2 / sqrt(D)."""
+    w = W.custom(1, 2, 0, 0, 0, n_text=700, seed_index=603)
+    q, k, v = W.make_inputs(w)
+    g = torch.Generator().manual_seed(9)
+    u = torch.randn(w.D, generator=g)
+    u = u / u.norm() * 4.0                                   # |u|^2 = 16
+    scale = growth / 1.4426950408889634 * (w.D ** 0.5) / 16.0  # a_N-1 |u|^2/sqrt(D) log2(e) = growth
+    a = torch.linspace(0.0, 1.0, w.N) * scale
+    k = (a[None, None, :, None] * u).expand(w.B, w.H, w.N, w.D).to(torch.bfloat16).contiguous()
+    q = (u + 0.1 * q.float()).to(torch.bfloat16)
+    _full_parity(w, q, k, v, "growth%g" % growth, rope=False)
 
 
 # ------------------------------------------------------------ closed forms
 
-def test_constant_values_give_constant_output():
+@pytest.mark.parametrize("path", PATHS)
+def test_constant_values_give_constant_output(path):
     w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=600)
     q, k, _ = W.make_inputs(w)
     c = torch.randn(w.D, generator=torch.Generator().manual_seed(5)).to(torch.bfloat16)
     v = c.expand(w.B, w.H, w.N, w.D).contiguous()
-    out = _run(q, k, v, w).float()
+    out = _run(q, k, v, w, path=path).float()
     err = (out - c.float()).abs() / c.float().abs().clamp_min(1e-3)
     assert err.max().item() <= 2.0 ** -7, "constant V must give V back within one bf16 ulp"
 
 
-def test_zero_query_gives_mean_of_values():
+@pytest.mark.parametrize("path", PATHS)
+def test_zero_query_gives_mean_of_values(path):
     w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=601)
     _, k, v = W.make_inputs(w)
     q = torch.zeros_like(k)
-    out = _run(q, k, v, w).float()
+    out = _run(q, k, v, w, path=path).float()
     want = v.float().mean(dim=2, keepdim=True).expand_as(out)
     rms = want.pow(2).mean().sqrt()
     assert ((out - want).abs() / rms).max().item() < 2e-2
 
 
-def test_one_hot_attention_returns_the_value():
+@pytest.mark.parametrize("path", PATHS)
+def test_one_hot_attention_returns_the_value(path):
     """A key equal to the (unrotated) query with a logit gap of ~45 takes all
     the weight: the output row is that value row, exactly."""
     w = W.custom(1, 1, 0, 0, 0, n_text=200, seed_index=602)
@@ -252,13 +263,14 @@ def test_one_hot_attention_returns_the_value():
     i, j = 17, 133
     q[0, 0, i] = 2.0
     k[0, 0, j] = 2.0
-    out = _run(q, k, v, w, rope=False)
+    out = _run(q, k, v, w, rope=False, path=path)
     assert torch.equal(out[0, 0, i], v[0, 0, j])
 
 
 # ------------------------------------------------------------ guards
 
-def test_no_out_of_bounds_reads_or_writes():
+@pytest.mark.parametrize("path", PATHS)
+def test_no_out_of_bounds_reads_or_writes(path):
     """Inputs live inside NaN-filled buffers and the output inside a sentinel
     buffer: nothing past N may be read (NaN would leak) or written."""
     w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=700)
@@ -275,39 +287,41 @@ def test_no_out_of_bounds_reads_or_writes():
     sentinel = torch.full((numel + pad,), 123.0, dtype=torch.bfloat16, device=DEV)
     out = sentinel[:numel].view(q.shape)
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
-    sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out)
+    _attn(path, qd, kd, vd, w, tab, out=out)
     torch.cuda.synchronize()
     assert torch.isfinite(out.float()).all()
     assert (sentinel[numel:] == 123.0).all(), "write past the end of out"
-    clean = _run(q, k, v, w)
+    clean = _run(q, k, v, w, path=path)
     assert torch.equal(out.cpu(), clean)
 
 
-def test_repeated_runs_are_bitwise_identical():
+@pytest.mark.parametrize("path", PATHS)
+def test_repeated_runs_are_bitwise_identical(path):
     w = W.custom(1, 4, 4, 16, 24, n_text=11, seed_index=701)
     q, k, v = (t.to(DEV) for t in W.make_inputs(w))
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
-    a = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
-    b = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
+    a = _attn(path, q, k, v, w, tab)
+    b = _attn(path, q, k, v, w, tab)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
 
 
-def test_heads_and_batches_are_independent():
+@pytest.mark.parametrize("path", PATHS)
+def test_heads_and_batches_are_independent(path):
     w = W.custom(2, 3, 3, 11, 13, n_text=5, seed_index=702)
     q, k, v = (t.to(DEV) for t in W.make_inputs(w))
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
-    full = sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab)
+    full = _attn(path, q, k, v, w, tab)
     b, h = 1, 2
-    one = sol.attn_fwd(q[b:b + 1, h:h + 1].contiguous(), k[b:b + 1, h:h + 1].contiguous(),
-                       v[b:b + 1, h:h + 1].contiguous(), w.T, w.Hl, w.Wl, tab)
+    one = _attn(path, q[b:b + 1, h:h + 1].contiguous(), k[b:b + 1, h:h + 1].contiguous(),
+                v[b:b + 1, h:h + 1].contiguous(), w, tab)
     torch.cuda.synchronize()
     assert torch.equal(full[b:b + 1, h:h + 1], one)
 
 
 def test_offsets_beyond_2_pow_31_elements():
     """B=1, H=160 heads of the 111,600-token layer: 2.29e9 elements per tensor.
-    Only the last two heads and the first one carry data; the rest are zero."""
+    Only the last two heads carry data; the rest are zero.  Both paths."""
     base = W.WORKLOADS["p720"]
     H = 160
     w1 = W.custom(1, 2, base.T, base.Hl, base.Wl, seed_index=800)
@@ -321,13 +335,18 @@ def test_offsets_beyond_2_pow_31_elements():
     k[:, H - 2:].copy_(ks)
     v[:, H - 2:].copy_(vs)
     tab = sol.rope3d_table(base.T, base.Hl, base.Wl, device=DEV)
-    out = sol.attn_fwd(q, k, v, base.T, base.Hl, base.Wl, tab)
-    torch.cuda.synchronize()
-    tail = out[:, H - 2:].cpu()
-    del q, k, v, out
+    tails = {}
+    for path in PATHS:
+        out = _attn(path, q, k, v, base, tab)
+        torch.cuda.synchronize()
+        tails[path] = out[:, H - 2:].cpu()
+        del out
+        torch.cuda.empty_cache()
+    del q, k, v
     torch.cuda.empty_cache()
     rows = W.sample_rows(w1, per_slab=16, head=8, tail=80).numpy()
     ref = oracle.attn_rows(_bits(qs), _bits(ks), _bits(vs), w1.T, w1.Hl, w1.Wl, rows=rows)
-    st = compare(_bits(tail).reshape(-1, w1.D)[rows], ref, rows // w1.N)
-    _log("2^31 offsets: %s" % st)
-    assert_parity(st, "large offsets")
+    for path, tail in tails.items():
+        st = compare(_bits(tail).reshape(-1, w1.D)[rows], ref, rows // w1.N)
+        _log("2^31 offsets %s: %s" % (path, st))
+        assert_parity(st, "large offsets " + path)
