@@ -106,13 +106,19 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
  * paper's reference-KV cache, Sec. 5, reuses one key/value set across
  * denoising steps) or that time the stages apart.
  *
- * sol_prepare_kv: one HBM pass, k_rot = fp16(bf16(R(pos) k)) (the rotation
- * and bf16 rounding of sol_rope3d, then converted to fp16) and v_f16 =
- * fp16(v).  The conversions are exact for 2^-14 <= |x| < 65504; smaller
- * values keep fp16's 2^-24 absolute resolution, larger ones overflow to inf
- * (inputs outside that range are outside what this path supports).  k_rot,
- * v_f16: [B][H][N][D] fp16, 16-byte aligned, not overlapping each other, k
- * or v.  rope_tab_dev as in sol_attn_fwd.
+ * sol_prepare_kv: one pass over k and v into the prepared-path format.  Per
+ * (b, h) slab, ceil(N/32) tiles of 32 keys; each tile is 8 KB of K and 8 KB of
+ * V (fp16) in the order the attention kernel's MFMA fragments read them, so a
+ * tile is copied into LDS whole and every fragment read is linear:
+ *   K tile, 64-lane block kk (0..7), lane l + 32h: K^[key l][dims 16kk+8h..+7],
+ *     K^ = fp16(bf16(R(pos) k)) -- the rotation and rounding of sol_rope3d;
+ *   V tile, block j = 4s + c (0..7), lane l + 32h, element i (0..7):
+ *     fp16(v)[key 16s + 8(i/4) + 4h + i%4][dim 32c + l].
+ * Keys past N are zero.  The fp16 conversions are exact for 2^-14 <= |x| <
+ * 65504; smaller values keep fp16's 2^-24 absolute resolution, larger ones
+ * overflow to inf (outside what this path supports).  k_prep, v_prep: device
+ * buffers of sol_prepared_kv_bytes(B, H, N, D) bytes each, 16-byte aligned,
+ * not overlapping each other, k or v.  rope_tab_dev as in sol_attn_fwd.
  *
  * sol_attn_fwd_prepared: attention on prepared K/V; q is rotated and rounded
  * to bf16 in its tile load, then scaled by log2(e)/sqrt(D) and rounded to
@@ -122,21 +128,22 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
  * key tile; a row block whose probabilities would leave the fp16 range
  * (scores more than 15 binades above that reference) is written as NaN and
  * recomputed by the second, which raises the reference as it goes.  out must
- * not overlap q, k_rot or v_f16.
+ * not overlap q, k_prep or v_prep.
  *
  * The result differs from sol_attn_fwd's by rounding only (same contract and
  * error bound; the fp16 score operands and the reference max change the last
  * bits).
  */
-int sol_prepare_kv(const void* k, const void* v, void* k_rot, void* v_f16, int B, int H, int N,
+size_t sol_prepared_kv_bytes(int B, int H, int N, int D);
+int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H, int N,
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
-int sol_attn_fwd_prepared(const void* q, const void* k_rot, const void* v_f16, void* out, int B,
+int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
                           int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                           sol_stream_t stream);
 
 /*
- * Bytes of device workspace sol_attn_fwd_ws needs: room for k_rot then
- * v_f16, 2 * B*H*N*D * 2 bytes.  0 for invalid sizes.
+ * Bytes of device workspace sol_attn_fwd_ws needs: room for k_prep then
+ * v_prep, 2 * sol_prepared_kv_bytes(B, H, N, D).  0 for invalid sizes.
  */
 size_t sol_attn_workspace_bytes(int B, int H, int N, int D);
 
@@ -146,7 +153,7 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int D);
  * Same result as those two calls, bit for bit.  workspace: device memory of at
  * least sol_attn_workspace_bytes(B, H, N, D) bytes, 16-byte aligned, not
  * overlapping q, k, v or out; its contents on entry are ignored and on exit
- * hold k_rot then v_f16.  Other arguments and errors as sol_attn_fwd.
+ * hold k_prep then v_prep.  Other arguments and errors as sol_attn_fwd.
  */
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
                     int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,

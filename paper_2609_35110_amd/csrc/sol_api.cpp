@@ -136,52 +136,58 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
   return ok();
 }
 
-size_t sol_attn_workspace_bytes(int B, int H, int N, int D) {
-  if (B < 1 || H < 1 || N < 1 || D < 1) return 0;
-  return 2 * (size_t)B * H * N * D * 2;
+size_t sol_prepared_kv_bytes(int B, int H, int N, int D) {
+  if (B < 1 || H < 1 || N < 1 || D != 128 || N > SOL_MAX_TOKENS) return 0;
+  return (size_t)B * H * (size_t)sol::prepared_tile_elems(N) * 2;
 }
 
-int sol_prepare_kv(const void* k, const void* v, void* k_rot, void* v_f16, int B, int H, int N,
+size_t sol_attn_workspace_bytes(int B, int H, int N, int D) {
+  return 2 * sol_prepared_kv_bytes(B, H, N, D);
+}
+
+int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H, int N,
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
-  if (!k || !v || !k_rot || !v_f16) return fail(SOL_ERR_INVALID_ARG, "k, v, k_rot, v_f16 must not be NULL");
+  if (!k || !v || !k_prep || !v_prep) return fail(SOL_ERR_INVALID_ARG, "k, v, k_prep, v_prep must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
-  if (!aligned16(k) || !aligned16(v) || !aligned16(k_rot) || !aligned16(v_f16))
-    return fail(SOL_ERR_INVALID_ARG, "k, v, k_rot, v_f16 must be 16-byte aligned");
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_prep) || !aligned16(v_prep))
+    return fail(SOL_ERR_INVALID_ARG, "k, v, k_prep, v_prep must be 16-byte aligned");
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   const size_t bytes = (size_t)B * H * N * D * 2;
-  if (overlaps(k_rot, bytes, k, bytes) || overlaps(k_rot, bytes, v, bytes) ||
-      overlaps(v_f16, bytes, k, bytes) || overlaps(v_f16, bytes, v, bytes) ||
-      overlaps(k_rot, bytes, v_f16, bytes))
-    return fail(SOL_ERR_INVALID_ARG, "k_rot / v_f16 overlap each other or k, v");
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
+  if (overlaps(k_prep, pbytes, k, bytes) || overlaps(k_prep, pbytes, v, bytes) ||
+      overlaps(v_prep, pbytes, k, bytes) || overlaps(v_prep, pbytes, v, bytes) ||
+      overlaps(k_prep, pbytes, v_prep, pbytes))
+    return fail(SOL_ERR_INVALID_ARG, "k_prep / v_prep overlap each other or k, v");
   const int64_t nv = (int64_t)T * Hl * Wl;
   const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
   hipError_t e = sol::launch_prepare_kv(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                                        static_cast<uint16_t*>(k_rot), static_cast<uint16_t*>(v_f16), B * H,
+                                        static_cast<uint16_t*>(k_prep), static_cast<uint16_t*>(v_prep), B * H,
                                         g, tab, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "prepare_kv launch: %s", hipGetErrorString(e));
   return ok();
 }
 
-int sol_attn_fwd_prepared(const void* q, const void* k_rot, const void* v_f16, void* out, int B,
+int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
                           int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                           sol_stream_t stream) {
-  if (!q || !k_rot || !v_f16 || !out) return fail(SOL_ERR_INVALID_ARG, "q, k_rot, v_f16, out must not be NULL");
+  if (!q || !k_prep || !v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "q, k_prep, v_prep, out must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
-  if (!aligned16(q) || !aligned16(k_rot) || !aligned16(v_f16) || !aligned16(out))
-    return fail(SOL_ERR_INVALID_ARG, "q, k_rot, v_f16, out must be 16-byte aligned");
+  if (!aligned16(q) || !aligned16(k_prep) || !aligned16(v_prep) || !aligned16(out))
+    return fail(SOL_ERR_INVALID_ARG, "q, k_prep, v_prep, out must be 16-byte aligned");
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   const size_t bytes = (size_t)B * H * N * D * 2;
-  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k_rot, bytes) || overlaps(out, bytes, v_f16, bytes))
-    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_rot or v_f16");
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
+  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k_prep, pbytes) || overlaps(out, bytes, v_prep, pbytes))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep or v_prep");
   if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
   const int64_t nv = (int64_t)T * Hl * Wl;
   const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
-  hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_rot),
-                                               static_cast<const uint16_t*>(v_f16), static_cast<uint16_t*>(out),
+  hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
+                                               static_cast<const uint16_t*>(v_prep), static_cast<uint16_t*>(out),
                                                B * H, g, tab, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_prepared launch: %s", hipGetErrorString(e));
   return ok();
@@ -204,11 +210,11 @@ int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int 
     return fail(SOL_ERR_INVALID_ARG, "workspace overlaps q, k, v or out");
   if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k, bytes) || overlaps(out, bytes, v, bytes))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k or v");
-  uint16_t* k_rot = static_cast<uint16_t*>(workspace);
-  uint16_t* v_f16 = k_rot + (size_t)B * H * N * D;
-  st = sol_prepare_kv(k, v, k_rot, v_f16, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
+  uint16_t* k_prep = static_cast<uint16_t*>(workspace);
+  uint16_t* v_prep = k_prep + sol_prepared_kv_bytes(B, H, N, D) / 2;
+  st = sol_prepare_kv(k, v, k_prep, v_prep, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
   if (st != SOL_OK) return st;
-  return sol_attn_fwd_prepared(q, k_rot, v_f16, out, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
+  return sol_attn_fwd_prepared(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
 }
 
 const char* sol_status_string(int status) {

@@ -34,12 +34,16 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 // Prepared path: k_rot / v_f16 (each BH * N * D 16-bit elements) receive the
 // rotated K and the fp16 V in one pass; the attention kernel then rotates only
 // q and copies prepared tiles.
-hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_rot,
-                             uint16_t* v_f16, int BH, const SeqGrid& g, const float2* tab,
+// Prepared K/V: per (b, h) slab, ceil(N/32) tiles of 32 keys, 8 KB of K and
+// 8 KB of V each, in the fragment order of the prepared-path kernel.
+hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_prep,
+                             uint16_t* v_prep, int BH, const SeqGrid& g, const float2* tab,
                              hipStream_t stream);
-hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_rot,
-                                    const uint16_t* v_f16, uint16_t* out, int BH,
+hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
+                                    const uint16_t* v_prep, uint16_t* out, int BH,
                                     const SeqGrid& g, const float2* tab, hipStream_t stream);
+// fp16 elements of one (b, h) slab of prepared K (or V).
+int64_t prepared_tile_elems(int N);
 
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
 int64_t attn_max_workgroups(int N, int BH);

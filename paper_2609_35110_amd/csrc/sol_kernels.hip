@@ -142,28 +142,71 @@ __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x
   }
 }
 
-// One pass over K and V for the workspace path: K^ = rotated K (bf16, the same
-// rounding as the fused tile load), V converted to fp16.  One thread per
-// 16-byte chunk of one (b, h) slab; grid.y walks the slabs.
+// Prepared K/V for the prepared-path kernel: per (b, h) slab and 32-key tile,
+// 8 KB of K and 8 KB of V, each laid out in the order the kernel's MFMA
+// fragments are read, so one tile is one contiguous copy into LDS and every
+// fragment read is one linear ds_read_b128 (64 lanes x 16 bytes, no bank
+// conflicts, immediate offsets).
+//   K tile: [kk 0..7][lane 0..63][8]: lane = r + 32 hh holds K^[key r][16kk + 8hh ..+7],
+//     K^ the rotated key rounded to bf16 (as every rotation here), then fp16.
+//   V tile: [j 0..7][lane 0..63][8], j = 4 kst + db: lane = l + 32 hh holds
+//     V[key 16kst + 8(i/4) + 4hh + i%4][dim 32db + l] for i = 0..7, fp16 -- the
+//     key order of the fp16 probability words the PV MFMA multiplies it with.
+// Keys past N are zero.  One workgroup per tile; grid.y walks the slabs.
+constexpr int kPrepTile = 32;             // keys per prepared tile
+constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
+
 template <bool kRope>
 __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ k,
                                                       const uint4* __restrict__ v,
-                                                      uint4* __restrict__ kh, uint4* __restrict__ v16,
+                                                      uint4* __restrict__ kp, uint4* __restrict__ vp,
                                                       int64_t bh_count, SeqGrid g,
                                                       const float2* __restrict__ tab) {
-  const int64_t per_slab = (int64_t)g.n * kChunks;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= per_slab) return;
-  const int n = (int)(i / kChunks);
-  const int cc = (int)(i % kChunks);
-  const Pos p = kRope ? token_pos(n, g) : Pos{0, 0, 0, false};
-  const int pair0 = (kRope && p.rot) ? tab_pair(cc, p, g) : 0;
+  __shared__ __attribute__((aligned(16))) uint16_t vt[kPrepTile * (D + 8)];
+  const int N = g.n;
+  const int n_tiles = (N + kPrepTile - 1) / kPrepTile;
+  const int tile = blockIdx.x;
+  const int t = threadIdx.x;
+  // This thread's two 16-byte chunks of the tile: row r, chunk cc (dims 8cc..8cc+7).
+  int r[2], cc[2], pair0[2];
+  bool valid[2], rot[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int c = t + 256 * u;
+    r[u] = c >> 4;
+    cc[u] = c & 15;
+    const int n = tile * kPrepTile + r[u];
+    valid[u] = n < N;
+    Pos p{0, 0, 0, false};
+    if (kRope && valid[u]) p = token_pos(n, g);
+    rot[u] = kRope && p.rot;
+    pair0[u] = rot[u] ? tab_pair(cc[u], p, g) : 0;
+  }
+  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
   for (int64_t bh = blockIdx.y; bh < bh_count; bh += gridDim.y) {
-    const int64_t idx = bh * per_slab + i;
-    uint4 x = k[idx];
-    if (kRope && p.rot) x = rope_chunk(x, tab, pair0);
-    kh[idx] = bf16x8_to_f16x8(x);
-    v16[idx] = bf16x8_to_f16x8(v[idx]);
+    const size_t row0 = (size_t)bh * N + (size_t)tile * kPrepTile;
+    uint4* kt = kp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
+    uint4* vtile = vp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      uint4 x = valid[u] ? k[(row0 + r[u]) * kChunks + cc[u]] : zero;
+      if (rot[u]) x = rope_chunk(x, tab, pair0[u]);
+      kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(x);
+      const uint4 y = valid[u] ? v[(row0 + r[u]) * kChunks + cc[u]] : zero;
+      *reinterpret_cast<uint4*>(&vt[r[u] * (D + 8) + cc[u] * 8]) = bf16x8_to_f16x8(y);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = t + 256 * u;
+      const int j = c >> 6, ln = c & 63;
+      const int kst = j >> 2, db = j & 3, l = ln & 31, h = ln >> 5;
+      const uint16_t* col = vt + (16 * kst + 4 * h) * (D + 8) + 32 * db + l;
+      auto el = [&](int i) { return (uint32_t)col[(8 * (i >> 2) + (i & 3)) * (D + 8)]; };
+      vtile[c] = make_uint4(el(0) | el(1) << 16, el(2) | el(3) << 16, el(4) | el(5) << 16,
+                            el(6) | el(7) << 16);
+    }
+    __syncthreads();
   }
 }
 
@@ -533,6 +576,17 @@ __device__ __forceinline__ void mfma_wait() { asm volatile("s_nop 7\n\ts_nop 7\n
 __device__ __forceinline__ void pin(uint32_t& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
+// End of a prepared-path iteration: all but the last four vector-memory
+// operations of this wave (this iteration's tile copies into LDS) complete,
+// its LDS operations complete, then the workgroup barrier -- after which
+// every wave's completed copies are visible.
+__device__ __forceinline__ void dma_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt 4, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Attention on prepared K/V: k holds the rotated keys and v the values, both
 // as fp16.  The query rows are rotated and rounded to bf16 like every rotation
 // here, then multiplied by c = log2(e)/sqrt(D) and rounded to fp16, so the
@@ -557,18 +611,19 @@ __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 // LDS holds three K tiles (read K(i+1), prefetch K(i+2), write K(i+3) over
 // K(i)) and two V tiles (read V(i), write V(i+1) over V(i-1)); an LDS-only
 // barrier ends each iteration, so the global loads stay in flight across it.
-constexpr int BN2 = 32;                // keys per tile of the prepared-path kernel
-constexpr int kKTile = BN2 * KS;       // elements per K tile in LDS
-constexpr int kVTile = BN2 * VS;       // elements per V tile in LDS
-constexpr int kKBufs = 4;              // K tiles in LDS
+constexpr int BN2 = kPrepTile;         // keys per tile of the prepared-path kernel
+constexpr int kKBufs = 5;              // K tiles in LDS
+constexpr int kVBufs = 3;              // V tiles in LDS
+// Descriptor word 3 of a raw buffer resource (32-bit data, no format swizzle).
+constexpr int kBufferDword3 = 0x00020000;
 
 template <bool kRope, bool kRobust>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
                           const float2* __restrict__ tab, int n_qtiles, float c_log2) {
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKBufs * kKTile];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2 * kVTile];
+  __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -580,8 +635,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int N = g.n;
   const size_t slab = (size_t)bh * N * D;
   const uint16_t* __restrict__ qs = q + slab;
-  const uint16_t* __restrict__ ks = k + slab;
-  const uint16_t* __restrict__ vs = v + slab;
+  const int n_tiles = (N + BN2 - 1) / BN2;
+  const size_t pslab = (size_t)bh * n_tiles * kPrepTileElems;
   // Materialise the output pointer now: a kernel-argument load left in flight
   // into the main loop makes every LDS wait there a full lgkmcnt(0).
   uint16_t* out_slab = out + slab;
@@ -617,45 +672,48 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
   }
 
-  // ---- staging: thread moves chunks c0 and c0 + 8 of tile row rr, of K and of V.
-  const int rr = tid >> 3;
-  const int c0 = tid & 7;
-  uint4 kreg0, kreg1, vreg0, vreg1;  // separate scalars: an array of uint4 stays in scratch
-  auto load_k = [&](int kv0) __attribute__((always_inline)) {
-    const uint4* src = reinterpret_cast<const uint4*>(ks + (size_t)min(kv0 + rr, N - 1) * D);
-    kreg0 = src[c0];
-    kreg1 = src[c0 + 8];
+  // ---- staging: each prepared tile (8 KB) is copied into LDS by buffer loads
+  // that write LDS directly: wave w moves the 1 KB blocks 2w and 2w + 1.  Tile
+  // indices past the end are clamped (the copies are never read).
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t slab_bytes = (uint32_t)n_tiles * (kPrepTileElems * 2);
+  const __amdgpu_buffer_rsrc_t rsrc_k =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(k + pslab), (short)0, (int)slab_bytes, kBufferDword3);
+  const __amdgpu_buffer_rsrc_t rsrc_v =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(v + pslab), (short)0, (int)slab_bytes, kBufferDword3);
+  // Written as inline assembly: through the builtin the compiler would wait
+  // for every copy in flight (vmcnt 0) before any read of the same LDS array,
+  // since it cannot tell the ring's buffers apart; here dma_barrier() alone
+  // orders the copies (M0, the LDS base of the copy, is saved and restored).
+  auto dma_tile = [&](const __amdgpu_buffer_rsrc_t& rs, uint16_t* lds_tile, int tile)
+      __attribute__((always_inline)) {
+    const uint32_t tb = (uint32_t)min(tile, n_tiles - 1) * (kPrepTileElems * 2);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int blk = 2 * wave_s + u;
+      const uint32_t lds_addr = (uint32_t)(uintptr_t)(
+          (__attribute__((address_space(3))) uint16_t*)(lds_tile + blk * 512));
+      uint32_t m0_saved;
+      asm volatile(
+          "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\t"
+          "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+          : "=&s"(m0_saved)
+          : "s"(lds_addr), "v"(lane * 16), "s"(rs), "s"(tb + blk * 1024)
+          : "memory");
+    }
   };
-  auto load_v = [&](int kv0) __attribute__((always_inline)) {
-    const uint4* src = reinterpret_cast<const uint4*>(vs + (size_t)min(kv0 + rr, N - 1) * D);
-    vreg0 = src[c0];
-    vreg1 = src[c0 + 8];
+  auto dma_k = [&](int tile) __attribute__((always_inline)) {
+    dma_tile(rsrc_k, k_lds + (tile % kKBufs) * kPrepTileElems, tile);
   };
-  auto store_k = [&](int buf) __attribute__((always_inline)) {
-    uint16_t* dst = k_lds + buf * kKTile + rr * KS + c0 * 8;
-    *reinterpret_cast<uint4*>(dst) = kreg0;
-    *reinterpret_cast<uint4*>(dst + 64) = kreg1;
+  auto dma_v = [&](int tile) __attribute__((always_inline)) {
+    dma_tile(rsrc_v, v_lds + (tile % kVBufs) * kPrepTileElems, tile);
   };
-  auto store_v = [&](int buf) __attribute__((always_inline)) {
-    uint16_t* dst = v_lds + buf * kVTile + rr * VS + c0 * 8;
-    *reinterpret_cast<uint4*>(dst) = vreg0;
-    *reinterpret_cast<uint4*>(dst + 64) = vreg1;
+  // Fragment kk of K tile `tile` / fragment j = 4 kst + db of V tile `tile`.
+  auto kfrag = [&](int tile, int kk) __attribute__((always_inline)) {
+    return *reinterpret_cast<const f16x8*>(k_lds + (tile % kKBufs) * kPrepTileElems + kk * 512 + lane * 8);
   };
-
-  // A fragment of K: lane (l32, hh) holds key l32, dims 16kk + 8hh .. +7.
-  const uint16_t* const k_lane = k_lds + l32 * KS + hh * 8;
-  auto kfrag = [&](int buf, int kk) __attribute__((always_inline)) {
-    return *reinterpret_cast<const f16x8*>(k_lane + buf * kKTile + kk * 16);
-  };
-  const int g16 = lane >> 4, i16 = lane & 15;
-  const uint16_t* const v_lane =
-      v_lds + (4 * (g16 >> 1) + (i16 >> 2)) * VS + 16 * (g16 & 1) + 4 * (i16 & 3);
-  // V^T fragment j = (kst, db) = (j / 4, j % 4) of tile buffer buf.
-  auto vfrag = [&](int buf, int j) __attribute__((always_inline)) {
-    const uint16_t* p0 = v_lane + buf * kVTile + 16 * (j >> 2) * VS + 32 * (j & 3);
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 8 * VS));
-    return __builtin_bit_cast(f16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  auto vfrag = [&](int tile, int j) __attribute__((always_inline)) {
+    return *reinterpret_cast<const f16x8*>(v_lds + (tile % kVBufs) * kPrepTileElems + j * 512 + lane * 8);
   };
 
   f32x16 o[2][4];
@@ -694,9 +752,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   };
   const int n_kv = (N + BN2 - 1) / BN2;
   // Read-ahead rings: K fragments 4 chunks ahead (kr[kk % 4] holds fragment kk
-  // of the tile being multiplied), V^T fragments 2 chunks ahead (vr[j % 3]).
+  // of the tile being multiplied), V^T fragments 3 chunks ahead (vr[j % 4]).
   f16x8 kr[4];
-  f16x8 vr[3];
+  f16x8 vr[4];
   // Words of P(i): qb0 words come from the previous phase B, qb1 words from
   // this phase A.  lsum[qb] are their fp32 row sums (two chains per block).
   // Iteration i:
@@ -704,23 +762,28 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   //   phase B (8 chunks): PV(i) MFMAs (qb0, qb1 per V fragment) + P(i+1) qb0 word j
   auto iteration = [&](int i, f32x16* cs, f32x16* ns, uint32_t* p0_cur, uint32_t* p0_next,
                        float* l0_cur, float* l0_next) __attribute__((always_inline)) {
-    // K(j) lives in buffer j % 4 from iteration j-3 (or the prologue) to j+1.
-    const int kb_old = i & 3, kb_cur = (i + 1) & 3, kb_next = (i + 2) & 3, kb_free = (i + 3) & 3;
-    const int vb = i & 1;
+    // K tile j sits in buffer j % 5 from its copy (iteration j-4, or the
+    // prologue) to iteration j+1; V tile j in buffer j % 3 from iteration j-2
+    // to iteration j.
     // ---- phase A
     uint32_t p1[8];
     float l1[2] = {0.0f, 0.0f};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      if (j == 0) {
+      if (kRobust) {
+        // The second pass spills; only MFMAs the compiler sees are safe next
+        // to its spill code.
+        ns[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[0][j], j == 0 ? bias[0] : ns[0], 0, 0, 0);
+        ns[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[1][j], j == 0 ? bias[1] : ns[1], 0, 0, 0);
+      } else if (j == 0) {
         mfma_s_first(ns[0], kr[0], qf[0][0], bias[0]);
         mfma_s_first(ns[1], kr[0], qf[1][0], bias[1]);
       } else {
         mfma_s_next(ns[0], kr[j & 3], qf[0][j]);
         mfma_s_next(ns[1], kr[j & 3], qf[1][j]);
       }
-      if (j < 4) kr[j] = kfrag(kb_cur, j + 4);
-      if (j >= 6) vr[j - 6] = vfrag(vb, j - 6);
+      if (j < 4) kr[j] = kfrag(i + 1, j + 4);
+      if (j >= 5) vr[j - 5] = vfrag(i, j - 5);
       const float ea = __builtin_amdgcn_exp2f(cs[1][2 * j]);
       const float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
       f16x2 h;
@@ -748,7 +811,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
           f32x16 t = bias[qb];
 #pragma unroll
           for (int kk = 0; kk < 8; ++kk)
-            t = __builtin_amdgcn_mfma_f32_32x32x16_f16(kfrag(kb_old, kk), qf[qb][kk], t, 0, 0, 0);
+            t = __builtin_amdgcn_mfma_f32_32x32x16_f16(kfrag(i, kk), qf[qb][kk], t, 0, 0, 0);
           if ((i + 1) * BN2 > N) mask_block(i, t);
           const float delta = fmaxf(tile_max(t), 0.0f);
           const float alpha = __builtin_amdgcn_exp2f(-delta);
@@ -809,14 +872,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
-      o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j % 3], pf[0][kst], o[0][db], 0, 0, 0);
-      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j % 3], pf[1][kst], o[1][db], 0, 0, 0);
-      if (j + 2 < 8) vr[(j + 2) % 3] = vfrag(vb, j + 2);
-      if (j == 1) store_k(kb_free);    // K(i+3) over K(i)
-      if (j == 2) store_v(vb ^ 1);     // V(i+1) over V(i-1)
-      if (j == 3) load_k((i + 4) * BN2);
-      if (j == 4) load_v((i + 2) * BN2);
-      if (j >= 4) kr[j - 4] = kfrag(kb_next, j - 4);
+      o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[0][kst], o[0][db], 0, 0, 0);
+      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[1][kst], o[1][db], 0, 0, 0);
+      if (j + 3 < 8) vr[(j + 3) & 3] = vfrag(i, j + 3);
+      if (j == 1) dma_k(i + 4);  // over K(i-1)
+      if (j == 2) dma_v(i + 2);  // over V(i-1)
+      if (j >= 4) kr[j - 4] = kfrag(i + 2, j - 4);
       const float ea = __builtin_amdgcn_exp2f(ns[0][2 * j]);
       const float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
       f16x2 h;
@@ -830,22 +891,21 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       pin(l0_next[1]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    lds_barrier();
+    // The copies issued in the previous iteration (K(i+3), V(i+1)) must have
+    // landed: only this iteration's four may still be in flight.
+    dma_barrier();
   };
 
-  // ---- prologue: K(0..2) and V(0) into LDS; K(3), V(1) in registers; S(0)
+  // ---- prologue: K(0..2) and V(0) in LDS, K(3) and V(1) on their way; S(0)
   // against m = its own max; the qb0 words of P(0).
-  load_k(0);
-  load_v(0);
-  store_k(0);
-  store_v(0);
-  load_k(BN2);
-  store_k(1);
-  load_k(2 * BN2);
-  store_k(2);
-  load_k(3 * BN2);
-  load_v(BN2);
+  dma_k(0);
+  dma_v(0);
+  dma_k(1);
+  dma_k(2);
+  __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
+  dma_k(3);
+  dma_v(1);
   // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
   // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
   // such copies.
@@ -884,7 +944,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
   for (int t = 0; t < 4; ++t) kr[t] = kfrag(1, t);
   mfma_wait();
-  lds_barrier();  // K(3) will overwrite K(0)
 
   int i = 0;
   for (; i + 1 < n_kv; i += 2) {
@@ -956,45 +1015,49 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   return hipGetLastError();
 }
 
-hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_rot,
-                             uint16_t* v_f16, int BH, const SeqGrid& g, const float2* tab,
+hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_prep,
+                             uint16_t* v_prep, int BH, const SeqGrid& g, const float2* tab,
                              hipStream_t stream) {
-  const int64_t per_slab = (int64_t)g.n * kChunks;
-  const dim3 pgrid((unsigned)((per_slab + 255) / 256), (unsigned)(BH < 65535 ? BH : 65535));
+  const int n_tiles = (g.n + kPrepTile - 1) / kPrepTile;
+  const dim3 pgrid((unsigned)n_tiles, (unsigned)(BH < 65535 ? BH : 65535));
   if (tab != nullptr)
     hipLaunchKernelGGL(prep_kv_kernel<true>, pgrid, dim3(256), 0, stream,
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
-                       reinterpret_cast<uint4*>(k_rot), reinterpret_cast<uint4*>(v_f16),
+                       reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
                        (int64_t)BH, g, tab);
   else
     hipLaunchKernelGGL(prep_kv_kernel<false>, pgrid, dim3(256), 0, stream,
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
-                       reinterpret_cast<uint4*>(k_rot), reinterpret_cast<uint4*>(v_f16),
+                       reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
                        (int64_t)BH, g, tab);
   return hipGetLastError();
 }
 
-hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_rot,
-                                    const uint16_t* v_f16, uint16_t* out, int BH,
+int64_t prepared_tile_elems(int N) {
+  return (int64_t)((N + kPrepTile - 1) / kPrepTile) * kPrepTileElems;
+}
+
+hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
+                                    const uint16_t* v_prep, uint16_t* out, int BH,
                                     const SeqGrid& g, const float2* tab, hipStream_t stream) {
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   if (tab != nullptr)
-    hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_rot,
-                       v_f16, out, g, tab, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_prep,
+                       v_prep, out, g, tab, n_qtiles, c_log2);
   else
-    hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_rot,
-                       v_f16, out, g, tab, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_prep,
+                       v_prep, out, g, tab, n_qtiles, c_log2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // Second pass over the row blocks whose probabilities left the fp16 range.
   if (tab != nullptr)
-    hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_rot,
-                       v_f16, out, g, tab, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_prep,
+                       v_prep, out, g, tab, n_qtiles, c_log2);
   else
-    hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_rot,
-                       v_f16, out, g, tab, n_qtiles, c_log2);
+    hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_prep,
+                       v_prep, out, g, tab, n_qtiles, c_log2);
   return hipGetLastError();
 }
 

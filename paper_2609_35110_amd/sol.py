@@ -51,6 +51,8 @@ def lib():
         L.sol_prepare_kv.restype = i32
         L.sol_attn_fwd_prepared.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_attn_fwd_prepared.restype = i32
+        L.sol_prepared_kv_bytes.argtypes = [i32, i32, i32, i32]
+        L.sol_prepared_kv_bytes.restype = sz
         L.sol_attn_workspace_bytes.argtypes = [i32, i32, i32, i32]
         L.sol_attn_workspace_bytes.restype = sz
         L.sol_attn_fwd_ws.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, sz, P]
@@ -83,12 +85,16 @@ def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
     return lib().sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
 
 
-def sol_prepare_kv(k, v, k_rot, v_f16, B, H, N, D, T, Hl, Wl, rope_tab, stream):
-    return lib().sol_prepare_kv(k, v, k_rot, v_f16, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+def sol_prepare_kv(k, v, k_prep, v_prep, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_prepare_kv(k, v, k_prep, v_prep, B, H, N, D, T, Hl, Wl, rope_tab, stream)
 
 
-def sol_attn_fwd_prepared(q, k_rot, v_f16, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
-    return lib().sol_attn_fwd_prepared(q, k_rot, v_f16, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+def sol_prepared_kv_bytes(B, H, N, D):
+    return lib().sol_prepared_kv_bytes(B, H, N, D)
+
+
+def sol_attn_fwd_prepared(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_attn_fwd_prepared(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
 
 
 def sol_attn_workspace_bytes(B, H, N, D):
@@ -213,39 +219,45 @@ def attn_fwd_ws(q, k, v, T, Hl, Wl, table=None, workspace=None, out=None):
     return out
 
 
-def _check_16bit(name, t, shape):
-    if not isinstance(t, torch.Tensor) or t.dtype not in (torch.bfloat16, torch.float16):
-        raise TypeError("%s must be a bfloat16 or float16 tensor" % name)
-    if not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
-        raise ValueError("%s must be a contiguous device tensor of shape %s" % (name, tuple(shape)))
+def _check_prepared(name, t, nbytes, device):
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float16:
+        raise TypeError("%s must be a float16 tensor" % name)
+    if not t.is_cuda or t.device != device or not t.is_contiguous() or t.numel() * 2 < nbytes:
+        raise ValueError("%s must be a contiguous float16 tensor on %s of at least %d bytes"
+                         % (name, device, nbytes))
 
 
-def prepare_kv(k, v, T, Hl, Wl, table=None, k_rot=None, v_f16=None):
-    """(k_rot, v_f16), both float16: K rotated (rounded to bf16 like every
-    rotation, then converted) and V converted, one pass."""
+def prepare_kv(k, v, T, Hl, Wl, table=None, k_prep=None, v_prep=None):
+    """(k_prep, v_prep): K rotated (rounded to bf16 like every rotation, then
+    fp16) and V in fp16, in the prepared path's tile layout (flat float16
+    tensors of sol_prepared_kv_bytes bytes each)."""
     _check_tensor("k", k)
     _check_tensor("v", v, k.shape)
     B, H, N, D = k.shape
-    k_rot = torch.empty(k.shape, dtype=torch.float16, device=k.device) if k_rot is None else k_rot
-    v_f16 = torch.empty(k.shape, dtype=torch.float16, device=k.device) if v_f16 is None else v_f16
-    _check_16bit("k_rot", k_rot, k.shape)
-    _check_16bit("v_f16", v_f16, k.shape)
+    nbytes = sol_prepared_kv_bytes(B, H, N, D)
+    if k_prep is None:
+        k_prep = torch.empty(nbytes // 2, dtype=torch.float16, device=k.device)
+    if v_prep is None:
+        v_prep = torch.empty(nbytes // 2, dtype=torch.float16, device=k.device)
+    _check_prepared("k_prep", k_prep, nbytes, k.device)
+    _check_prepared("v_prep", v_prep, nbytes, k.device)
     check(sol_prepare_kv(ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
-                         ctypes.c_void_p(k_rot.data_ptr()), ctypes.c_void_p(v_f16.data_ptr()),
+                         ctypes.c_void_p(k_prep.data_ptr()), ctypes.c_void_p(v_prep.data_ptr()),
                          B, H, N, D, T, Hl, Wl, _table_ptr(table, k.device), _stream(k)))
-    return k_rot, v_f16
+    return k_prep, v_prep
 
 
-def attn_fwd_prepared(q, k_rot, v_f16, T, Hl, Wl, table=None, out=None):
+def attn_fwd_prepared(q, k_prep, v_prep, T, Hl, Wl, table=None, out=None):
     """Attention on prepare_kv's outputs; q rotated in the tile load."""
     _check_tensor("q", q)
-    _check_16bit("k_rot", k_rot, q.shape)
-    _check_16bit("v_f16", v_f16, q.shape)
     B, H, N, D = q.shape
+    nbytes = sol_prepared_kv_bytes(B, H, N, D)
+    _check_prepared("k_prep", k_prep, nbytes, q.device)
+    _check_prepared("v_prep", v_prep, nbytes, q.device)
     if out is None:
         out = torch.empty_like(q)
     _check_tensor("out", out, q.shape)
-    check(sol_attn_fwd_prepared(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_rot.data_ptr()),
-                                ctypes.c_void_p(v_f16.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+    check(sol_attn_fwd_prepared(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
+                                ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                                 B, H, N, D, T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
     return out

@@ -83,8 +83,12 @@ def attn_ws(q=A, k=Bp, v=C, out=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab
 
 
 def test_workspace_size(L):
-    assert sol.sol_attn_workspace_bytes(1, 40, 111600, 128) == 2 * 40 * 111600 * 128 * 2
+    # 3488 tiles of 32 keys per slab (the last one padded), 8 KB of K and 8 KB of V each
+    assert sol.sol_prepared_kv_bytes(1, 40, 111600, 128) == 40 * 3488 * 32 * 128 * 2
+    assert sol.sol_attn_workspace_bytes(1, 40, 111600, 128) == 2 * 40 * 3488 * 32 * 128 * 2
+    assert sol.sol_prepared_kv_bytes(2, 3, 33, 128) == 2 * 3 * 2 * 32 * 128 * 2
     assert sol.sol_attn_workspace_bytes(0, 1, 1, 128) == 0
+    assert sol.sol_prepared_kv_bytes(1, 1, 1, 64) == 0
 
 
 @pytest.mark.parametrize("kw,status,fragment", [
@@ -104,15 +108,15 @@ def test_attn_fwd_ws_rejects_before_any_hip_call(L, kw, status, fragment):
 
 @pytest.mark.parametrize("kw,status,fragment", [
     (dict(k=None), -1, "NULL"),
-    (dict(k_rot=P(0x100008)), -1, "aligned"),
-    (dict(k_rot=Bp), -1, "overlap"),
-    (dict(v_f16=P(0x300000 + 4096)), -1, "overlap"),
+    (dict(k_prep=P(0x100008)), -1, "aligned"),
+    (dict(k_prep=Bp), -1, "overlap"),
+    (dict(v_prep=P(0x300000 + 4096)), -1, "overlap"),
     (dict(D=32), -2, "head dim"),
 ])
 def test_prepare_kv_rejects_before_any_hip_call(L, kw, status, fragment):
-    args = dict(k=A, v=Bp, k_rot=C, v_f16=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
+    args = dict(k=A, v=Bp, k_prep=C, v_prep=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
     args.update(kw)
-    st = sol.sol_prepare_kv(args["k"], args["v"], args["k_rot"], args["v_f16"], args["B"], args["H"],
+    st = sol.sol_prepare_kv(args["k"], args["v"], args["k_prep"], args["v_prep"], args["B"], args["H"],
                             args["N"], args["D"], args["T"], args["Hl"], args["Wl"], args["tab"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
@@ -121,13 +125,13 @@ def test_prepare_kv_rejects_before_any_hip_call(L, kw, status, fragment):
 @pytest.mark.parametrize("kw,status,fragment", [
     (dict(q=None), -1, "NULL"),
     (dict(out=C), -1, "overlaps"),
-    (dict(v_f16=P(0x300008)), -1, "aligned"),
+    (dict(v_prep=P(0x300008)), -1, "aligned"),
     (dict(N=100, T=9), -1, "more tokens"),
 ])
 def test_attn_fwd_prepared_rejects_before_any_hip_call(L, kw, status, fragment):
-    args = dict(q=A, k_rot=Bp, v_f16=C, out=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
+    args = dict(q=A, k_prep=Bp, v_prep=C, out=Dp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB)
     args.update(kw)
-    st = sol.sol_attn_fwd_prepared(args["q"], args["k_rot"], args["v_f16"], args["out"], args["B"],
+    st = sol.sol_attn_fwd_prepared(args["q"], args["k_prep"], args["v_prep"], args["out"], args["B"],
                                    args["H"], args["N"], args["D"], args["T"], args["Hl"], args["Wl"],
                                    args["tab"], None)
     assert st == status, sol.sol_last_error()

@@ -185,12 +185,31 @@ def test_fused_rotation_equals_prerotated(shape):
     assert torch.equal(fused, pre)
 
 
+def _prepared_layout(k_hat, v):
+    """The prepared-path tile layout, rebuilt with plain tensor indexing from
+    the rotated keys k_hat (bf16) and the values v: per slab, 32-key tiles
+    (zero past N); K tile [kk][h][key l][8 dims 16kk+8h..]; V tile
+    [s][c][h][l][i] = v[key 16s + 8(i//4) + 4h + i%4][dim 32c + l]."""
+    B, H, N, D = v.shape
+    nt = (N + 31) // 32
+    pad = nt * 32 - N
+    kf = torch.nn.functional.pad(k_hat.to(torch.float16), (0, 0, 0, pad)).view(B * H, nt, 32, 8, 2, 8)
+    k_ref = kf.permute(0, 1, 3, 4, 2, 5).reshape(-1)
+    vf = torch.nn.functional.pad(v.to(torch.float16), (0, 0, 0, pad)).view(B * H, nt, 32, D)
+    s_, h_, i_ = torch.meshgrid(torch.arange(2), torch.arange(2), torch.arange(8), indexing="ij")
+    keys = (16 * s_ + 8 * (i_ // 4) + 4 * h_ + i_ % 4).to(v.device)      # [s][h][i]
+    g = vf[:, :, keys, :]                                                # [bh][t][s][h][i][D]
+    g = g.view(B * H, nt, 2, 2, 8, 4, 32)                               # D -> [c][l]
+    v_ref = g.permute(0, 1, 2, 5, 3, 6, 4).reshape(-1)                   # [s][c][h][l][i]
+    return k_ref, v_ref
+
+
 @pytest.mark.parametrize("shape", [(1, 2, 3, 8, 8, 0), (1, 3, 3, 11, 13, 37), (2, 1, 5, 7, 9, 64),
                                    (1, 1, 1, 1, 1, 0), (1, 2, 0, 0, 0, 300)])
 def test_workspace_path_is_the_two_prepared_calls(shape):
     """sol_attn_fwd_ws == sol_prepare_kv then sol_attn_fwd_prepared, bit for
-    bit; the workspace (and prepare_kv) hold K rotated by sol_rope3d then
-    converted to fp16, and V converted to fp16."""
+    bit; the workspace (and prepare_kv) hold exactly the documented tile
+    layout of K rotated by sol_rope3d and of V, both in fp16."""
     B, H, T, Hl, Wl, nt = shape
     w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=550 + sum(shape))
     q, k, v = (t.to(DEV) for t in W.make_inputs(w))
@@ -198,16 +217,18 @@ def test_workspace_path_is_the_two_prepared_calls(shape):
     ws = sol.attn_workspace(q)
     ws.fill_(0xFF)  # contents on entry are ignored
     a = sol.attn_fwd_ws(q, k, v, T, Hl, Wl, tab, workspace=ws)
-    k_f16, v_f16 = sol.prepare_kv(k, v, T, Hl, Wl, tab)
-    b = sol.attn_fwd_prepared(q, k_f16, v_f16, T, Hl, Wl, tab)
-    want_k = (sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k).to(torch.float16)
+    k_prep, v_prep = sol.prepare_kv(k, v, T, Hl, Wl, tab)
+    b = sol.attn_fwd_prepared(q, k_prep, v_prep, T, Hl, Wl, tab)
+    k_hat = sol.rope3d(k, T, Hl, Wl, tab) if tab is not None else k
+    k_ref, v_ref = _prepared_layout(k_hat, v)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
-    n = q.numel()
-    assert torch.equal(ws[: 2 * n].view(torch.float16).view(q.shape), want_k)
-    assert torch.equal(ws[2 * n: 4 * n].view(torch.float16).view(q.shape), v.to(torch.float16))
-    assert torch.equal(k_f16, want_k)
-    assert torch.equal(v_f16, v.to(torch.float16))
+    n = k_ref.numel()
+    assert k_prep.numel() == n and v_prep.numel() == n
+    assert torch.equal(k_prep, k_ref)
+    assert torch.equal(v_prep, v_ref)
+    assert torch.equal(ws[: 2 * n].view(torch.float16), k_ref)
+    assert torch.equal(ws[2 * n: 4 * n].view(torch.float16), v_ref)
 
 
 @pytest.mark.parametrize("growth", [24.0, 300.0])
