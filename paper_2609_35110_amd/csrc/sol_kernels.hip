@@ -44,6 +44,18 @@ constexpr int kChunks = D / 8;  // 16-byte chunks (8 bf16 = 4 rotary pairs) per 
 
 // n / d for 0 <= n < 2^23, d >= 1: float reciprocal estimate (off by at most
 // one) and one integer correction.
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
+// XCD w % 8), and each XCD has its own L2.  Renumber them so that XCD x gets
+// one contiguous range of work items: the workgroups an XCD runs at the same
+// time then stream the same (b, h) slab's K and V through its L2 together.
+// A bijection on [0, n) for any n.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_local_id(int w, int n) {
+  const int xcd = w % kXcds, local = w / kXcds;
+  const int per = n / kXcds, rem = n % kXcds;
+  return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
 __device__ __forceinline__ int div_exact(int n, int d, float inv) {
   int q = (int)((float)n * inv);
   int r = n - q * d;
@@ -630,8 +642,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int wave = tid >> 6;
   const int hh = lane >> 5;
   const int l32 = lane & 31;
-  const int bh = blockIdx.x / n_qtiles;
-  const int qt = blockIdx.x - bh * n_qtiles;
+  const int wg = xcd_local_id(blockIdx.x, gridDim.x);
+  const int bh = wg / n_qtiles;
+  const int qt = wg - bh * n_qtiles;
   const int N = g.n;
   const size_t slab = (size_t)bh * N * D;
   const uint16_t* __restrict__ qs = q + slab;
