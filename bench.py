@@ -142,15 +142,15 @@ def main():
     torch.cuda.synchronize()
 
     ws = sol.attn_workspace(qd)
-    n_el = qd.numel()
-    k_rot = ws[: 2 * n_el].view(torch.bfloat16).view(qd.shape)
-    v_f16 = ws[2 * n_el: 4 * n_el].view(torch.float16).view(qd.shape)
+    n_prep = sol.sol_prepared_kv_bytes(w.B, w.H, w.N, w.D) // 2
+    k_prep = ws.view(torch.float16)[:n_prep]
+    v_prep = ws.view(torch.float16)[n_prep: 2 * n_prep]
 
     def launches(path):
         """The launches of one step, in order: [(name, fn)]."""
         if path == "prepared":
-            return [("prepare_kv", lambda: sol.prepare_kv(kd, vd, w.T, w.Hl, w.Wl, tab, k_rot, v_f16)),
-                    ("attn_fwd_prepared", lambda: sol.attn_fwd_prepared(qd, k_rot, v_f16, w.T, w.Hl, w.Wl,
+            return [("prepare_kv", lambda: sol.prepare_kv(kd, vd, w.T, w.Hl, w.Wl, tab, k_prep, v_prep)),
+                    ("attn_fwd_prepared", lambda: sol.attn_fwd_prepared(qd, k_prep, v_prep, w.T, w.Hl, w.Wl,
                                                                         tab, out=out))]
         return [("attn_fwd", lambda: sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out))]
 
@@ -206,7 +206,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        # MFMA operand type: the fused path multiplies bf16, the prepared path
+        # fp16 (bf16 inputs and output, fp32 accumulation in both)
+        "dtype": "bf16" if args.path == "fused" else "f16",
         "data": "synthetic (seeded N(0,1) bf16 q/k/v of the layer's shape)",
         "config": {
             "workload": "%s: %s" % (w.name, w.describe()),
