@@ -580,9 +580,16 @@ __device__ __forceinline__ void mfma_s_first(f32x16& d, const f16x8& k, const f1
 __device__ __forceinline__ void mfma_s_next(f32x16& d, const f16x8& k, const f16x8& q) {
   asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+v"(d) : "v"(k), "a"(q));
 }
-// More wait states than an 8-pass MFMA needs before its result is read or
-// written by the VALU (or its VALU-written operand is read by an MFMA).
-__device__ __forceinline__ void mfma_wait() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory"); }
+// 16 wait states: more than the 12 an 8-pass MFMA result needs before the VALU
+// reads or overwrites it.
+__device__ __forceinline__ void mfma_wait() { asm volatile("s_nop 7\n\ts_nop 7" ::: "memory"); }
+// Two fp32 values as an fp16 pair (RNE), the low half first.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  f16x2 h;
+  h[0] = (_Float16)lo;
+  h[1] = (_Float16)hi;
+  return __builtin_bit_cast(uint32_t, h);
+}
 // Keep a value computed where it stands: IR passes would otherwise sink the
 // softmax arithmetic of a chunk to its first use and undo the interleaving.
 __device__ __forceinline__ void pin(uint32_t& x) { asm volatile("" : "+v"(x)); }
@@ -590,11 +597,13 @@ __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
 // End of a prepared-path iteration: all but the last four vector-memory
 // operations of this wave (this iteration's tile copies into LDS) complete,
-// its LDS operations complete, then the workgroup barrier -- after which
-// every wave's completed copies are visible.
+// all but its last four LDS reads (the first K(i+2) fragments, from a buffer
+// no copy touches next) complete, then the workgroup barrier -- after which
+// every wave's completed copies are visible and no wave still reads a buffer
+// the next copies overwrite.
 __device__ __forceinline__ void dma_barrier() {
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt 4, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_waitcnt(0x0474);  // vmcnt 4, expcnt 7, lgkmcnt 4
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -612,20 +621,23 @@ __device__ __forceinline__ void dma_barrier() {
 // feeds two MFMAs (one per 32-query block).  4 waves (one per SIMD, 256 query
 // rows per workgroup), the 2 x 4 output accumulators and Q' in AGPRs, 32-key
 // tiles so that the scores of two tiles fit in VGPRs.  With one wave per SIMD
-// nothing hides a stall, so each iteration i is laid out by hand in chunks of
-// two MFMAs (sched_barrier fences keep the order):
-//   phase A: S(i+1) = K(i+1) Q'^T - m (16 MFMAs) beside P(i) = exp2(S(i)) and
-//     its row sums on the VALU; the K fragments are read 4 chunks ahead, the
-//     first V(i) fragments during the last chunks;
-//   phase B: O^T += V(i)^T P(i)^T (16 MFMAs) beside the copy of K(i+3) and
-//     V(i+1) from registers into LDS, the loads of K(i+4) and V(i+2), and the
-//     reads of the first K(i+2) fragments for the next phase A.
-// LDS holds three K tiles (read K(i+1), prefetch K(i+2), write K(i+3) over
-// K(i)) and two V tiles (read V(i), write V(i+1) over V(i-1)); an LDS-only
-// barrier ends each iteration, so the global loads stay in flight across it.
+// the wave issues in order and nothing hides a stall, so each iteration i is
+// laid out by hand in slots of ONE MFMA followed by the VALU and memory work
+// that runs in its shadow (sched_barrier fences keep the order; two MFMAs in a
+// row would leave the first one's shadow empty):
+//   phase A: S(i+1) = K(i+1) Q'^T - m (16 MFMAs) beside the qb1 half of
+//     P(i) = exp2(S(i)) and its row sums; K fragments are read four MFMA pairs
+//     ahead, the first V(i) fragments during the last pairs;
+//   phase B: O^T += V(i)^T P(i)^T (16 MFMAs) beside the qb0 half of P(i+1),
+//     the copies of K(i+4) and V(i+2) into LDS (one 1 KB block in each of four
+//     slots) and the reads of the first K(i+2) fragments for the next phase A.
+// Each pair of slots packs the previous pair's two probabilities (software
+// pipelined: an exponential is never read by the very next instruction).
+// LDS holds rings of eight K tiles and four V tiles (96 KB); the barrier that
+// ends an iteration waits only for the copies issued one iteration earlier.
 constexpr int BN2 = kPrepTile;         // keys per tile of the prepared-path kernel
-constexpr int kKBufs = 5;              // K tiles in LDS
-constexpr int kVBufs = 3;              // V tiles in LDS
+constexpr int kKBufs = 8;              // K tiles in LDS (a power of two: ring
+constexpr int kVBufs = 4;              // V tiles in LDS  offsets are masks)
 // Descriptor word 3 of a raw buffer resource (32-bit data, no format swizzle).
 constexpr int kBufferDword3 = 0x00020000;
 
@@ -694,39 +706,40 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       __builtin_amdgcn_make_buffer_rsrc((void*)(k + pslab), (short)0, (int)slab_bytes, kBufferDword3);
   const __amdgpu_buffer_rsrc_t rsrc_v =
       __builtin_amdgcn_make_buffer_rsrc((void*)(v + pslab), (short)0, (int)slab_bytes, kBufferDword3);
-  // Written as inline assembly: through the builtin the compiler would wait
-  // for every copy in flight (vmcnt 0) before any read of the same LDS array,
-  // since it cannot tell the ring's buffers apart; here dma_barrier() alone
-  // orders the copies (M0, the LDS base of the copy, is saved and restored).
-  auto dma_tile = [&](const __amdgpu_buffer_rsrc_t& rs, uint16_t* lds_tile, int tile)
+  // One 1 KB block per call, as inline assembly: through the builtin the
+  // compiler would wait for every copy in flight (vmcnt 0) before any read of
+  // the same LDS array, since it cannot tell the ring's buffers apart; here
+  // dma_barrier() alone orders the copies.  M0 carries the LDS base of the
+  // copy, with the one wait state a VMEM read of M0 needs after an SALU write
+  // of it.  M0 is declared clobbered: the compiler itself uses M0 nowhere in
+  // these kernels (no LDS DMA builtin, no indirect register indexing, no
+  // message), which a build test checks on the generated code.
+  auto dma_blk = [&](const __amdgpu_buffer_rsrc_t& rs, uint16_t* lds_tile, int tile, int u)
       __attribute__((always_inline)) {
     const uint32_t tb = (uint32_t)min(tile, n_tiles - 1) * (kPrepTileElems * 2);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int blk = 2 * wave_s + u;
-      const uint32_t lds_addr = (uint32_t)(uintptr_t)(
-          (__attribute__((address_space(3))) uint16_t*)(lds_tile + blk * 512));
-      uint32_t m0_saved;
-      asm volatile(
-          "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\t"
-          "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
-          : "=&s"(m0_saved)
-          : "s"(lds_addr), "v"(lane * 16), "s"(rs), "s"(tb + blk * 1024)
-          : "memory");
-    }
+    const int blk = 2 * wave_s + u;
+    const uint32_t lds_addr = (uint32_t)(uintptr_t)(
+        (__attribute__((address_space(3))) uint16_t*)(lds_tile + blk * 512));
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"  // M0 is a reserved register
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(lds_addr), "v"(lane * 16), "s"(rs), "s"(tb + blk * 1024)
+                 : "memory", "m0");
+#pragma clang diagnostic pop
   };
-  auto dma_k = [&](int tile) __attribute__((always_inline)) {
-    dma_tile(rsrc_k, k_lds + (tile % kKBufs) * kPrepTileElems, tile);
+  auto dma_k = [&](int tile, int u) __attribute__((always_inline)) {
+    dma_blk(rsrc_k, k_lds + (tile & (kKBufs - 1)) * kPrepTileElems, tile, u);
   };
-  auto dma_v = [&](int tile) __attribute__((always_inline)) {
-    dma_tile(rsrc_v, v_lds + (tile % kVBufs) * kPrepTileElems, tile);
+  auto dma_v = [&](int tile, int u) __attribute__((always_inline)) {
+    dma_blk(rsrc_v, v_lds + (tile & (kVBufs - 1)) * kPrepTileElems, tile, u);
   };
   // Fragment kk of K tile `tile` / fragment j = 4 kst + db of V tile `tile`.
   auto kfrag = [&](int tile, int kk) __attribute__((always_inline)) {
-    return *reinterpret_cast<const f16x8*>(k_lds + (tile % kKBufs) * kPrepTileElems + kk * 512 + lane * 8);
+    return *reinterpret_cast<const f16x8*>(k_lds + (tile & (kKBufs - 1)) * kPrepTileElems + kk * 512 + lane * 8);
   };
   auto vfrag = [&](int tile, int j) __attribute__((always_inline)) {
-    return *reinterpret_cast<const f16x8*>(v_lds + (tile % kVBufs) * kPrepTileElems + j * 512 + lane * 8);
+    return *reinterpret_cast<const f16x8*>(v_lds + (tile & (kVBufs - 1)) * kPrepTileElems + j * 512 + lane * 8);
   };
 
   f32x16 o[2][4];
@@ -769,53 +782,72 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   f16x8 kr[4];
   f16x8 vr[4];
   // Words of P(i): qb0 words come from the previous phase B, qb1 words from
-  // this phase A.  lsum[qb] are their fp32 row sums (two chains per block).
+  // this phase A.  l0/l1 are their fp32 row sums (two chains per block).
   // Iteration i:
-  //   phase A (8 chunks): S(i+1) MFMAs (qb0, qb1 per K fragment) + P(i) qb1 word j
-  //   phase B (8 chunks): PV(i) MFMAs (qb0, qb1 per V fragment) + P(i+1) qb0 word j
+  //   phase A (8 slot pairs): S(i+1) MFMAs (qb0, then qb1, per K fragment) +
+  //     P(i) qb1 word j
+  //   phase B (8 slot pairs): PV(i) MFMAs (qb0, then qb1, per V fragment) +
+  //     P(i+1) qb0 word j
   auto iteration = [&](int i, f32x16* cs, f32x16* ns, uint32_t* p0_cur, uint32_t* p0_next,
                        float* l0_cur, float* l0_next) __attribute__((always_inline)) {
-    // K tile j sits in buffer j % 5 from its copy (iteration j-4, or the
-    // prologue) to iteration j+1; V tile j in buffer j % 3 from iteration j-2
-    // to iteration j.
+    // K tile j sits in buffer j % 8 from its copy (iteration j-4, or the
+    // prologue) to iteration j+4; V tile j in buffer j % 4 from iteration j-2
+    // to iteration j+2.
     // ---- phase A
     uint32_t p1[8];
-    float l1[2] = {0.0f, 0.0f};
+    float l1[2];
+    float pa = 0.0f, pb = 0.0f;  // the previous pair's probabilities
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
+      // slot 1: S MFMA of block 0; exponential of register 2j; pack and
+      // odd-chain add of word j-1.
       if (kRobust) {
         // The second pass spills; only MFMAs the compiler sees are safe next
         // to its spill code.
         ns[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[0][j], j == 0 ? bias[0] : ns[0], 0, 0, 0);
-        ns[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[1][j], j == 0 ? bias[1] : ns[1], 0, 0, 0);
       } else if (j == 0) {
         mfma_s_first(ns[0], kr[0], qf[0][0], bias[0]);
-        mfma_s_first(ns[1], kr[0], qf[1][0], bias[1]);
       } else {
         mfma_s_next(ns[0], kr[j & 3], qf[0][j]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      float ea = __builtin_amdgcn_exp2f(cs[1][2 * j]);
+      pin(ea);
+      if (j > 0) {
+        p1[j - 1] = pack_f16x2(pa, pb);
+        l1[1] = j == 1 ? pb : l1[1] + pb;
+        pin(p1[j - 1]);
+        pin(l1[1]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // slot 2: S MFMA of block 1; fragment reads; exponential of register
+      // 2j + 1 and even-chain add.
+      if (kRobust) {
+        ns[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[1][j], j == 0 ? bias[1] : ns[1], 0, 0, 0);
+      } else if (j == 0) {
+        mfma_s_first(ns[1], kr[0], qf[1][0], bias[1]);
+      } else {
         mfma_s_next(ns[1], kr[j & 3], qf[1][j]);
       }
+      __builtin_amdgcn_sched_barrier(0);
       if (j < 4) kr[j] = kfrag(i + 1, j + 4);
       if (j >= 5) vr[j - 5] = vfrag(i, j - 5);
-      const float ea = __builtin_amdgcn_exp2f(cs[1][2 * j]);
-      const float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
-      f16x2 h;
-      h[0] = (_Float16)ea;
-      h[1] = (_Float16)eb;
-      p1[j] = __builtin_bit_cast(uint32_t, h);
-      l1[0] += ea;
-      l1[1] += eb;
-      pin(p1[j]);
+      float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
+      pin(eb);
+      l1[0] = j == 0 ? ea : l1[0] + ea;
       pin(l1[0]);
-      pin(l1[1]);
       __builtin_amdgcn_sched_barrier(0);
+      pa = ea;
+      pb = eb;
     }
+    p1[7] = pack_f16x2(pa, pb);
+    l1[1] += pb;
     {
       const float s0 = l0_cur[0] + l0_cur[1], s1 = l1[0] + l1[1];
       if (!kRobust) ovf = fmaxf(ovf, fmaxf(s0, s1));
       if (kRobust && __any(fmaxf(s0, s1) > kP16SumLimit)) {
         // Rare: a score of tile i exceeds m by more than 15.  Per query block:
-        // S(i) again from K(i) (still in its buffer until the next iteration),
+        // S(i) again from K(i) (its buffer is not reused for four iterations),
         // m raised to its max where it exceeds m, O and l rescaled, the next
         // tile's scores moved to the new m, and the words of P(i) redone.
 #pragma unroll
@@ -878,32 +910,50 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // MFMAs, invisible to it, still write or read them.
     mfma_wait();
     asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
-    if (i + 1 < n_kv && (i + 2) * BN2 > N) mask_tile(i + 1, ns);
+    if (__builtin_expect(i + 1 < n_kv && (i + 2) * BN2 > N, 0)) mask_tile(i + 1, ns);
     __builtin_amdgcn_sched_barrier(0);
     // ---- phase B
-    l0_next[0] = l0_next[1] = 0.0f;
+    pa = pb = 0.0f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
+      // slot 1: PV MFMA of block 0; exponential of register 2j of S(i+1)
+      // block 0; pack and odd-chain add of word j-1; a copy block in pairs
+      // 1, 2, 3 and 5.
       o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[0][kst], o[0][db], 0, 0, 0);
-      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[1][kst], o[1][db], 0, 0, 0);
-      if (j + 3 < 8) vr[(j + 3) & 3] = vfrag(i, j + 3);
-      if (j == 1) dma_k(i + 4);  // over K(i-1)
-      if (j == 2) dma_v(i + 2);  // over V(i-1)
-      if (j >= 4) kr[j - 4] = kfrag(i + 2, j - 4);
-      const float ea = __builtin_amdgcn_exp2f(ns[0][2 * j]);
-      const float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
-      f16x2 h;
-      h[0] = (_Float16)ea;
-      h[1] = (_Float16)eb;
-      p0_next[j] = __builtin_bit_cast(uint32_t, h);
-      l0_next[0] += ea;
-      l0_next[1] += eb;
-      pin(p0_next[j]);
-      pin(l0_next[0]);
-      pin(l0_next[1]);
       __builtin_amdgcn_sched_barrier(0);
+      float ea = __builtin_amdgcn_exp2f(ns[0][2 * j]);
+      pin(ea);
+      if (j > 0) {
+        p0_next[j - 1] = pack_f16x2(pa, pb);
+        l0_next[1] = j == 1 ? pb : l0_next[1] + pb;
+        pin(p0_next[j - 1]);
+        pin(l0_next[1]);
+      }
+      if (j == 1) dma_k(i + 4, 0);  // over K(i-4)
+      if (j == 2) dma_v(i + 2, 0);  // over V(i-2)
+      if (j == 3) dma_k(i + 4, 1);
+      if (j == 5) dma_v(i + 2, 1);
+      __builtin_amdgcn_sched_barrier(0);
+      // slot 2: PV MFMA of block 1; the V read ahead, then the K(i+2) read
+      // ahead (the empty statement keeps them in this order: the last four K
+      // reads are the LDS reads the closing barrier leaves in flight);
+      // exponential of register 2j + 1 and even-chain add.
+      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[1][kst], o[1][db], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j + 3 < 8) vr[(j + 3) & 3] = vfrag(i, j + 3);
+      asm volatile("" ::: "memory");
+      if (j >= 4) kr[j - 4] = kfrag(i + 2, j - 4);
+      float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
+      pin(eb);
+      l0_next[0] = j == 0 ? ea : l0_next[0] + ea;
+      pin(l0_next[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      pa = ea;
+      pb = eb;
     }
+    p0_next[7] = pack_f16x2(pa, pb);
+    l0_next[1] += pb;
     // The copies issued in the previous iteration (K(i+3), V(i+1)) must have
     // landed: only this iteration's four may still be in flight.
     dma_barrier();
@@ -911,14 +961,20 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 
   // ---- prologue: K(0..2) and V(0) in LDS, K(3) and V(1) on their way; S(0)
   // against m = its own max; the qb0 words of P(0).
-  dma_k(0);
-  dma_v(0);
-  dma_k(1);
-  dma_k(2);
+  dma_k(0, 0);
+  dma_k(0, 1);
+  dma_v(0, 0);
+  dma_v(0, 1);
+  dma_k(1, 0);
+  dma_k(1, 1);
+  dma_k(2, 0);
+  dma_k(2, 1);
   __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
-  dma_k(3);
-  dma_v(1);
+  dma_k(3, 0);
+  dma_k(3, 1);
+  dma_v(1, 0);
+  dma_v(1, 1);
   // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
   // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
   // such copies.

@@ -1,0 +1,147 @@
+"""Checks on the generated gfx950 code of the prepared-path attention kernel
+(CPU only: hipcc cross-compiles the kernels to assembly).
+
+The first-pass kernel issues its score MFMAs and its LDS tile copies as inline
+assembly, which the compiler's hazard recognizer and register allocator do not
+see.  These tests check the properties that make that safe on the code the
+compiler actually produced:
+  * no instruction reads or overwrites a score MFMA's result registers, or
+    overwrites its accumulator input, within the 12 wait states an 8-pass
+    MFMA needs (no VALU access may fall inside its latency);
+  * the second-pass kernels contain no inline-assembly MFMA at all;
+  * M0, which the copies set without saving it, is used by nothing else.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2609_35110_amd import build as pkg_build
+
+SRC = os.path.join(pkg_build.CSRC, "sol_kernels.hip")
+WAIT_STATES = 12  # an 8-pass XDL MFMA result, VALU read or write
+
+
+@pytest.fixture(scope="module")
+def asm_text(tmp_path_factory):
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    flags = [f for f in pkg_build.HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    out = str(tmp_path_factory.mktemp("asm") / "sol_kernels.s")
+    cmd = [hipcc] + flags + ["--cuda-device-only", "-S", "-I", pkg_build.INCLUDE, "-I", pkg_build.CSRC,
+                             "-x", "hip", SRC, "-o", out]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr[-2000:]
+    return open(out).read()
+
+
+def functions(text, name):
+    """(mangled name, body lines) of every function whose name contains `name`."""
+    out = []
+    for m in re.finditer(r"^(\S*%s\S*):\s*(;.*)?$" % re.escape(name), text, re.M):
+        end = text.index(".Lfunc_end", m.end())
+        out.append((m.group(1), text[m.end():end].split("\n")))
+    return out
+
+
+def instructions(lines):
+    """[(text, in_inline_asm)] without comments, directives and labels."""
+    res, in_asm = [], False
+    for ln in lines:
+        if ";;#ASMSTART" in ln:
+            in_asm = True
+            continue
+        if ";;#ASMEND" in ln:
+            in_asm = False
+            continue
+        t = ln.split(";")[0].strip()
+        if not t or t.startswith(".") or t.endswith(":"):
+            continue
+        res.append((t, in_asm))
+    return res
+
+
+def regs(tok):
+    m = re.match(r"([va])\[(\d+):(\d+)\]$", tok)
+    if m:
+        return {(m.group(1), i) for i in range(int(m.group(2)), int(m.group(3)) + 1)}
+    m = re.match(r"([va])(\d+)$", tok)
+    return {(m.group(1), int(m.group(2)))} if m else set()
+
+
+def operands(t):
+    return [x.strip() for x in t.split(None, 1)[1].split(",")] if " " in t else []
+
+
+STORE_PREFIXES = ("ds_write", "global_store", "buffer_store", "scratch_store", "flat_store")
+
+
+def test_first_pass_score_mfma_latency_respected(asm_text):
+    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if "Lb0EEEv" in f[0]]
+    assert len(kernels) == 2
+    for name, body in kernels:
+        ins = instructions(body)
+        n_asm = 0
+        for i, (t, in_asm) in enumerate(ins):
+            if not (in_asm and t.startswith("v_mfma")):
+                continue
+            n_asm += 1
+            ops = operands(t)
+            dst, srcc = regs(ops[0]), regs(ops[3])
+            ws = 0
+            for t2, _ in ins[i + 1:]:
+                if ws >= WAIT_STATES:
+                    break
+                m = re.match(r"s_nop (\d+)", t2)
+                if m:
+                    ws += int(m.group(1)) + 1
+                    continue
+                ws += 1
+                if t2.startswith("s_"):
+                    continue  # scalar code touches no VGPRs
+                if t2.startswith("v_mfma"):
+                    # a chained MFMA (same accumulator) is interlocked; any
+                    # other use of the result as an operand is not
+                    o2 = operands(t2)
+                    assert not ((regs(o2[1]) | regs(o2[2])) & dst), "%s: %r reads %r" % (name, t2, t)
+                    assert regs(o2[3]) == dst or not (regs(o2[3]) & dst), "%s: %r" % (name, t2)
+                    continue
+                ops2 = operands(t2)
+                if not ops2:
+                    continue
+                if t2.startswith(STORE_PREFIXES):
+                    written, read = set(), set().union(*(regs(x) for x in ops2))
+                else:
+                    written, read = regs(ops2[0]), set().union(set(), *(regs(x) for x in ops2[1:]))
+                assert not (written & (dst | srcc)), "%s: %r overwrites registers of %r" % (name, t2, t)
+                assert not (read & dst), "%s: %r reads the result of %r too early" % (name, t2, t)
+        assert n_asm >= 32, "%s: expected the score MFMAs as inline assembly" % name
+
+
+def test_second_pass_has_no_inline_asm_mfma(asm_text):
+    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if "Lb1EEEv" in f[0]]
+    assert len(kernels) == 2
+    for name, body in kernels:
+        assert not any(in_asm and t.startswith("v_mfma") for t, in_asm in instructions(body)), name
+
+
+def test_m0_used_only_by_tile_copies(asm_text):
+    kernels = functions(asm_text, "attn_prepared_kernel")
+    assert len(kernels) == 4
+    implicit_m0 = ("s_movrel", "v_movrel", "s_sendmsg", "ds_gws", "v_interp", "ds_append", "ds_consume",
+                   "ds_ordered", "s_setreg")
+    for name, body in kernels:
+        ins = instructions(body)
+        copies = 0
+        for i, (t, in_asm) in enumerate(ins):
+            assert not t.startswith(implicit_m0), "%s: %r uses M0" % (name, t)
+            if re.search(r"\bm0\b", t):
+                assert in_asm and re.match(r"s_mov_b32 m0, s\d+$", t), "%s: %r" % (name, t)
+                assert ins[i + 1][0] == "s_nop 0" and ins[i + 2][0].startswith("buffer_load_dwordx4"), name
+            if t.startswith(("buffer_load", "global_load")) and t.endswith(" lds"):
+                assert in_asm and re.match(r"s_mov_b32 m0, s\d+$", ins[i - 2][0]), "%s: %r" % (name, t)
+                copies += 1
+        assert copies >= 12, name
