@@ -590,6 +590,15 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
   h[1] = (_Float16)hi;
   return __builtin_bit_cast(uint32_t, h);
 }
+// Sum of two fp16 pairs, lane-wise (v_pk_add_f16).
+__device__ __forceinline__ uint32_t add_f16x2(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, a) + __builtin_bit_cast(f16x2, b));
+}
+// The two halves of an fp16 pair added in fp32.
+__device__ __forceinline__ float sum_f16x2(uint32_t a) {
+  const f16x2 h = __builtin_bit_cast(f16x2, a);
+  return (float)h[0] + (float)h[1];
+}
 // Keep a value computed where it stands: IR passes would otherwise sink the
 // softmax arithmetic of a chunk to its first use and undo the interleaving.
 __device__ __forceinline__ void pin(uint32_t& x) { asm volatile("" : "+v"(x)); }
@@ -597,13 +606,20 @@ __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
 // End of a prepared-path iteration: all but the last four vector-memory
 // operations of this wave (this iteration's tile copies into LDS) complete,
-// all but its last four LDS reads (the first K(i+2) fragments, from a buffer
-// no copy touches next) complete, then the workgroup barrier -- after which
-// every wave's completed copies are visible and no wave still reads a buffer
-// the next copies overwrite.
+// then the workgroup barrier -- after which every wave's completed copies are
+// visible.  No LDS read needs to complete first: the next iteration's copies
+// overwrite tiles whose fragments every wave read (and waited for) at least
+// one iteration earlier.  The count of four holds only where the compiler
+// issues no memory instruction of its own in the loop (the first pass: a
+// build test checks it); the second pass, whose spill code does, waits for
+// every copy (kAll).
+template <bool kAll>
 __device__ __forceinline__ void dma_barrier() {
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x0474);  // vmcnt 4, expcnt 7, lgkmcnt 4
+  if (kAll)
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt 0, expcnt 7, lgkmcnt 15
+  else
+    __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt 4, expcnt 7, lgkmcnt 15 (no LDS wait)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -626,13 +642,16 @@ __device__ __forceinline__ void dma_barrier() {
 // that runs in its shadow (sched_barrier fences keep the order; two MFMAs in a
 // row would leave the first one's shadow empty):
 //   phase A: S(i+1) = K(i+1) Q'^T - m (16 MFMAs) beside the qb1 half of
-//     P(i) = exp2(S(i)) and its row sums; K fragments are read four MFMA pairs
-//     ahead, the first V(i) fragments during the last pairs;
+//     P(i) = exp2(S(i)), and the reads of K(i+2) into the K fragment
+//     registers as each fragment of K(i+1) is used;
 //   phase B: O^T += V(i)^T P(i)^T (16 MFMAs) beside the qb0 half of P(i+1),
-//     the copies of K(i+4) and V(i+2) into LDS (one 1 KB block in each of four
-//     slots) and the reads of the first K(i+2) fragments for the next phase A.
+//     the reads of V(i+1) into the V fragment registers, and the copies of
+//     K(i+4) and V(i+3) into LDS (one 1 KB block in each of four slots).
 // Each pair of slots packs the previous pair's two probabilities (software
-// pipelined: an exponential is never read by the very next instruction).
+// pipelined: an exponential is never read by the very next instruction).  A
+// row sum is the sum of the fp16 words themselves -- the very probabilities
+// the PV MFMAs multiply -- added as fp16 pairs in a tree of seven
+// v_pk_add_f16 per block and tile, then in fp32 across tiles.
 // LDS holds rings of eight K tiles and four V tiles (96 KB); the barrier that
 // ends an iteration waits only for the copies issued one iteration earlier.
 constexpr int BN2 = kPrepTile;         // keys per tile of the prepared-path kernel
@@ -649,6 +668,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
 
+  // pin() in the first pass only.  The second pass spills, and with the empty
+  // asm statements in place the compiler put a spill reload of an MFMA's
+  // accumulator registers inside that MFMA's latency (seen in the generated
+  // code: the second pass then got whole query blocks wrong); without them its
+  // hazard handling is complete.  A build test checks every MFMA.
+  auto keep = [&](auto& x) __attribute__((always_inline)) {
+    if (!kRobust) pin(x);
+  };
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -777,73 +804,75 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     return fmaxf(mx, __shfl_xor(mx, 32));
   };
   const int n_kv = (N + BN2 - 1) / BN2;
-  // Read-ahead rings: K fragments 4 chunks ahead (kr[kk % 4] holds fragment kk
-  // of the tile being multiplied), V^T fragments 3 chunks ahead (vr[j % 4]).
-  f16x8 kr[4];
-  f16x8 vr[4];
+  // Fragment registers, a whole tile ahead: kr[kk] holds fragment kk of the K
+  // tile being multiplied (then of the next one), vr[j] fragment j of the V
+  // tile (then of the next one).
+  f16x8 kr[8];
+  f16x8 vr[8];
   // Words of P(i): qb0 words come from the previous phase B, qb1 words from
-  // this phase A.  l0/l1 are their fp32 row sums (two chains per block).
+  // this phase A.  l0/l1 are their row sums over the tile.
   // Iteration i:
   //   phase A (8 slot pairs): S(i+1) MFMAs (qb0, then qb1, per K fragment) +
   //     P(i) qb1 word j
   //   phase B (8 slot pairs): PV(i) MFMAs (qb0, then qb1, per V fragment) +
   //     P(i+1) qb0 word j
   auto iteration = [&](int i, f32x16* cs, f32x16* ns, uint32_t* p0_cur, uint32_t* p0_next,
-                       float* l0_cur, float* l0_next) __attribute__((always_inline)) {
-    // K tile j sits in buffer j % 8 from its copy (iteration j-4, or the
-    // prologue) to iteration j+4; V tile j in buffer j % 4 from iteration j-2
-    // to iteration j+2.
+                       float& l0_cur, float& l0_next) __attribute__((always_inline)) {
+    // K tile t sits in buffer t % 8 from its copy (iteration t-4, or the
+    // prologue) to iteration t+4, read in iteration t-2 (and by the second
+    // pass's rare path in iteration t); V tile t in buffer t % 4 from its copy
+    // (iteration t-3) to iteration t+1, read in iteration t-1.
     // ---- phase A
     uint32_t p1[8];
-    float l1[2];
+    float l1;
+    uint32_t t01 = 0, t23 = 0, t03 = 0, t45 = 0;  // fp16 pair sums of the words
     float pa = 0.0f, pb = 0.0f;  // the previous pair's probabilities
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      // slot 1: S MFMA of block 0; exponential of register 2j; pack and
-      // odd-chain add of word j-1.
+      // slot 1: S MFMA of block 0; exponential of register 2j; pack of
+      // word j-1.
       if (kRobust) {
         // The second pass spills; only MFMAs the compiler sees are safe next
         // to its spill code.
-        ns[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[0][j], j == 0 ? bias[0] : ns[0], 0, 0, 0);
+        ns[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j], qf[0][j], j == 0 ? bias[0] : ns[0], 0, 0, 0);
       } else if (j == 0) {
         mfma_s_first(ns[0], kr[0], qf[0][0], bias[0]);
       } else {
-        mfma_s_next(ns[0], kr[j & 3], qf[0][j]);
+        mfma_s_next(ns[0], kr[j], qf[0][j]);
       }
       __builtin_amdgcn_sched_barrier(0);
       float ea = __builtin_amdgcn_exp2f(cs[1][2 * j]);
-      pin(ea);
+      keep(ea);
       if (j > 0) {
         p1[j - 1] = pack_f16x2(pa, pb);
-        l1[1] = j == 1 ? pb : l1[1] + pb;
-        pin(p1[j - 1]);
-        pin(l1[1]);
+        keep(p1[j - 1]);
       }
       __builtin_amdgcn_sched_barrier(0);
-      // slot 2: S MFMA of block 1; fragment reads; exponential of register
-      // 2j + 1 and even-chain add.
+      // slot 2: S MFMA of block 1; fragment kk = j of K(i+2) into the register
+      // just used; exponential of register 2j + 1; a step of the word-sum tree.
       if (kRobust) {
-        ns[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j & 3], qf[1][j], j == 0 ? bias[1] : ns[1], 0, 0, 0);
+        ns[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j], qf[1][j], j == 0 ? bias[1] : ns[1], 0, 0, 0);
       } else if (j == 0) {
         mfma_s_first(ns[1], kr[0], qf[1][0], bias[1]);
       } else {
-        mfma_s_next(ns[1], kr[j & 3], qf[1][j]);
+        mfma_s_next(ns[1], kr[j], qf[1][j]);
       }
       __builtin_amdgcn_sched_barrier(0);
-      if (j < 4) kr[j] = kfrag(i + 1, j + 4);
-      if (j >= 5) vr[j - 5] = vfrag(i, j - 5);
+      kr[j] = kfrag(i + 2, j);
       float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
-      pin(eb);
-      l1[0] = j == 0 ? ea : l1[0] + ea;
-      pin(l1[0]);
+      keep(eb);
+      if (j == 2) { t01 = add_f16x2(p1[0], p1[1]); keep(t01); }
+      if (j == 4) { t23 = add_f16x2(p1[2], p1[3]); keep(t23); }
+      if (j == 5) { t03 = add_f16x2(t01, t23); keep(t03); }
+      if (j == 6) { t45 = add_f16x2(p1[4], p1[5]); keep(t45); }
       __builtin_amdgcn_sched_barrier(0);
       pa = ea;
       pb = eb;
     }
     p1[7] = pack_f16x2(pa, pb);
-    l1[1] += pb;
+    l1 = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p1[6], p1[7]))));
     {
-      const float s0 = l0_cur[0] + l0_cur[1], s1 = l1[0] + l1[1];
+      const float s0 = l0_cur, s1 = l1;
       if (!kRobust) ovf = fmaxf(ovf, fmaxf(s0, s1));
       if (kRobust && __any(fmaxf(s0, s1) > kP16SumLimit)) {
         // Rare: a score of tile i exceeds m by more than 15.  Per query block:
@@ -882,18 +911,13 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
             la += ea;
             lb += eb;
           }
-          if (qb == 0) {
-            l0_cur[0] = la;
-            l0_cur[1] = lb;
-          } else {
-            l1[0] = la;
-            l1[1] = lb;
-          }
+          if (qb == 0) l0_cur = la + lb;
+          else l1 = la + lb;
           mfma_wait();
         }
       }
-      l_run[0] += l0_cur[0] + l0_cur[1];
-      l_run[1] += l1[0] + l1[1];
+      l_run[0] += l0_cur;
+      l_run[1] += l1;
     }
     f16x8 pf[2][2];
 #pragma unroll
@@ -909,58 +933,55 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // iteration) the compiler would otherwise reuse their registers while the
     // MFMAs, invisible to it, still write or read them.
     mfma_wait();
-    asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
+    if (!kRobust) asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
     if (__builtin_expect(i + 1 < n_kv && (i + 2) * BN2 > N, 0)) mask_tile(i + 1, ns);
     __builtin_amdgcn_sched_barrier(0);
     // ---- phase B
     pa = pb = 0.0f;
+    t01 = t23 = t03 = t45 = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
       // slot 1: PV MFMA of block 0; exponential of register 2j of S(i+1)
-      // block 0; pack and odd-chain add of word j-1; a copy block in pairs
-      // 1, 2, 3 and 5.
-      o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[0][kst], o[0][db], 0, 0, 0);
+      // block 0; pack of word j-1; a copy block in pairs 1, 2, 3 and 5.
+      o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j], pf[0][kst], o[0][db], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
       float ea = __builtin_amdgcn_exp2f(ns[0][2 * j]);
-      pin(ea);
+      keep(ea);
       if (j > 0) {
         p0_next[j - 1] = pack_f16x2(pa, pb);
-        l0_next[1] = j == 1 ? pb : l0_next[1] + pb;
-        pin(p0_next[j - 1]);
-        pin(l0_next[1]);
+        keep(p0_next[j - 1]);
       }
       if (j == 1) dma_k(i + 4, 0);  // over K(i-4)
-      if (j == 2) dma_v(i + 2, 0);  // over V(i-2)
+      if (j == 2) dma_v(i + 3, 0);  // over V(i-1), read in iteration i-2
       if (j == 3) dma_k(i + 4, 1);
-      if (j == 5) dma_v(i + 2, 1);
+      if (j == 5) dma_v(i + 3, 1);
       __builtin_amdgcn_sched_barrier(0);
-      // slot 2: PV MFMA of block 1; the V read ahead, then the K(i+2) read
-      // ahead (the empty statement keeps them in this order: the last four K
-      // reads are the LDS reads the closing barrier leaves in flight);
-      // exponential of register 2j + 1 and even-chain add.
-      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j & 3], pf[1][kst], o[1][db], 0, 0, 0);
+      // slot 2: PV MFMA of block 1; fragment j of V(i+1) into the register
+      // just used; exponential of register 2j + 1; a step of the word-sum tree.
+      o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j], pf[1][kst], o[1][db], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
-      if (j + 3 < 8) vr[(j + 3) & 3] = vfrag(i, j + 3);
-      asm volatile("" ::: "memory");
-      if (j >= 4) kr[j - 4] = kfrag(i + 2, j - 4);
+      vr[j] = vfrag(i + 1, j);
       float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
-      pin(eb);
-      l0_next[0] = j == 0 ? ea : l0_next[0] + ea;
-      pin(l0_next[0]);
+      keep(eb);
+      if (j == 2) { t01 = add_f16x2(p0_next[0], p0_next[1]); keep(t01); }
+      if (j == 4) { t23 = add_f16x2(p0_next[2], p0_next[3]); keep(t23); }
+      if (j == 5) { t03 = add_f16x2(t01, t23); keep(t03); }
+      if (j == 6) { t45 = add_f16x2(p0_next[4], p0_next[5]); keep(t45); }
       __builtin_amdgcn_sched_barrier(0);
       pa = ea;
       pb = eb;
     }
     p0_next[7] = pack_f16x2(pa, pb);
-    l0_next[1] += pb;
-    // The copies issued in the previous iteration (K(i+3), V(i+1)) must have
+    l0_next = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p0_next[6], p0_next[7]))));
+    // The copies issued in the previous iteration (K(i+3), V(i+2)) must have
     // landed: only this iteration's four may still be in flight.
-    dma_barrier();
+    dma_barrier<kRobust>();
   };
 
-  // ---- prologue: K(0..2) and V(0) in LDS, K(3) and V(1) on their way; S(0)
-  // against m = its own max; the qb0 words of P(0).
+  // ---- prologue: K(0..2) and V(0..1) in LDS, K(3) and V(2) on their way;
+  // S(0) against m = its own max; the qb0 words of P(0); the fragment
+  // registers loaded with K(1) and V(0).
   dma_k(0, 0);
   dma_k(0, 1);
   dma_v(0, 0);
@@ -969,12 +990,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   dma_k(1, 1);
   dma_k(2, 0);
   dma_k(2, 1);
+  dma_v(1, 0);
+  dma_v(1, 1);
   __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
   dma_k(3, 0);
   dma_k(3, 1);
-  dma_v(1, 0);
-  dma_v(1, 1);
+  dma_v(2, 0);
+  dma_v(2, 1);
   // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
   // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
   // such copies.
@@ -998,20 +1021,24 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
   }
   uint32_t pA[8], pB[8];
-  float lA[2] = {0.0f, 0.0f}, lB[2] = {0.0f, 0.0f};
+  float lA = 0.0f, lB = 0.0f;
+  {
+    float la = 0.0f, lb = 0.0f;
 #pragma unroll
-  for (int w = 0; w < 8; ++w) {
-    const float ea = __builtin_amdgcn_exp2f(sa[0][2 * w]);
-    const float eb = __builtin_amdgcn_exp2f(sa[0][2 * w + 1]);
-    f16x2 h;
-    h[0] = (_Float16)ea;
-    h[1] = (_Float16)eb;
-    pA[w] = __builtin_bit_cast(uint32_t, h);
-    lA[0] += ea;
-    lA[1] += eb;
+    for (int w = 0; w < 8; ++w) {
+      const float ea = __builtin_amdgcn_exp2f(sa[0][2 * w]);
+      const float eb = __builtin_amdgcn_exp2f(sa[0][2 * w + 1]);
+      pA[w] = pack_f16x2(ea, eb);
+      la += ea;
+      lb += eb;
+    }
+    lA = la + lb;
   }
 #pragma unroll
-  for (int t = 0; t < 4; ++t) kr[t] = kfrag(1, t);
+  for (int t = 0; t < 8; ++t) {
+    kr[t] = kfrag(1, t);
+    vr[t] = vfrag(0, t);
+  }
   mfma_wait();
 
   int i = 0;

@@ -5,9 +5,9 @@ The first-pass kernel issues its score MFMAs and its LDS tile copies as inline
 assembly, which the compiler's hazard recognizer and register allocator do not
 see.  These tests check the properties that make that safe on the code the
 compiler actually produced:
-  * no instruction reads or overwrites a score MFMA's result registers, or
+  * no instruction reads or overwrites an MFMA's result registers, or
     overwrites its accumulator input, within the 12 wait states an 8-pass
-    MFMA needs (no VALU access may fall inside its latency);
+    MFMA needs -- for the inline MFMAs and the compiler's own alike;
   * the second-pass kernels contain no inline-assembly MFMA at all;
   * M0, which the copies set without saving it, is used by nothing else.
 """
@@ -79,16 +79,19 @@ def operands(t):
 STORE_PREFIXES = ("ds_write", "global_store", "buffer_store", "scratch_store", "flat_store")
 
 
-def test_first_pass_score_mfma_latency_respected(asm_text):
-    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if "Lb0EEEv" in f[0]]
-    assert len(kernels) == 2
+def test_mfma_latency_respected(asm_text):
+    """Every MFMA of the four kernels, inline or not: the compiler's own
+    hazard handling is checked too (it once let a spill reload overwrite an
+    accumulator still being read)."""
+    kernels = functions(asm_text, "attn_prepared_kernel")
+    assert len(kernels) == 4
     for name, body in kernels:
         ins = instructions(body)
         n_asm = 0
         for i, (t, in_asm) in enumerate(ins):
-            if not (in_asm and t.startswith("v_mfma")):
+            if not t.startswith("v_mfma"):
                 continue
-            n_asm += 1
+            n_asm += in_asm
             ops = operands(t)
             dst, srcc = regs(ops[0]), regs(ops[3])
             ws = 0
@@ -114,11 +117,14 @@ def test_first_pass_score_mfma_latency_respected(asm_text):
                     continue
                 if t2.startswith(STORE_PREFIXES):
                     written, read = set(), set().union(*(regs(x) for x in ops2))
+                elif t2.endswith(" lds"):  # a copy into LDS: its operand is an address
+                    written, read = set(), set().union(*(regs(x) for x in ops2))
                 else:
                     written, read = regs(ops2[0]), set().union(set(), *(regs(x) for x in ops2[1:]))
                 assert not (written & (dst | srcc)), "%s: %r overwrites registers of %r" % (name, t2, t)
                 assert not (read & dst), "%s: %r reads the result of %r too early" % (name, t2, t)
-        assert n_asm >= 32, "%s: expected the score MFMAs as inline assembly" % name
+        if "Lb0EEEv" in name:
+            assert n_asm >= 32, "%s: expected the score MFMAs as inline assembly" % name
 
 
 def test_second_pass_has_no_inline_asm_mfma(asm_text):
@@ -145,3 +151,24 @@ def test_m0_used_only_by_tile_copies(asm_text):
                 assert in_asm and re.match(r"s_mov_b32 m0, s\d+$", ins[i - 2][0]), "%s: %r" % (name, t)
                 copies += 1
         assert copies >= 12, name
+
+
+def test_first_pass_copy_count_waits_see_only_copies(asm_text):
+    """The closing barrier's vmcnt(4) assumes the last four vector-memory
+    instructions of the wave are its tile copies: between two such waits the
+    compiler must issue no load, store or spill of its own."""
+    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if "Lb0EEEv" in f[0]]
+    for name, body in kernels:
+        ins = instructions(body)
+        assert not any(t.startswith("scratch_") for t, _ in ins), "%s spills" % name
+        since, n_waits = [], 0
+        for t, in_asm in ins:
+            if t.startswith(("buffer_", "global_", "flat_")):
+                since.append((t, in_asm))
+            if t.startswith("s_waitcnt") and "vmcnt" in t:
+                if "vmcnt(4)" in t:
+                    n_waits += 1
+                    others = [x for x, a in since if not (a and x.endswith(" lds"))]
+                    assert not others, "%s: %r before a copy-count wait" % (name, others[:3])
+                since = []
+        assert n_waits >= 2, name
