@@ -583,6 +583,8 @@ __device__ __forceinline__ void mfma_s_next(f32x16& d, const f16x8& k, const f16
 // 16 wait states: more than the 12 an 8-pass MFMA result needs before the VALU
 // reads or overwrites it.
 __device__ __forceinline__ void mfma_wait() { asm volatile("s_nop 7\n\ts_nop 7" ::: "memory"); }
+// 4 wait states, after a dozen independent instructions have already issued.
+__device__ __forceinline__ void mfma_wait_tail() { asm volatile("s_nop 3" ::: "memory"); }
 // Two fp32 values as an fp16 pair (RNE), the low half first.
 __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
   f16x2 h;
@@ -918,7 +920,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       }
       l_run[0] += l0_cur;
       l_run[1] += l1;
+      keep(l_run[0]);
+      keep(l_run[1]);
+      if (!kRobust) keep(ovf);
     }
+    // The tail above runs in the shadow of the last score MFMAs and counts
+    // toward their latency (pinned here: the compiler would otherwise sink it
+    // past the branch below).
+    __builtin_amdgcn_sched_barrier(0);
     f16x8 pf[2][2];
 #pragma unroll
     for (int kst = 0; kst < 2; ++kst) {
@@ -927,14 +936,19 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       pf[1][kst] = __builtin_bit_cast(f16x8, make_uint4(p1[4 * kst], p1[4 * kst + 1],
                                                         p1[4 * kst + 2], p1[4 * kst + 3]));
     }
-    // S(i+1) is read by the VALU from here on: its MFMAs must have landed, and
-    // a ragged last tile is masked first.  The empty statement keeps the score
-    // MFMAs' results and srcC live up to here: where they are dead (the last
-    // iteration) the compiler would otherwise reuse their registers while the
-    // MFMAs, invisible to it, still write or read them.
-    mfma_wait();
+    // S(i+1) is read by the VALU from here on: its MFMAs must have landed (the
+    // tail above and these wait states make the 12 an 8-pass result needs; a
+    // build test checks the count), and a ragged last tile is masked first.
+    // The empty statement keeps the score MFMAs' results and srcC live up to
+    // here: where they are dead (the last iteration) the compiler would
+    // otherwise reuse their registers while the MFMAs, invisible to it, still
+    // write or read them.
+    mfma_wait_tail();
     if (!kRobust) asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
-    if (__builtin_expect(i + 1 < n_kv && (i + 2) * BN2 > N, 0)) mask_tile(i + 1, ns);
+    if (__builtin_expect(i + 1 < n_kv && (i + 2) * BN2 > N, 0)) {
+      mfma_wait();
+      mask_tile(i + 1, ns);
+    }
     __builtin_amdgcn_sched_barrier(0);
     // ---- phase B
     pa = pb = 0.0f;
@@ -974,6 +988,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
     p0_next[7] = pack_f16x2(pa, pb);
     l0_next = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p0_next[6], p0_next[7]))));
+    keep(p0_next[7]);
+    keep(l0_next);
     // The copies issued in the previous iteration (K(i+3), V(i+2)) must have
     // landed: only this iteration's four may still be in flight.
     dma_barrier<kRobust>();
