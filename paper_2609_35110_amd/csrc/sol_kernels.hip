@@ -861,12 +861,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       }
       __builtin_amdgcn_sched_barrier(0);
       kr[j] = kfrag(i + 2, j);
-      float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
-      keep(eb);
       if (j == 2) { t01 = add_f16x2(p1[0], p1[1]); keep(t01); }
       if (j == 4) { t23 = add_f16x2(p1[2], p1[3]); keep(t23); }
       if (j == 5) { t03 = add_f16x2(t01, t23); keep(t03); }
       if (j == 6) { t45 = add_f16x2(p1[4], p1[5]); keep(t45); }
+      float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
+      keep(eb);
       __builtin_amdgcn_sched_barrier(0);
       pa = ea;
       pb = eb;
@@ -976,12 +976,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j], pf[1][kst], o[1][db], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
       vr[j] = vfrag(i + 1, j);
-      float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
-      keep(eb);
       if (j == 2) { t01 = add_f16x2(p0_next[0], p0_next[1]); keep(t01); }
       if (j == 4) { t23 = add_f16x2(p0_next[2], p0_next[3]); keep(t23); }
       if (j == 5) { t03 = add_f16x2(t01, t23); keep(t03); }
       if (j == 6) { t45 = add_f16x2(p0_next[4], p0_next[5]); keep(t45); }
+      float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
+      keep(eb);
       __builtin_amdgcn_sched_barrier(0);
       pa = ea;
       pb = eb;
