@@ -81,6 +81,14 @@ def nearest_bf16(x):
     return np.take_along_axis(cands, idx[..., None], axis=-1)[..., 0]
 
 
+def rms_norm_np(x, gamma, eps):
+    """x / sqrt(mean(x^2) + eps) * gamma over the last axis (the head's D
+    entries), float64: the QK normalization of Sec. 3.5's fusion group 2."""
+    x = np.asarray(x, dtype=np.float64)
+    ms = np.mean(np.square(x), axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * np.asarray(gamma, dtype=np.float64)
+
+
 def attention_np(qh, kh, v):
     """softmax(qh kh^T / sqrt(D)) v over the last two axes, float64, materialised."""
     D = qh.shape[-1]
@@ -89,16 +97,35 @@ def attention_np(qh, kh, v):
     return np.matmul(p, v), p
 
 
-def fused_reference(q_bits, k_bits, v_bits, T, Hl, Wl, contract=True,
-                    split=(32, 48, 48), base=10000.0):
-    """The whole path on [B, H, N, D] bf16 bits: rotate q, k (rounding once to
-    bf16 in contract mode), then exact attention.  Returns (out, probs)."""
-    q = bf16_bits_to_f64(q_bits)
-    k = bf16_bits_to_f64(k_bits)
-    v = bf16_bits_to_f64(v_bits)
-    N, D = q.shape[-2], q.shape[-1]
-    ang = rope_angles(grid_positions(N, T, Hl, Wl), D, split, base)
-    qh, kh = rope_np(q, ang), rope_np(k, ang)
+def prepare_np(x_bits, T, Hl, Wl, gamma=None, eps=0.0, rope=True, contract=True,
+               split=(32, 48, 48), base=10000.0):
+    """One side (queries or keys) of the path on bf16 bits [..., N, D]: optional
+    RMS normalisation, then the rotation, then (contract) one bf16 rounding of
+    every row that was changed.  float64 out."""
+    x = bf16_bits_to_f64(x_bits)
+    N, D = x.shape[-2], x.shape[-1]
+    changed = np.zeros(N, dtype=bool)
+    if gamma is not None:
+        x = rms_norm_np(x, gamma, eps)
+        changed[:] = True
+    if rope:
+        pos = grid_positions(N, T, Hl, Wl)
+        x = rope_np(x, rope_angles(pos, D, split, base))
+        changed |= pos[:, 0] >= 0
     if contract:
-        qh, kh = nearest_bf16(qh), nearest_bf16(kh)
+        x = np.where(changed[:, None], nearest_bf16(x), x)
+    return x
+
+
+def fused_reference(q_bits, k_bits, v_bits, T, Hl, Wl, contract=True,
+                    split=(32, 48, 48), base=10000.0, q_gamma=None, k_gamma=None, eps=0.0,
+                    kv_grid=None, rope_k=True):
+    """The whole path on bf16 bits q [B, H, Nq, D], k, v [B, H, Nkv, D]:
+    normalise (when a gamma is given) and rotate q and k (rounding once to bf16
+    in contract mode), then exact attention.  The keys use kv_grid when given,
+    else the queries' grid.  Returns (out, probs)."""
+    v = bf16_bits_to_f64(v_bits)
+    Tk, Hlk, Wlk = kv_grid if kv_grid is not None else (T, Hl, Wl)
+    qh = prepare_np(q_bits, T, Hl, Wl, q_gamma, eps, True, contract, split, base)
+    kh = prepare_np(k_bits, Tk, Hlk, Wlk, k_gamma, eps, rope_k, contract, split, base)
     return attention_np(qh, kh, v)

@@ -12,8 +12,13 @@
  *   attention collectives": the SDPA term that dominates the denoising step;
  *   Sec. 3.4: its cost grows with the square of the token count) applied to
  *   queries and keys that first pass through the partial/3D rotary embedding
- *   of Sec. 3.5 (fusion group 2, "QK normalization with partial RoPE"; the
- *   normalization half is not part of this path).
+ *   of Sec. 3.5 (fusion group 2, "QK normalization with partial RoPE").  The
+ *   normalization half is optional: when a weight vector gamma is given, each
+ *   head's D-vector is first RMS-normalised,
+ *     x <- gamma * x / sqrt(mean_d(x_d^2) + eps),
+ *   over every token (prefix included), then rotated; the bf16 input is the
+ *   rounding point the paper keeps ahead of QK normalization (Sec. 3.5,
+ *   "LoRA fusion"), and nothing is rounded between normalization and rotation.
  *
  *   Sequence packing (Sec. 3.4 "Safety rails"): the Nt = N - T*Hl*Wl leading
  *   tokens are a prefix (text) that is not rotated; token n >= Nt is the
@@ -25,9 +30,10 @@
  *   width d, the pair (2i, 2i+1) is the complex number x_{2i} + j x_{2i+1},
  *   multiplied by exp(j * pos * base^(-2i/d)).
  *
- *   Rounding point ("contract" mode, the default): the rotated q and k are
- *   rounded to bf16 (round to nearest, ties to even) once, as any bf16 matrix
- *   unit must consume them.  contract = 0 keeps them in double (diagnostic).
+ *   Rounding point ("contract" mode, the default): the rotated (and, with
+ *   gamma, normalised) q and k are rounded to bf16 (round to nearest, ties to
+ *   even) once, as any bf16 matrix unit must consume them.  contract = 0 keeps
+ *   them in double (diagnostic).
  *
  *   Attention per (b, h, query i), the plain two-pass definition:
  *     s_j = <q_i, k_j> / sqrt(D)               for every key j < N
@@ -87,6 +93,7 @@ void solref_round_bf16(const double* x, uint16_t* y, int64_t n) {
 static int token_position(int64_t n, int N, int T, int Hl, int Wl, int* pt, int* ph, int* pw) {
   int64_t nv = (int64_t)T * Hl * Wl;
   int64_t nt = (int64_t)N - nv;
+  if (nv == 0) return 0; /* empty grid: every token is prefix */
   if (n < nt) return 0;
   int64_t r = n - nt;
   *pt = (int)(r / ((int64_t)Hl * Wl));
@@ -118,18 +125,35 @@ static void rotate_vector(double* x, int D, int dt, int dh, int dw, double base,
   (void)D;
 }
 
-/* Rotate rows of a bf16 tensor [BH][N][D] and write doubles.  If contract,
- * the rotated values are rounded to bf16 (then widened back, exactly). */
+/* RMS normalisation of one D-vector (in place, double): the root mean square
+ * over the head's D entries, eps added under the root, then the per-dimension
+ * weight gamma[d]. */
+static void rms_normalize(double* x, int D, const double* gamma, double eps) {
+  double ss = 0.0;
+  for (int d = 0; d < D; ++d) ss += x[d] * x[d];
+  const double inv = 1.0 / sqrt(ss / (double)D + eps);
+  for (int d = 0; d < D; ++d) x[d] = x[d] * inv * gamma[d];
+}
+
+/* One row of a bf16 tensor [BH][N][D] -> doubles: normalised first when gamma
+ * is given, then rotated.  If contract and either step changed the row, the
+ * result is rounded to bf16 (then widened back, exactly). */
 static void rotate_row(const uint16_t* src, double* dst, int64_t n, int N, int D,
                        int T, int Hl, int Wl, int dt, int dh, int dw, double base,
-                       int use_rope, int contract) {
+                       int use_rope, int contract, const double* gamma, double eps) {
   for (int d = 0; d < D; ++d) dst[d] = bf16_to_double(src[d]);
+  int changed = 0;
+  if (gamma) {
+    rms_normalize(dst, D, gamma, eps);
+    changed = 1;
+  }
   int pt, ph, pw;
   if (use_rope && token_position(n, N, T, Hl, Wl, &pt, &ph, &pw)) {
     rotate_vector(dst, D, dt, dh, dw, base, pt, ph, pw);
-    if (contract)
-      for (int d = 0; d < D; ++d) dst[d] = bf16_to_double(double_to_bf16(dst[d]));
+    changed = 1;
   }
+  if (contract && changed)
+    for (int d = 0; d < D; ++d) dst[d] = bf16_to_double(double_to_bf16(dst[d]));
 }
 
 /* Rotation in double, no rounding: x, y are double [rows][D]; row r is token r mod N. */
@@ -150,21 +174,49 @@ void solref_rope3d(const uint16_t* x, uint16_t* y, int64_t rows, int N, int D,
   double* buf = (double*)malloc(sizeof(double) * (size_t)D);
   for (int64_t r = 0; r < rows; ++r) {
     int64_t n = r % N;
-    rotate_row(x + r * D, buf, n, N, D, T, Hl, Wl, dt, dh, dw, base, 1, 0);
+    rotate_row(x + r * D, buf, n, N, D, T, Hl, Wl, dt, dh, dw, base, 1, 0, NULL, 0.0);
     for (int d = 0; d < D; ++d) y[r * D + d] = double_to_bf16(buf[d]);
+  }
+  free(buf);
+}
+
+/* Contract-mode QK normalisation + rotation of a bf16 tensor: normalise with
+ * gamma[D] and eps, rotate, all in double, round once to bf16.  rope = 0
+ * normalises only.  contract = 0 writes the doubles to yf (diagnostic) and
+ * leaves y untouched; y or yf may be NULL when unused. */
+void solref_qknorm_rope3d(const uint16_t* x, uint16_t* y, double* yf, int64_t rows, int N, int D,
+                          int T, int Hl, int Wl, int dt, int dh, int dw, double base, int rope,
+                          const double* gamma, double eps, int contract) {
+  double* buf = (double*)malloc(sizeof(double) * (size_t)D);
+  for (int64_t r = 0; r < rows; ++r) {
+    int64_t n = r % N;
+    rotate_row(x + r * D, buf, n, N, D, T, Hl, Wl, dt, dh, dw, base, rope, 0, gamma, eps);
+    for (int d = 0; d < D; ++d) {
+      if (contract) y[r * D + d] = double_to_bf16(buf[d]);
+      else yf[r * D + d] = buf[d];
+    }
   }
   free(buf);
 }
 
 /* ------------------------------------------------------------------ attention */
 
+/* Where the rows of one side (queries, or keys and values) sit in their
+ * sequence, and what is done to them before the products. */
+typedef struct {
+  int N, T, Hl, Wl;       /* sequence length and latent grid (prefix = N - T*Hl*Wl) */
+  int rope;               /* rotate (3D rotary embedding) */
+  const double* gamma;    /* RMS-normalise with these D weights first, or NULL */
+} side_t;
+
 typedef struct {
   /* one (b,h) slab */
-  const uint16_t* q;      /* [N][D] */
-  const double* khat;     /* [N][D] rotated keys */
-  const double* vd;       /* [N][D] */
-  int N, D, T, Hl, Wl, dt, dh, dw, use_rope, contract;
-  double base;
+  const uint16_t* q;      /* [Nq][D] */
+  const double* khat;     /* [Nkv][D] prepared keys */
+  const double* vd;       /* [Nkv][D] */
+  side_t qs;
+  int Nkv, D, dt, dh, dw, contract;
+  double base, eps;
   const int64_t* qrows;   /* query indices within the slab */
   float* out;             /* [nq][D] */
   int64_t nq;
@@ -173,14 +225,14 @@ typedef struct {
 } slab_job;
 
 static void attend_one(slab_job* J, int64_t idx, double* s, double* qhat, double* acc) {
-  const int N = J->N, D = J->D;
+  const int Nkv = J->Nkv, D = J->D;
   int64_t i = J->qrows[idx];
-  rotate_row(J->q + i * D, qhat, i, N, D, J->T, J->Hl, J->Wl, J->dt, J->dh, J->dw, J->base,
-             J->use_rope, J->contract);
+  rotate_row(J->q + i * D, qhat, i, J->qs.N, D, J->qs.T, J->qs.Hl, J->qs.Wl, J->dt, J->dh, J->dw,
+             J->base, J->qs.rope, J->contract, J->qs.gamma, J->eps);
   const double scale = 1.0 / sqrt((double)D);
   /* pass 1: logits and their maximum */
   double m = -INFINITY;
-  for (int j = 0; j < N; ++j) {
+  for (int j = 0; j < Nkv; ++j) {
     const double* kj = J->khat + (int64_t)j * D;
     double dot = 0.0;
     for (int d = 0; d < D; ++d) dot += qhat[d] * kj[d];
@@ -190,7 +242,7 @@ static void attend_one(slab_job* J, int64_t idx, double* s, double* qhat, double
   /* pass 2: exponentials, normaliser, weighted sum of values */
   double l = 0.0;
   for (int d = 0; d < D; ++d) acc[d] = 0.0;
-  for (int j = 0; j < N; ++j) {
+  for (int j = 0; j < Nkv; ++j) {
     double p = exp(s[j] - m);
     l += p;
     const double* vj = J->vd + (int64_t)j * D;
@@ -205,25 +257,26 @@ typedef struct {
   const uint16_t* vs;
   double* khat;
   double* vd;
-  int N, D, T, Hl, Wl, dt, dh, dw, use_rope, contract;
-  double base;
+  side_t kside;
+  int D, dt, dh, dw, contract;
+  double base, eps;
   int64_t next;
   pthread_mutex_t lock;
 } keys_job;
 
 static void* keys_worker(void* arg) {
   keys_job* J = (keys_job*)arg;
-  const int D = J->D;
+  const int D = J->D, N = J->kside.N;
   for (;;) {
     pthread_mutex_lock(&J->lock);
     int64_t j0 = J->next;
     J->next += 256;
     pthread_mutex_unlock(&J->lock);
-    if (j0 >= J->N) break;
-    int64_t j1 = j0 + 256 < J->N ? j0 + 256 : J->N;
+    if (j0 >= N) break;
+    int64_t j1 = j0 + 256 < N ? j0 + 256 : N;
     for (int64_t j = j0; j < j1; ++j) {
-      rotate_row(J->ks + j * D, J->khat + j * D, j, J->N, D, J->T, J->Hl, J->Wl, J->dt, J->dh,
-                 J->dw, J->base, J->use_rope, J->contract);
+      rotate_row(J->ks + j * D, J->khat + j * D, j, N, D, J->kside.T, J->kside.Hl, J->kside.Wl,
+                 J->dt, J->dh, J->dw, J->base, J->kside.rope, J->contract, J->kside.gamma, J->eps);
       for (int d = 0; d < D; ++d) J->vd[j * D + d] = bf16_to_double(J->vs[j * D + d]);
     }
   }
@@ -232,7 +285,7 @@ static void* keys_worker(void* arg) {
 
 static void* slab_worker(void* arg) {
   slab_job* J = (slab_job*)arg;
-  double* s = (double*)malloc(sizeof(double) * (size_t)J->N);
+  double* s = (double*)malloc(sizeof(double) * (size_t)J->Nkv);
   double* qhat = (double*)malloc(sizeof(double) * (size_t)J->D);
   double* acc = (double*)malloc(sizeof(double) * (size_t)J->D);
   for (;;) {
@@ -254,68 +307,85 @@ int solref_num_threads(void) {
   return 1;
 }
 
+static int bad_side(const side_t* s, int D, int dt, int dh, int dw) {
+  if (s->N < 1) return 1;
+  if (s->rope && ((int64_t)s->T * s->Hl * s->Wl > s->N || dt + dh + dw > D || s->T < 0 ||
+                  s->Hl < 0 || s->Wl < 0))
+    return 1;
+  return 0;
+}
+
 /*
- * Attention output for selected query rows.
- *   q,k,v    : bf16 bits [B][H][N][D]
- *   rows     : global row ids r = (b*H + h)*N + i, grouped by (b,h) in any order
- *   out      : float [nrows][D], row k is the output for rows[k]
- *   use_rope : 0 = plain attention (no rotation anywhere)
- *   nthreads : <= 0 means every CPU in the affinity mask
+ * Attention output for selected query rows, queries and keys of any lengths.
+ *   q          : bf16 bits [B][H][Nq][D];  k, v : bf16 bits [B][H][Nkv][D]
+ *   q side     : grid Tq x Hlq x Wlq of the Nq queries, rotated if rope_q,
+ *                RMS-normalised first with q_gamma[D] if it is not NULL
+ *   k side     : likewise for the Nkv keys (grid Tk x Hlk x Wlk, rope_k,
+ *                k_gamma); values are never changed
+ *   eps        : added under the root of every RMS normalisation
+ *   rows       : global row ids r = (b*H + h)*Nq + i, grouped by (b,h) in any order
+ *   out        : float [nrows][D], row k is the output for rows[k]
+ *   nthreads   : <= 0 means every CPU in the affinity mask
  * Returns 0, or -1 on bad arguments / allocation failure.
  */
-int solref_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                     int B, int H, int N, int D, int T, int Hl, int Wl,
-                     int dt, int dh, int dw, double base, int use_rope, int contract,
-                     const int64_t* rows, int64_t nrows, float* out, int nthreads) {
-  if (B < 1 || H < 1 || N < 1 || D < 2 || !q || !k || !v || !out || (nrows > 0 && !rows)) return -1;
-  if (use_rope && ((int64_t)T * Hl * Wl > N || dt + dh + dw > D || T < 0 || Hl < 0 || Wl < 0)) return -1;
+int solref_attn_rows_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int H,
+                        int Nq, int Nkv, int D, int Tq, int Hlq, int Wlq, int Tk, int Hlk, int Wlk,
+                        int dt, int dh, int dw, double base, int rope_q, int rope_k, int contract,
+                        const double* q_gamma, const double* k_gamma, double eps,
+                        const int64_t* rows, int64_t nrows, float* out, int nthreads) {
+  const side_t qs = {Nq, Tq, Hlq, Wlq, rope_q, q_gamma};
+  const side_t ks = {Nkv, Tk, Hlk, Wlk, rope_k, k_gamma};
+  if (B < 1 || H < 1 || D < 2 || !q || !k || !v || !out || (nrows > 0 && !rows)) return -1;
+  if (bad_side(&qs, D, dt, dh, dw) || bad_side(&ks, D, dt, dh, dw) || !(eps >= 0.0)) return -1;
   if (nthreads <= 0) nthreads = solref_num_threads();
-  const int64_t slab = (int64_t)N * D;
+  const int64_t qslab = (int64_t)Nq * D, kslab = (int64_t)Nkv * D;
   int64_t* qrows = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nrows > 0 ? nrows : 1));
   int64_t* where = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nrows > 0 ? nrows : 1));
   float* obuf = (float*)malloc(sizeof(float) * (size_t)(nrows > 0 ? nrows : 1) * D);
-  double* khat = (double*)malloc(sizeof(double) * (size_t)slab);
-  double* vd = (double*)malloc(sizeof(double) * (size_t)slab);
+  double* khat = (double*)malloc(sizeof(double) * (size_t)kslab);
+  double* vd = (double*)malloc(sizeof(double) * (size_t)kslab);
   pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
   if (!qrows || !where || !obuf || !khat || !vd || !th) {
     free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
     return -1;
   }
+  for (int64_t r = 0; r < nrows; ++r) {
+    if (rows[r] < 0 || rows[r] >= (int64_t)B * H * Nq) {
+      free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
+      return -1;
+    }
+  }
   for (int64_t bh = 0; bh < (int64_t)B * H; ++bh) {
     /* collect the requested rows of this slab */
     int64_t nq = 0;
     for (int64_t r = 0; r < nrows; ++r) {
-      if (rows[r] < 0 || rows[r] >= (int64_t)B * H * N) {
-        free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
-        return -1;
-      }
-      if (rows[r] / N == bh) {
-        qrows[nq] = rows[r] % N;
+      if (rows[r] / Nq == bh) {
+        qrows[nq] = rows[r] % Nq;
         where[nq] = r;
         ++nq;
       }
     }
     if (nq == 0) continue;
     keys_job K;
-    K.ks = k + bh * slab;
-    K.vs = v + bh * slab;
+    K.ks = k + bh * kslab;
+    K.vs = v + bh * kslab;
     K.khat = khat;
     K.vd = vd;
-    K.N = N; K.D = D; K.T = T; K.Hl = Hl; K.Wl = Wl;
-    K.dt = dt; K.dh = dh; K.dw = dw; K.base = base;
-    K.use_rope = use_rope; K.contract = contract;
+    K.kside = ks;
+    K.D = D; K.dt = dt; K.dh = dh; K.dw = dw; K.base = base; K.eps = eps;
+    K.contract = contract;
     K.next = 0;
     pthread_mutex_init(&K.lock, NULL);
     for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, keys_worker, &K);
     for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
     pthread_mutex_destroy(&K.lock);
     slab_job J;
-    J.q = q + bh * slab;
+    J.q = q + bh * qslab;
     J.khat = khat;
     J.vd = vd;
-    J.N = N; J.D = D; J.T = T; J.Hl = Hl; J.Wl = Wl;
-    J.dt = dt; J.dh = dh; J.dw = dw; J.base = base;
-    J.use_rope = use_rope; J.contract = contract;
+    J.qs = qs;
+    J.Nkv = Nkv; J.D = D; J.dt = dt; J.dh = dh; J.dw = dw; J.base = base; J.eps = eps;
+    J.contract = contract;
     J.qrows = qrows;
     J.out = obuf;
     J.nq = nq;
@@ -329,4 +399,15 @@ int solref_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
   }
   free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
   return 0;
+}
+
+/* Self-attention of one sequence (queries and keys the same N tokens, one
+ * grid, no normalisation): solref_attn_rows_ex with both sides alike. */
+int solref_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                     int B, int H, int N, int D, int T, int Hl, int Wl,
+                     int dt, int dh, int dw, double base, int use_rope, int contract,
+                     const int64_t* rows, int64_t nrows, float* out, int nthreads) {
+  return solref_attn_rows_ex(q, k, v, B, H, N, N, D, T, Hl, Wl, T, Hl, Wl, dt, dh, dw, base,
+                             use_rope, use_rope, contract, NULL, NULL, 0.0, rows, nrows, out,
+                             nthreads);
 }

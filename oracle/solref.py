@@ -44,6 +44,13 @@ class Oracle:
         lib.solref_attn_rows.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
                                          i32, i32, i32, f64, i32, i32, P, i64, P, i32]
         lib.solref_attn_rows.restype = ctypes.c_int
+        lib.solref_attn_rows_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
+                                            i32, i32, i32, i32, i32, i32, f64, i32, i32, i32,
+                                            P, P, f64, P, i64, P, i32]
+        lib.solref_attn_rows_ex.restype = ctypes.c_int
+        lib.solref_qknorm_rope3d.argtypes = [P, P, P, i64, i32, i32, i32, i32, i32, i32, i32,
+                                             i32, f64, i32, P, f64, i32]
+        lib.solref_qknorm_rope3d.restype = None
         lib.solref_num_threads.argtypes = []
         lib.solref_num_threads.restype = ctypes.c_int
         self.lib = lib
@@ -78,30 +85,71 @@ class Oracle:
                                split[0], split[1], split[2], base)
         return y
 
+    def qknorm_rope3d(self, x_bits, T, Hl, Wl, gamma, eps, rope=True, contract=True,
+                      split=DEFAULT_SPLIT, base=ROPE_BASE) -> np.ndarray:
+        """RMS normalisation with weights gamma[D] and eps, then (if rope) the
+        3D rotation, of bf16 bits x[..., N, D], all in double.  contract: round
+        once to bf16 (uint16 bits out); else float64 out."""
+        x = _u16(x_bits)
+        N, D = x.shape[-2], x.shape[-1]
+        g = np.ascontiguousarray(gamma, dtype=np.float64)
+        if g.shape != (D,):
+            raise ValueError("gamma must hold D = %d weights" % D)
+        if contract:
+            y, yf = np.empty_like(x), None
+        else:
+            y, yf = None, np.empty(x.shape, dtype=np.float64)
+        self.lib.solref_qknorm_rope3d(_ptr(x), None if y is None else _ptr(y),
+                                      None if yf is None else _ptr(yf), x.size // D, N, D, T, Hl,
+                                      Wl, split[0], split[1], split[2], base, int(bool(rope)),
+                                      _ptr(g), float(eps), int(bool(contract)))
+        return y if contract else yf
+
     def attn_rows(self, q, k, v, T, Hl, Wl, rows=None, rope=True, contract=True,
-                  split=DEFAULT_SPLIT, base=ROPE_BASE, threads=0) -> np.ndarray:
+                  split=DEFAULT_SPLIT, base=ROPE_BASE, threads=0, q_gamma=None, k_gamma=None,
+                  eps=0.0, kv_grid=None, rope_k=None) -> np.ndarray:
         """Attention output (float32) for selected global query rows.
 
-        q, k, v : uint16 bf16 bits, [B, H, N, D]
-        rows    : int64 global row ids (b*H + h)*N + i; None = every row
-        returns : float32 [len(rows), D] (or [B, H, N, D] when rows is None)
+        q       : uint16 bf16 bits, [B, H, Nq, D]; k, v: [B, H, Nkv, D]
+        T, Hl, Wl : latent grid of the queries (and of the keys unless kv_grid)
+        rows    : int64 global row ids (b*H + h)*Nq + i; None = every row
+        q_gamma, k_gamma : RMS-normalisation weights [D] of the queries / keys
+                  (None: not normalised); eps under the root
+        kv_grid : (T, Hl, Wl) of the keys when it differs from the queries'
+        rope_k  : rotate the keys (default: as rope)
+        returns : float32 [len(rows), D] (or [B, H, Nq, D] when rows is None)
         """
         q, k, v = _u16(q), _u16(k), _u16(v)
-        if q.ndim != 4 or q.shape != k.shape or q.shape != v.shape:
-            raise ValueError("q, k, v must share one [B, H, N, D] shape")
-        B, H, N, D = q.shape
+        if q.ndim != 4 or k.ndim != 4 or k.shape != v.shape or q.shape[:2] != k.shape[:2] \
+                or q.shape[3] != k.shape[3]:
+            raise ValueError("q must be [B, H, Nq, D] and k, v one [B, H, Nkv, D] shape")
+        B, H, Nq, D = q.shape
+        Nkv = k.shape[2]
+        Tk, Hlk, Wlk = kv_grid if kv_grid is not None else (T, Hl, Wl)
+        rope_k = rope if rope_k is None else rope_k
+        gam = []
+        for g in (q_gamma, k_gamma):
+            if g is None:
+                gam.append(None)
+                continue
+            g = np.ascontiguousarray(g, dtype=np.float64)
+            if g.shape != (D,):
+                raise ValueError("gamma must hold D = %d weights" % D)
+            gam.append(g)
         full = rows is None
         if full:
-            rows = np.arange(B * H * N, dtype=np.int64)
+            rows = np.arange(B * H * Nq, dtype=np.int64)
         rows = np.ascontiguousarray(rows, dtype=np.int64)
         out = np.empty((rows.size, D), dtype=np.float32)
-        rc = self.lib.solref_attn_rows(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, T, Hl, Wl,
-                                       split[0], split[1], split[2], base, int(bool(rope)),
-                                       int(bool(contract)), _ptr(rows), rows.size, _ptr(out),
-                                       threads)
+        rc = self.lib.solref_attn_rows_ex(
+            _ptr(q), _ptr(k), _ptr(v), B, H, Nq, Nkv, D, T, Hl, Wl, Tk, Hlk, Wlk,
+            split[0], split[1], split[2], base, int(bool(rope)), int(bool(rope_k)),
+            int(bool(contract)), None if gam[0] is None else _ptr(gam[0]),
+            None if gam[1] is None else _ptr(gam[1]), float(eps), _ptr(rows), rows.size,
+            _ptr(out), threads)
         if rc != 0:
             raise ValueError("oracle rejected the arguments (rc=%d)" % rc)
-        return out.reshape(B, H, N, D) if full else out
+        return out.reshape(B, H, Nq, D) if full else out
 
 
 _default = None
@@ -134,6 +182,12 @@ def rope3d_bf16(x_bits, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE):
     return default().rope3d_bf16(x_bits, T, Hl, Wl, split, base)
 
 
+def qknorm_rope3d(x_bits, T, Hl, Wl, gamma, eps, rope=True, contract=True,
+                  split=DEFAULT_SPLIT, base=ROPE_BASE):
+    return default().qknorm_rope3d(x_bits, T, Hl, Wl, gamma, eps, rope, contract, split, base)
+
+
 def attn_rows(q, k, v, T, Hl, Wl, rows=None, rope=True, contract=True,
-              split=DEFAULT_SPLIT, base=ROPE_BASE, threads=0):
-    return default().attn_rows(q, k, v, T, Hl, Wl, rows, rope, contract, split, base, threads)
+              split=DEFAULT_SPLIT, base=ROPE_BASE, threads=0, **kw):
+    return default().attn_rows(q, k, v, T, Hl, Wl, rows, rope, contract, split, base, threads,
+                               **kw)

@@ -374,4 +374,158 @@ def pin_attention_rows_and_threads(o):
     assert np.array_equal(sub, full.reshape(-1, D)[rows])
 
 
+# ------------------------------------------------- QK normalization (RMSNorm)
+
+def _gamma(rng, spread=0.3):
+    """Non-uniform per-dimension weights (bf16-exact values, as model weights)."""
+    return _f(_bits(1.0 + spread * rng.standard_normal(D)))
+
+
+def pin_qknorm_vs_torch_rms_norm(o):
+    """Without rotation the normalisation is torch's rms_norm over the head's D
+    entries (float64, weight gamma, eps under the root): in double, and after
+    the one bf16 rounding."""
+    rng = np.random.default_rng(30)
+    for std, eps in [(1.0, 1e-6), (7.0, 0.0), (0.01, 1e-3)]:
+        x = _rand_bits(rng, (2, 3, 21, D), std)
+        g = _gamma(rng)
+        want = torch.nn.functional.rms_norm(torch.from_numpy(_f(x)), (D,),
+                                            weight=torch.from_numpy(g), eps=eps).numpy()
+        got64 = o.qknorm_rope3d(x, 0, 0, 0, g, eps, rope=False, contract=False)
+        assert np.allclose(got64, want, rtol=1e-14, atol=0), "normalisation differs from rms_norm"
+        got = _f(o.qknorm_rope3d(x, 0, 0, 0, g, eps, rope=False))
+        assert np.array_equal(got, brute.nearest_bf16(want)), "normalised rows not rounded once"
+
+
+def pin_qknorm_unit_rms_rows_unchanged(o):
+    """Rows whose root mean square is exactly 1 (entries +-1), unit weights and
+    eps = 0: normalisation is the identity, so the result is the plain
+    rotation (latent tokens) or the input itself (prefix tokens)."""
+    rng = np.random.default_rng(31)
+    T, Hl, Wl, nt = 2, 3, 4, 5
+    N = nt + T * Hl * Wl
+    x = _bits(rng.choice([-1.0, 1.0], size=(1, 2, N, D)))
+    got = o.qknorm_rope3d(x, T, Hl, Wl, np.ones(D), 0.0)
+    assert np.array_equal(got, o.rope3d_bf16(x, T, Hl, Wl, SPLIT, BASE))
+    assert np.array_equal(got[:, :, :nt], x[:, :, :nt])
+
+
+def pin_qknorm_gamma_closed_form(o):
+    """A row of ones has mean square 1, so its normalised value is
+    gamma / sqrt(1 + eps), dimension by dimension (prefix token: no rotation)."""
+    rng = np.random.default_rng(32)
+    g = _gamma(rng, 0.8)
+    x = _bits(np.ones((1, 1, 3, D)))
+    for eps in (0.0, 0.25, 3.0):
+        got = o.qknorm_rope3d(x, 0, 0, 0, g, eps, contract=False)
+        assert np.allclose(got, np.broadcast_to(g / math.sqrt(1.0 + eps), got.shape),
+                           rtol=1e-15, atol=0)
+
+
+def pin_qknorm_scale_invariance(o):
+    """With eps = 0 the normalisation removes any positive scale of a row: rows
+    scaled by powers of two (exact in bf16) give the same bits."""
+    rng = np.random.default_rng(33)
+    T, Hl, Wl = 2, 3, 4
+    N = 3 + T * Hl * Wl
+    x = _rand_bits(rng, (1, 2, N, D))
+    g = _gamma(rng)
+    scale = np.exp2(rng.integers(-6, 7, size=(1, 2, N, 1))).astype(np.float64)
+    xs = _bits(_f(x) * scale)
+    assert np.array_equal(o.qknorm_rope3d(x, T, Hl, Wl, g, 0.0), o.qknorm_rope3d(xs, T, Hl, Wl, g, 0.0))
+
+
+def pin_qknorm_numpy_twin(o):
+    """Normalise-then-rotate in C equals the numpy twin (rms_norm_np, then the
+    complex rotation), with non-uniform weights that make the order matter."""
+    rng = np.random.default_rng(34)
+    T, Hl, Wl, nt = 3, 4, 5, 6
+    N = nt + T * Hl * Wl
+    x = _rand_bits(rng, (2, 2, N, D), 2.0)
+    g = _gamma(rng, 0.5)
+    got = o.qknorm_rope3d(x, T, Hl, Wl, g, 1e-6, contract=False)
+    want = brute.prepare_np(x, T, Hl, Wl, g, 1e-6, contract=False)
+    assert np.allclose(got, want, rtol=0, atol=1e-12)
+    assert np.array_equal(_f(o.qknorm_rope3d(x, T, Hl, Wl, g, 1e-6)), brute.nearest_bf16(want))
+
+
+def pin_attention_qknorm_vs_brute(o):
+    """Attention with normalised and rotated q and k equals the numpy twin."""
+    rng = np.random.default_rng(35)
+    T, Hl, Wl, nt = 2, 3, 4, 4
+    N = nt + T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D), 3.0) for _ in range(3))
+    gq, gk = _gamma(rng, 0.5), _gamma(rng, 0.5)
+    got = o.attn_rows(q, k, v, T, Hl, Wl, q_gamma=gq, k_gamma=gk, eps=1e-6)
+    want, _ = brute.fused_reference(q, k, v, T, Hl, Wl, q_gamma=gq, k_gamma=gk, eps=1e-6)
+    assert np.allclose(got, want, atol=2e-6, rtol=1e-6)
+
+
+def pin_attention_qknorm_ignores_row_scale(o):
+    """With eps = 0, scaling any query or key row by a power of two changes
+    nothing (both sides are normalised before the products)."""
+    rng = np.random.default_rng(36)
+    T, Hl, Wl = 2, 2, 5
+    N = 3 + T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(3))
+    gq, gk = _gamma(rng), _gamma(rng)
+    sq = np.exp2(rng.integers(-5, 6, size=(1, 2, N, 1))).astype(np.float64)
+    sk = np.exp2(rng.integers(-5, 6, size=(1, 2, N, 1))).astype(np.float64)
+    a = o.attn_rows(q, k, v, T, Hl, Wl, q_gamma=gq, k_gamma=gk, eps=0.0)
+    b = o.attn_rows(_bits(_f(q) * sq), _bits(_f(k) * sk), v, T, Hl, Wl, q_gamma=gq, k_gamma=gk,
+                    eps=0.0)
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------- queries and keys of other lengths
+
+def pin_attention_kv_lengths_vs_sdpa(o):
+    """Nq queries against Nkv != Nq keys, nothing rotated: torch SDPA (float64)."""
+    rng = np.random.default_rng(37)
+    for nq, nkv in [(37, 130), (130, 5), (1, 64)]:
+        q = _rand_bits(rng, (2, 2, nq, D))
+        k, v = (_rand_bits(rng, (2, 2, nkv, D)) for _ in range(2))
+        got = o.attn_rows(q, k, v, 0, 0, 0, rope=False)
+        assert got.shape == (2, 2, nq, D)
+        want = _sdpa64(_f(q), _f(k), _f(v))
+        assert np.allclose(got, want, atol=2e-6, rtol=1e-6)
+
+
+def pin_attention_prefix_queries_of_self_attention(o):
+    """Queries that are the text prefix of a sequence (Nq = Nt, unrotated)
+    against that whole sequence's keys give exactly the first Nt rows of the
+    sequence's self-attention."""
+    rng = np.random.default_rng(38)
+    T, Hl, Wl, nt = 2, 3, 4, 9
+    N = nt + T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(3))
+    full = o.attn_rows(q, k, v, T, Hl, Wl)
+    part = o.attn_rows(np.ascontiguousarray(q[:, :, :nt]), k, v, 0, 0, 0, kv_grid=(T, Hl, Wl))
+    assert np.array_equal(part, full[:, :, :nt])
+
+
+def pin_attention_kv_segments_commute(o):
+    """Keys and values made of two segments, each rotated with its own grid
+    and then given as prepared keys: the order of the segments does not
+    matter, and the result equals the numpy twin."""
+    rng = np.random.default_rng(39)
+    Tq, Hlq, Wlq = 2, 3, 3
+    nq = 4 + Tq * Hlq * Wlq
+    q = _rand_bits(rng, (1, 2, nq, D))
+    segs = [((1, 4, 5), 3), ((2, 2, 2), 0)]  # (grid, prefix tokens)
+    kh, vs = [], []
+    for (T, Hl, Wl), nt in segs:
+        n = nt + T * Hl * Wl
+        k = _rand_bits(rng, (1, 2, n, D))
+        kh.append(o.rope3d_bf16(k, T, Hl, Wl, SPLIT, BASE))
+        vs.append(_rand_bits(rng, (1, 2, n, D)))
+    ab = o.attn_rows(q, np.concatenate(kh, 2), np.concatenate(vs, 2), Tq, Hlq, Wlq, rope_k=False)
+    ba = o.attn_rows(q, np.concatenate(kh[::-1], 2), np.concatenate(vs[::-1], 2), Tq, Hlq, Wlq,
+                     rope_k=False)
+    assert np.allclose(ab, ba, atol=1e-7, rtol=0)
+    want, _ = brute.fused_reference(q, np.concatenate(kh, 2), np.concatenate(vs, 2), Tq, Hlq, Wlq,
+                                    rope_k=False)
+    assert np.allclose(ab, want, atol=2e-6, rtol=1e-6)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

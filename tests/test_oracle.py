@@ -62,6 +62,27 @@ def test_oracle_rejects_bad_arguments(orc):
 
 # ------------------------------------------------------------ mutation test
 
+_NORM_THEN_ROTATE = """  if (gamma) {
+    rms_normalize(dst, D, gamma, eps);
+    changed = 1;
+  }
+  int pt, ph, pw;
+  if (use_rope && token_position(n, N, T, Hl, Wl, &pt, &ph, &pw)) {
+    rotate_vector(dst, D, dt, dh, dw, base, pt, ph, pw);
+    changed = 1;
+  }
+"""
+_ROTATE_THEN_NORM = """  int pt, ph, pw;
+  if (use_rope && token_position(n, N, T, Hl, Wl, &pt, &ph, &pw)) {
+    rotate_vector(dst, D, dt, dh, dw, base, pt, ph, pw);
+    changed = 1;
+  }
+  if (gamma) {
+    rms_normalize(dst, D, gamma, eps);
+    changed = 1;
+  }
+"""
+
 MUTANTS = [
     ("rotation turns the wrong way",
      "x[off + 2 * i] = re * c - im * s;\n      x[off + 2 * i + 1] = re * s + im * c;",
@@ -81,9 +102,24 @@ MUTANTS = [
     ("ties rounded away from zero",
      "if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;",
      "if (rem >= 0.5) fl += 1.0;"),
-    ("rotated q/k not rounded to bf16", "    if (contract)\n", "    if (0)\n"),
+    ("rotated q/k not rounded to bf16", "  if (contract && changed)\n", "  if (0)\n"),
     ("dot product skips the last dim", "for (int d = 0; d < D; ++d) dot += qhat[d] * kj[d];",
      "for (int d = 0; d < D - 1; ++d) dot += qhat[d] * kj[d];"),
+    # QK normalization
+    ("norm: mean over the head dim dropped", "sqrt(ss / (double)D + eps)", "sqrt(ss + eps)"),
+    ("norm: eps outside the root", "1.0 / sqrt(ss / (double)D + eps)",
+     "1.0 / (sqrt(ss / (double)D) + eps)"),
+    ("norm: square root missing", "1.0 / sqrt(ss / (double)D + eps)", "1.0 / (ss / (double)D + eps)"),
+    ("norm: weights not applied", "x[d] = x[d] * inv * gamma[d];", "x[d] = x[d] * inv;"),
+    ("norm: weights reversed", "x[d] * inv * gamma[d]", "x[d] * inv * gamma[D - 1 - d]"),
+    ("norm: applied after the rotation", _NORM_THEN_ROTATE, _ROTATE_THEN_NORM),
+    ("norm: prefix tokens skipped", "  if (gamma) {\n    rms_normalize",
+     "  if (gamma && n >= (int64_t)N - (int64_t)T * Hl * Wl) {\n    rms_normalize"),
+    ("norm: keys not normalised", "J->base, J->kside.rope, J->contract, J->kside.gamma, J->eps);",
+     "J->base, J->kside.rope, J->contract, NULL, J->eps);"),
+    # queries and keys of different lengths
+    ("key count taken from the queries", "for (int j = 0; j < Nkv; ++j) {\n    const double* kj",
+     "for (int j = 0; j < Nkv && j < J->qs.N; ++j) {\n    const double* kj"),
 ]
 
 
