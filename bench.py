@@ -1,11 +1,15 @@
 """Benchmark of the fused 3D-RoPE + softmax attention layer on one MI355X.
 
-A step is one call of sol_attn_fwd over the whole workload (every batch and
-head of one attention layer): 3D rotary embedding of q and k fused into the
-tile loads, softmax(q^ k^T / sqrt(D)) v, bf16 out.  Inputs are resident in
-HBM before the timed region starts.
+A step is one pass of the whole path over one layer (every batch and head):
+by default the prepared path -- sol_prepare_kv_ex (k rotated, k and v
+converted to fp16 tiles, one pass) then sol_attn_fwd_prepared_ex (q rotated in
+its tile load, softmax(q^ k^T / sqrt(D)) v, bf16 out); --path fused times
+sol_attn_fwd (q and k rotated in every tile load).  The p720n workload adds
+the QK normalization ahead of the rotation; ref720 attends to a cached
+reference segment prepared once, before the timed steps.  Inputs are resident
+in HBM before the timed region starts.
 
-Prints ONE JSON line: throughput in TFLOP/s (4 N^2 D H B algorithmic flops
+Prints ONE JSON line: throughput in TFLOP/s (4 Nq Nkv D H B algorithmic flops
 per layer), ms per layer, the fraction of the dense bf16 MFMA peak measured
 with HIP events on the kernel's stream, the CPU oracle timed on a bounded
 row sample of the same workload, and the parity of those rows.
@@ -51,7 +55,7 @@ def measured_traffic(workload_name, kernel):
     return entry.get("bytes_per_launch")
 
 
-def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread):
+def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread, ref_kv=None):
     """Time the oracle on a bounded, seeded sample of query rows of slab (0, 0)
     against all keys; check those rows of the GPU output against it."""
     import numpy as np
@@ -67,10 +71,21 @@ def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread):
     rows = np.sort(torch.randperm(w.N, generator=gen)[:n_rows].numpy()).astype(np.int64)
     # the oracle needs slab (0, 0) only
     qb, kb, vb = (W.as_bits(t[:1, :1].contiguous()) for t in (q, k, v))
+    kw = {}
+    if w.qk_norm:
+        gq, gk = W.norm_weights(w)
+        kw = dict(q_gamma=gq.numpy(), k_gamma=gk.numpy(), eps=W.QK_NORM_EPS)
     t0 = time.perf_counter()
-    ref = oracle.attn_rows(qb, kb, vb, w.T, w.Hl, w.Wl, rows=rows, threads=threads)
+    if ref_kv is not None:
+        # keys: the cached reference segment (its own grid), then the own tokens
+        krb, vrb = (W.as_bits(t[:1, :1].contiguous()) for t in ref_kv)
+        kb = np.concatenate([oracle.rope3d_bf16(krb, *w.ref_grid),
+                             oracle.rope3d_bf16(kb, w.T, w.Hl, w.Wl)], 2)
+        vb = np.concatenate([vrb, vb], 2)
+        kw["rope_k"] = False
+    ref = oracle.attn_rows(qb, kb, vb, w.T, w.Hl, w.Wl, rows=rows, threads=threads, **kw)
     dt = time.perf_counter() - t0
-    flops = 4.0 * w.N * w.D * n_rows
+    flops = 4.0 * w.n_kv * w.D * n_rows
     got = W.as_bits(out_gpu[0, 0].cpu()).reshape(w.N, w.D)[rows]
     par = compare(got, ref, np.zeros(n_rows, np.int64))
     cpu = {
@@ -79,7 +94,7 @@ def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread):
         "cores": threads,
         "kind": "oracle",
         "sample": "%d query rows (seeded) of head (0,0) against all %d keys, fp64 C oracle, %.1f s; "
-                  "full layer extrapolates to %.0f s" % (n_rows, w.N, dt, dt * w.B * w.H * w.N / n_rows),
+                  "full layer extrapolates to %.0f s" % (n_rows, w.n_kv, dt, dt * w.B * w.H * w.N / n_rows),
     }
     return cpu, par
 
@@ -101,7 +116,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="p720", help="tiny | low | p480 | p720 | share")
+    ap.add_argument("--workload", default="p720",
+                    help="tiny | low | p480 | p720 | share | p720n (QK normalization) | "
+                         "ref720 (cached reference keys)")
     ap.add_argument("--path", default="prepared", choices=["fused", "prepared"],
                     help="prepared: sol_prepare_kv (K rotated, V to fp16, one pass) then "
                          "sol_attn_fwd_prepared (q rotated in its tile load); fused: sol_attn_fwd "
@@ -141,17 +158,32 @@ def main():
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=dev)
     torch.cuda.synchronize()
 
-    ws = sol.attn_workspace(qd)
-    n_prep = sol.sol_prepared_kv_bytes(w.B, w.H, w.N, w.D) // 2
-    k_prep = ws.view(torch.float16)[:n_prep]
-    v_prep = ws.view(torch.float16)[n_prep: 2 * n_prep]
+    k_prep, v_prep = sol.prepared_kv_buffers(w.B, w.H, w.n_kv, dev)
+    gq = gk = None
+    if w.qk_norm:
+        gq, gk = (g.to(dev) for g in W.norm_weights(w))
+    ref_kv = None
+    if w.n_ref:
+        # the cached reference keys and values: prepared once, outside the step
+        ref_kv = W.make_ref_inputs(w)
+        rtab = sol.rope3d_table(*w.ref_grid, device=dev)
+        sol.prepare_kv_ex(ref_kv[0].to(dev), ref_kv[1].to(dev), *w.ref_grid, rtab, k_prep, v_prep,
+                          key0=0, n_kv=w.n_kv)
+        torch.cuda.synchronize()
+    special = w.qk_norm or w.n_ref
+    if special and args.path == "fused":
+        print("the fused path has neither QK normalization nor a key cache", file=sys.stderr)
+        sys.exit(2)
 
     def launches(path):
         """The launches of one step, in order: [(name, fn)]."""
         if path == "prepared":
-            return [("prepare_kv", lambda: sol.prepare_kv(kd, vd, w.T, w.Hl, w.Wl, tab, k_prep, v_prep)),
-                    ("attn_fwd_prepared", lambda: sol.attn_fwd_prepared(qd, k_prep, v_prep, w.T, w.Hl, w.Wl,
-                                                                        tab, out=out))]
+            return [("prepare_kv", lambda: sol.prepare_kv_ex(kd, vd, w.T, w.Hl, w.Wl, tab, k_prep, v_prep,
+                                                             key0=w.n_ref, n_kv=w.n_kv, gamma=gk,
+                                                             eps=W.QK_NORM_EPS)),
+                    ("attn_fwd_prepared", lambda: sol.attn_fwd_prepared_ex(qd, k_prep, v_prep, w.n_kv, w.T, w.Hl,
+                                                                           w.Wl, tab, gamma=gq,
+                                                                           eps=W.QK_NORM_EPS, out=out))]
         return [("attn_fwd", lambda: sol.attn_fwd(qd, kd, vd, w.T, w.Hl, w.Wl, tab, out=out))]
 
     def timed(path, steps, warmup):
@@ -191,8 +223,10 @@ def main():
     log("timed %d steps (%s): %.3f ms/step, %s %.3f ms avg (median %.3f) -> %.1f TFLOP/s"
         % (args.steps, args.path, ms_step, main_kernel, ms_launch, ms_median, tflops))
     other = "fused" if args.path == "prepared" else "prepared"
-    ms_other, per_other = timed(other, min(3, args.steps), 1)
-    log("other path (%s): %.3f ms/step" % (other, ms_other))
+    ms_other = None
+    if not special:
+        ms_other, _ = timed(other, min(3, args.steps), 1)
+        log("other path (%s): %.3f ms/step" % (other, ms_other))
 
     traffic = measured_traffic(w.name, main_kernel)
     result = {
@@ -213,17 +247,18 @@ def main():
         "config": {
             "workload": "%s: %s" % (w.name, w.describe()),
             "B": w.B, "H": w.H, "N": w.N, "D": w.D, "grid": [w.T, w.Hl, w.Wl], "n_text": w.n_text,
+            "n_kv": w.n_kv, "qk_norm": w.qk_norm,
             "rope": ("3d (32/48/48, base 1e4) fused into the q and k tile loads" if args.path == "fused"
                      else "3d (32/48/48, base 1e4): q in the tile load, k in a one-pass prologue"),
             "path": ("sol_attn_fwd" if args.path == "fused"
-                     else "sol_prepare_kv + sol_attn_fwd_prepared"),
+                     else "sol_prepare_kv_ex + sol_attn_fwd_prepared_ex"),
         },
         "ms_per_layer": ms_step,
         "kernel_ms_median": ms_median,
         "pct_peak_bf16": 100.0 * tflops / PEAK_BF16_TFLOPS,
         "kernel_ms": {name: sum(v) / len(v) for name, v in per.items()},
-        "other_path": {"path": other, "ms_per_step": ms_other,
-                       "tflops": w.flops / (ms_other * 1e-3) / 1e12},
+        "other_path": None if ms_other is None else {
+            "path": other, "ms_per_step": ms_other, "tflops": w.flops / (ms_other * 1e-3) / 1e12},
         "roofline": {
             "kernel": main_kernel,
             "bound": "mfma",
@@ -236,7 +271,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        cpu, par = cpu_baseline(w, q, k, v, out, args.cpu_rows_per_thread)
+        cpu, par = cpu_baseline(w, q, k, v, out, args.cpu_rows_per_thread, ref_kv)
         result["cpu_baseline"] = cpu
         result["parity"] = par
         from parity import passes

@@ -87,6 +87,25 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
                const float* rope_tab_dev, sol_stream_t stream);
 
 /*
+ * QK normalization ahead of the rotation (Sec. 3.5, fusion group 2, "QK
+ * normalization with partial RoPE"), standalone:
+ *   y = bf16(R(pos) (x * gamma / sqrt(mean_d(x_d^2) + eps)))
+ * per token and head: the root mean square is taken over the head's D entries
+ * of the bf16 input (the rounding point the paper keeps ahead of QK
+ * normalization, Sec. 3.5 "LoRA fusion"), everything is fp32, and the result
+ * is rounded to bf16 once, after the rotation.  Every token is normalised;
+ * prefix tokens are not rotated.  gamma_dev: D fp32 weights in device memory,
+ * 16-byte aligned, or NULL (no normalisation: exactly sol_rope3d).  eps >= 0
+ * and finite (an all-zero row with eps = 0 gives NaN, as the formula does).
+ * Other arguments as sol_rope3d.  The same normalisation runs in the
+ * prepared path below (sol_prepare_kv_ex, sol_attn_fwd_prepared_ex), to the
+ * same bits: the sum of squares follows one fixed order in every kernel.
+ */
+int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
+                      const float* rope_tab_dev, const float* gamma_dev, float eps,
+                      sol_stream_t stream);
+
+/*
  * out = softmax(q^ k^T / sqrt(D)) v with q^, k^ rotated and rounded to bf16
  * inside the kernel (fused into the tile loads).  fp32 logits, softmax
  * statistics and accumulators.  The second product takes the probabilities
@@ -140,6 +159,45 @@ int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int
 int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
                           int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                           sol_stream_t stream);
+
+/*
+ * The prepared path, generalised.
+ *
+ * sol_prepare_kv_ex: the N keys and values of every (b, h) slab of k, v
+ * ([B][H][N][D] bf16) become keys key0 .. key0 + N - 1 of a prepared sequence
+ * of n_kv keys (buffers of sol_prepared_kv_bytes(B, H, n_kv, D) bytes, the
+ * layout of sol_prepare_kv).  The rotation uses this call's own grid T x Hl x
+ * Wl (its first N - T*Hl*Wl keys are an unrotated prefix); with k_gamma_dev
+ * the keys are RMS-normalised first, as in sol_qknorm_rope3d.  Several calls
+ * fill one prepared sequence from several sources -- the paper's reference-KV
+ * cache (Sec. 5, "Reference KV caching mechanism"): the reference tokens'
+ * keys and values are prepared once, at the first denoising step, and later
+ * steps prepare only their own tokens into the rest of the sequence.  Calls
+ * write only their own keys (a tile shared with another call's keys is
+ * written element by element) and the zero padding past n_kv, so their order
+ * does not matter.  0 <= key0, key0 + N <= n_kv <= SOL_MAX_TOKENS.
+ * sol_prepare_kv(...) is sol_prepare_kv_ex with key0 = 0, n_kv = N and no
+ * normalisation.
+ *
+ * sol_attn_fwd_prepared_ex: N query rows per slab (q, out: [B][H][N][D],
+ * rotated with the grid T x Hl x Wl, RMS-normalised first with q_gamma_dev)
+ * against the n_kv prepared keys: out = softmax(q^ k^T / sqrt(D)) v over all
+ * of them (n_kv may differ from N).  Every key must have been written by a
+ * sol_prepare_kv_ex call.  sol_attn_fwd_prepared(...) is this call with n_kv
+ * = N and no normalisation.
+ *
+ * gamma pointers: D fp32 device weights, 16-byte aligned, or NULL; eps as in
+ * sol_qknorm_rope3d (ignored when the pointer is NULL).  Other arguments,
+ * ownership and errors as sol_prepare_kv / sol_attn_fwd_prepared.
+ */
+int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H,
+                      int N, int key0, int n_kv, int D, int T, int Hl, int Wl,
+                      const float* rope_tab_dev, const float* k_gamma_dev, float eps,
+                      sol_stream_t stream);
+int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_prep, void* out,
+                             int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl,
+                             const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                             sol_stream_t stream);
 
 /*
  * Bytes of device workspace sol_attn_fwd_ws needs: room for k_prep then

@@ -45,6 +45,15 @@ int check_shape(int B, int H, int N, int D, int T, int Hl, int Wl) {
   return SOL_OK;
 }
 
+// The QK-normalisation arguments: no weights (eps ignored), or 16-byte
+// aligned device weights with a finite eps >= 0.
+int check_norm(const float* gamma, float eps) {
+  if (!gamma) return SOL_OK;
+  if (!aligned16(gamma)) return fail(SOL_ERR_INVALID_ARG, "gamma must be 16-byte aligned");
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(SOL_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  return SOL_OK;
+}
+
 }  // namespace
 
 sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl) {
@@ -95,8 +104,9 @@ int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int
   return ok();
 }
 
-int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
-               const float* rope_tab_dev, sol_stream_t stream) {
+int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
+                      const float* rope_tab_dev, const float* gamma_dev, float eps,
+                      sol_stream_t stream) {
   if (!x || !y) return fail(SOL_ERR_INVALID_ARG, "x and y must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
@@ -104,14 +114,22 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
   const int64_t nv = (int64_t)T * Hl * Wl;
   if (nv > 0 && !rope_tab_dev) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev is NULL for a non-empty grid");
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  st = check_norm(gamma_dev, eps);
+  if (st != SOL_OK) return st;
   const size_t bytes = (size_t)B * H * N * D * 2;
   if (x != y && overlaps(x, bytes, y, bytes)) return fail(SOL_ERR_INVALID_ARG, "x and y partially overlap");
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
   hipError_t e = sol::launch_rope3d(static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y),
-                                    (int64_t)B * H * N, g, reinterpret_cast<const float2*>(rope_tab_dev),
-                                    reinterpret_cast<hipStream_t>(stream));
+                                    (int64_t)B * H * N, g,
+                                    nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr,
+                                    gamma_dev, eps, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "rope3d launch: %s", hipGetErrorString(e));
   return ok();
+}
+
+int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
+               const float* rope_tab_dev, sol_stream_t stream) {
+  return sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab_dev, nullptr, 0.0f, stream);
 }
 
 int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int D,
@@ -145,16 +163,25 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int D) {
   return 2 * sol_prepared_kv_bytes(B, H, N, D);
 }
 
-int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H, int N,
-                   int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
+int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H,
+                      int N, int key0, int n_kv, int D, int T, int Hl, int Wl,
+                      const float* rope_tab_dev, const float* k_gamma_dev, float eps,
+                      sol_stream_t stream) {
   if (!k || !v || !k_prep || !v_prep) return fail(SOL_ERR_INVALID_ARG, "k, v, k_prep, v_prep must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if (n_kv < 1 || n_kv > SOL_MAX_TOKENS)
+    return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
+  if (key0 < 0 || (int64_t)key0 + N > n_kv)
+    return fail(SOL_ERR_INVALID_ARG, "keys [%d, %lld) do not fit a sequence of n_kv=%d", key0,
+                (long long)key0 + N, n_kv);
   if (!aligned16(k) || !aligned16(v) || !aligned16(k_prep) || !aligned16(v_prep))
     return fail(SOL_ERR_INVALID_ARG, "k, v, k_prep, v_prep must be 16-byte aligned");
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  st = check_norm(k_gamma_dev, eps);
+  if (st != SOL_OK) return st;
   const size_t bytes = (size_t)B * H * N * D * 2;
-  const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
   if (overlaps(k_prep, pbytes, k, bytes) || overlaps(k_prep, pbytes, v, bytes) ||
       overlaps(v_prep, pbytes, k, bytes) || overlaps(v_prep, pbytes, v, bytes) ||
       overlaps(k_prep, pbytes, v_prep, pbytes))
@@ -164,22 +191,34 @@ int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
   hipError_t e = sol::launch_prepare_kv(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                                         static_cast<uint16_t*>(k_prep), static_cast<uint16_t*>(v_prep), B * H,
-                                        g, tab, reinterpret_cast<hipStream_t>(stream));
+                                        g, tab, key0, n_kv, k_gamma_dev, eps,
+                                        reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "prepare_kv launch: %s", hipGetErrorString(e));
   return ok();
 }
 
-int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
-                          int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
-                          sol_stream_t stream) {
+int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H, int N,
+                   int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
+  return sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, 0, N, D, T, Hl, Wl, rope_tab_dev, nullptr,
+                           0.0f, stream);
+}
+
+int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_prep, void* out,
+                             int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl,
+                             const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                             sol_stream_t stream) {
   if (!q || !k_prep || !v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "q, k_prep, v_prep, out must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if (n_kv < 1 || n_kv > SOL_MAX_TOKENS)
+    return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
   if (!aligned16(q) || !aligned16(k_prep) || !aligned16(v_prep) || !aligned16(out))
     return fail(SOL_ERR_INVALID_ARG, "q, k_prep, v_prep, out must be 16-byte aligned");
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  st = check_norm(q_gamma_dev, eps);
+  if (st != SOL_OK) return st;
   const size_t bytes = (size_t)B * H * N * D * 2;
-  const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
   if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k_prep, pbytes) || overlaps(out, bytes, v_prep, pbytes))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep or v_prep");
   if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
@@ -188,9 +227,17 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
   hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
                                                static_cast<const uint16_t*>(v_prep), static_cast<uint16_t*>(out),
-                                               B * H, g, tab, reinterpret_cast<hipStream_t>(stream));
+                                               B * H, g, n_kv, tab, q_gamma_dev, eps,
+                                               reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_prepared launch: %s", hipGetErrorString(e));
   return ok();
+}
+
+int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
+                          int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                          sol_stream_t stream) {
+  return sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, N, D, T, Hl, Wl, rope_tab_dev,
+                                  nullptr, 0.0f, stream);
 }
 
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
@@ -229,6 +276,6 @@ const char* sol_status_string(int status) {
 
 const char* sol_last_error(void) { return g_last_error; }
 
-int sol_version(void) { return 100; }
+int sol_version(void) { return 101; }
 
 }  // extern "C"

@@ -24,24 +24,30 @@ struct SeqGrid {
 
 SeqGrid make_grid(int N, int T, int Hl, int Wl);
 
+// gamma != nullptr: RMS-normalise every row with these D weights first.
 hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int64_t rows, const SeqGrid& g,
-                         const float2* tab, hipStream_t stream);
+                         const float2* tab, const float* gamma, float eps, hipStream_t stream);
 
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                            uint16_t* out, int BH, const SeqGrid& g, const float2* tab,
                            hipStream_t stream);
 
-// Prepared path: k_rot / v_f16 (each BH * N * D 16-bit elements) receive the
-// rotated K and the fp16 V in one pass; the attention kernel then rotates only
-// q and copies prepared tiles.
-// Prepared K/V: per (b, h) slab, ceil(N/32) tiles of 32 keys, 8 KB of K and
-// 8 KB of V each, in the fragment order of the prepared-path kernel.
+// Prepared path.  Prepared K/V: per (b, h) slab, ceil(n_kv/32) tiles of 32
+// keys, 8 KB of K and 8 KB of V each, in the fragment order of the
+// prepared-path kernel.  launch_prepare_kv writes the g.n source keys of every
+// slab to keys key0 .. key0 + g.n - 1 of such a sequence of n_kv keys (rotated
+// with grid g; normalised first when gamma != nullptr), plus the zero padding
+// past n_kv when it covers the last tile.
 hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_prep,
                              uint16_t* v_prep, int BH, const SeqGrid& g, const float2* tab,
+                             int key0, int n_kv, const float* gamma, float eps,
                              hipStream_t stream);
+// g.n query rows (rotated with grid g, normalised first when q_gamma !=
+// nullptr) against n_kv prepared keys.
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, uint16_t* out, int BH,
-                                    const SeqGrid& g, const float2* tab, hipStream_t stream);
+                                    const SeqGrid& g, int n_kv, const float2* tab,
+                                    const float* q_gamma, float eps, hipStream_t stream);
 // fp16 elements of one (b, h) slab of prepared K (or V).
 int64_t prepared_tile_elems(int N);
 

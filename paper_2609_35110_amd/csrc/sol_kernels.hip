@@ -109,18 +109,31 @@ __device__ __forceinline__ uint4 bf16x8_to_f16x8(uint4 x) {
                     bf16x2_to_f16x2(x.w));
 }
 
-// Rotate the 4 interleaved pairs held in one 16-byte chunk:
+// The eight bf16 values of a 16-byte chunk as fp32 (exact), and back (RNE).
+__device__ __forceinline__ void unpack_bf16x8(uint4 x, float (&f)[8]) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    f[2 * u] = __uint_as_float(w[u] << 16);
+    f[2 * u + 1] = __uint_as_float(w[u] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ uint4 pack_bf16x8(const float (&f)[8]) {
+  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                    pack_bf16x2(f[6], f[7]));
+}
+
+// Rotate the 4 interleaved pairs of one 16-byte chunk, held as fp32:
 //   (a, b) -> (a cos - b sin, a sin + b cos), fp32, then bf16 RNE.
 // The one function every rotation in this library goes through, so the
 // standalone rotation and the fused tile loads agree bit for bit.
-__device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) {
+__device__ __forceinline__ uint4 rope_rotate_f32(const float (&f)[8], float4 cs01, float4 cs23) {
   const float c[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
   const float s[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
-  uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  uint32_t w[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const float a = __uint_as_float(w[u] << 16);
-    const float b = __uint_as_float(w[u] & 0xffff0000u);
+    const float a = f[2 * u], b = f[2 * u + 1];
     const float ar = __builtin_fmaf(a, c[u], -(b * s[u]));
     const float br = __builtin_fmaf(a, s[u], b * c[u]);
     w[u] = pack_bf16x2(ar, br);
@@ -128,29 +141,91 @@ __device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) 
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+__device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) {
+  float f[8];
+  unpack_bf16x8(x, f);
+  return rope_rotate_f32(f, cs01, cs23);
+}
+
 __device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ tab, int pair0) {
   return rope_rotate(x, *reinterpret_cast<const float4*>(tab + pair0),
                      *reinterpret_cast<const float4*>(tab + pair0 + 2));
 }
 
+// ------------------------------------------------------- QK normalization
+
+// RMS normalisation of one head's row ahead of the rotation (Sec. 3.5, fusion
+// group 2, "QK normalization with partial RoPE"): x gamma / sqrt(mean(x^2) +
+// eps), in fp32, nothing rounded before the rotation.  The sum of squares
+// follows one fixed order whichever lanes hold the row -- per 16-byte chunk c
+// an fma chain over its eight entries, then a binary tree over the 16 chunk
+// sums pairing c with c^1, then c^2, c^4, c^8 -- so every kernel normalises a
+// row to the same bits (fp32 addition is commutative, so a butterfly over the
+// lanes and a tree inside one lane give the same sums).
+__device__ __forceinline__ float chunk_sumsq(uint4 x) {
+  float f[8];
+  unpack_bf16x8(x, f);
+  float s = f[0] * f[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) s = __builtin_fmaf(f[e], f[e], s);
+  return s;
+}
+// The tree over 16 consecutive lanes that hold chunks 0..15 of one row.
+__device__ __forceinline__ float row_sumsq_lanes16(float p) {
+  p += __shfl_xor(p, 1);
+  p += __shfl_xor(p, 2);
+  p += __shfl_xor(p, 4);
+  p += __shfl_xor(p, 8);
+  return p;
+}
+__device__ __forceinline__ float rms_inv(float sumsq, float eps) {
+  return 1.0f / __builtin_sqrtf(sumsq * (1.0f / D) + eps);
+}
+// Chunk cc (dims 8cc..8cc+7) of a row, normalised: (x inv) gamma, fp32.
+__device__ __forceinline__ void norm_chunk(uint4 x, float inv, const float* __restrict__ gamma,
+                                           int cc, float (&f)[8]) {
+  unpack_bf16x8(x, f);
+  const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * cc);
+  const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * cc + 4);
+  const float gm[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f[e] = (f[e] * inv) * gm[e];
+}
+// Chunk cc of a query or key row as it enters the products: normalised when
+// gamma is given (inv from the row's sum of squares), rotated when rot (table
+// pairs from pair0), rounded to bf16.
+__device__ __forceinline__ uint4 qk_chunk(uint4 x, const float* __restrict__ gamma, float inv, int cc,
+                                          bool rot, const float2* __restrict__ tab, int pair0) {
+  if (gamma == nullptr) return rot ? rope_chunk(x, tab, pair0) : x;
+  float f[8];
+  norm_chunk(x, inv, gamma, cc, f);
+  if (!rot) return pack_bf16x8(f);
+  return rope_rotate_f32(f, *reinterpret_cast<const float4*>(tab + pair0),
+                         *reinterpret_cast<const float4*>(tab + pair0 + 2));
+}
+
 // --------------------------------------------------------- standalone rotary
 
 // One thread per 16-byte chunk of one (b, h) slab; grid.y walks the slabs.
+// gamma != NULL: each row is RMS-normalised first (the 16 chunks of a row sit
+// in 16 consecutive lanes; rows are never split across waves).
 __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x,
                                                      uint4* __restrict__ y, int64_t bh_count,
-                                                     SeqGrid g, const float2* __restrict__ tab) {
+                                                     SeqGrid g, const float2* __restrict__ tab,
+                                                     const float* __restrict__ gamma, float eps) {
   const int64_t per_slab = (int64_t)g.n * kChunks;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= per_slab) return;
+  if (i >= per_slab) return;  // whole rows: the lanes of a row leave together
   const int n = (int)(i / kChunks);
   const int cc = (int)(i % kChunks);
   const Pos p = token_pos(n, g);
-  const int pair0 = p.rot ? tab_pair(cc, p, g) : 0;
+  const bool rot = p.rot && tab != nullptr;
+  const int pair0 = rot ? tab_pair(cc, p, g) : 0;
   for (int64_t bh = blockIdx.y; bh < bh_count; bh += gridDim.y) {
     const int64_t idx = bh * per_slab + i;
-    uint4 v = x[idx];
-    if (p.rot) v = rope_chunk(v, tab, pair0);
-    y[idx] = v;
+    const uint4 v = x[idx];
+    const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(v)), eps) : 1.0f;
+    y[idx] = qk_chunk(v, gamma, inv, cc, rot, tab, pair0);
   }
 }
 
@@ -160,11 +235,17 @@ __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x
 // fragment read is one linear ds_read_b128 (64 lanes x 16 bytes, no bank
 // conflicts, immediate offsets).
 //   K tile: [kk 0..7][lane 0..63][8]: lane = r + 32 hh holds K^[key r][16kk + 8hh ..+7],
-//     K^ the rotated key rounded to bf16 (as every rotation here), then fp16.
+//     K^ the rotated (and, with gamma, first normalised) key rounded to bf16
+//     (as every rotation here), then fp16.
 //   V tile: [j 0..7][lane 0..63][8], j = 4 kst + db: lane = l + 32 hh holds
 //     V[key 16kst + 8(i/4) + 4hh + i%4][dim 32db + l] for i = 0..7, fp16 -- the
 //     key order of the fp16 probability words the PV MFMA multiplies it with.
-// Keys past N are zero.  One workgroup per tile; grid.y walks the slabs.
+// The source holds g.n keys per slab; they land at keys key0 .. key0 + g.n - 1
+// of a prepared sequence of n_kv keys (several calls fill one sequence from
+// several sources, e.g. cached reference keys and the current step's).  Keys
+// past n_kv are zero.  A tile that also holds keys of another source is
+// written element by element, only where this call owns the key.  One
+// workgroup per tile (from tile0 on); grid.y walks the slabs.
 constexpr int kPrepTile = 32;             // keys per prepared tile
 constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
 
@@ -173,38 +254,47 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
                                                       const uint4* __restrict__ v,
                                                       uint4* __restrict__ kp, uint4* __restrict__ vp,
                                                       int64_t bh_count, SeqGrid g,
-                                                      const float2* __restrict__ tab) {
+                                                      const float2* __restrict__ tab, int key0,
+                                                      int n_kv, int tile0,
+                                                      const float* __restrict__ gamma, float eps) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPrepTile * (D + 8)];
-  const int N = g.n;
-  const int n_tiles = (N + kPrepTile - 1) / kPrepTile;
-  const int tile = blockIdx.x;
+  const int n_src = g.n;
+  const int n_tiles = (n_kv + kPrepTile - 1) / kPrepTile;  // tiles per prepared slab
+  const int tile = tile0 + blockIdx.x;
   const int t = threadIdx.x;
+  const int first = tile * kPrepTile;
+  // Key dst of this tile is written by this call when it is one of its own
+  // (key0 <= dst < key0 + n_src) or padding past the sequence (dst >= n_kv).
+  auto owned = [&](int dst) { return (dst >= key0 && dst - key0 < n_src) || dst >= n_kv; };
+  const bool whole = first >= key0 && min(first + kPrepTile, n_kv) <= key0 + n_src;
   // This thread's two 16-byte chunks of the tile: row r, chunk cc (dims 8cc..8cc+7).
-  int r[2], cc[2], pair0[2];
+  int r[2], cc[2], pair0[2], src[2];
   bool valid[2], rot[2];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int c = t + 256 * u;
     r[u] = c >> 4;
     cc[u] = c & 15;
-    const int n = tile * kPrepTile + r[u];
-    valid[u] = n < N;
+    src[u] = first + r[u] - key0;
+    valid[u] = src[u] >= 0 && src[u] < n_src;
     Pos p{0, 0, 0, false};
-    if (kRope && valid[u]) p = token_pos(n, g);
+    if (kRope && valid[u]) p = token_pos(src[u], g);
     rot[u] = kRope && p.rot;
     pair0[u] = rot[u] ? tab_pair(cc[u], p, g) : 0;
   }
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
   for (int64_t bh = blockIdx.y; bh < bh_count; bh += gridDim.y) {
-    const size_t row0 = (size_t)bh * N + (size_t)tile * kPrepTile;
+    const size_t row0 = (size_t)bh * n_src;
     uint4* kt = kp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
     uint4* vtile = vp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      uint4 x = valid[u] ? k[(row0 + r[u]) * kChunks + cc[u]] : zero;
-      if (rot[u]) x = rope_chunk(x, tab, pair0[u]);
-      kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(x);
-      const uint4 y = valid[u] ? v[(row0 + r[u]) * kChunks + cc[u]] : zero;
+      const uint4 x = valid[u] ? k[(row0 + src[u]) * kChunks + cc[u]] : zero;
+      // every lane takes part in the row sums (rows sit in 16 aligned lanes)
+      const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(x)), eps) : 1.0f;
+      const uint4 xr = valid[u] ? qk_chunk(x, gamma, inv, cc[u], rot[u], tab, pair0[u]) : zero;
+      if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(xr);
+      const uint4 y = valid[u] ? v[(row0 + src[u]) * kChunks + cc[u]] : zero;
       *reinterpret_cast<uint4*>(&vt[r[u] * (D + 8) + cc[u] * 8]) = bf16x8_to_f16x8(y);
     }
     __syncthreads();
@@ -214,9 +304,17 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
       const int j = c >> 6, ln = c & 63;
       const int kst = j >> 2, db = j & 3, l = ln & 31, h = ln >> 5;
       const uint16_t* col = vt + (16 * kst + 4 * h) * (D + 8) + 32 * db + l;
+      auto key = [&](int i) { return 16 * kst + 4 * h + 8 * (i >> 2) + (i & 3); };
       auto el = [&](int i) { return (uint32_t)col[(8 * (i >> 2) + (i & 3)) * (D + 8)]; };
-      vtile[c] = make_uint4(el(0) | el(1) << 16, el(2) | el(3) << 16, el(4) | el(5) << 16,
-                            el(6) | el(7) << 16);
+      if (whole) {
+        vtile[c] = make_uint4(el(0) | el(1) << 16, el(2) | el(3) << 16, el(4) | el(5) << 16,
+                              el(6) | el(7) << 16);
+      } else {
+        uint16_t* dst = reinterpret_cast<uint16_t*>(vtile + c);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (owned(first + key(i))) dst[i] = (uint16_t)el(i);
+      }
     }
     __syncthreads();
   }
@@ -543,18 +641,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
 
 // ------------------------------------------------- attention on prepared K/V
 
-// Workgroup barrier that orders LDS only: this wave's LDS operations complete
-// (lgkmcnt 0), then s_barrier.  Unlike __syncthreads it does not drain
-// outstanding global loads (vmcnt), so a tile load issued before the barrier
-// keeps streaming across it.  The empty asm statements keep the compiler from
-// moving memory accesses across the barrier.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt 63, expcnt 7, lgkmcnt 0
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // bf16 x8 -> fp32, times s (fp32, RNE) -> fp16 x8 (RNE).
 __device__ __forceinline__ f16x8 bf16x8_to_f16x8_scaled(uint4 x, float s) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
@@ -666,7 +752,8 @@ template <bool kRope, bool kRobust>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
-                          const float2* __restrict__ tab, int n_qtiles, float c_log2) {
+                          const float2* __restrict__ tab, int n_qtiles, float c_log2, int n_keys,
+                          const float* __restrict__ q_gamma, float eps) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
 
@@ -686,8 +773,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int wg = xcd_local_id(blockIdx.x, gridDim.x);
   const int bh = wg / n_qtiles;
   const int qt = wg - bh * n_qtiles;
-  const int N = g.n;
-  const size_t slab = (size_t)bh * N * D;
+  const int Nq = g.n;  // query rows of the slab (the grid describes them)
+  const int N = n_keys;  // keys of the slab
+  const size_t slab = (size_t)bh * Nq * D;
   const uint16_t* __restrict__ qs = q + slab;
   const int n_tiles = (N + BN2 - 1) / BN2;
   const size_t pslab = (size_t)bh * n_tiles * kPrepTileElems;
@@ -703,26 +791,44 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const int row = qrow_first + 32 * qb;
-      if (hh == 0 && row < N) marked |= (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
+      if (hh == 0 && row < Nq) marked |= (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
     }
     if (!__syncthreads_or(marked)) return;
   }
 
-  // ---- Q' fragments of the wave's two 32-row blocks, rotated in the load.
+  // ---- Q' fragments of the wave's two 32-row blocks, normalised (q_gamma)
+  // and rotated in the load.  A lane holds the even (hh = 0) or odd chunks of
+  // its row; the sum of squares pairs them across the lane halves first, then
+  // runs the rest of the fixed tree in the lane.
   const int qrow0 = qrow_first;  // block qb holds row qrow0 + 32 qb
   f16x8 qf[2][8];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    const int row = min(qrow0 + 32 * qb, N - 1);
+    const int row = min(qrow0 + 32 * qb, Nq - 1);
     const uint4* src = reinterpret_cast<const uint4*>(qs + (size_t)row * D);
     Pos p{0, 0, 0, false};
     if (kRope) p = token_pos(row, g);
+    uint4 x[8];
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) x[kk] = src[2 * kk + hh];
+    float inv = 1.0f;
+    if (q_gamma != nullptr) {
+      float s1[8];
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) {
+        const float pk = chunk_sumsq(x[kk]);
+        s1[kk] = pk + __shfl_xor(pk, 32);  // chunks 2kk and 2kk + 1
+      }
+      const float s3a = (s1[0] + s1[1]) + (s1[2] + s1[3]);
+      const float s3b = (s1[4] + s1[5]) + (s1[6] + s1[7]);
+      inv = rms_inv(s3a + s3b, eps);
+    }
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       const int cc = 2 * kk + hh;
-      uint4 x = src[cc];
-      if (kRope) x = rope_chunk(x, tab, tab_pair(cc, p, g));  // prefix: exact identity
-      qf[qb][kk] = bf16x8_to_f16x8_scaled(x, c_log2);
+      // kRope: prefix rows turn by the origin's table entries, an exact identity
+      const uint4 y = qk_chunk(x[kk], q_gamma, inv, cc, kRope, tab, kRope ? tab_pair(cc, p, g) : 0);
+      qf[qb][kk] = bf16x8_to_f16x8_scaled(y, c_log2);
     }
   }
 
@@ -1073,12 +1179,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     const int row = qrow0 + 32 * qb;
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.0f / l_tot;
-    if (row < N && marked) {
+    if (row < Nq && marked) {
       uint16_t* dst = out_slab + (size_t)row * D;
 #pragma unroll
       for (int c = 0; c < 8; ++c)
         *reinterpret_cast<uint4*>(dst + 64 * hh + 8 * c) = make_uint4(0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u);
-    } else if (row < N) {
+    } else if (row < Nq) {
       uint16_t* dst = out_slab + (size_t)row * D;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
@@ -1097,14 +1203,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 }  // namespace
 
 hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int64_t rows, const SeqGrid& g,
-                         const float2* tab, hipStream_t stream) {
+                         const float2* tab, const float* gamma, float eps, hipStream_t stream) {
   const int64_t per_slab = (int64_t)g.n * kChunks;
   const int64_t bh_count = rows / g.n;
   const unsigned gx = (unsigned)((per_slab + 255) / 256);
   const unsigned gy = (unsigned)(bh_count < 65535 ? bh_count : 65535);
   hipLaunchKernelGGL(rope3d_kernel, dim3(gx, gy), dim3(256), 0, stream,
                      reinterpret_cast<const uint4*>(x), reinterpret_cast<uint4*>(y), bh_count, g,
-                     tab);
+                     tab, gamma, eps);
   return hipGetLastError();
 }
 
@@ -1129,19 +1235,21 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 
 hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_prep,
                              uint16_t* v_prep, int BH, const SeqGrid& g, const float2* tab,
+                             int key0, int n_kv, const float* gamma, float eps,
                              hipStream_t stream) {
-  const int n_tiles = (g.n + kPrepTile - 1) / kPrepTile;
-  const dim3 pgrid((unsigned)n_tiles, (unsigned)(BH < 65535 ? BH : 65535));
+  const int tile0 = key0 / kPrepTile;
+  const int tile1 = (key0 + g.n - 1) / kPrepTile;  // last tile holding one of these keys
+  const dim3 pgrid((unsigned)(tile1 - tile0 + 1), (unsigned)(BH < 65535 ? BH : 65535));
   if (tab != nullptr)
     hipLaunchKernelGGL(prep_kv_kernel<true>, pgrid, dim3(256), 0, stream,
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
                        reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
-                       (int64_t)BH, g, tab);
+                       (int64_t)BH, g, tab, key0, n_kv, tile0, gamma, eps);
   else
     hipLaunchKernelGGL(prep_kv_kernel<false>, pgrid, dim3(256), 0, stream,
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
                        reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
-                       (int64_t)BH, g, tab);
+                       (int64_t)BH, g, tab, key0, n_kv, tile0, gamma, eps);
   return hipGetLastError();
 }
 
@@ -1151,26 +1259,30 @@ int64_t prepared_tile_elems(int N) {
 
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, uint16_t* out, int BH,
-                                    const SeqGrid& g, const float2* tab, hipStream_t stream) {
+                                    const SeqGrid& g, int n_kv, const float2* tab,
+                                    const float* q_gamma, float eps, hipStream_t stream) {
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
-  if (tab != nullptr)
-    hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_prep,
-                       v_prep, out, g, tab, n_qtiles, c_log2);
-  else
-    hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_prep,
-                       v_prep, out, g, tab, n_qtiles, c_log2);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // Second pass over the row blocks whose probabilities left the fp16 range.
-  if (tab != nullptr)
-    hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_prep,
-                       v_prep, out, g, tab, n_qtiles, c_log2);
-  else
-    hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_prep,
-                       v_prep, out, g, tab, n_qtiles, c_log2);
-  return hipGetLastError();
+  // First pass, then the second over the row blocks whose probabilities left
+  // the fp16 range.
+  for (int pass = 0; pass < 2; ++pass) {
+    if (tab != nullptr && pass == 0)
+      hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_prep,
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+    else if (pass == 0)
+      hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_prep,
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+    else if (tab != nullptr)
+      hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_prep,
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+    else
+      hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_prep,
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 int64_t attn_max_workgroups(int N, int BH) { return (int64_t)((N + BM - 1) / BM) * BH; }

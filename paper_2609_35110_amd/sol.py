@@ -1,8 +1,10 @@
 """Python binding of libsol.so (include/sol.h): argument marshalling only.
 
 The ``sol_*`` functions mirror the C ABI one to one (device pointers and
-streams as integers).  ``rope3d_table``, ``rope3d`` and ``attn_fwd`` take torch
-tensors and pass their device pointers and the current HIP stream.  Every
+streams as integers).  The other functions (``rope3d_table``, ``rope3d``,
+``qknorm_rope3d``, ``attn_fwd``, ``prepare_kv[_ex]``, ``attn_fwd_prepared[_ex]``
+...) take torch tensors and pass their device pointers and the current HIP
+stream.  Every
 step of the computation runs in the HIP library; there is no fallback: if
 libsol.so is missing or fails to load, every call raises.
 """
@@ -57,6 +59,15 @@ def lib():
         L.sol_attn_workspace_bytes.restype = sz
         L.sol_attn_fwd_ws.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, sz, P]
         L.sol_attn_fwd_ws.restype = i32
+        f32 = ctypes.c_float
+        L.sol_qknorm_rope3d.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32, P]
+        L.sol_qknorm_rope3d.restype = i32
+        L.sol_prepare_kv_ex.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32,
+                                        P, P, f32, P]
+        L.sol_prepare_kv_ex.restype = i32
+        L.sol_attn_fwd_prepared_ex.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
+                                               P, P, f32, P]
+        L.sol_attn_fwd_prepared_ex.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
         L.sol_last_error.argtypes = []
@@ -79,6 +90,22 @@ def sol_rope3d_table(host_tab, n_floats, D, T, Hl, Wl, base):
 
 def sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream):
     return lib().sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, stream):
+    return lib().sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, stream)
+
+
+def sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl, rope_tab, gamma,
+                      eps, stream):
+    return lib().sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl,
+                                   rope_tab, gamma, eps, stream)
+
+
+def sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl, rope_tab, gamma,
+                             eps, stream):
+    return lib().sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl,
+                                          rope_tab, gamma, eps, stream)
 
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
@@ -176,6 +203,29 @@ def rope3d(x, T, Hl, Wl, table, out=None):
     return out
 
 
+def _gamma_ptr(gamma, dev):
+    if gamma is None:
+        return None
+    if (not isinstance(gamma, torch.Tensor) or gamma.dtype != torch.float32 or gamma.device != dev
+            or not gamma.is_contiguous() or gamma.shape != (HEAD_DIM,)):
+        raise ValueError("gamma must be a contiguous float32 tensor of %d weights on %s"
+                         % (HEAD_DIM, dev))
+    return ctypes.c_void_p(gamma.data_ptr())
+
+
+def qknorm_rope3d(x, T, Hl, Wl, table, gamma, eps=1e-6, out=None):
+    """out = bf16(R(pos) rms_norm(x; gamma, eps)) for x [B, H, N, D] bf16."""
+    _check_tensor("x", x)
+    B, H, N, D = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    _check_tensor("out", out, x.shape)
+    check(sol_qknorm_rope3d(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H,
+                            N, D, T, Hl, Wl, _table_ptr(table, x.device),
+                            _gamma_ptr(gamma, x.device), float(eps), _stream(x)))
+    return out
+
+
 def attn_fwd(q, k, v, T, Hl, Wl, table=None, out=None):
     """softmax(q^ k^T / sqrt(D)) v with the 3D rotary embedding fused (table=None: none)."""
     _check_tensor("q", q)
@@ -260,4 +310,48 @@ def attn_fwd_prepared(q, k_prep, v_prep, T, Hl, Wl, table=None, out=None):
     check(sol_attn_fwd_prepared(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                                 ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                                 B, H, N, D, T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
+    return out
+
+
+def prepared_kv_buffers(B, H, n_kv, device):
+    """Two zero-initialised float16 buffers for a prepared sequence of n_kv keys."""
+    n = sol_prepared_kv_bytes(B, H, n_kv, HEAD_DIM) // 2
+    return (torch.zeros(n, dtype=torch.float16, device=device),
+            torch.zeros(n, dtype=torch.float16, device=device))
+
+
+def prepare_kv_ex(k, v, T, Hl, Wl, table, k_prep, v_prep, key0=0, n_kv=None, gamma=None, eps=1e-6):
+    """Write k, v [B, H, N, D] (rotated with grid T x Hl x Wl, normalised with
+    gamma if given) as keys key0 .. key0 + N - 1 of the prepared sequence of
+    n_kv keys held by k_prep, v_prep."""
+    _check_tensor("k", k)
+    _check_tensor("v", v, k.shape)
+    B, H, N, D = k.shape
+    n_kv = N if n_kv is None else n_kv
+    nbytes = sol_prepared_kv_bytes(B, H, n_kv, D)
+    _check_prepared("k_prep", k_prep, nbytes, k.device)
+    _check_prepared("v_prep", v_prep, nbytes, k.device)
+    check(sol_prepare_kv_ex(ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
+                            ctypes.c_void_p(k_prep.data_ptr()), ctypes.c_void_p(v_prep.data_ptr()),
+                            B, H, N, key0, n_kv, D, T, Hl, Wl, _table_ptr(table, k.device),
+                            _gamma_ptr(gamma, k.device), float(eps), _stream(k)))
+    return k_prep, v_prep
+
+
+def attn_fwd_prepared_ex(q, k_prep, v_prep, n_kv, T, Hl, Wl, table=None, gamma=None, eps=1e-6,
+                         out=None):
+    """q [B, H, N, D] (rotated with grid T x Hl x Wl, normalised with gamma if
+    given) against the n_kv prepared keys of k_prep, v_prep."""
+    _check_tensor("q", q)
+    B, H, N, D = q.shape
+    nbytes = sol_prepared_kv_bytes(B, H, n_kv, D)
+    _check_prepared("k_prep", k_prep, nbytes, q.device)
+    _check_prepared("v_prep", v_prep, nbytes, q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensor("out", out, q.shape)
+    check(sol_attn_fwd_prepared_ex(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
+                                   ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                   B, H, N, n_kv, D, T, Hl, Wl, _table_ptr(table, q.device),
+                                   _gamma_ptr(gamma, q.device), float(eps), _stream(q)))
     return out

@@ -14,6 +14,13 @@ public dataset; every tensor here is synthetic:
 * ``p720``  : B=1, H=40, grid 31x45x80 (N=111,600), N(0,1)
 * ``share`` : B=2, H=5,  grid 31x45x80 + 512 text tokens first (N=112,112);
               video N(0,1), text q N(0,1), text k/v N(0, 0.5^2)
+* ``p720n`` : ``p720`` before QK normalization (Sec. 3.5, fusion group 2):
+              every q and k row scaled by 2^e, e uniform in [-4, 4] per token,
+              and per-dimension weights gamma_q, gamma_k
+* ``ref720``: the reference-KV cache of Sec. 5 at 720p: queries = 512 text
+              tokens + grid 31x45x80 (Nq=112,112); keys = one cached
+              reference video (grid 8x45x80, 28,800 tokens, its own positions
+              from 0) followed by the queries' own tokens (Nkv=140,912)
 
 Recipe: every (tensor, b, h) slab has its own torch CPU ``Generator``, seeded
 with ``slab_seed(seed, tensor, b*H + h)`` where seed = 20260903 + config index
@@ -23,6 +30,13 @@ nearest even.  The boosted keys are ``randperm(N)[:N//100]`` from a generator
 seeded with ``slab_seed(seed, 3, 0)``, the same tokens in every head, multiplied
 by 8 after the bf16 cast (exact).  Slabs are independent, so they are drawn in
 parallel and any single slab can be regenerated alone.
+
+QK-normalisation workloads (``qk_norm``): the q and k rows are then multiplied
+by 2^e (exact), e = ``randint(-4, 5)`` per token from generators seeded with
+``slab_seed(seed, 4 or 5, b*H + h)``; the weights are bf16-exact float32
+values 1 + 0.25 N(0,1) (``slab_seed(seed, 6 or 7, 0)``).  Reference segments
+(``n_ref``): k and v of the cached tokens are drawn like the video rows, with
+tensor ids 8 and 9.
 """
 from concurrent.futures import ThreadPoolExecutor
 import os
@@ -48,6 +62,8 @@ class Workload:
     text_kv_std: float = 1.0    # std of the text-prefix k and v draws
     boost_frac: float = 0.0     # fraction of key tokens multiplied by boost
     boost: float = 1.0
+    qk_norm: bool = False       # q, k rows drawn at random scales; norm weights given
+    ref_grid: tuple = ()        # grid (T, Hl, Wl) of a cached reference segment
     D: int = HEAD_DIM
 
     @property
@@ -63,15 +79,33 @@ class Workload:
         return SEED_BASE + self.index
 
     @property
+    def n_ref(self) -> int:
+        """Tokens of the cached reference segment (0: none)."""
+        if not self.ref_grid:
+            return 0
+        T, Hl, Wl = self.ref_grid
+        return T * Hl * Wl
+
+    @property
+    def n_kv(self) -> int:
+        """Keys per (b, h): the reference segment, then the N own tokens."""
+        return self.n_ref + self.N
+
+    @property
     def flops(self) -> float:
-        """Algorithmic flops of one layer: 4 N^2 D per (b, h)."""
-        return 4.0 * self.N * self.N * self.D * self.H * self.B
+        """Algorithmic flops of one layer: 4 Nq Nkv D per (b, h)."""
+        return 4.0 * self.N * self.n_kv * self.D * self.H * self.B
 
     def describe(self) -> str:
         s = "B=%d H=%d D=%d grid %dx%dx%d" % (self.B, self.H, self.D, self.T, self.Hl, self.Wl)
         if self.n_text:
             s += " + %d text" % self.n_text
-        return s + " (N=%d)" % self.N
+        s += " (N=%d)" % self.N
+        if self.n_ref:
+            s += ", cached reference grid %dx%dx%d (Nkv=%d)" % (self.ref_grid + (self.n_kv,))
+        if self.qk_norm:
+            s += ", QK norm"
+        return s
 
 
 WORKLOADS = {
@@ -80,7 +114,12 @@ WORKLOADS = {
     "p480": Workload("p480", 2, 1, 40, 31, 30, 52, boost_frac=0.01, boost=8.0),
     "p720": Workload("p720", 3, 1, 40, 31, 45, 80),
     "share": Workload("share", 4, 2, 5, 31, 45, 80, n_text=512, text_kv_std=0.5),
+    "p720n": Workload("p720n", 5, 1, 40, 31, 45, 80, qk_norm=True),
+    "ref720": Workload("ref720", 6, 1, 40, 31, 45, 80, n_text=512, ref_grid=(8, 45, 80)),
 }
+
+# eps under the root of the QK normalisation in the qk_norm workloads
+QK_NORM_EPS = 1e-6
 
 
 def custom(B, H, T, Hl, Wl, n_text=0, seed_index=100, **kw) -> Workload:
@@ -132,6 +171,44 @@ def make_inputs(w: Workload, seed: int = None, threads: int = None):
     idx = boosted_tokens(w, seed)
     if idx.numel():
         out[1][:, :, idx, :] *= torch.tensor(w.boost, dtype=torch.bfloat16)
+    if w.qk_norm:
+        for t in (0, 1):
+            x = out[t].view(w.B * w.H, w.N, w.D)
+            for bh in range(w.B * w.H):
+                gen = torch.Generator().manual_seed(slab_seed(seed, 4 + t, bh))
+                e = torch.randint(-4, 5, (w.N, 1), generator=gen).to(torch.float32)
+                x[bh].mul_(torch.exp2(e).to(torch.bfloat16))  # powers of two: exact
+    return tuple(out)
+
+
+def norm_weights(w: Workload, seed: int = None):
+    """(gamma_q, gamma_k): float32 [D] QK-normalisation weights, bf16-exact
+    values 1 + 0.25 N(0,1)."""
+    seed = w.seed if seed is None else seed
+    res = []
+    for t in (6, 7):
+        gen = torch.Generator().manual_seed(slab_seed(seed, t, 0))
+        g = 1.0 + 0.25 * torch.randn(w.D, generator=gen, dtype=torch.float32)
+        res.append(g.to(torch.bfloat16).to(torch.float32))
+    return tuple(res)
+
+
+def make_ref_inputs(w: Workload, seed: int = None, threads: int = None):
+    """(k_ref, v_ref): the cached reference segment's keys and values, bf16
+    [B, H, n_ref, D], drawn like video rows (N(0,1) times the workload scale)."""
+    seed = w.seed if seed is None else seed
+    rw = Workload("ref", w.index, w.B, w.H, *w.ref_grid, scale=w.scale, D=w.D)
+    out = [torch.empty((w.B, w.H, w.n_ref, w.D), dtype=torch.bfloat16) for _ in range(2)]
+    jobs = [(t, bh) for t in range(2) for bh in range(w.B * w.H)]
+    if threads is None:
+        threads = min(16, len(os.sched_getaffinity(0)))
+
+    def run(job):
+        t, bh = job
+        _fill_slab(out[t].view(w.B * w.H, w.n_ref, w.D)[bh], seed, 8 + t, bh, rw)
+
+    with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
+        list(ex.map(run, jobs))
     return tuple(out)
 
 

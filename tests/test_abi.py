@@ -39,7 +39,7 @@ def test_status_strings(L):
     assert sol.sol_status_string(0) == "ok"
     for s in (-1, -2, -3):
         assert sol.sol_status_string(s) not in ("ok", "unknown status")
-    assert sol.sol_version() == 100
+    assert sol.sol_version() == 101
 
 
 # Fake, 16-byte aligned device addresses: every call below is rejected on the
@@ -150,6 +150,65 @@ def test_rope3d_rejects_before_any_hip_call(L, kw, status):
     args.update(kw)
     st = sol.sol_rope3d(args["x"], args["y"], args["B"], args["H"], args["N"], args["D"],
                         args["T"], args["Hl"], args["Wl"], args["tab"], None)
+    assert st == status, sol.sol_last_error()
+
+
+G = P(0x20000000)  # fake, aligned device address of normalisation weights
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(key0=-1), -1, "do not fit"),
+    (dict(key0=100, n_kv=291), -1, "do not fit"),     # 100 + 192 > 291
+    (dict(n_kv=0), -1, "n_kv"),
+    (dict(n_kv=(1 << 23) + 1), -2, "n_kv"),
+    (dict(gamma=P(0x20000004)), -1, "gamma must be 16-byte aligned"),
+    (dict(eps=-1e-6), -1, "eps"),
+    (dict(eps=float("nan")), -1, "eps"),
+    (dict(k_prep=P(0x200000 + 4096)), -1, "overlap"),   # k_prep inside v
+    (dict(T=9), -1, "more tokens"),
+])
+def test_prepare_kv_ex_rejects_before_any_hip_call(L, kw, status, fragment):
+    args = dict(k=A, v=Bp, k_prep=P(0x1000000), v_prep=P(0x2000000), B=1, H=2, N=192, key0=0,
+                n_kv=192, D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6)
+    args.update(kw)
+    st = sol.sol_prepare_kv_ex(args["k"], args["v"], args["k_prep"], args["v_prep"], args["B"],
+                               args["H"], args["N"], args["key0"], args["n_kv"], args["D"], args["T"],
+                               args["Hl"], args["Wl"], args["tab"], args["gamma"], args["eps"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(n_kv=0), -1, "n_kv"),
+    (dict(gamma=P(0x20000008)), -1, "gamma must be 16-byte aligned"),
+    (dict(eps=float("inf")), -1, "eps"),
+    (dict(out=P(0x1000000 + 256)), -1, "overlaps"),   # out inside k_prep of 1000 keys
+    (dict(D=64), -2, "head dim"),
+])
+def test_attn_fwd_prepared_ex_rejects_before_any_hip_call(L, kw, status, fragment):
+    args = dict(q=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=192, n_kv=1000,
+                D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6)
+    args.update(kw)
+    st = sol.sol_attn_fwd_prepared_ex(args["q"], args["k_prep"], args["v_prep"], args["out"],
+                                      args["B"], args["H"], args["N"], args["n_kv"], args["D"],
+                                      args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"],
+                                      args["eps"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(gamma=P(0x20000002)), -1),
+    (dict(eps=-0.5), -1),
+    (dict(tab=None), -1),
+    (dict(D=96), -2),
+])
+def test_qknorm_rope3d_rejects_before_any_hip_call(L, kw, status):
+    args = dict(x=A, y=Bp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6)
+    args.update(kw)
+    st = sol.sol_qknorm_rope3d(args["x"], args["y"], args["B"], args["H"], args["N"], args["D"],
+                               args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"],
+                               args["eps"], None)
     assert st == status, sol.sol_last_error()
 
 
