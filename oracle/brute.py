@@ -129,3 +129,41 @@ def fused_reference(q_bits, k_bits, v_bits, T, Hl, Wl, contract=True,
     qh = prepare_np(q_bits, T, Hl, Wl, q_gamma, eps, True, contract, split, base)
     kh = prepare_np(k_bits, Tk, Hlk, Wlk, k_gamma, eps, rope_k, contract, split, base)
     return attention_np(qh, kh, v)
+
+
+def e4m3_values():
+    """The value of every FP8 E4M3 code 0..255 (OCP E4M3FN: bias 7, 3 mantissa
+    bits, no infinities, 0x7F and 0xFF NaN), float64 [256], from the format's
+    definition."""
+    vals = np.empty(256, dtype=np.float64)
+    for c in range(256):
+        s = -1.0 if c & 0x80 else 1.0
+        e = (c >> 3) & 0xF
+        m = c & 7
+        if e == 0xF and m == 7:
+            vals[c] = np.nan
+        elif e == 0:
+            vals[c] = s * m * 2.0 ** -9
+        else:
+            vals[c] = s * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+    return vals
+
+
+def nearest_e4m3(x):
+    """Round float64 to the nearest finite E4M3 code by searching all of them
+    (ties to the even code, saturating at +-448); finite inputs.  uint8 codes."""
+    # beyond 448 the nearest finite code is +-448; clipping first keeps the
+    # distances below exact for huge inputs
+    x = np.clip(np.asarray(x, dtype=np.float64), -512.0, 512.0)
+    vals = e4m3_values()
+    codes = np.array([c for c in range(256) if np.isfinite(vals[c]) and c != 0x80], dtype=np.int64)
+    cv = vals[codes]
+    dist = np.abs(x[..., None] - cv)
+    best = dist.min(axis=-1, keepdims=True)
+    tie = dist == best
+    even = (codes & 1) == 0
+    pick = np.where(tie.sum(-1, keepdims=True) > 1, tie & even, tie)
+    c = codes[np.argmax(pick, axis=-1)]
+    # signed zero: keep the sign of x (code 0x80 is -0)
+    c = np.where((cv[np.argmax(pick, axis=-1)] == 0) & np.signbit(x), 0x80, c)
+    return c.astype(np.uint8)

@@ -89,6 +89,40 @@ void solref_round_bf16(const double* x, uint16_t* y, int64_t n) {
   for (int64_t i = 0; i < n; ++i) y[i] = double_to_bf16(x[i]);
 }
 
+/* double -> FP8 E4M3 code (the OCP "E4M3FN" format: sign, 4 exponent bits of
+ * bias 7, 3 mantissa bits; no infinities; codes 0x7F/0xFF are NaN; largest
+ * finite value 448, smallest subnormal 2^-9), round to nearest, ties to even,
+ * saturating: every |x| >= 448 (infinities included) gives +-448.  This is the
+ * raw E4M3 output the paper's attention hands to the next GEMM with unit
+ * scales (Sec. 3.5, "Joint optimization with quantized communication"). */
+static uint8_t double_to_e4m3(double x) {
+  if (isnan(x)) return 0x7f;
+  uint8_t sign = signbit(x) ? 0x80 : 0;
+  double a = fabs(x);
+  if (a >= 448.0) return sign | 0x7e;
+  if (a == 0.0) return sign;
+  int e;
+  (void)frexp(a, &e);
+  e -= 1;                  /* 2^e <= a < 2^(e+1) */
+  if (e < -6) e = -6;      /* subnormal range: fixed quantum 2^-9 */
+  double quantum = ldexp(1.0, e - 3);
+  double n = a / quantum;  /* exact: power-of-two division */
+  double fl = floor(n);
+  double rem = n - fl;
+  if (rem > 0.5 || (rem == 0.5 && ((int64_t)fl & 1))) fl += 1.0;
+  int m = (int)fl;         /* significand in units of the quantum: 0..16 */
+  if (m == 16) {           /* rounded up into the next binade */
+    m = 8;
+    e += 1;
+  }
+  if (m < 8) return sign | (uint8_t)m;  /* subnormal (e == -6) */
+  return sign | (uint8_t)(((e + 7) << 3) | (m - 8));
+}
+
+void solref_round_e4m3(const double* x, uint8_t* y, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) y[i] = double_to_e4m3(x[i]);
+}
+
 /* Position of token n on each axis; returns 0 for a prefix (unrotated) token. */
 static int token_position(int64_t n, int N, int T, int Hl, int Wl, int* pt, int* ph, int* pw) {
   int64_t nv = (int64_t)T * Hl * Wl;

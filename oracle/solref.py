@@ -37,6 +37,8 @@ class Oracle:
         i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         lib.solref_round_bf16.argtypes = [P, P, i64]
         lib.solref_round_bf16.restype = None
+        lib.solref_round_e4m3.argtypes = [P, P, i64]
+        lib.solref_round_e4m3.restype = None
         lib.solref_rope3d_f64.argtypes = [P, P, i64, i32, i32, i32, i32, i32, i32, i32, i32, f64]
         lib.solref_rope3d_f64.restype = None
         lib.solref_rope3d.argtypes = [P, P, i64, i32, i32, i32, i32, i32, i32, i32, i32, f64]
@@ -65,6 +67,13 @@ class Oracle:
         x = np.ascontiguousarray(x, dtype=np.float64)
         y = np.empty(x.shape, dtype=np.uint16)
         self.lib.solref_round_bf16(_ptr(x), _ptr(y), x.size)
+        return y
+
+    def round_e4m3(self, x) -> np.ndarray:
+        """float64 -> FP8 E4M3 codes (uint8): round to nearest even, saturating at +-448."""
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        y = np.empty(x.shape, dtype=np.uint8)
+        self.lib.solref_round_e4m3(_ptr(x), _ptr(y), x.size)
         return y
 
     def rope3d_f64(self, x, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE) -> np.ndarray:
@@ -172,6 +181,10 @@ def num_threads():
 
 def round_bf16(x):
     return default().round_bf16(x)
+
+
+def round_e4m3(x):
+    return default().round_e4m3(x)
 
 
 def rope3d_f64(x, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE):

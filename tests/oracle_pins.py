@@ -528,4 +528,58 @@ def pin_attention_kv_segments_commute(o):
     assert np.allclose(ab, want, atol=2e-6, rtol=1e-6)
 
 
+# ------------------------------------------------------- FP8 E4M3 output codes
+
+def _e4m3_torch_codes(x):
+    t = torch.from_numpy(np.asarray(x, dtype=np.float32)).to(torch.float8_e4m3fn)
+    return t.view(torch.uint8).numpy()
+
+
+def _e4m3_test_values(rng):
+    """Random values over the whole range (subnormals included), every exact
+    midpoint between neighbouring finite codes, and the codes themselves."""
+    vals = brute.e4m3_values()
+    fin = np.sort(np.unique(vals[np.isfinite(vals)]))
+    mids = (fin[:-1] + fin[1:]) / 2
+    x = rng.standard_normal(20000) * np.exp2(rng.uniform(-11, 9, 20000))
+    return np.concatenate([x, mids, fin, -mids])
+
+
+def pin_e4m3_decode_table_is_torch(o):
+    """The format's definition (numpy twin) decodes every code as torch's
+    float8_e4m3fn does (library routine)."""
+    want = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = brute.e4m3_values()
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    assert np.array_equal(got[~np.isnan(got)], want[~np.isnan(want)])
+
+
+def pin_e4m3_round_vs_torch(o):
+    """Inside the finite range (|x| < 464, where rounding cannot pass 448) the
+    oracle's codes are torch's float8_e4m3fn conversion (round to nearest
+    even), midpoints and subnormals included."""
+    rng = np.random.default_rng(50)
+    x = _e4m3_test_values(rng)
+    x = x[np.abs(x) < 464].astype(np.float32).astype(np.float64)  # float32-exact inputs
+    assert np.array_equal(o.round_e4m3(x), _e4m3_torch_codes(x))
+
+
+def pin_e4m3_round_vs_brute(o):
+    """The oracle's codes are the nearest finite code found by search (ties to
+    the even code), saturating at +-448, over the whole range."""
+    rng = np.random.default_rng(51)
+    x = np.concatenate([_e4m3_test_values(rng), [449.0, -500.0, 1e6, -3e38]])
+    assert np.array_equal(o.round_e4m3(x), brute.nearest_e4m3(x))
+
+
+def pin_e4m3_saturation_and_specials(o):
+    """Beyond the largest finite value (448) every input saturates, infinities
+    included; NaN stays NaN; every finite code round-trips."""
+    got = o.round_e4m3(np.array([448.0, 464.0, 1e4, np.inf, -np.inf, -449.0, np.nan, 0.0, -0.0]))
+    assert got.tolist() == [0x7E, 0x7E, 0x7E, 0x7E, 0xFE, 0xFE, 0x7F, 0x00, 0x80]
+    vals = brute.e4m3_values()
+    codes = np.array([c for c in range(256) if np.isfinite(vals[c])])
+    assert np.array_equal(o.round_e4m3(vals[codes]), codes.astype(np.uint8))
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -117,6 +117,12 @@ MUTANTS = [
      "  if (gamma && n >= (int64_t)N - (int64_t)T * Hl * Wl) {\n    rms_normalize"),
     ("norm: keys not normalised", "J->base, J->kside.rope, J->contract, J->kside.gamma, J->eps);",
      "J->base, J->kside.rope, J->contract, NULL, J->eps);"),
+    # FP8 E4M3 output codes
+    ("e4m3: ties rounded away from zero", "if (rem > 0.5 || (rem == 0.5 && ((int64_t)fl & 1))) fl += 1.0;",
+     "if (rem >= 0.5) fl += 1.0;"),
+    ("e4m3: subnormal quantum halved", "if (e < -6) e = -6;", "if (e < -7) e = -7;"),
+    ("e4m3: exponent bias 8", "((e + 7) << 3)", "((e + 8) << 3)"),
+    ("e4m3: no saturation", "if (a >= 448.0) return sign | 0x7e;", "if (a >= 480.0) return sign | 0x7f;"),
     # queries and keys of different lengths
     ("key count taken from the queries", "for (int j = 0; j < Nkv; ++j) {\n    const double* kj",
      "for (int j = 0; j < Nkv && j < J->qs.N; ++j) {\n    const double* kj"),
