@@ -54,6 +54,12 @@ enum {
   SOL_ERR_HIP = -3          /* the HIP runtime reported an error */
 };
 
+/* Output formats of sol_attn_fwd_prepared_ex. */
+enum {
+  SOL_OUT_BF16 = 0,    /* bf16, round to nearest even (every other entry point) */
+  SOL_OUT_FP8_E4M3 = 1 /* FP8 E4M3 bytes with unit scale (see sol_attn_fwd_prepared_ex) */
+};
+
 /* Largest N the kernels accept (token indices stay exact in float32 arithmetic). */
 #define SOL_MAX_TOKENS (1 << 23)
 
@@ -183,8 +189,14 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
  * rotated with the grid T x Hl x Wl, RMS-normalised first with q_gamma_dev)
  * against the n_kv prepared keys: out = softmax(q^ k^T / sqrt(D)) v over all
  * of them (n_kv may differ from N).  Every key must have been written by a
- * sol_prepare_kv_ex call.  sol_attn_fwd_prepared(...) is this call with n_kv
- * = N and no normalisation.
+ * sol_prepare_kv_ex call.  out_format SOL_OUT_BF16: out is bf16 (2 bytes per
+ * element); SOL_OUT_FP8_E4M3: out holds one FP8 E4M3 byte per element (OCP
+ * E4M3FN: bias 7, 3 mantissa bits, no infinities, 0x7F NaN) with unit scale --
+ * the raw E4M3 values the paper's attention hands to the quantized output
+ * projection (Sec. 3.5, "Joint optimization with quantized communication") --
+ * rounded to nearest even from the fp32 result and saturated at +-448.
+ * sol_attn_fwd_prepared(...) is this call with n_kv = N, no normalisation and
+ * bf16 output.
  *
  * gamma pointers: D fp32 device weights, 16-byte aligned, or NULL; eps as in
  * sol_qknorm_rope3d (ignored when the pointer is NULL).  Other arguments,
@@ -197,7 +209,7 @@ int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, 
 int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_prep, void* out,
                              int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl,
                              const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                             sol_stream_t stream);
+                             int out_format, sol_stream_t stream);
 
 /*
  * Bytes of device workspace sol_attn_fwd_ws needs: room for k_prep then

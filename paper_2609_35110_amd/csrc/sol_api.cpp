@@ -206,7 +206,7 @@ int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int
 int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_prep, void* out,
                              int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl,
                              const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                             sol_stream_t stream) {
+                             int out_format, sol_stream_t stream) {
   if (!q || !k_prep || !v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "q, k_prep, v_prep, out must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
@@ -217,17 +217,20 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   st = check_norm(q_gamma_dev, eps);
   if (st != SOL_OK) return st;
+  if (out_format != SOL_OUT_BF16 && out_format != SOL_OUT_FP8_E4M3)
+    return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
   const size_t bytes = (size_t)B * H * N * D * 2;
+  const size_t obytes = out_format == SOL_OUT_BF16 ? bytes : bytes / 2;
   const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
-  if (overlaps(out, bytes, q, bytes) || overlaps(out, bytes, k_prep, pbytes) || overlaps(out, bytes, v_prep, pbytes))
+  if (overlaps(out, obytes, q, bytes) || overlaps(out, obytes, k_prep, pbytes) || overlaps(out, obytes, v_prep, pbytes))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep or v_prep");
   if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
   const int64_t nv = (int64_t)T * Hl * Wl;
   const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
   hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
-                                               static_cast<const uint16_t*>(v_prep), static_cast<uint16_t*>(out),
-                                               B * H, g, n_kv, tab, q_gamma_dev, eps,
+                                               static_cast<const uint16_t*>(v_prep), out, B * H, g, n_kv, tab,
+                                               q_gamma_dev, eps, out_format == SOL_OUT_FP8_E4M3,
                                                reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_prepared launch: %s", hipGetErrorString(e));
   return ok();
@@ -237,7 +240,7 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
                           int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                           sol_stream_t stream) {
   return sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, N, D, T, Hl, Wl, rope_tab_dev,
-                                  nullptr, 0.0f, stream);
+                                  nullptr, 0.0f, SOL_OUT_BF16, stream);
 }
 
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,

@@ -43,11 +43,13 @@ hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_p
                              int key0, int n_kv, const float* gamma, float eps,
                              hipStream_t stream);
 // g.n query rows (rotated with grid g, normalised first when q_gamma !=
-// nullptr) against n_kv prepared keys.
+// nullptr) against n_kv prepared keys; out is bf16, or FP8 E4M3 bytes when
+// out_fp8.
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
-                                    const uint16_t* v_prep, uint16_t* out, int BH,
+                                    const uint16_t* v_prep, void* out, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
-                                    const float* q_gamma, float eps, hipStream_t stream);
+                                    const float* q_gamma, float eps, bool out_fp8,
+                                    hipStream_t stream);
 // fp16 elements of one (b, h) slab of prepared K (or V).
 int64_t prepared_tile_elems(int N);
 

@@ -692,6 +692,24 @@ __device__ __forceinline__ float sum_f16x2(uint32_t a) {
 __device__ __forceinline__ void pin(uint32_t& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
+// fp32 -> FP8 E4M3 code (the OCP E4M3FN format: bias 7, 3 mantissa bits, no
+// infinities, 0x7F NaN), round to nearest even, saturating at +-448
+// (infinities too).  The raw E4M3 output the paper's attention hands to the
+// next GEMM with unit scales (Sec. 3.5, "Joint optimization with quantized
+// communication").  Normal results keep 3 of fp32's 23 mantissa bits by an
+// integer round-to-nearest-even on the bit pattern, then move the exponent
+// from fp32's bias 127 to 7; below 2^-6 the quantum is fixed at 2^-9.
+__device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
+  const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80u;
+  const float a = __builtin_fabsf(x);
+  if (__builtin_isnan(a)) return 0x7Fu;
+  if (a >= 448.0f) return sign | 0x7Eu;
+  if (a < 0.015625f) return sign | (uint32_t)__builtin_rintf(a * 512.0f);  // 0..8, exact product
+  const uint32_t ua = __float_as_uint(a);
+  const uint32_t r = (ua + 0x7FFFFu + ((ua >> 20) & 1u)) >> 20;  // exponent:mantissa, rounded
+  return sign | (r - (120u << 3));
+}
+
 // End of a prepared-path iteration: all but the last four vector-memory
 // operations of this wave (this iteration's tile copies into LDS) complete,
 // then the workgroup barrier -- after which every wave's completed copies are
@@ -753,7 +771,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
                           const float2* __restrict__ tab, int n_qtiles, float c_log2, int n_keys,
-                          const float* __restrict__ q_gamma, float eps) {
+                          const float* __restrict__ q_gamma, float eps, int out_fp8) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
 
@@ -783,6 +801,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   // into the main loop makes every LDS wait there a full lgkmcnt(0).
   uint16_t* out_slab = out + slab;
   asm volatile("" : "+s"(out_slab));
+  // out_fp8: one E4M3 byte per element instead of a bf16 pair
+  uint8_t* out8_slab = reinterpret_cast<uint8_t*>(out) + slab;
+  asm volatile("" : "+s"(out8_slab), "+s"(out_fp8));
   const int qrow_first = qt * BM + wave * 64 + l32;
   if (kRobust) {
     // Second pass: only the row blocks the first pass marked (NaN rows) are
@@ -791,7 +812,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const int row = qrow_first + 32 * qb;
-      if (hh == 0 && row < Nq) marked |= (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
+      if (hh == 0 && row < Nq)
+        marked |= out_fp8 ? (out8_slab[(size_t)row * D] & 0x7F) == 0x7F
+                          : (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
     }
     if (!__syncthreads_or(marked)) return;
   }
@@ -1172,13 +1195,35 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 
   // ---- epilogue: out = O / l; register j of block (qb, db) is dim 32db + 8(j/4) + 4hh + j%4.
   // A first-pass wave whose probabilities left the fp16 range writes its rows
-  // as NaN instead (bf16 0x7FC0): the second pass recomputes exactly those.
+  // as NaN instead (bf16 0x7FC0, E4M3 0x7F): the second pass recomputes
+  // exactly those.
   const bool marked = !kRobust && __any(ovf > kP16SumLimit);
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int row = qrow0 + 32 * qb;
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.0f / l_tot;
+    if (out_fp8) {
+      if (row >= Nq) continue;
+      uint8_t* dst = out8_slab + (size_t)row * D;
+      if (marked) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          *reinterpret_cast<uint4*>(dst + 64 * hh + 16 * c) = make_uint4(0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu);
+        continue;
+      }
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          uint32_t w = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w |= f32_to_e4m3(o[qb][db][4 * g4 + e] * inv) << (8 * e);
+          *reinterpret_cast<uint32_t*>(dst + 32 * db + 8 * g4 + 4 * hh) = w;
+        }
+      }
+      continue;
+    }
     if (row < Nq && marked) {
       uint16_t* dst = out_slab + (size_t)row * D;
 #pragma unroll
@@ -1258,9 +1303,12 @@ int64_t prepared_tile_elems(int N) {
 }
 
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
-                                    const uint16_t* v_prep, uint16_t* out, int BH,
+                                    const uint16_t* v_prep, void* out_v, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
-                                    const float* q_gamma, float eps, hipStream_t stream) {
+                                    const float* q_gamma, float eps, bool out_fp8,
+                                    hipStream_t stream) {
+  uint16_t* out = static_cast<uint16_t*>(out_v);
+  const int fp8 = out_fp8 ? 1 : 0;
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
@@ -1269,16 +1317,16 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   for (int pass = 0; pass < 2; ++pass) {
     if (tab != nullptr && pass == 0)
       hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
     else if (pass == 0)
       hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
     else if (tab != nullptr)
       hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
     else
       hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps);
+                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

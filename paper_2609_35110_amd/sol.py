@@ -21,6 +21,8 @@ SOL_OK = 0
 SOL_ERR_INVALID_ARG = -1
 SOL_ERR_UNSUPPORTED = -2
 SOL_ERR_HIP = -3
+SOL_OUT_BF16 = 0
+SOL_OUT_FP8_E4M3 = 1
 HEAD_DIM = 128
 ROPE_BASE = 10000.0
 
@@ -66,7 +68,7 @@ def lib():
                                         P, P, f32, P]
         L.sol_prepare_kv_ex.restype = i32
         L.sol_attn_fwd_prepared_ex.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
-                                               P, P, f32, P]
+                                               P, P, f32, i32, P]
         L.sol_attn_fwd_prepared_ex.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
@@ -103,9 +105,9 @@ def sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl, r
 
 
 def sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl, rope_tab, gamma,
-                             eps, stream):
+                             eps, out_format, stream):
     return lib().sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl,
-                                          rope_tab, gamma, eps, stream)
+                                          rope_tab, gamma, eps, out_format, stream)
 
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
@@ -339,19 +341,28 @@ def prepare_kv_ex(k, v, T, Hl, Wl, table, k_prep, v_prep, key0=0, n_kv=None, gam
 
 
 def attn_fwd_prepared_ex(q, k_prep, v_prep, n_kv, T, Hl, Wl, table=None, gamma=None, eps=1e-6,
-                         out=None):
+                         out=None, fp8=False):
     """q [B, H, N, D] (rotated with grid T x Hl x Wl, normalised with gamma if
-    given) against the n_kv prepared keys of k_prep, v_prep."""
+    given) against the n_kv prepared keys of k_prep, v_prep.  fp8: the output
+    is FP8 E4M3 codes (uint8 [B, H, N, D], unit scale) instead of bf16."""
     _check_tensor("q", q)
     B, H, N, D = q.shape
     nbytes = sol_prepared_kv_bytes(B, H, n_kv, D)
     _check_prepared("k_prep", k_prep, nbytes, q.device)
     _check_prepared("v_prep", v_prep, nbytes, q.device)
-    if out is None:
-        out = torch.empty_like(q)
-    _check_tensor("out", out, q.shape)
+    if fp8:
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.uint8, device=q.device)
+        if (out.dtype != torch.uint8 or tuple(out.shape) != tuple(q.shape) or not out.is_contiguous()
+                or out.device != q.device):
+            raise ValueError("an E4M3 out must be a contiguous uint8 tensor of q's shape and device")
+    else:
+        if out is None:
+            out = torch.empty_like(q)
+        _check_tensor("out", out, q.shape)
     check(sol_attn_fwd_prepared_ex(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                                    ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                                    B, H, N, n_kv, D, T, Hl, Wl, _table_ptr(table, q.device),
-                                   _gamma_ptr(gamma, q.device), float(eps), _stream(q)))
+                                   _gamma_ptr(gamma, q.device), float(eps),
+                                   SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16, _stream(q)))
     return out

@@ -184,15 +184,19 @@ def test_prepare_kv_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     (dict(eps=float("inf")), -1, "eps"),
     (dict(out=P(0x1000000 + 256)), -1, "overlaps"),   # out inside k_prep of 1000 keys
     (dict(D=64), -2, "head dim"),
+    (dict(fmt=2), -1, "out_format"),
+    (dict(fmt=-1), -1, "out_format"),
+    (dict(out=P(0x100000 - 49152)), -1, "overlaps"),   # 96 KB of bf16 out would reach q
+    (dict(out=P(0x100000 - 49152 + 16), fmt=1), -1, "overlaps"),  # 48 KB of E4M3 out reaches q
 ])
 def test_attn_fwd_prepared_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     args = dict(q=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=192, n_kv=1000,
-                D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6)
+                D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6, fmt=0)
     args.update(kw)
     st = sol.sol_attn_fwd_prepared_ex(args["q"], args["k_prep"], args["v_prep"], args["out"],
                                       args["B"], args["H"], args["N"], args["n_kv"], args["D"],
                                       args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"],
-                                      args["eps"], None)
+                                      args["eps"], args["fmt"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
 
