@@ -167,3 +167,32 @@ def nearest_e4m3(x):
     # signed zero: keep the sign of x (code 0x80 is -0)
     c = np.where((cv[np.argmax(pick, axis=-1)] == 0) & np.signbit(x), 0x80, c)
     return c.astype(np.uint8)
+
+
+def sparse_route_np(qh, kh, n_prefix, tau, qblk, kblk):
+    """Block routing on the prepared rows qh, kh [..., N, D] (float64): mean-pooled
+    blocks, scaled dot products, threshold mean + tau * std (numpy's population
+    std), plus the prefix key blocks, the first best block, and every key block
+    for query blocks holding a prefix row.  Returns (mask bool [..., nqb, nkb], scores)."""
+    N, D = qh.shape[-2], qh.shape[-1]
+    nqb, nkb = -(-N // qblk), -(-N // kblk)
+    qbar = np.stack([qh[..., I * qblk:(I + 1) * qblk, :].mean(-2) for I in range(nqb)], -2)
+    kbar = np.stack([kh[..., J * kblk:(J + 1) * kblk, :].mean(-2) for J in range(nkb)], -2)
+    s = np.matmul(qbar, np.swapaxes(kbar, -1, -2)) / np.sqrt(D)
+    thr = s.mean(-1, keepdims=True) + tau * s.std(-1, keepdims=True)
+    mask = s > thr
+    best = np.argmax(s, axis=-1)
+    np.put_along_axis(mask, best[..., None], True, axis=-1)
+    mask[..., :, (np.arange(nkb) * kblk) < n_prefix] = True
+    mask[..., (np.arange(nqb) * qblk) < n_prefix, :] = True
+    return mask, s
+
+
+def sparse_attention_np(qh, kh, v, mask, qblk, kblk):
+    """Exact attention where query i sees only the keys of the key blocks
+    mask[i // qblk] keeps: the full score matrix with -inf elsewhere, scipy softmax."""
+    N, D = qh.shape[-2], qh.shape[-1]
+    s = np.matmul(qh, np.swapaxes(kh, -1, -2)) / np.sqrt(D)
+    keys = np.repeat(np.repeat(mask, qblk, axis=-2), kblk, axis=-1)[..., :N, :kh.shape[-2]]
+    s = np.where(keys, s, -np.inf)
+    return np.matmul(softmax(s, axis=-1), v)

@@ -251,6 +251,8 @@ typedef struct {
   side_t qs;
   int Nkv, D, dt, dh, dw, contract;
   double base, eps;
+  const uint8_t* bmask;   /* block mask of the slab [nqb][nkb], or NULL (dense) */
+  int qblk, kblk, nkb;    /* query / key block sizes, key blocks per slab */
   const int64_t* qrows;   /* query indices within the slab */
   float* out;             /* [nq][D] */
   int64_t nq;
@@ -264,6 +266,8 @@ static void attend_one(slab_job* J, int64_t idx, double* s, double* qhat, double
   rotate_row(J->q + i * D, qhat, i, J->qs.N, D, J->qs.T, J->qs.Hl, J->qs.Wl, J->dt, J->dh, J->dw,
              J->base, J->qs.rope, J->contract, J->qs.gamma, J->eps);
   const double scale = 1.0 / sqrt((double)D);
+  /* keys this query may attend to: all, or those of its block's kept key blocks */
+  const uint8_t* keep = J->bmask ? J->bmask + (i / J->qblk) * (int64_t)J->nkb : NULL;
   /* pass 1: logits and their maximum */
   double m = -INFINITY;
   for (int j = 0; j < Nkv; ++j) {
@@ -271,12 +275,14 @@ static void attend_one(slab_job* J, int64_t idx, double* s, double* qhat, double
     double dot = 0.0;
     for (int d = 0; d < D; ++d) dot += qhat[d] * kj[d];
     s[j] = dot * scale;
+    if (keep && !keep[j / J->kblk]) s[j] = -INFINITY;
     if (s[j] > m) m = s[j];
   }
   /* pass 2: exponentials, normaliser, weighted sum of values */
   double l = 0.0;
   for (int d = 0; d < D; ++d) acc[d] = 0.0;
   for (int j = 0; j < Nkv; ++j) {
+    if (s[j] == -INFINITY) continue; /* a key outside the kept blocks */
     double p = exp(s[j] - m);
     l += p;
     const double* vj = J->vd + (int64_t)j * D;
@@ -362,14 +368,18 @@ static int bad_side(const side_t* s, int D, int dt, int dh, int dw) {
  *   nthreads   : <= 0 means every CPU in the affinity mask
  * Returns 0, or -1 on bad arguments / allocation failure.
  */
-int solref_attn_rows_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int H,
-                        int Nq, int Nkv, int D, int Tq, int Hlq, int Wlq, int Tk, int Hlk, int Wlk,
-                        int dt, int dh, int dw, double base, int rope_q, int rope_k, int contract,
-                        const double* q_gamma, const double* k_gamma, double eps,
-                        const int64_t* rows, int64_t nrows, float* out, int nthreads) {
+static int attn_rows_impl(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int H,
+                          int Nq, int Nkv, int D, int Tq, int Hlq, int Wlq, int Tk, int Hlk, int Wlk,
+                          int dt, int dh, int dw, double base, int rope_q, int rope_k, int contract,
+                          const double* q_gamma, const double* k_gamma, double eps,
+                          const uint8_t* bmask, int qblk, int kblk,
+                          const int64_t* rows, int64_t nrows, float* out, int nthreads) {
   const side_t qs = {Nq, Tq, Hlq, Wlq, rope_q, q_gamma};
   const side_t ks = {Nkv, Tk, Hlk, Wlk, rope_k, k_gamma};
   if (B < 1 || H < 1 || D < 2 || !q || !k || !v || !out || (nrows > 0 && !rows)) return -1;
+  if (bmask && (qblk < 1 || kblk < 1)) return -1;
+  const int nqb = bmask ? (Nq + qblk - 1) / qblk : 0;
+  const int nkb = bmask ? (Nkv + kblk - 1) / kblk : 0;
   if (bad_side(&qs, D, dt, dh, dw) || bad_side(&ks, D, dt, dh, dw) || !(eps >= 0.0)) return -1;
   if (nthreads <= 0) nthreads = solref_num_threads();
   const int64_t qslab = (int64_t)Nq * D, kslab = (int64_t)Nkv * D;
@@ -419,6 +429,8 @@ int solref_attn_rows_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v,
     J.vd = vd;
     J.qs = qs;
     J.Nkv = Nkv; J.D = D; J.dt = dt; J.dh = dh; J.dw = dw; J.base = base; J.eps = eps;
+    J.bmask = bmask ? bmask + bh * (int64_t)nqb * nkb : NULL;
+    J.qblk = qblk; J.kblk = kblk; J.nkb = nkb;
     J.contract = contract;
     J.qrows = qrows;
     J.out = obuf;
@@ -432,6 +444,113 @@ int solref_attn_rows_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v,
     for (int64_t r = 0; r < nq; ++r) memcpy(out + where[r] * D, obuf + r * D, sizeof(float) * D);
   }
   free(qrows); free(where); free(obuf); free(khat); free(vd); free(th);
+  return 0;
+}
+
+int solref_attn_rows_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int H,
+                        int Nq, int Nkv, int D, int Tq, int Hlq, int Wlq, int Tk, int Hlk, int Wlk,
+                        int dt, int dh, int dw, double base, int rope_q, int rope_k, int contract,
+                        const double* q_gamma, const double* k_gamma, double eps,
+                        const int64_t* rows, int64_t nrows, float* out, int nthreads) {
+  return attn_rows_impl(q, k, v, B, H, Nq, Nkv, D, Tq, Hlq, Wlq, Tk, Hlk, Wlk, dt, dh, dw, base,
+                        rope_q, rope_k, contract, q_gamma, k_gamma, eps, NULL, 0, 0, rows, nrows,
+                        out, nthreads);
+}
+
+/* Block-sparse attention: as solref_attn_rows_ex, but query i of slab bh
+ * attends only to the keys of the key blocks J (kblk keys each, from key 0)
+ * with bmask[bh][i / qblk][J] != 0 (bmask: [B*H][ceil(Nq/qblk)][ceil(Nkv/kblk)]);
+ * the softmax runs over those keys alone. */
+int solref_attn_rows_sparse(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int H,
+                            int Nq, int Nkv, int D, int Tq, int Hlq, int Wlq, int Tk, int Hlk,
+                            int Wlk, int dt, int dh, int dw, double base, int rope_q, int rope_k,
+                            int contract, const double* q_gamma, const double* k_gamma, double eps,
+                            const uint8_t* bmask, int qblk, int kblk, const int64_t* rows,
+                            int64_t nrows, float* out, int nthreads) {
+  if (!bmask) return -1;
+  return attn_rows_impl(q, k, v, B, H, Nq, Nkv, D, Tq, Hlq, Wlq, Tk, Hlk, Wlk, dt, dh, dw, base,
+                        rope_q, rope_k, contract, q_gamma, k_gamma, eps, bmask, qblk, kblk, rows,
+                        nrows, out, nthreads);
+}
+
+/*
+ * Block routing of the block-sparse attention (Sec. 3.4, "Per-step dynamic
+ * sparsity" and "Safety rails and the exact prefix KV sink"), for the
+ * self-attention of B*H slabs of N tokens (grid T x Hl x Wl; the first
+ * Nt = N - T*Hl*Wl tokens are the prefix).  Query blocks of qblk rows and key
+ * blocks of kblk keys, both counted from token 0.  With q^, k^ the rows as they
+ * enter the products (normalised if a gamma is given, rotated if rope, rounded
+ * to bf16 if contract):
+ *   qbar_I = mean of q^_i over the rows of block I, kbar_J likewise for keys;
+ *   s_IJ  = <qbar_I, kbar_J> / sqrt(D)          (the block-level score);
+ *   mu_I, sigma_I = mean and population standard deviation of s_IJ over all J;
+ *   key block J is kept for query block I iff s_IJ > mu_I + tau sigma_I, or J
+ *   holds a prefix key (the exact prefix sink), or J is the first block with
+ *   the largest s_IJ (so no block attends to nothing); a query block that
+ *   holds a prefix row keeps every key block (prefix queries attend densely).
+ * Outputs (each may be NULL): mask [B*H][nqb][nkb] (1 = kept), scores s_IJ
+ * [B*H][nqb][nkb] and thresholds mu_I + tau sigma_I [B*H][nqb].
+ */
+int solref_sparse_route(const uint16_t* q, const uint16_t* k, int BH, int N, int D, int T, int Hl,
+                        int Wl, int dt, int dh, int dw, double base, int rope, int contract,
+                        const double* q_gamma, const double* k_gamma, double eps, int qblk,
+                        int kblk, double tau, uint8_t* mask, double* scores, double* thr) {
+  if (BH < 1 || N < 1 || D < 2 || qblk < 1 || kblk < 1 || !q || !k) return -1;
+  if ((int64_t)T * Hl * Wl > N || T < 0 || Hl < 0 || Wl < 0) return -1;
+  const int64_t nt = (int64_t)N - (int64_t)T * Hl * Wl;
+  const int nqb = (N + qblk - 1) / qblk, nkb = (N + kblk - 1) / kblk;
+  double* qbar = (double*)calloc((size_t)nqb * D, sizeof(double));
+  double* kbar = (double*)calloc((size_t)nkb * D, sizeof(double));
+  double* row = (double*)malloc(sizeof(double) * (size_t)D);
+  double* s = (double*)malloc(sizeof(double) * (size_t)nkb);
+  if (!qbar || !kbar || !row || !s) {
+    free(qbar); free(kbar); free(row); free(s);
+    return -1;
+  }
+  const double scale = 1.0 / sqrt((double)D);
+  for (int64_t bh = 0; bh < BH; ++bh) {
+    const uint16_t* qs = q + bh * (int64_t)N * D;
+    const uint16_t* ks = k + bh * (int64_t)N * D;
+    memset(qbar, 0, sizeof(double) * (size_t)nqb * D);
+    memset(kbar, 0, sizeof(double) * (size_t)nkb * D);
+    for (int64_t n = 0; n < N; ++n) {
+      rotate_row(qs + n * D, row, n, N, D, T, Hl, Wl, dt, dh, dw, base, rope, contract, q_gamma, eps);
+      for (int d = 0; d < D; ++d) qbar[(n / qblk) * D + d] += row[d];
+      rotate_row(ks + n * D, row, n, N, D, T, Hl, Wl, dt, dh, dw, base, rope, contract, k_gamma, eps);
+      for (int d = 0; d < D; ++d) kbar[(n / kblk) * D + d] += row[d];
+    }
+    for (int I = 0; I < nqb; ++I) {
+      const int64_t rows = (I + 1) * (int64_t)qblk <= N ? qblk : N - (int64_t)I * qblk;
+      for (int d = 0; d < D; ++d) qbar[I * D + d] /= (double)rows;
+    }
+    for (int J = 0; J < nkb; ++J) {
+      const int64_t keys = (J + 1) * (int64_t)kblk <= N ? kblk : N - (int64_t)J * kblk;
+      for (int d = 0; d < D; ++d) kbar[J * D + d] /= (double)keys;
+    }
+    for (int I = 0; I < nqb; ++I) {
+      double mu = 0.0, var = 0.0;
+      int best = 0;
+      for (int J = 0; J < nkb; ++J) {
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d) dot += qbar[I * D + d] * kbar[J * D + d];
+        s[J] = dot * scale;
+        mu += s[J];
+        if (s[J] > s[best]) best = J;
+      }
+      mu /= (double)nkb;
+      for (int J = 0; J < nkb; ++J) var += (s[J] - mu) * (s[J] - mu);
+      const double t = mu + tau * sqrt(var / (double)nkb);
+      const int dense = (int64_t)I * qblk < nt; /* the block holds a prefix row */
+      const int64_t o = (bh * nqb + I) * (int64_t)nkb;
+      for (int J = 0; J < nkb; ++J) {
+        const int sink = (int64_t)J * kblk < nt; /* the block holds a prefix key */
+        if (mask) mask[o + J] = (uint8_t)(dense || sink || J == best || s[J] > t);
+        if (scores) scores[o + J] = s[J];
+      }
+      if (thr) thr[bh * nqb + I] = t;
+    }
+  }
+  free(qbar); free(kbar); free(row); free(s);
   return 0;
 }
 

@@ -50,6 +50,13 @@ class Oracle:
                                             i32, i32, i32, i32, i32, i32, f64, i32, i32, i32,
                                             P, P, f64, P, i64, P, i32]
         lib.solref_attn_rows_ex.restype = ctypes.c_int
+        lib.solref_attn_rows_sparse.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
+                                                i32, i32, i32, i32, i32, i32, f64, i32, i32, i32,
+                                                P, P, f64, P, i32, i32, P, i64, P, i32]
+        lib.solref_attn_rows_sparse.restype = ctypes.c_int
+        lib.solref_sparse_route.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, f64,
+                                            i32, i32, P, P, f64, i32, i32, f64, P, P, P]
+        lib.solref_sparse_route.restype = ctypes.c_int
         lib.solref_qknorm_rope3d.argtypes = [P, P, P, i64, i32, i32, i32, i32, i32, i32, i32,
                                              i32, f64, i32, P, f64, i32]
         lib.solref_qknorm_rope3d.restype = None
@@ -114,9 +121,34 @@ class Oracle:
                                       _ptr(g), float(eps), int(bool(contract)))
         return y if contract else yf
 
+    def sparse_route(self, q, k, T, Hl, Wl, tau, qblk=256, kblk=128, rope=True, contract=True,
+                     q_gamma=None, k_gamma=None, eps=0.0, split=DEFAULT_SPLIT, base=ROPE_BASE):
+        """Block routing of the block-sparse attention for the self-attention of
+        q, k [B, H, N, D] (bf16 bits).  Returns (mask uint8 [B, H, nqb, nkb],
+        scores float64 [B, H, nqb, nkb], thresholds float64 [B, H, nqb])."""
+        q, k = _u16(q), _u16(k)
+        if q.ndim != 4 or q.shape != k.shape:
+            raise ValueError("q, k must share one [B, H, N, D] shape")
+        B, H, N, D = q.shape
+        nqb, nkb = -(-N // qblk), -(-N // kblk)
+        gq, gk = (None if g is None else np.ascontiguousarray(g, dtype=np.float64)
+                  for g in (q_gamma, k_gamma))
+        mask = np.empty((B, H, nqb, nkb), dtype=np.uint8)
+        scores = np.empty((B, H, nqb, nkb), dtype=np.float64)
+        thr = np.empty((B, H, nqb), dtype=np.float64)
+        rc = self.lib.solref_sparse_route(
+            _ptr(q), _ptr(k), B * H, N, D, T, Hl, Wl, split[0], split[1], split[2], base,
+            int(bool(rope)), int(bool(contract)), None if gq is None else _ptr(gq),
+            None if gk is None else _ptr(gk), float(eps), qblk, kblk, float(tau), _ptr(mask),
+            _ptr(scores), _ptr(thr))
+        if rc != 0:
+            raise ValueError("oracle rejected the arguments (rc=%d)" % rc)
+        return mask, scores, thr
+
     def attn_rows(self, q, k, v, T, Hl, Wl, rows=None, rope=True, contract=True,
                   split=DEFAULT_SPLIT, base=ROPE_BASE, threads=0, q_gamma=None, k_gamma=None,
-                  eps=0.0, kv_grid=None, rope_k=None) -> np.ndarray:
+                  eps=0.0, kv_grid=None, rope_k=None, block_mask=None, qblk=256,
+                  kblk=128) -> np.ndarray:
         """Attention output (float32) for selected global query rows.
 
         q       : uint16 bf16 bits, [B, H, Nq, D]; k, v: [B, H, Nkv, D]
@@ -126,6 +158,8 @@ class Oracle:
                   (None: not normalised); eps under the root
         kv_grid : (T, Hl, Wl) of the keys when it differs from the queries'
         rope_k  : rotate the keys (default: as rope)
+        block_mask : uint8 [B, H, ceil(Nq/qblk), ceil(Nkv/kblk)]: query i attends
+                  only to the keys of the key blocks its query block keeps
         returns : float32 [len(rows), D] (or [B, H, Nq, D] when rows is None)
         """
         q, k, v = _u16(q), _u16(k), _u16(v)
@@ -150,12 +184,18 @@ class Oracle:
             rows = np.arange(B * H * Nq, dtype=np.int64)
         rows = np.ascontiguousarray(rows, dtype=np.int64)
         out = np.empty((rows.size, D), dtype=np.float32)
-        rc = self.lib.solref_attn_rows_ex(
-            _ptr(q), _ptr(k), _ptr(v), B, H, Nq, Nkv, D, T, Hl, Wl, Tk, Hlk, Wlk,
-            split[0], split[1], split[2], base, int(bool(rope)), int(bool(rope_k)),
-            int(bool(contract)), None if gam[0] is None else _ptr(gam[0]),
-            None if gam[1] is None else _ptr(gam[1]), float(eps), _ptr(rows), rows.size,
-            _ptr(out), threads)
+        common = (_ptr(q), _ptr(k), _ptr(v), B, H, Nq, Nkv, D, T, Hl, Wl, Tk, Hlk, Wlk,
+                  split[0], split[1], split[2], base, int(bool(rope)), int(bool(rope_k)),
+                  int(bool(contract)), None if gam[0] is None else _ptr(gam[0]),
+                  None if gam[1] is None else _ptr(gam[1]), float(eps))
+        if block_mask is None:
+            rc = self.lib.solref_attn_rows_ex(*common, _ptr(rows), rows.size, _ptr(out), threads)
+        else:
+            bm = np.ascontiguousarray(block_mask, dtype=np.uint8)
+            if bm.shape != (B, H, -(-Nq // qblk), -(-Nkv // kblk)):
+                raise ValueError("block_mask must be [B, H, ceil(Nq/qblk), ceil(Nkv/kblk)]")
+            rc = self.lib.solref_attn_rows_sparse(*common, _ptr(bm), qblk, kblk, _ptr(rows),
+                                                  rows.size, _ptr(out), threads)
         if rc != 0:
             raise ValueError("oracle rejected the arguments (rc=%d)" % rc)
         return out.reshape(B, H, Nq, D) if full else out
@@ -198,6 +238,10 @@ def rope3d_bf16(x_bits, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE):
 def qknorm_rope3d(x_bits, T, Hl, Wl, gamma, eps, rope=True, contract=True,
                   split=DEFAULT_SPLIT, base=ROPE_BASE):
     return default().qknorm_rope3d(x_bits, T, Hl, Wl, gamma, eps, rope, contract, split, base)
+
+
+def sparse_route(q, k, T, Hl, Wl, tau, **kw):
+    return default().sparse_route(q, k, T, Hl, Wl, tau, **kw)
 
 
 def attn_rows(q, k, v, T, Hl, Wl, rows=None, rope=True, contract=True,

@@ -702,7 +702,8 @@ __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
   const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80u;
   const float a = __builtin_fabsf(x);
-  if (__builtin_isnan(a)) return 0x7Fu;
+  // NaN by its bits: the library is built with -fno-honor-nans
+  if ((__float_as_uint(x) & 0x7FFFFFFFu) > 0x7F800000u) return 0x7Fu;
   if (a >= 448.0f) return sign | 0x7Eu;
   if (a < 0.015625f) return sign | (uint32_t)__builtin_rintf(a * 512.0f);  // 0..8, exact product
   const uint32_t ua = __float_as_uint(a);

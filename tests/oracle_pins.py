@@ -582,4 +582,93 @@ def pin_e4m3_saturation_and_specials(o):
     assert np.array_equal(o.round_e4m3(vals[codes]), codes.astype(np.uint8))
 
 
+# ----------------------------------------------------- block-sparse attention
+
+def pin_sparse_route_vs_numpy_twin(o):
+    """The C routing (pooled blocks, scores, mean + tau std threshold, sinks)
+    equals the numpy twin, with and without QK normalisation, ragged blocks."""
+    rng = np.random.default_rng(60)
+    T, Hl, Wl, nt = 2, 6, 10, 37
+    N = nt + T * Hl * Wl
+    q, k = (_rand_bits(rng, (1, 2, N, D)) for _ in range(2))
+    for tau, gq, gk in [(1.0, None, None), (0.25, _gamma(rng), _gamma(rng))]:
+        m, sc, _ = o.sparse_route(q, k, T, Hl, Wl, tau, qblk=32, kblk=16, q_gamma=gq, k_gamma=gk,
+                                  eps=1e-6)
+        qh = brute.prepare_np(q, T, Hl, Wl, gq, 1e-6)
+        kh = brute.prepare_np(k, T, Hl, Wl, gk, 1e-6)
+        mb, sb = brute.sparse_route_np(qh, kh, nt, tau, 32, 16)
+        assert np.allclose(sc, sb, rtol=0, atol=1e-12)
+        assert np.array_equal(m.astype(bool), mb)
+        assert 0.1 < m[:, :, 2:].mean() < 0.9, "routing should drop and keep blocks here"
+
+
+def pin_sparse_threshold_closed_form(o):
+    """Unrotated rows on one direction e: query rows a e, key block J rows c_J e,
+    so s_J = a c_J / sqrt(D); c = (1, 2, 3, 10): mean 4, population std
+    sqrt(12.5) (units a / sqrt(D)).  tau = 0.5 keeps block 3 only; -0.5 keeps
+    blocks 2, 3 (the sample std would also keep block 1); -1.1 keeps all.  With
+    one block kept, every query sees 8 equal keys: out = mean of their v."""
+    e = np.zeros(D)
+    e[5] = 1.0
+    c = [1.0, 2.0, 3.0, 10.0]
+    q = _bits(np.tile(0.5 * e, (1, 1, 32, 1)))
+    k = _bits(np.concatenate([np.tile(cj * e, (1, 1, 8, 1)) for cj in c], axis=2))
+    rng = np.random.default_rng(61)
+    v = _rand_bits(rng, (1, 1, 32, D))
+    for tau, want in [(0.5, [0, 0, 0, 1]), (-0.5, [0, 0, 1, 1]), (-1.1, [1, 1, 1, 1])]:
+        m, _, _ = o.sparse_route(q, k, 1, 1, 32, tau, qblk=32, kblk=8, rope=False)
+        assert m.reshape(-1).tolist() == want, (tau, m.reshape(-1).tolist())
+    m, _, _ = o.sparse_route(q, k, 1, 1, 32, 0.5, qblk=32, kblk=8, rope=False)
+    out = o.attn_rows(q, k, v, 1, 1, 32, rope=False, block_mask=m, qblk=32, kblk=8)
+    assert np.allclose(out[0, 0], _f(v)[0, 0, 24:].mean(0)[None, :], atol=1e-6)
+
+
+def pin_sparse_dense_limit(o):
+    """tau -> -inf keeps every block, and the sparse attention is then the
+    dense one bit for bit."""
+    rng = np.random.default_rng(62)
+    T, Hl, Wl, nt = 2, 5, 7, 11
+    N = nt + T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(3))
+    m, _, _ = o.sparse_route(q, k, T, Hl, Wl, -1e30, qblk=16, kblk=8)
+    assert m.all()
+    a = o.attn_rows(q, k, v, T, Hl, Wl, block_mask=m, qblk=16, kblk=8)
+    assert np.array_equal(a, o.attn_rows(q, k, v, T, Hl, Wl))
+
+
+def pin_sparse_prefix_sink_and_prefix_queries(o):
+    """tau -> +inf: a video query block keeps exactly the key blocks holding a
+    prefix key plus its best block; a query block holding a prefix row keeps
+    every key block."""
+    rng = np.random.default_rng(63)
+    T, Hl, Wl, nt = 2, 6, 8, 21
+    N = nt + T * Hl * Wl
+    q, k = (_rand_bits(rng, (1, 1, N, D)) for _ in range(2))
+    m, sc, _ = o.sparse_route(q, k, T, Hl, Wl, 1e30, qblk=16, kblk=8)
+    m = m[0, 0].astype(bool)
+    sink = np.arange(m.shape[1]) * 8 < nt
+    for I in range(m.shape[0]):
+        if I * 16 < nt:
+            assert m[I].all()
+        else:
+            want = sink.copy()
+            want[np.argmax(sc[0, 0, I])] = True
+            assert np.array_equal(m[I], want)
+
+
+def pin_sparse_attention_vs_numpy_twin(o):
+    """Attention restricted to the kept key blocks equals the numpy twin's
+    masked softmax on the full score matrix."""
+    rng = np.random.default_rng(64)
+    T, Hl, Wl, nt = 2, 5, 8, 9
+    N = nt + T * Hl * Wl
+    q, k, v = (_rand_bits(rng, (1, 2, N, D)) for _ in range(3))
+    m, _, _ = o.sparse_route(q, k, T, Hl, Wl, 0.5, qblk=16, kblk=8)
+    got = o.attn_rows(q, k, v, T, Hl, Wl, block_mask=m, qblk=16, kblk=8)
+    qh, kh = brute.prepare_np(q, T, Hl, Wl), brute.prepare_np(k, T, Hl, Wl)
+    want = brute.sparse_attention_np(qh, kh, _f(v), m.astype(bool), 16, 8)
+    assert np.allclose(got, want, atol=2e-6, rtol=1e-6)
+    assert not np.allclose(got, o.attn_rows(q, k, v, T, Hl, Wl), atol=1e-3), "mask had no effect"
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -123,6 +123,14 @@ MUTANTS = [
     ("e4m3: subnormal quantum halved", "if (e < -6) e = -6;", "if (e < -7) e = -7;"),
     ("e4m3: exponent bias 8", "((e + 7) << 3)", "((e + 8) << 3)"),
     ("e4m3: no saturation", "if (a >= 448.0) return sign | 0x7e;", "if (a >= 480.0) return sign | 0x7f;"),
+    # block-sparse routing and attention
+    ("sparse: sample standard deviation", "sqrt(var / (double)nkb)", "sqrt(var / (double)(nkb - 1))"),
+    ("sparse: threshold below the mean", "mu + tau * sqrt", "mu - tau * sqrt"),
+    ("sparse: prefix sink dropped", "const int sink = (int64_t)J * kblk < nt;", "const int sink = 0;"),
+    ("sparse: prefix queries not dense", "const int dense = (int64_t)I * qblk < nt;", "const int dense = 0;"),
+    ("sparse: best block not kept", "dense || sink || J == best || s[J] > t", "dense || sink || s[J] > t"),
+    ("sparse: key blocks summed, not averaged", "kbar[J * D + d] /= (double)keys;", "(void)keys;"),
+    ("sparse: mask ignored", "if (keep && !keep[j / J->kblk]) s[j] = -INFINITY;", "(void)keep;"),
     # queries and keys of different lengths
     ("key count taken from the queries", "for (int j = 0; j < Nkv; ++j) {\n    const double* kj",
      "for (int j = 0; j < Nkv && j < J->qs.N; ++j) {\n    const double* kj"),
