@@ -123,6 +123,10 @@ def main():
                     help="prepared: sol_prepare_kv (K rotated, V to fp16, one pass) then "
                          "sol_attn_fwd_prepared (q rotated in its tile load); fused: sol_attn_fwd "
                          "(q and k rotated in every tile load)")
+    ap.add_argument("--tau", type=float, default=None,
+                    help="block-sparse attention with this threshold parameter (the paper's "
+                         "refinement steps use 1.0, 1.25, 1.5); the step is then sol_prepare_kv_ex + "
+                         "sol_sparse_route + sol_attn_fwd_sparse")
     ap.add_argument("--cpu-rows-per-thread", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -170,13 +174,28 @@ def main():
         sol.prepare_kv_ex(ref_kv[0].to(dev), ref_kv[1].to(dev), *w.ref_grid, rtab, k_prep, v_prep,
                           key0=0, n_kv=w.n_kv)
         torch.cuda.synchronize()
-    special = w.qk_norm or w.n_ref
+    sparse = args.tau is not None
+    special = w.qk_norm or w.n_ref or sparse
     if special and args.path == "fused":
-        print("the fused path has neither QK normalization nor a key cache", file=sys.stderr)
+        print("the fused path has neither QK normalization, nor a key cache, nor block sparsity",
+              file=sys.stderr)
         sys.exit(2)
+    if sparse and w.n_ref:
+        print("block-sparse attention is the self-attention of one sequence (no key cache)",
+              file=sys.stderr)
+        sys.exit(2)
+    sws = sol.sparse_workspace(qd) if sparse else None
 
     def launches(path):
         """The launches of one step, in order: [(name, fn)]."""
+        if path == "prepared" and sparse:
+            return [("prepare_kv", lambda: sol.prepare_kv_ex(kd, vd, w.T, w.Hl, w.Wl, tab, k_prep, v_prep,
+                                                             gamma=gk, eps=W.QK_NORM_EPS)),
+                    ("sparse_route", lambda: sol.sparse_route(qd, k_prep, w.T, w.Hl, w.Wl, tab, args.tau,
+                                                              workspace=sws, gamma=gq, eps=W.QK_NORM_EPS)),
+                    ("attn_fwd_sparse", lambda: sol.attn_fwd_sparse(qd, k_prep, v_prep, w.T, w.Hl, w.Wl, tab,
+                                                                    sws, gamma=gq, eps=W.QK_NORM_EPS,
+                                                                    out=out))]
         if path == "prepared":
             return [("prepare_kv", lambda: sol.prepare_kv_ex(kd, vd, w.T, w.Hl, w.Wl, tab, k_prep, v_prep,
                                                              key0=w.n_ref, n_kv=w.n_kv, gamma=gk,
@@ -213,13 +232,34 @@ def main():
         return total / steps, per
 
     ms_step, per = timed(args.path, args.steps, args.warmup)
-    main_kernel = "attn_fwd" if args.path == "fused" else "attn_fwd_prepared"
+    main_kernel = "attn_fwd" if args.path == "fused" else ("attn_fwd_sparse" if sparse else "attn_fwd_prepared")
     kern = per[main_kernel]
     ms_launch = sum(kern) / len(kern)
     ks = sorted(kern)
     ms_median = ks[len(ks) // 2]
     tflops = w.flops / (ms_step * 1e-3) / 1e12
     achieved = w.flops / (ms_launch * 1e-3) / 1e12
+    sparsity = None
+    if sparse:
+        # flops the sparse kernel executes: each query block's rows times the
+        # keys of its kept blocks, 4 D per (query, key) pair
+        counts, blocks = sol.sparse_routing(sws, w.B, w.H, w.N)
+        counts = counts.cpu().to(torch.int64)
+        blocks = blocks.cpu().to(torch.int64)
+        nkb = blocks.shape[-1]
+        keys_in = torch.clamp(w.N - torch.arange(nkb) * sol.SPARSE_KEY_BLOCK, max=sol.SPARSE_KEY_BLOCK)
+        kept = torch.arange(nkb)[None, None, None, :] < counts[..., None]
+        kept_keys = (keys_in[blocks.clamp(0, nkb - 1)] * kept).sum(-1)            # [B, H, nqb]
+        nqb = counts.shape[-1]
+        rows = torch.clamp(w.N - torch.arange(nqb) * sol.SPARSE_QUERY_BLOCK, max=sol.SPARSE_QUERY_BLOCK)
+        pairs = float((kept_keys * rows).sum())
+        exec_flops = 4.0 * w.D * pairs
+        sparsity = {"tau": args.tau, "density": pairs / (w.B * w.H * float(w.N) ** 2),
+                    "executed_flops": exec_flops,
+                    "executed_tflops": exec_flops / (ms_launch * 1e-3) / 1e12}
+        achieved = sparsity["executed_tflops"]
+        log("block-sparse tau=%g: density %.4f, %.1f executed TFLOP/s in %s"
+            % (args.tau, sparsity["density"], achieved, main_kernel))
     log("timed %d steps (%s): %.3f ms/step, %s %.3f ms avg (median %.3f) -> %.1f TFLOP/s"
         % (args.steps, args.path, ms_step, main_kernel, ms_launch, ms_median, tflops))
     other = "fused" if args.path == "prepared" else "prepared"
@@ -257,6 +297,7 @@ def main():
         "kernel_ms_median": ms_median,
         "pct_peak_bf16": 100.0 * tflops / PEAK_BF16_TFLOPS,
         "kernel_ms": {name: sum(v) / len(v) for name, v in per.items()},
+        "block_sparse": sparsity,
         "other_path": None if ms_other is None else {
             "path": other, "ms_per_step": ms_other, "tflops": w.flops / (ms_other * 1e-3) / 1e12},
         "roofline": {
@@ -269,7 +310,9 @@ def main():
             "traffic": traffic,
         },
     }
-    if not args.no_cpu_baseline:
+    if sparse:
+        result["metric"] = METRIC + " (block-sparse: dense-equivalent flops)"
+    if not args.no_cpu_baseline and not sparse:
         log("cpu baseline (oracle) ...")
         cpu, par = cpu_baseline(w, q, k, v, out, args.cpu_rows_per_thread, ref_kv)
         result["cpu_baseline"] = cpu

@@ -212,6 +212,49 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
                              int out_format, sol_stream_t stream);
 
 /*
+ * Block-sparse attention (Sec. 3.4, "Per-step dynamic sparsity" and "Safety
+ * rails and the exact prefix KV sink"): the paper's training-free routing by
+ * online thresholding, for the self-attention of N tokens on prepared K/V.
+ *
+ * Query blocks of 256 rows and key blocks of 128 keys, both counted from token
+ * 0.  With q^, k^ the rows as they enter the products (normalised with
+ * q_gamma_dev / the keys' own preparation, rotated, rounded to bf16):
+ *   qbar_I = mean of q^ over block I, kbar_J = mean of k^ over block J,
+ *   s_IJ = <qbar_I, kbar_J> / sqrt(D)  (fp32; the block-level score),
+ *   mu_I, sigma_I = mean and population standard deviation over all J;
+ *   key block J is kept for query block I iff s_IJ > mu_I + tau sigma_I, or
+ *   J holds a prefix key (the first N - T*Hl*Wl tokens: an exact sink), or J
+ *   is I's first largest-score block; a query block holding a prefix row
+ *   keeps every key block (prefix queries attend densely).
+ * Each query row then attends, exactly, to the keys of its block's kept key
+ * blocks only.  tau -> -inf keeps everything (dense); the paper's refinement
+ * steps use tau = 1.0, 1.25, 1.5.
+ *
+ * sol_sparse_route: pools q and the prepared keys (k_prep from
+ * sol_prepare_kv[_ex], key0 = 0, n_kv = N) and writes the routing into the
+ * workspace: bytes [0, 4*B*H*nqb): int32 counts[b*H + h][I] of kept blocks;
+ * from offset ceil256(4*B*H*nqb): uint16 blocks[b*H + h][I][0..nkb), the
+ * kept block indices of (b, h, I) in ascending order (the first counts[..]
+ * entries are meaningful); then pooled queries and keys (fp32).
+ * nqb = ceil(N/256), nkb = ceil(N/128).  tau finite.
+ * sol_attn_fwd_sparse: the attention under that routing (the workspace as
+ * sol_sparse_route left it), bf16 or E4M3 output as sol_attn_fwd_prepared_ex.
+ * The workspace is sol_sparse_workspace_bytes(B, H, N, D) bytes of device
+ * memory, 16-byte aligned, not overlapping q, k_prep, v_prep or out.
+ * N <= 2^20 (SOL_ERR_UNSUPPORTED beyond: the kept-block list of a query block
+ * is staged in LDS).  Other arguments and errors as sol_attn_fwd_prepared_ex;
+ * sol_sparse_workspace_bytes returns 0 for invalid or unsupported sizes.
+ */
+size_t sol_sparse_workspace_bytes(int B, int H, int N, int D);
+int sol_sparse_route(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
+                     int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                     float tau, void* workspace, size_t workspace_bytes, sol_stream_t stream);
+int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
+                        int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                        const float* q_gamma_dev, float eps, const void* workspace,
+                        size_t workspace_bytes, int out_format, sol_stream_t stream);
+
+/*
  * Bytes of device workspace sol_attn_fwd_ws needs: room for k_prep then
  * v_prep, 2 * sol_prepared_kv_bytes(B, H, N, D).  0 for invalid sizes.
  */

@@ -54,6 +54,30 @@ int check_norm(const float* gamma, float eps) {
   return SOL_OK;
 }
 
+// Common checks of the two block-sparse entry points.
+int check_sparse(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
+                 int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                 const void* workspace, size_t workspace_bytes) {
+  if (!q || !k_prep) return fail(SOL_ERR_INVALID_ARG, "q and k_prep must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  if (N > sol::sparse_max_tokens())
+    return fail(SOL_ERR_UNSUPPORTED, "block-sparse attention takes N <= %d (got %d)", sol::sparse_max_tokens(), N);
+  if (!aligned16(q) || !aligned16(k_prep)) return fail(SOL_ERR_INVALID_ARG, "q and k_prep must be 16-byte aligned");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  st = check_norm(q_gamma_dev, eps);
+  if (st != SOL_OK) return st;
+  const size_t need = sol_sparse_workspace_bytes(B, H, N, D);
+  if (!workspace) return fail(SOL_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned16(workspace)) return fail(SOL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  if (workspace_bytes < need)
+    return fail(SOL_ERR_INVALID_ARG, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(workspace, need, q, bytes) || overlaps(workspace, need, k_prep, sol_prepared_kv_bytes(B, H, N, D)))
+    return fail(SOL_ERR_INVALID_ARG, "workspace overlaps q or k_prep");
+  return SOL_OK;
+}
+
 }  // namespace
 
 sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl) {
@@ -231,7 +255,7 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
   hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
                                                static_cast<const uint16_t*>(v_prep), out, B * H, g, n_kv, tab,
                                                q_gamma_dev, eps, out_format == SOL_OUT_FP8_E4M3,
-                                               reinterpret_cast<hipStream_t>(stream));
+                                               nullptr, nullptr, 0, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_prepared launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -241,6 +265,64 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
                           sol_stream_t stream) {
   return sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, N, D, T, Hl, Wl, rope_tab_dev,
                                   nullptr, 0.0f, SOL_OUT_BF16, stream);
+}
+
+size_t sol_sparse_workspace_bytes(int B, int H, int N, int D) {
+  if (B < 1 || H < 1 || N < 1 || D != sol::kHeadDim || N > sol::sparse_max_tokens()) return 0;
+  if ((int64_t)B * H > INT32_MAX) return 0;
+  size_t off[4];
+  return sol::sparse_workspace_offsets(B * H, N, off);
+}
+
+int sol_sparse_route(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
+                     int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                     float tau, void* workspace, size_t workspace_bytes, sol_stream_t stream) {
+  int st = check_sparse(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab_dev, q_gamma_dev, eps, workspace,
+                        workspace_bytes);
+  if (st != SOL_OK) return st;
+  if (!std::isfinite(tau)) return fail(SOL_ERR_INVALID_ARG, "tau must be finite");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  hipError_t e = sol::launch_sparse_route(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
+                                          B * H, g, tab, q_gamma_dev, eps, tau, workspace,
+                                          reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "sparse_route launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
+                        int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                        const float* q_gamma_dev, float eps, const void* workspace,
+                        size_t workspace_bytes, int out_format, sol_stream_t stream) {
+  int st = check_sparse(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab_dev, q_gamma_dev, eps, workspace,
+                        workspace_bytes);
+  if (st != SOL_OK) return st;
+  if (!v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must not be NULL");
+  if (!aligned16(v_prep) || !aligned16(out)) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must be 16-byte aligned");
+  if (out_format != SOL_OUT_BF16 && out_format != SOL_OUT_FP8_E4M3)
+    return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  const size_t obytes = out_format == SOL_OUT_BF16 ? bytes : bytes / 2;
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
+  const size_t need = sol_sparse_workspace_bytes(B, H, N, D);
+  if (overlaps(out, obytes, q, bytes) || overlaps(out, obytes, k_prep, pbytes) ||
+      overlaps(out, obytes, v_prep, pbytes) || overlaps(out, obytes, workspace, need))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep, v_prep or the workspace");
+  if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  size_t off[4];
+  sol::sparse_workspace_offsets(B * H, N, off);
+  const char* ws = static_cast<const char*>(workspace);
+  hipError_t e = sol::launch_attn_fwd_prepared(
+      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep), static_cast<const uint16_t*>(v_prep),
+      out, B * H, g, N, tab, q_gamma_dev, eps, out_format == SOL_OUT_FP8_E4M3,
+      reinterpret_cast<const uint16_t*>(ws + off[1]), reinterpret_cast<const int*>(ws + off[0]),
+      (N + 127) / 128, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_sparse launch: %s", hipGetErrorString(e));
+  return ok();
 }
 
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,

@@ -1,0 +1,193 @@
+// Device helpers shared by the HIP kernels (sol_kernels.hip, sol_sparse.hip):
+// token positions on the latent grid, bf16/fp16 conversions, the 3D rotary
+// embedding of one 16-byte chunk, the QK normalisation, and the prepared-path
+// tile size.  Every rotation and normalisation in the library goes through
+// these functions, so all kernels produce the same bits for the same row.
+#pragma once
+
+#include "sol_internal.h"
+
+namespace sol {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int D = kHeadDim;
+constexpr int kChunks = D / 8;  // 16-byte chunks (8 bf16 = 4 rotary pairs) per row
+
+// ------------------------------------------------------------ rotary helpers
+
+// n / d for 0 <= n < 2^23, d >= 1: float reciprocal estimate (off by at most
+// one) and one integer correction.
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
+// XCD w % 8), and each XCD has its own L2.  Renumber them so that XCD x gets
+// one contiguous range of work items: the workgroups an XCD runs at the same
+// time then stream the same (b, h) slab's K and V through its L2 together.
+// A bijection on [0, n) for any n.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_local_id(int w, int n) {
+  const int xcd = w % kXcds, local = w / kXcds;
+  const int per = n / kXcds, rem = n % kXcds;
+  return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
+__device__ __forceinline__ int div_exact(int n, int d, float inv) {
+  int q = (int)((float)n * inv);
+  int r = n - q * d;
+  q += (r >= d) - (r < 0);
+  return q;
+}
+
+struct Pos {
+  int t, h, w;
+  bool rot;  // false for prefix tokens, which are not rotated
+};
+
+__device__ __forceinline__ Pos token_pos(int n, const SeqGrid& g) {
+  Pos p;
+  int r = n - g.nt;
+  p.rot = r >= 0;
+  r = r < 0 ? 0 : r;
+  p.t = div_exact(r, g.hw, g.inv_hw);
+  const int rem = r - p.t * g.hw;
+  p.h = div_exact(rem, g.Wl, g.inv_wl);
+  p.w = rem - p.h * g.Wl;
+  return p;
+}
+
+// First table pair of 16-byte chunk cc (head dims [8cc, 8cc+8)) at position p.
+// Chunks 0-3 carry t, 4-9 carry h, 10-15 carry w (the 32/48/48 split).
+__device__ __forceinline__ int tab_pair(int cc, const Pos& p, const SeqGrid& g) {
+  if (cc < 4) return p.t * 16 + 4 * cc;
+  if (cc < 10) return g.tab_h + p.h * 24 + 4 * (cc - 4);
+  return g.tab_w + p.w * 24 + 4 * (cc - 10);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  bf16x2 r;
+  r[0] = (__bf16)a;  // v_cvt_pk_bf16_f32: round to nearest even
+  r[1] = (__bf16)b;
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// bf16 pair (one 32-bit word) -> fp16 pair: exact for |x| < 65504 (fp16
+// subnormals below 2^-14 keep 2^-24 absolute resolution).
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+  f16x2 r;
+  r[0] = (_Float16)__uint_as_float(w << 16);
+  r[1] = (_Float16)__uint_as_float(w & 0xffff0000u);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ uint4 bf16x8_to_f16x8(uint4 x) {
+  return make_uint4(bf16x2_to_f16x2(x.x), bf16x2_to_f16x2(x.y), bf16x2_to_f16x2(x.z),
+                    bf16x2_to_f16x2(x.w));
+}
+
+// The eight bf16 values of a 16-byte chunk as fp32 (exact), and back (RNE).
+__device__ __forceinline__ void unpack_bf16x8(uint4 x, float (&f)[8]) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    f[2 * u] = __uint_as_float(w[u] << 16);
+    f[2 * u + 1] = __uint_as_float(w[u] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ uint4 pack_bf16x8(const float (&f)[8]) {
+  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                    pack_bf16x2(f[6], f[7]));
+}
+
+// Rotate the 4 interleaved pairs of one 16-byte chunk, held as fp32:
+//   (a, b) -> (a cos - b sin, a sin + b cos), fp32, then bf16 RNE.
+// The one function every rotation in this library goes through, so the
+// standalone rotation and the fused tile loads agree bit for bit.
+__device__ __forceinline__ uint4 rope_rotate_f32(const float (&f)[8], float4 cs01, float4 cs23) {
+  const float c[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
+  const float s[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
+  uint32_t w[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const float a = f[2 * u], b = f[2 * u + 1];
+    const float ar = __builtin_fmaf(a, c[u], -(b * s[u]));
+    const float br = __builtin_fmaf(a, s[u], b * c[u]);
+    w[u] = pack_bf16x2(ar, br);
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) {
+  float f[8];
+  unpack_bf16x8(x, f);
+  return rope_rotate_f32(f, cs01, cs23);
+}
+
+__device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ tab, int pair0) {
+  return rope_rotate(x, *reinterpret_cast<const float4*>(tab + pair0),
+                     *reinterpret_cast<const float4*>(tab + pair0 + 2));
+}
+
+// ------------------------------------------------------- QK normalization
+
+// RMS normalisation of one head's row ahead of the rotation (Sec. 3.5, fusion
+// group 2, "QK normalization with partial RoPE"): x gamma / sqrt(mean(x^2) +
+// eps), in fp32, nothing rounded before the rotation.  The sum of squares
+// follows one fixed order whichever lanes hold the row -- per 16-byte chunk c
+// an fma chain over its eight entries, then a binary tree over the 16 chunk
+// sums pairing c with c^1, then c^2, c^4, c^8 -- so every kernel normalises a
+// row to the same bits (fp32 addition is commutative, so a butterfly over the
+// lanes and a tree inside one lane give the same sums).
+__device__ __forceinline__ float chunk_sumsq(uint4 x) {
+  float f[8];
+  unpack_bf16x8(x, f);
+  float s = f[0] * f[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) s = __builtin_fmaf(f[e], f[e], s);
+  return s;
+}
+// The tree over 16 consecutive lanes that hold chunks 0..15 of one row.
+__device__ __forceinline__ float row_sumsq_lanes16(float p) {
+  p += __shfl_xor(p, 1);
+  p += __shfl_xor(p, 2);
+  p += __shfl_xor(p, 4);
+  p += __shfl_xor(p, 8);
+  return p;
+}
+__device__ __forceinline__ float rms_inv(float sumsq, float eps) {
+  return 1.0f / __builtin_sqrtf(sumsq * (1.0f / D) + eps);
+}
+// Chunk cc (dims 8cc..8cc+7) of a row, normalised: (x inv) gamma, fp32.
+__device__ __forceinline__ void norm_chunk(uint4 x, float inv, const float* __restrict__ gamma,
+                                           int cc, float (&f)[8]) {
+  unpack_bf16x8(x, f);
+  const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * cc);
+  const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * cc + 4);
+  const float gm[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) f[e] = (f[e] * inv) * gm[e];
+}
+// Chunk cc of a query or key row as it enters the products: normalised when
+// gamma is given (inv from the row's sum of squares), rotated when rot (table
+// pairs from pair0), rounded to bf16.
+__device__ __forceinline__ uint4 qk_chunk(uint4 x, const float* __restrict__ gamma, float inv, int cc,
+                                          bool rot, const float2* __restrict__ tab, int pair0) {
+  if (gamma == nullptr) return rot ? rope_chunk(x, tab, pair0) : x;
+  float f[8];
+  norm_chunk(x, inv, gamma, cc, f);
+  if (!rot) return pack_bf16x8(f);
+  return rope_rotate_f32(f, *reinterpret_cast<const float4*>(tab + pair0),
+                         *reinterpret_cast<const float4*>(tab + pair0 + 2));
+}
+
+// Prepared K/V tiles: 32 keys, 8 KB of fp16 each for K and for V.
+constexpr int kPrepTile = 32;                  // keys per prepared tile
+constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
+
+}  // namespace
+}  // namespace sol

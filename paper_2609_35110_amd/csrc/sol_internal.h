@@ -45,13 +45,30 @@ hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_p
 // g.n query rows (rotated with grid g, normalised first when q_gamma !=
 // nullptr) against n_kv prepared keys; out is bf16, or FP8 E4M3 bytes when
 // out_fp8.
+// blocks != nullptr: block-sparse, each 256-row query block attends only to
+// the counts[...] key blocks of 128 keys listed for it in blocks (nkb entries
+// per query block, ascending).
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, void* out, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
                                     const float* q_gamma, float eps, bool out_fp8,
+                                    const uint16_t* blocks, const int* counts, int nkb,
                                     hipStream_t stream);
 // fp16 elements of one (b, h) slab of prepared K (or V).
 int64_t prepared_tile_elems(int N);
+
+// Block-sparse routing (sol_sparse.hip).  Workspace sections, byte offsets
+// off[0..3]: counts int32 [BH][nqb], blocks uint16 [BH][nqb][nkb], pooled
+// queries fp32 [BH][nqb][D], pooled keys fp32 [BH][nkb][D] (nqb = ceil(N/256),
+// nkb = ceil(N/128)); returns the total size.
+size_t sparse_workspace_offsets(int BH, int N, size_t off[4]);
+// Largest N the block-sparse path takes (its key-block lists live in LDS).
+int sparse_max_tokens();
+// Pools q (rotated with grid g, normalised with q_gamma) and the prepared
+// keys, then routes every query block with threshold parameter tau.
+hipError_t launch_sparse_route(const uint16_t* q, const uint16_t* k_prep, int BH, const SeqGrid& g,
+                               const float2* tab, const float* q_gamma, float eps, float tau,
+                               void* workspace, hipStream_t stream);
 
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
 int64_t attn_max_workgroups(int N, int BH);

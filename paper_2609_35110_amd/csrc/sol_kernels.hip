@@ -24,185 +24,10 @@
 //     new tile max exceeds it by more than 2^8 in probability units, so the
 //     64-register output rescale is almost never executed.  Exact: numerator
 //     and denominator always share the same reference max.
-#include "sol_internal.h"
+#include "sol_device.h"
 
 namespace sol {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-
-constexpr int D = kHeadDim;
-constexpr int kChunks = D / 8;  // 16-byte chunks (8 bf16 = 4 rotary pairs) per row
-
-// ------------------------------------------------------------ rotary helpers
-
-// n / d for 0 <= n < 2^23, d >= 1: float reciprocal estimate (off by at most
-// one) and one integer correction.
-// Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
-// XCD w % 8), and each XCD has its own L2.  Renumber them so that XCD x gets
-// one contiguous range of work items: the workgroups an XCD runs at the same
-// time then stream the same (b, h) slab's K and V through its L2 together.
-// A bijection on [0, n) for any n.
-constexpr int kXcds = 8;
-__device__ __forceinline__ int xcd_local_id(int w, int n) {
-  const int xcd = w % kXcds, local = w / kXcds;
-  const int per = n / kXcds, rem = n % kXcds;
-  return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
-}
-
-__device__ __forceinline__ int div_exact(int n, int d, float inv) {
-  int q = (int)((float)n * inv);
-  int r = n - q * d;
-  q += (r >= d) - (r < 0);
-  return q;
-}
-
-struct Pos {
-  int t, h, w;
-  bool rot;  // false for prefix tokens, which are not rotated
-};
-
-__device__ __forceinline__ Pos token_pos(int n, const SeqGrid& g) {
-  Pos p;
-  int r = n - g.nt;
-  p.rot = r >= 0;
-  r = r < 0 ? 0 : r;
-  p.t = div_exact(r, g.hw, g.inv_hw);
-  const int rem = r - p.t * g.hw;
-  p.h = div_exact(rem, g.Wl, g.inv_wl);
-  p.w = rem - p.h * g.Wl;
-  return p;
-}
-
-// First table pair of 16-byte chunk cc (head dims [8cc, 8cc+8)) at position p.
-// Chunks 0-3 carry t, 4-9 carry h, 10-15 carry w (the 32/48/48 split).
-__device__ __forceinline__ int tab_pair(int cc, const Pos& p, const SeqGrid& g) {
-  if (cc < 4) return p.t * 16 + 4 * cc;
-  if (cc < 10) return g.tab_h + p.h * 24 + 4 * (cc - 4);
-  return g.tab_w + p.w * 24 + 4 * (cc - 10);
-}
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  bf16x2 r;
-  r[0] = (__bf16)a;  // v_cvt_pk_bf16_f32: round to nearest even
-  r[1] = (__bf16)b;
-  return __builtin_bit_cast(uint32_t, r);
-}
-
-// bf16 pair (one 32-bit word) -> fp16 pair: exact for |x| < 65504 (fp16
-// subnormals below 2^-14 keep 2^-24 absolute resolution).
-__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
-  f16x2 r;
-  r[0] = (_Float16)__uint_as_float(w << 16);
-  r[1] = (_Float16)__uint_as_float(w & 0xffff0000u);
-  return __builtin_bit_cast(uint32_t, r);
-}
-
-__device__ __forceinline__ uint4 bf16x8_to_f16x8(uint4 x) {
-  return make_uint4(bf16x2_to_f16x2(x.x), bf16x2_to_f16x2(x.y), bf16x2_to_f16x2(x.z),
-                    bf16x2_to_f16x2(x.w));
-}
-
-// The eight bf16 values of a 16-byte chunk as fp32 (exact), and back (RNE).
-__device__ __forceinline__ void unpack_bf16x8(uint4 x, float (&f)[8]) {
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    f[2 * u] = __uint_as_float(w[u] << 16);
-    f[2 * u + 1] = __uint_as_float(w[u] & 0xffff0000u);
-  }
-}
-__device__ __forceinline__ uint4 pack_bf16x8(const float (&f)[8]) {
-  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
-                    pack_bf16x2(f[6], f[7]));
-}
-
-// Rotate the 4 interleaved pairs of one 16-byte chunk, held as fp32:
-//   (a, b) -> (a cos - b sin, a sin + b cos), fp32, then bf16 RNE.
-// The one function every rotation in this library goes through, so the
-// standalone rotation and the fused tile loads agree bit for bit.
-__device__ __forceinline__ uint4 rope_rotate_f32(const float (&f)[8], float4 cs01, float4 cs23) {
-  const float c[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
-  const float s[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
-  uint32_t w[4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const float a = f[2 * u], b = f[2 * u + 1];
-    const float ar = __builtin_fmaf(a, c[u], -(b * s[u]));
-    const float br = __builtin_fmaf(a, s[u], b * c[u]);
-    w[u] = pack_bf16x2(ar, br);
-  }
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-__device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) {
-  float f[8];
-  unpack_bf16x8(x, f);
-  return rope_rotate_f32(f, cs01, cs23);
-}
-
-__device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ tab, int pair0) {
-  return rope_rotate(x, *reinterpret_cast<const float4*>(tab + pair0),
-                     *reinterpret_cast<const float4*>(tab + pair0 + 2));
-}
-
-// ------------------------------------------------------- QK normalization
-
-// RMS normalisation of one head's row ahead of the rotation (Sec. 3.5, fusion
-// group 2, "QK normalization with partial RoPE"): x gamma / sqrt(mean(x^2) +
-// eps), in fp32, nothing rounded before the rotation.  The sum of squares
-// follows one fixed order whichever lanes hold the row -- per 16-byte chunk c
-// an fma chain over its eight entries, then a binary tree over the 16 chunk
-// sums pairing c with c^1, then c^2, c^4, c^8 -- so every kernel normalises a
-// row to the same bits (fp32 addition is commutative, so a butterfly over the
-// lanes and a tree inside one lane give the same sums).
-__device__ __forceinline__ float chunk_sumsq(uint4 x) {
-  float f[8];
-  unpack_bf16x8(x, f);
-  float s = f[0] * f[0];
-#pragma unroll
-  for (int e = 1; e < 8; ++e) s = __builtin_fmaf(f[e], f[e], s);
-  return s;
-}
-// The tree over 16 consecutive lanes that hold chunks 0..15 of one row.
-__device__ __forceinline__ float row_sumsq_lanes16(float p) {
-  p += __shfl_xor(p, 1);
-  p += __shfl_xor(p, 2);
-  p += __shfl_xor(p, 4);
-  p += __shfl_xor(p, 8);
-  return p;
-}
-__device__ __forceinline__ float rms_inv(float sumsq, float eps) {
-  return 1.0f / __builtin_sqrtf(sumsq * (1.0f / D) + eps);
-}
-// Chunk cc (dims 8cc..8cc+7) of a row, normalised: (x inv) gamma, fp32.
-__device__ __forceinline__ void norm_chunk(uint4 x, float inv, const float* __restrict__ gamma,
-                                           int cc, float (&f)[8]) {
-  unpack_bf16x8(x, f);
-  const float4 g0 = *reinterpret_cast<const float4*>(gamma + 8 * cc);
-  const float4 g1 = *reinterpret_cast<const float4*>(gamma + 8 * cc + 4);
-  const float gm[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-#pragma unroll
-  for (int e = 0; e < 8; ++e) f[e] = (f[e] * inv) * gm[e];
-}
-// Chunk cc of a query or key row as it enters the products: normalised when
-// gamma is given (inv from the row's sum of squares), rotated when rot (table
-// pairs from pair0), rounded to bf16.
-__device__ __forceinline__ uint4 qk_chunk(uint4 x, const float* __restrict__ gamma, float inv, int cc,
-                                          bool rot, const float2* __restrict__ tab, int pair0) {
-  if (gamma == nullptr) return rot ? rope_chunk(x, tab, pair0) : x;
-  float f[8];
-  norm_chunk(x, inv, gamma, cc, f);
-  if (!rot) return pack_bf16x8(f);
-  return rope_rotate_f32(f, *reinterpret_cast<const float4*>(tab + pair0),
-                         *reinterpret_cast<const float4*>(tab + pair0 + 2));
-}
 
 // --------------------------------------------------------- standalone rotary
 
@@ -246,8 +71,6 @@ __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x
 // past n_kv are zero.  A tile that also holds keys of another source is
 // written element by element, only where this call owns the key.  One
 // workgroup per tile (from tile0 on); grid.y walks the slabs.
-constexpr int kPrepTile = 32;             // keys per prepared tile
-constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
 
 template <bool kRope>
 __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ k,
@@ -767,14 +590,29 @@ constexpr int kVBufs = 4;              // V tiles in LDS  offsets are masks)
 // Descriptor word 3 of a raw buffer resource (32-bit data, no format swizzle).
 constexpr int kBufferDword3 = 0x00020000;
 
-template <bool kRope, bool kRobust>
+// kSparse: block-sparse attention (Sec. 3.4, "Per-step dynamic sparsity").
+// The workgroup's 256 query rows are one routing query block; it attends only
+// to the key blocks (kSparseKeyBlock keys = 4 tiles each) listed for it in
+// blocks[(bh * n_qtiles + qt) * nkb ..] (ascending, counts[bh * n_qtiles + qt]
+// of them).  The list is staged into LDS once; the loop walks the listed
+// tiles in order -- LDS ring slots follow the walk, copies read the listed
+// tile -- and looks each list entry up an iteration phase ahead of its use,
+// so no LDS wait for it falls inside the MFMA slots.
+constexpr int kSparseKeyBlock = 128;  // keys per routing key block
+constexpr int kSparseQueryBlock = 256;  // query rows per routing query block (= BM)
+constexpr int kMaxSparseBlocks = 8192;  // key blocks per slab the LDS list holds (N <= 2^20)
+
+template <bool kRope, bool kRobust, bool kSparse>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
                           const float2* __restrict__ tab, int n_qtiles, float c_log2, int n_keys,
-                          const float* __restrict__ q_gamma, float eps, int out_fp8) {
+                          const float* __restrict__ q_gamma, float eps, int out_fp8,
+                          const uint16_t* __restrict__ blocks, const int* __restrict__ counts,
+                          int nkb) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
+  __shared__ uint16_t blist[kSparse ? kMaxSparseBlocks : 1];
 
   // pin() in the first pass only.  The second pass spills, and with the empty
   // asm statements in place the compiler put a spill reload of an MFMA's
@@ -806,6 +644,25 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   uint8_t* out8_slab = reinterpret_cast<uint8_t*>(out) + slab;
   asm volatile("" : "+s"(out8_slab), "+s"(out_fp8));
   const int qrow_first = qt * BM + wave * 64 + l32;
+  // Tiles the workgroup walks: every tile of the slab, or the listed blocks'.
+  int n_kv = (N + BN2 - 1) / BN2;
+  if (kSparse) {
+    // counts and entries are clamped to the slab, whatever the list holds, so
+    // every copy stays inside the slab's prepared tiles
+    const size_t qb = (size_t)bh * n_qtiles + qt;
+    const int cnt = min(max(counts[qb], 1), min(nkb, kMaxSparseBlocks));
+    for (int e = tid; e < cnt; e += 256) blist[e] = (uint16_t)min((int)blocks[qb * nkb + e], nkb - 1);
+    n_kv = 4 * cnt;
+    __syncthreads();
+  }
+  // Slab tile of walk position t (clamped to the walk; a listed block's
+  // tiles past the slab's last are clamped by the copy and masked whole).
+  auto list_entry = [&](int t) __attribute__((always_inline)) {  // LDS read, no wait here
+    return (int)blist[min(t, n_kv - 1) >> 2];
+  };
+  auto slab_tile = [&](int t, int entry) __attribute__((always_inline)) {
+    return kSparse ? 4 * __builtin_amdgcn_readfirstlane(entry) + (min(t, n_kv - 1) & 3) : t;
+  };
   if (kRobust) {
     // Second pass: only the row blocks the first pass marked (NaN rows) are
     // recomputed; every other workgroup leaves at once.
@@ -887,11 +744,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
                  : "memory", "m0");
 #pragma clang diagnostic pop
   };
-  auto dma_k = [&](int tile, int u) __attribute__((always_inline)) {
-    dma_blk(rsrc_k, k_lds + (tile & (kKBufs - 1)) * kPrepTileElems, tile, u);
+  // Walk position t lands in ring slot t; the copy reads slab tile `tile`.
+  auto dma_k = [&](int t, int tile, int u) __attribute__((always_inline)) {
+    dma_blk(rsrc_k, k_lds + (t & (kKBufs - 1)) * kPrepTileElems, tile, u);
   };
-  auto dma_v = [&](int tile, int u) __attribute__((always_inline)) {
-    dma_blk(rsrc_v, v_lds + (tile & (kVBufs - 1)) * kPrepTileElems, tile, u);
+  auto dma_v = [&](int t, int tile, int u) __attribute__((always_inline)) {
+    dma_blk(rsrc_v, v_lds + (t & (kVBufs - 1)) * kPrepTileElems, tile, u);
   };
   // Fragment kk of K tile `tile` / fragment j = 4 kst + db of V tile `tile`.
   auto kfrag = [&](int tile, int kk) __attribute__((always_inline)) {
@@ -911,9 +769,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   float l_run[2] = {0.0f, 0.0f};
   float ovf = 0.0f;  // first pass: largest per-lane tile sum (above 2^15: rows marked)
 
-  // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of the tile.
-  auto mask_tile = [&](int it, f32x16* s) __attribute__((always_inline)) {
-    const int kv0 = it * BN2;
+  // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of the tile;
+  // the tile's first key is kv0.
+  auto mask_tile = [&](int kv0, f32x16* s) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       const int key = kv0 + 8 * (j >> 2) + 4 * hh + (j & 3);
@@ -923,8 +781,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       }
     }
   };
-  auto mask_block = [&](int it, f32x16& s) __attribute__((always_inline)) {
-    const int kv0 = it * BN2;
+  auto mask_block = [&](int kv0, f32x16& s) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < 16; ++j)
       if (kv0 + 8 * (j >> 2) + 4 * hh + (j & 3) >= N) s[j] = -__builtin_inff();
@@ -935,7 +792,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     for (int j = 2; j < 16; j += 2) mx = fmaxf(fmaxf(mx, s[j]), s[j + 1]);
     return fmaxf(mx, __shfl_xor(mx, 32));
   };
-  const int n_kv = (N + BN2 - 1) / BN2;
   // Fragment registers, a whole tile ahead: kr[kk] holds fragment kk of the K
   // tile being multiplied (then of the next one), vr[j] fragment j of the V
   // tile (then of the next one).
@@ -954,6 +810,16 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // prologue) to iteration t+4, read in iteration t-2 (and by the second
     // pass's rare path in iteration t); V tile t in buffer t % 4 from its copy
     // (iteration t-3) to iteration t+1, read in iteration t-1.
+    // Sparse walk: list entries of the tiles this iteration copies (i + 4,
+    // i + 3), masks (i + 1) and may recompute (i), read from LDS now and made
+    // scalar where they are used.
+    int e_k4 = 0, e_v3 = 0, e_m1 = 0, e_0 = 0;
+    if (kSparse) {
+      e_k4 = list_entry(i + 4);
+      e_v3 = list_entry(i + 3);
+      e_m1 = list_entry(i + 1);
+      if (kRobust) e_0 = list_entry(i);
+    }
     // ---- phase A
     uint32_t p1[8];
     float l1;
@@ -1018,7 +884,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
           for (int kk = 0; kk < 8; ++kk)
             t = __builtin_amdgcn_mfma_f32_32x32x16_f16(kfrag(i, kk), qf[qb][kk], t, 0, 0, 0);
-          if ((i + 1) * BN2 > N) mask_block(i, t);
+          const int kv0 = slab_tile(i, e_0) * BN2;
+          if (kv0 + BN2 > N) mask_block(kv0, t);
           const float delta = fmaxf(tile_max(t), 0.0f);
           const float alpha = __builtin_amdgcn_exp2f(-delta);
           m_ref[qb] += delta;
@@ -1075,14 +942,16 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // write or read them.
     mfma_wait_tail();
     if (!kRobust) asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
-    if (__builtin_expect(i + 1 < n_kv && (i + 2) * BN2 > N, 0)) {
+    const int kv_next = slab_tile(i + 1, e_m1) * BN2;  // first key of walk tile i + 1
+    if (__builtin_expect(i + 1 < n_kv && kv_next + BN2 > N, 0)) {
       mfma_wait();
-      mask_tile(i + 1, ns);
+      mask_tile(kv_next, ns);
     }
     __builtin_amdgcn_sched_barrier(0);
     // ---- phase B
     pa = pb = 0.0f;
     t01 = t23 = t03 = t45 = 0;
+    const int tile_k4 = slab_tile(i + 4, e_k4), tile_v3 = slab_tile(i + 3, e_v3);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
@@ -1096,10 +965,10 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
         p0_next[j - 1] = pack_f16x2(pa, pb);
         keep(p0_next[j - 1]);
       }
-      if (j == 1) dma_k(i + 4, 0);  // over K(i-4)
-      if (j == 2) dma_v(i + 3, 0);  // over V(i-1), read in iteration i-2
-      if (j == 3) dma_k(i + 4, 1);
-      if (j == 5) dma_v(i + 3, 1);
+      if (j == 1) dma_k(i + 4, tile_k4, 0);  // over K(i-4)
+      if (j == 2) dma_v(i + 3, tile_v3, 0);  // over V(i-1), read in iteration i-2
+      if (j == 3) dma_k(i + 4, tile_k4, 1);
+      if (j == 5) dma_v(i + 3, tile_v3, 1);
       __builtin_amdgcn_sched_barrier(0);
       // slot 2: PV MFMA of block 1; fragment j of V(i+1) into the register
       // just used; exponential of register 2j + 1; a step of the word-sum tree.
@@ -1128,22 +997,26 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   // ---- prologue: K(0..2) and V(0..1) in LDS, K(3) and V(2) on their way;
   // S(0) against m = its own max; the qb0 words of P(0); the fragment
   // registers loaded with K(1) and V(0).
-  dma_k(0, 0);
-  dma_k(0, 1);
-  dma_v(0, 0);
-  dma_v(0, 1);
-  dma_k(1, 0);
-  dma_k(1, 1);
-  dma_k(2, 0);
-  dma_k(2, 1);
-  dma_v(1, 0);
-  dma_v(1, 1);
+  auto walk_tile = [&](int t) __attribute__((always_inline)) {
+    return kSparse ? slab_tile(t, list_entry(t)) : t;
+  };
+  const int w0 = walk_tile(0), w1 = walk_tile(1), w2 = walk_tile(2), w3 = walk_tile(3);
+  dma_k(0, w0, 0);
+  dma_k(0, w0, 1);
+  dma_v(0, w0, 0);
+  dma_v(0, w0, 1);
+  dma_k(1, w1, 0);
+  dma_k(1, w1, 1);
+  dma_k(2, w2, 0);
+  dma_k(2, w2, 1);
+  dma_v(1, w1, 0);
+  dma_v(1, w1, 1);
   __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
-  dma_k(3, 0);
-  dma_k(3, 1);
-  dma_v(2, 0);
-  dma_v(2, 1);
+  dma_k(3, w3, 0);
+  dma_k(3, w3, 1);
+  dma_v(2, w2, 0);
+  dma_v(2, w2, 1);
   // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
   // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
   // such copies.
@@ -1156,10 +1029,44 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     sa[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[0][kk], sa[0], 0, 0, 0);
     sa[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[1][kk], sa[1], 0, 0, 0);
   }
-  if (BN2 > N) mask_tile(0, sa);
+  if (w0 * BN2 + BN2 > N) mask_tile(w0 * BN2, sa);
+  // The first pass also takes the reference max over each 32-row block's
+  // "diagonal" tile -- the keys at the rows' own positions (offset by n_keys -
+  // Nq, the layout of a cached prefix of keys) -- where a video DiT's local
+  // attention peaks: with the first tile alone, rows whose scores climb 11 or
+  // more binades above it overflow the fp16 word sums and are recomputed by
+  // the slower second pass.  The tile must be one the walk attends (always
+  // in the dense walk; looked up in the list for the sparse one), so the
+  // reference never exceeds the attended maximum.  Fragments are read
+  // straight from the prepared tile in global memory.
+  float m_diag[2] = {-__builtin_inff(), -__builtin_inff()};
+  if (!kRobust) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int key = min(max(qt * BM + wave * 64 + 32 * qb + (N - Nq), 0), N - 1);
+      const int tile = key / BN2;
+      bool attended = true;
+      if (kSparse) {
+        const int blk = key / kSparseKeyBlock;
+        bool hit = false;
+        for (int e = lane; e < n_kv / 4; e += 64) hit |= blist[e] == blk;
+        attended = __any(hit);
+      }
+      if (attended) {
+        const f16x8* kg = reinterpret_cast<const f16x8*>(k + pslab + (size_t)tile * kPrepTileElems);
+        f32x16 sd = f32x16{};
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk)
+          sd = __builtin_amdgcn_mfma_f32_32x32x16_f16(kg[kk * 64 + lane], qf[qb][kk], sd, 0, 0, 0);
+        if (tile * BN2 + BN2 > N) mask_block(tile * BN2, sd);
+        m_diag[qb] = tile_max(sd);
+      }
+    }
+  }
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    m_ref[qb] = tile_max(sa[qb]);  // finite: key 0 is always valid
+    // finite: the walk's first tile always holds a valid key
+    m_ref[qb] = fmaxf(tile_max(sa[qb]), m_diag[qb]);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       sa[qb][j] -= m_ref[qb];
@@ -1307,27 +1214,32 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, void* out_v, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
                                     const float* q_gamma, float eps, bool out_fp8,
+                                    const uint16_t* blocks, const int* counts, int nkb,
                                     hipStream_t stream) {
   uint16_t* out = static_cast<uint16_t*>(out_v);
   const int fp8 = out_fp8 ? 1 : 0;
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
+  const bool sparse = blocks != nullptr;
   // First pass, then the second over the row blocks whose probabilities left
   // the fp16 range.
   for (int pass = 0; pass < 2; ++pass) {
-    if (tab != nullptr && pass == 0)
-      hipLaunchKernelGGL((attn_prepared_kernel<true, false>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
-    else if (pass == 0)
-      hipLaunchKernelGGL((attn_prepared_kernel<false, false>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
-    else if (tab != nullptr)
-      hipLaunchKernelGGL((attn_prepared_kernel<true, true>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
-    else
-      hipLaunchKernelGGL((attn_prepared_kernel<false, true>), grid, dim3(256), 0, stream, q, k_prep,
-                         v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8);
+    const int sel = (tab != nullptr) * 4 + pass * 2 + sparse;
+#define SOL_LAUNCH_PREPARED(R, P, S)                                                            \
+  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S>), grid, dim3(256), 0, stream, q, k_prep, v_prep, \
+                     out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8, blocks, counts, nkb)
+    switch (sel) {
+      case 0: SOL_LAUNCH_PREPARED(false, false, false); break;
+      case 1: SOL_LAUNCH_PREPARED(false, false, true); break;
+      case 2: SOL_LAUNCH_PREPARED(false, true, false); break;
+      case 3: SOL_LAUNCH_PREPARED(false, true, true); break;
+      case 4: SOL_LAUNCH_PREPARED(true, false, false); break;
+      case 5: SOL_LAUNCH_PREPARED(true, false, true); break;
+      case 6: SOL_LAUNCH_PREPARED(true, true, false); break;
+      default: SOL_LAUNCH_PREPARED(true, true, true); break;
+    }
+#undef SOL_LAUNCH_PREPARED
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

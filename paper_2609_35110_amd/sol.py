@@ -70,6 +70,14 @@ def lib():
         L.sol_attn_fwd_prepared_ex.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
                                                P, P, f32, i32, P]
         L.sol_attn_fwd_prepared_ex.restype = i32
+        L.sol_sparse_workspace_bytes.argtypes = [i32, i32, i32, i32]
+        L.sol_sparse_workspace_bytes.restype = sz
+        L.sol_sparse_route.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32, f32, P,
+                                       sz, P]
+        L.sol_sparse_route.restype = i32
+        L.sol_attn_fwd_sparse.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32,
+                                          P, sz, i32, P]
+        L.sol_attn_fwd_sparse.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
         L.sol_last_error.argtypes = []
@@ -108,6 +116,22 @@ def sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl
                              eps, out_format, stream):
     return lib().sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl,
                                           rope_tab, gamma, eps, out_format, stream)
+
+
+def sol_sparse_workspace_bytes(B, H, N, D):
+    return lib().sol_sparse_workspace_bytes(B, H, N, D)
+
+
+def sol_sparse_route(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, tau, workspace,
+                     workspace_bytes, stream):
+    return lib().sol_sparse_route(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, tau,
+                                  workspace, workspace_bytes, stream)
+
+
+def sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps,
+                        workspace, workspace_bytes, out_format, stream):
+    return lib().sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab, gamma,
+                                     eps, workspace, workspace_bytes, out_format, stream)
 
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
@@ -365,4 +389,85 @@ def attn_fwd_prepared_ex(q, k_prep, v_prep, n_kv, T, Hl, Wl, table=None, gamma=N
                                    B, H, N, n_kv, D, T, Hl, Wl, _table_ptr(table, q.device),
                                    _gamma_ptr(gamma, q.device), float(eps),
                                    SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16, _stream(q)))
+    return out
+
+
+# ------------------------------------------------------- block-sparse attention
+
+SPARSE_QUERY_BLOCK = 256
+SPARSE_KEY_BLOCK = 128
+
+
+def sparse_workspace(q):
+    """A device workspace for the block-sparse routing of q's shape (uint8)."""
+    B, H, N, D = q.shape
+    n = sol_sparse_workspace_bytes(B, H, N, D)
+    if n == 0:
+        raise ValueError("block-sparse attention does not take this shape")
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def _check_workspace(ws, nbytes, device):
+    if (not isinstance(ws, torch.Tensor) or not ws.is_cuda or ws.device != device
+            or not ws.is_contiguous() or ws.numel() * ws.element_size() < nbytes):
+        raise ValueError("workspace must be a contiguous device tensor of at least %d bytes on %s"
+                         % (nbytes, device))
+
+
+def sparse_route(q, k_prep, T, Hl, Wl, table, tau, workspace=None, gamma=None, eps=1e-6):
+    """Route every 256-row query block of q [B, H, N, D] over the 128-key
+    blocks of the prepared keys (threshold mean + tau * std, prefix sink).
+    Returns the workspace holding the routing."""
+    _check_tensor("q", q)
+    B, H, N, D = q.shape
+    _check_prepared("k_prep", k_prep, sol_prepared_kv_bytes(B, H, N, D), q.device)
+    if workspace is None:
+        workspace = sparse_workspace(q)
+    nbytes = sol_sparse_workspace_bytes(B, H, N, D)
+    _check_workspace(workspace, nbytes, q.device)
+    check(sol_sparse_route(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()), B, H,
+                           N, D, T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(gamma, q.device),
+                           float(eps), float(tau), ctypes.c_void_p(workspace.data_ptr()),
+                           workspace.numel() * workspace.element_size(), _stream(q)))
+    return workspace
+
+
+def sparse_routing(workspace, B, H, N):
+    """(counts int32 [B, H, nqb], blocks int16 [B, H, nqb, nkb]) views of the
+    routing a sparse_route call left in the workspace (uint16 block indices
+    read as int16: they are below 2^13)."""
+    nqb = -(-N // SPARSE_QUERY_BLOCK)
+    nkb = -(-N // SPARSE_KEY_BLOCK)
+    n_counts = B * H * nqb
+    off = (4 * n_counts + 255) // 256 * 256
+    counts = workspace[: 4 * n_counts].view(torch.int32).view(B, H, nqb)
+    blocks = workspace[off: off + 2 * n_counts * nkb].view(torch.int16).view(B, H, nqb, nkb)
+    return counts, blocks
+
+
+def attn_fwd_sparse(q, k_prep, v_prep, T, Hl, Wl, table, workspace, gamma=None, eps=1e-6, out=None,
+                    fp8=False):
+    """Block-sparse attention under the routing held by the workspace."""
+    _check_tensor("q", q)
+    B, H, N, D = q.shape
+    nbytes = sol_prepared_kv_bytes(B, H, N, D)
+    _check_prepared("k_prep", k_prep, nbytes, q.device)
+    _check_prepared("v_prep", v_prep, nbytes, q.device)
+    _check_workspace(workspace, sol_sparse_workspace_bytes(B, H, N, D), q.device)
+    if fp8:
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.uint8, device=q.device)
+        if (out.dtype != torch.uint8 or tuple(out.shape) != tuple(q.shape) or not out.is_contiguous()
+                or out.device != q.device):
+            raise ValueError("an E4M3 out must be a contiguous uint8 tensor of q's shape and device")
+    else:
+        if out is None:
+            out = torch.empty_like(q)
+        _check_tensor("out", out, q.shape)
+    check(sol_attn_fwd_sparse(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
+                              ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H,
+                              N, D, T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(gamma, q.device),
+                              float(eps), ctypes.c_void_p(workspace.data_ptr()),
+                              workspace.numel() * workspace.element_size(),
+                              SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16, _stream(q)))
     return out

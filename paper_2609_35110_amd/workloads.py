@@ -17,6 +17,10 @@ public dataset; every tensor here is synthetic:
 * ``p720n`` : ``p720`` before QK normalization (Sec. 3.5, fusion group 2):
               every q and k row scaled by 2^e, e uniform in [-4, 4] per token,
               and per-dimension weights gamma_q, gamma_k
+* ``p720s`` : ``p720`` for the block-sparse attention (Sec. 3.4): q and k rows
+              share a per-head direction c (N(0,1) per head, added to every row
+              before the bf16 cast), so the rotary embedding makes attention
+              local in (t, h, w), as in a video DiT
 * ``ref720``: the reference-KV cache of Sec. 5 at 720p: queries = 512 text
               tokens + grid 31x45x80 (Nq=112,112); keys = one cached
               reference video (grid 8x45x80, 28,800 tokens, its own positions
@@ -36,7 +40,9 @@ by 2^e (exact), e = ``randint(-4, 5)`` per token from generators seeded with
 ``slab_seed(seed, 4 or 5, b*H + h)``; the weights are bf16-exact float32
 values 1 + 0.25 N(0,1) (``slab_seed(seed, 6 or 7, 0)``).  Reference segments
 (``n_ref``): k and v of the cached tokens are drawn like the video rows, with
-tensor ids 8 and 9.
+tensor ids 8 and 9.  Shared directions (``shared_dir`` = beta): c is drawn
+from ``slab_seed(seed, 10, b*H + h)`` and beta * c is added, in float32, to
+every q and k row of that slab before the bf16 cast.
 """
 from concurrent.futures import ThreadPoolExecutor
 import os
@@ -64,6 +70,7 @@ class Workload:
     boost: float = 1.0
     qk_norm: bool = False       # q, k rows drawn at random scales; norm weights given
     ref_grid: tuple = ()        # grid (T, Hl, Wl) of a cached reference segment
+    shared_dir: float = 0.0     # weight of a per-head direction shared by all q, k rows
     D: int = HEAD_DIM
 
     @property
@@ -116,7 +123,11 @@ WORKLOADS = {
     "share": Workload("share", 4, 2, 5, 31, 45, 80, n_text=512, text_kv_std=0.5),
     "p720n": Workload("p720n", 5, 1, 40, 31, 45, 80, qk_norm=True),
     "ref720": Workload("ref720", 6, 1, 40, 31, 45, 80, n_text=512, ref_grid=(8, 45, 80)),
+    "p720s": Workload("p720s", 7, 1, 40, 31, 45, 80, shared_dir=1.0),
 }
+
+# threshold parameters of the paper's three refinement steps (Sec. 3.4)
+SPARSE_TAUS = (1.0, 1.25, 1.5)
 
 # eps under the root of the QK normalisation in the qk_norm workloads
 QK_NORM_EPS = 1e-6
@@ -134,15 +145,23 @@ def slab_seed(seed: int, tensor: int, slab: int) -> int:
 
 def _fill_slab(dst, seed, tensor, slab, w: Workload):
     gen = torch.Generator().manual_seed(slab_seed(seed, tensor, slab))
+    shared = None
+    if w.shared_dir and tensor in (0, 1):
+        cgen = torch.Generator().manual_seed(slab_seed(seed, 10, slab))
+        shared = torch.randn(w.D, generator=cgen, dtype=torch.float32) * w.shared_dir
     if w.n_text:
         std = 1.0 if tensor == 0 else w.text_kv_std
         x = torch.randn((w.n_text, w.D), generator=gen, dtype=torch.float32)
         if std != 1.0:
             x.mul_(torch.tensor(std, dtype=torch.float32))
+        if shared is not None:
+            x.add_(shared)
         dst[: w.n_text].copy_(x)
     x = torch.randn((w.n_video, w.D), generator=gen, dtype=torch.float32)
     if w.scale != 1.0:
         x.mul_(torch.tensor(w.scale, dtype=torch.float32))
+    if shared is not None:
+        x.add_(shared)
     dst[w.n_text:].copy_(x)  # float32 -> bf16, round to nearest even
 
 

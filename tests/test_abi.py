@@ -216,6 +216,64 @@ def test_qknorm_rope3d_rejects_before_any_hip_call(L, kw, status):
     assert st == status, sol.sol_last_error()
 
 
+def test_sparse_workspace_size(L):
+    nqb, nkb = 436, 872  # N = 111,600
+    up = lambda x: (x + 255) // 256 * 256
+    o1 = up(40 * nqb * 4)
+    o2 = up(o1 + 40 * nqb * nkb * 2)
+    o3 = up(o2 + 40 * nqb * 128 * 4)
+    assert sol.sol_sparse_workspace_bytes(1, 40, 111600, 128) == up(o3 + 40 * nkb * 128 * 4)
+    assert sol.sol_sparse_workspace_bytes(1, 1, (1 << 20) + 1, 128) == 0
+    assert sol.sol_sparse_workspace_bytes(1, 1, 100, 64) == 0
+
+
+WSS = P(0x30000000)
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(N=(1 << 20) + 1, T=1, Hl=1, Wl=1), -2, "N <= "),
+    (dict(ws=None), -1, "workspace is NULL"),
+    (dict(ws_bytes=100), -1, "workspace needs"),
+    (dict(ws=P(0x30000004)), -1, "aligned"),
+    (dict(ws=P(0x100000 - 4096)), -1, "workspace overlaps"),
+    (dict(tau=float("nan")), -1, "tau"),
+    (dict(tau=float("inf")), -1, "tau"),
+    (dict(gamma=P(0x20000004)), -1, "gamma"),
+    (dict(k_prep=None), -1, "NULL"),
+])
+def test_sparse_route_rejects_before_any_hip_call(L, kw, status, fragment):
+    args = dict(q=A, k_prep=P(0x1000000), B=1, H=2, N=1000, D=128, T=1, Hl=10, Wl=100, tab=TAB,
+                gamma=None, eps=1e-6, tau=1.0, ws=WSS, ws_bytes=None)
+    args.update(kw)
+    if args["ws_bytes"] is None:
+        args["ws_bytes"] = sol.sol_sparse_workspace_bytes(args["B"], args["H"], min(args["N"], 1 << 20), 128)
+    st = sol.sol_sparse_route(args["q"], args["k_prep"], args["B"], args["H"], args["N"], args["D"],
+                              args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"], args["eps"],
+                              args["tau"], args["ws"], args["ws_bytes"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(out=P(0x30000000 + 64)), -1, "overlaps"),
+    (dict(fmt=3), -1, "out_format"),
+    (dict(v_prep=None), -1, "NULL"),
+    (dict(ws_bytes=10), -1, "workspace needs"),
+])
+def test_attn_fwd_sparse_rejects_before_any_hip_call(L, kw, status, fragment):
+    args = dict(q=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=1000, D=128, T=1,
+                Hl=10, Wl=100, tab=TAB, gamma=None, eps=1e-6, ws=WSS, ws_bytes=None, fmt=0)
+    args.update(kw)
+    if args["ws_bytes"] is None:
+        args["ws_bytes"] = sol.sol_sparse_workspace_bytes(1, 2, 1000, 128)
+    st = sol.sol_attn_fwd_sparse(args["q"], args["k_prep"], args["v_prep"], args["out"], args["B"],
+                                 args["H"], args["N"], args["D"], args["T"], args["Hl"], args["Wl"],
+                                 args["tab"], args["gamma"], args["eps"], args["ws"], args["ws_bytes"],
+                                 args["fmt"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
 def test_binding_rejects_wrong_dtype_and_device():
     import torch
     x = torch.zeros(1, 1, 4, 128, dtype=torch.float32)

@@ -1,0 +1,207 @@
+"""GPU parity of the block-sparse attention (sol_sparse_route +
+sol_attn_fwd_sparse), through the C ABI, against the oracle.
+
+Routing is an integer decision taken in floating point: the kernel scores in
+fp32, the oracle in double, so a key block whose score lies within rounding
+distance of the threshold (or of the best score) may be kept by one and not
+the other.  The routing check therefore requires the two masks to agree on
+every other block; the attention check then runs the oracle under the
+kernel's own routing, so it tests the sparse attention exactly.
+
+Errors are normalised per output row here: the shared-direction inputs that
+make attention local also make output magnitudes differ by an order of
+magnitude between rows of one slab (rows attending to a few keys against rows
+averaging many), so a slab's RMS is not the scale of most of its rows -- even
+the correctly rounded bf16 output exceeds the gate under it (max 0.030 on the
+first shape) -- while each row's own RMS is.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_35110_amd import sol
+from paper_2609_35110_amd import workloads as W
+
+from parity import assert_parity, compare
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+QB, KB = sol.SPARSE_QUERY_BLOCK, sol.SPARSE_KEY_BLOCK
+EPS = W.QK_NORM_EPS
+# a block's score closer than this (relative to the slab's largest |score|)
+# to the threshold or to the best score may be decided either way
+SCORE_TOL = 1e-4
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    sol.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _bits(t):
+    return W.as_bits(t.cpu())
+
+
+def _run_sparse(w, q, k, v, tau, gq=None, gk=None, fp8=False):
+    """prepare_kv_ex + sparse_route + attn_fwd_sparse; returns (out, gpu mask)."""
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV) if w.n_video else None
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    kp, vp = sol.prepared_kv_buffers(w.B, w.H, w.N, DEV)
+    sol.prepare_kv_ex(kd, vd, w.T, w.Hl, w.Wl, tab, kp, vp,
+                      gamma=None if gk is None else gk.to(DEV), eps=EPS)
+    gqd = None if gq is None else gq.to(DEV)
+    ws = sol.sparse_route(qd, kp, w.T, w.Hl, w.Wl, tab, tau, gamma=gqd, eps=EPS)
+    out = sol.attn_fwd_sparse(qd, kp, vp, w.T, w.Hl, w.Wl, tab, ws, gamma=gqd, eps=EPS, fp8=fp8)
+    torch.cuda.synchronize()
+    return out, gpu_mask(ws, w.B, w.H, w.N)
+
+
+def gpu_mask(ws, B, H, N):
+    """The kept-block mask [B, H, nqb, nkb] of the routing in the workspace;
+    checks each list is strictly ascending and in range."""
+    counts, blocks = sol.sparse_routing(ws, B, H, N)
+    counts, blocks = counts.cpu().numpy(), blocks.cpu().numpy().astype(np.int64)
+    nqb, nkb = blocks.shape[2], blocks.shape[3]
+    mask = np.zeros((B, H, nqb, nkb), dtype=np.uint8)
+    for b in range(B):
+        for h in range(H):
+            for I in range(nqb):
+                c = counts[b, h, I]
+                assert 1 <= c <= nkb
+                lst = blocks[b, h, I, :c]
+                assert (np.diff(lst) > 0).all() and lst[0] >= 0 and lst[-1] < nkb
+                mask[b, h, I, lst] = 1
+    return mask
+
+
+def check_routing(got, q, k, w, tau, gq=None, gk=None, slabs=None):
+    """GPU mask vs the oracle's routing on the given (b, h) slabs: equal except
+    on blocks within SCORE_TOL of the threshold or of the best score."""
+    qb, kb = _bits(q), _bits(k)
+    B, H = w.B, w.H
+    slabs = slabs if slabs is not None else [(b, h) for b in range(B) for h in range(H)]
+    n_diff = n_tot = 0
+    for b, h in slabs:
+        want, sc, thr = oracle.sparse_route(
+            np.ascontiguousarray(qb[b:b + 1, h:h + 1]), np.ascontiguousarray(kb[b:b + 1, h:h + 1]),
+            w.T, w.Hl, w.Wl, tau, qblk=QB, kblk=KB,
+            q_gamma=None if gq is None else gq.numpy(), k_gamma=None if gk is None else gk.numpy(),
+            eps=EPS)
+        want, sc, thr = want[0, 0], sc[0, 0], thr[0, 0]
+        g = got[b, h]
+        diff = g != want
+        scale = np.abs(sc).max()
+        near_thr = np.abs(sc - thr[:, None]) <= SCORE_TOL * scale
+        near_best = np.abs(sc - sc.max(axis=1, keepdims=True)) <= SCORE_TOL * scale
+        bad = diff & ~near_thr & ~near_best
+        assert not bad.any(), "slab %s: %d routing decisions differ away from the threshold" % (
+            (b, h), bad.sum())
+        n_diff += int(diff.sum())
+        n_tot += diff.size
+    return n_diff, n_tot
+
+
+SHAPES = [
+    # (B, H, T, Hl, Wl, n_text, tau)
+    (1, 2, 4, 16, 16, 0, 1.0),        # N=1024: 4 query blocks, 8 key blocks
+    (1, 2, 3, 21, 25, 37, 1.25),      # N=1612: ragged blocks, a prefix inside block 0
+    (2, 1, 5, 14, 18, 300, 0.5),      # N=1560: prefix spans query block 1 and key blocks 0-2
+    (1, 1, 2, 30, 40, 0, 1.5),        # N=2400
+    (1, 2, 1, 5, 7, 0, 1.0),          # N=35: one block each way
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_sparse_full_parity(shape):
+    B, H, T, Hl, Wl, nt, tau = shape
+    w = W.custom(B, H, T, Hl, Wl, n_text=nt, seed_index=1000 + sum(shape[:6]), shared_dir=1.0)
+    q, k, v = W.make_inputs(w)
+    out, mask = _run_sparse(w, q, k, v, tau)
+    n_diff, n_tot = check_routing(mask, q, k, w, tau)
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), T, Hl, Wl, block_mask=mask, qblk=QB, kblk=KB)
+    R = B * H * w.N
+    st = compare(_bits(out).reshape(R, w.D), ref.reshape(R, w.D), np.arange(R))
+    _log("sparse %s tau=%g: density %.3f, %d/%d routing decisions at rounding distance; %s"
+         % (w.describe(), tau, mask.mean(), n_diff, n_tot, st))
+    assert_parity(st, "sparse")
+
+
+def test_sparse_dense_limit_is_the_dense_kernel():
+    """tau = -1e30 keeps every key block: the walk is the dense walk (plus
+    whole masked tiles past N), bit for bit the dense prepared path."""
+    w = W.custom(1, 2, 3, 11, 13, n_text=37, seed_index=1050)
+    q, k, v = W.make_inputs(w)
+    out, mask = _run_sparse(w, q, k, v, -1e30)
+    assert mask.all()
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    kp, vp = sol.prepare_kv(k.to(DEV), v.to(DEV), w.T, w.Hl, w.Wl, tab)
+    dense = sol.attn_fwd_prepared(q.to(DEV), kp, vp, w.T, w.Hl, w.Wl, tab)
+    torch.cuda.synchronize()
+    assert torch.equal(out.cpu(), dense.cpu())
+
+
+def test_sparse_prefix_sink_and_dense_prefix_queries():
+    """tau = +1e30: a video query block keeps the prefix key blocks and its
+    best block only; query blocks with prefix rows keep everything."""
+    w = W.custom(1, 2, 3, 16, 16, n_text=300, seed_index=1060, shared_dir=1.0)
+    q, k, v = W.make_inputs(w)
+    out, mask = _run_sparse(w, q, k, v, 1e30)
+    nkb = mask.shape[-1]
+    sink = np.arange(nkb) * KB < w.n_text
+    for I in range(mask.shape[2]):
+        if I * QB < w.n_text:
+            assert mask[:, :, I].all()
+        else:
+            assert (mask[:, :, I, sink] == 1).all()
+            assert (mask[:, :, I, ~sink].sum(-1) <= 1).all()  # at most the best block
+    check_routing(mask, q, k, w, 1e30)
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, block_mask=mask, qblk=QB,
+                           kblk=KB)
+    R = w.B * w.H * w.N
+    st = compare(_bits(out).reshape(R, w.D), ref.reshape(R, w.D), np.arange(R))
+    assert_parity(st, "sparse sink")
+
+
+def test_sparse_with_qknorm():
+    w = W.custom(1, 2, 4, 12, 20, n_text=64, seed_index=1070, qk_norm=True, shared_dir=1.0)
+    q, k, v = W.make_inputs(w)
+    gq, gk = W.norm_weights(w)
+    out, mask = _run_sparse(w, q, k, v, 1.0, gq=gq, gk=gk)
+    check_routing(mask, q, k, w, 1.0, gq=gq, gk=gk)
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, block_mask=mask, qblk=QB,
+                           kblk=KB, q_gamma=gq.numpy(), k_gamma=gk.numpy(), eps=EPS)
+    R = w.B * w.H * w.N
+    st = compare(_bits(out).reshape(R, w.D), ref.reshape(R, w.D), np.arange(R))
+    _log("sparse + qknorm: density %.3f; %s" % (mask.mean(), st))
+    assert_parity(st, "sparse + qknorm")
+
+
+@pytest.mark.parametrize("tau", [1.0, 1.5])
+def test_sparse_p720_sampled_parity(tau):
+    """Full 720p size (the refinement stage's shape), the paper's tau values:
+    routing of two heads against the oracle, sampled rows of every head under
+    the kernel's routing."""
+    w = W.WORKLOADS["p720s"]
+    _log("generating %s" % w.describe())
+    q, k, v = W.make_inputs(w)
+    out, mask = _run_sparse(w, q, k, v, tau)
+    n_diff, n_tot = check_routing(mask, q, k, w, tau, slabs=[(0, 0), (0, w.H - 1)])
+    rows = W.sample_rows(w, per_slab=8, head=32, tail=80).numpy()
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rows=rows, block_mask=mask,
+                           qblk=QB, kblk=KB)
+    got = _bits(out).reshape(-1, w.D)[rows]
+    st = compare(got, ref, rows)
+    _log("p720s tau=%g: density %.4f, %d/%d decisions at rounding distance; %s"
+         % (tau, mask.mean(), n_diff, n_tot, st))
+    assert_parity(st, "p720s")

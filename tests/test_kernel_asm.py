@@ -79,12 +79,24 @@ def operands(t):
 STORE_PREFIXES = ("ds_write", "global_store", "buffer_store", "scratch_store", "flat_store")
 
 
+def template_args(name):
+    """(kRope, kRobust, kSparse) of an attn_prepared_kernel instance from its mangled name."""
+    m = re.search(r"attn_prepared_kernelILb(\d)ELb(\d)ELb(\d)EE", name)
+    assert m, name
+    return tuple(bool(int(x)) for x in m.groups())
+
+
+def first_pass(name):
+    return not template_args(name)[1]
+
+
 def test_mfma_latency_respected(asm_text):
-    """Every MFMA of the four kernels, inline or not: the compiler's own
-    hazard handling is checked too (it once let a spill reload overwrite an
-    accumulator still being read)."""
+    """Every MFMA of the eight kernels (rotary or not, first or second pass,
+    dense or block-sparse), inline or not: the compiler's own hazard handling
+    is checked too (it once let a spill reload overwrite an accumulator still
+    being read)."""
     kernels = functions(asm_text, "attn_prepared_kernel")
-    assert len(kernels) == 4
+    assert len(kernels) == 8
     for name, body in kernels:
         ins = instructions(body)
         n_asm = 0
@@ -123,20 +135,20 @@ def test_mfma_latency_respected(asm_text):
                     written, read = regs(ops2[0]), set().union(set(), *(regs(x) for x in ops2[1:]))
                 assert not (written & (dst | srcc)), "%s: %r overwrites registers of %r" % (name, t2, t)
                 assert not (read & dst), "%s: %r reads the result of %r too early" % (name, t2, t)
-        if "Lb0EEEv" in name:
+        if first_pass(name):
             assert n_asm >= 32, "%s: expected the score MFMAs as inline assembly" % name
 
 
 def test_second_pass_has_no_inline_asm_mfma(asm_text):
-    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if "Lb1EEEv" in f[0]]
-    assert len(kernels) == 2
+    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if not first_pass(f[0])]
+    assert len(kernels) == 4
     for name, body in kernels:
         assert not any(in_asm and t.startswith("v_mfma") for t, in_asm in instructions(body)), name
 
 
 def test_m0_used_only_by_tile_copies(asm_text):
     kernels = functions(asm_text, "attn_prepared_kernel")
-    assert len(kernels) == 4
+    assert len(kernels) == 8
     implicit_m0 = ("s_movrel", "v_movrel", "s_sendmsg", "ds_gws", "v_interp", "ds_append", "ds_consume",
                    "ds_ordered", "s_setreg")
     for name, body in kernels:
@@ -154,19 +166,23 @@ def test_m0_used_only_by_tile_copies(asm_text):
 
 
 def test_first_pass_copy_count_waits_see_only_copies(asm_text):
-    """The closing barrier's vmcnt(4) assumes the last four vector-memory
-    instructions of the wave are its tile copies: between two such waits the
-    compiler must issue no load, store or spill of its own."""
-    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if "Lb0EEEv" in f[0]]
+    """The closing barrier's vmcnt(4) (a vmcnt(4) wait right before
+    s_barrier) assumes the last four vector-memory instructions of the wave are
+    its tile copies: between the previous vmcnt wait and such a barrier wait
+    the compiler must issue no load, store or spill of its own.  (Its own
+    vmcnt waits for its own loads, e.g. in the prologue, wait for at least as
+    much as they need: the counter retires in order.)"""
+    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if first_pass(f[0])]
+    assert len(kernels) == 4
     for name, body in kernels:
         ins = instructions(body)
         assert not any(t.startswith("scratch_") for t, _ in ins), "%s spills" % name
         since, n_waits = [], 0
-        for t, in_asm in ins:
+        for i, (t, in_asm) in enumerate(ins):
             if t.startswith(("buffer_", "global_", "flat_")):
                 since.append((t, in_asm))
             if t.startswith("s_waitcnt") and "vmcnt" in t:
-                if "vmcnt(4)" in t:
+                if "vmcnt(4)" in t and i + 1 < len(ins) and ins[i + 1][0] == "s_barrier":
                     n_waits += 1
                     others = [x for x, a in since if not (a and x.endswith(" lds"))]
                     assert not others, "%s: %r before a copy-count wait" % (name, others[:3])
