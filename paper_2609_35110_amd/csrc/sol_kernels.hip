@@ -594,10 +594,13 @@ constexpr int kBufferDword3 = 0x00020000;
 // The workgroup's 256 query rows are one routing query block; it attends only
 // to the key blocks (kSparseKeyBlock keys = 4 tiles each) listed for it in
 // blocks[(bh * n_qtiles + qt) * nkb ..] (ascending, counts[bh * n_qtiles + qt]
-// of them).  The list is staged into LDS once; the loop walks the listed
-// tiles in order -- LDS ring slots follow the walk, copies read the listed
-// tile -- and looks each list entry up an iteration phase ahead of its use,
-// so no LDS wait for it falls inside the MFMA slots.
+// of them).  The list is staged into LDS once, each word holding an entry and
+// the next one; the loop walks the listed tiles in order -- LDS ring slots
+// follow the walk, copies read the listed tile.  One LDS read per iteration,
+// issued at its start and made scalar a phase later, gives the tiles of both
+// copies (walk positions i + 3 and i + 4 lie in one block or two neighbours);
+// masks need no lookup, since only the last listed block can hold keys past
+// N.
 constexpr int kSparseKeyBlock = 128;  // keys per routing key block
 constexpr int kSparseQueryBlock = 256;  // query rows per routing query block (= BM)
 constexpr int kMaxSparseBlocks = 8192;  // key blocks per slab the LDS list holds (N <= 2^20)
@@ -612,7 +615,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
                           int nkb) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
-  __shared__ uint16_t blist[kSparse ? kMaxSparseBlocks : 1];
+  __shared__ uint32_t blist[kSparse ? kMaxSparseBlocks : 1];  // entry e | entry e + 1 << 16
 
   // pin() in the first pass only.  The second pass spills, and with the empty
   // asm statements in place the compiler put a spill reload of an MFMA's
@@ -646,22 +649,32 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int qrow_first = qt * BM + wave * 64 + l32;
   // Tiles the workgroup walks: every tile of the slab, or the listed blocks'.
   int n_kv = (N + BN2 - 1) / BN2;
+  int last_blk = 0;  // sparse: the last listed key block
   if (kSparse) {
     // counts and entries are clamped to the slab, whatever the list holds, so
     // every copy stays inside the slab's prepared tiles
     const size_t qb = (size_t)bh * n_qtiles + qt;
     const int cnt = min(max(counts[qb], 1), min(nkb, kMaxSparseBlocks));
-    for (int e = tid; e < cnt; e += 256) blist[e] = (uint16_t)min((int)blocks[qb * nkb + e], nkb - 1);
+    auto entry = [&](int e) { return (uint32_t)min((int)blocks[qb * nkb + min(e, cnt - 1)], nkb - 1); };
+    for (int e = tid; e < cnt; e += 256) blist[e] = entry(e) | entry(e + 1) << 16;
     n_kv = 4 * cnt;
+    last_blk = __builtin_amdgcn_readfirstlane((int)entry(cnt - 1));
     __syncthreads();
   }
   // Slab tile of walk position t (clamped to the walk; a listed block's
   // tiles past the slab's last are clamped by the copy and masked whole).
-  auto list_entry = [&](int t) __attribute__((always_inline)) {  // LDS read, no wait here
-    return (int)blist[min(t, n_kv - 1) >> 2];
+  auto walk_tile = [&](int t) __attribute__((always_inline)) {
+    if (!kSparse) return t;
+    t = min(t, n_kv - 1);
+    return 4 * __builtin_amdgcn_readfirstlane((int)(blist[t >> 2] & 0xFFFFu)) + (t & 3);
   };
-  auto slab_tile = [&](int t, int entry) __attribute__((always_inline)) {
-    return kSparse ? 4 * __builtin_amdgcn_readfirstlane(entry) + (min(t, n_kv - 1) & 3) : t;
+  // First key of walk position t where it may need masking: in the sparse
+  // walk only the last listed block's tiles can hold keys past N (every other
+  // block is whole); elsewhere 0, never masked (N >= 32 whenever a slab has
+  // two blocks).
+  auto mask_kv0 = [&](int t) __attribute__((always_inline)) {
+    if (!kSparse) return t * BN2;
+    return t >= n_kv - 4 ? (4 * last_blk + (t & 3)) * BN2 : 0;
   };
   if (kRobust) {
     // Second pass: only the row blocks the first pass marked (NaN rows) are
@@ -813,13 +826,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // Sparse walk: list entries of the tiles this iteration copies (i + 4,
     // i + 3), masks (i + 1) and may recompute (i), read from LDS now and made
     // scalar where they are used.
-    int e_k4 = 0, e_v3 = 0, e_m1 = 0, e_0 = 0;
-    if (kSparse) {
-      e_k4 = list_entry(i + 4);
-      e_v3 = list_entry(i + 3);
-      e_m1 = list_entry(i + 1);
-      if (kRobust) e_0 = list_entry(i);
-    }
+    uint32_t pair = 0;  // list word of walk position i + 3 (and the next entry)
+    if (kSparse) pair = blist[min(i + 3, n_kv - 1) >> 2];
     // ---- phase A
     uint32_t p1[8];
     float l1;
@@ -884,7 +892,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
           for (int kk = 0; kk < 8; ++kk)
             t = __builtin_amdgcn_mfma_f32_32x32x16_f16(kfrag(i, kk), qf[qb][kk], t, 0, 0, 0);
-          const int kv0 = slab_tile(i, e_0) * BN2;
+          const int kv0 = mask_kv0(i);
           if (kv0 + BN2 > N) mask_block(kv0, t);
           const float delta = fmaxf(tile_max(t), 0.0f);
           const float alpha = __builtin_amdgcn_exp2f(-delta);
@@ -942,7 +950,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // write or read them.
     mfma_wait_tail();
     if (!kRobust) asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
-    const int kv_next = slab_tile(i + 1, e_m1) * BN2;  // first key of walk tile i + 1
+    const int kv_next = mask_kv0(i + 1);  // first key of walk tile i + 1
     if (__builtin_expect(i + 1 < n_kv && kv_next + BN2 > N, 0)) {
       mfma_wait();
       mask_tile(kv_next, ns);
@@ -951,7 +959,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // ---- phase B
     pa = pb = 0.0f;
     t01 = t23 = t03 = t45 = 0;
-    const int tile_k4 = slab_tile(i + 4, e_k4), tile_v3 = slab_tile(i + 3, e_v3);
+    int tile_k4 = i + 4, tile_v3 = i + 3;
+    if (kSparse) {
+      const uint32_t w = __builtin_amdgcn_readfirstlane(pair);
+      const int t3 = min(i + 3, n_kv - 1), t4 = min(i + 4, n_kv - 1);
+      const int lo = (int)(w & 0xFFFFu), hi = (int)(w >> 16);
+      tile_v3 = 4 * lo + (t3 & 3);
+      tile_k4 = 4 * ((t4 >> 2) == (t3 >> 2) ? lo : hi) + (t4 & 3);
+    }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
@@ -997,9 +1012,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   // ---- prologue: K(0..2) and V(0..1) in LDS, K(3) and V(2) on their way;
   // S(0) against m = its own max; the qb0 words of P(0); the fragment
   // registers loaded with K(1) and V(0).
-  auto walk_tile = [&](int t) __attribute__((always_inline)) {
-    return kSparse ? slab_tile(t, list_entry(t)) : t;
-  };
   const int w0 = walk_tile(0), w1 = walk_tile(1), w2 = walk_tile(2), w3 = walk_tile(3);
   dma_k(0, w0, 0);
   dma_k(0, w0, 1);
@@ -1029,7 +1041,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     sa[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[0][kk], sa[0], 0, 0, 0);
     sa[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[1][kk], sa[1], 0, 0, 0);
   }
-  if (w0 * BN2 + BN2 > N) mask_tile(w0 * BN2, sa);
+  if (mask_kv0(0) + BN2 > N) mask_tile(mask_kv0(0), sa);
   // The first pass also takes the reference max over each 32-row block's
   // "diagonal" tile -- the keys at the rows' own positions (offset by n_keys -
   // Nq, the layout of a cached prefix of keys) -- where a video DiT's local
@@ -1049,7 +1061,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       if (kSparse) {
         const int blk = key / kSparseKeyBlock;
         bool hit = false;
-        for (int e = lane; e < n_kv / 4; e += 64) hit |= blist[e] == blk;
+        for (int e = lane; e < n_kv / 4; e += 64) hit |= (int)(blist[e] & 0xFFFFu) == blk;
         attended = __any(hit);
       }
       if (attended) {
