@@ -241,8 +241,8 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
  * sol_sparse_route left it), bf16 or E4M3 output as sol_attn_fwd_prepared_ex.
  * The workspace is sol_sparse_workspace_bytes(B, H, N, D) bytes of device
  * memory, 16-byte aligned, not overlapping q, k_prep, v_prep or out.
- * N <= 2^20 (SOL_ERR_UNSUPPORTED beyond: the kept-block list of a query block
- * is staged in LDS).  Other arguments and errors as sol_attn_fwd_prepared_ex;
+ * N <= 1,032,192 = 8064 key blocks (SOL_ERR_UNSUPPORTED beyond: the
+ * kept-block list of a query block is staged in LDS).  Other arguments and errors as sol_attn_fwd_prepared_ex;
  * sol_sparse_workspace_bytes returns 0 for invalid or unsupported sizes.
  */
 size_t sol_sparse_workspace_bytes(int B, int H, int N, int D);

@@ -189,5 +189,12 @@ __device__ __forceinline__ uint4 qk_chunk(uint4 x, const float* __restrict__ gam
 constexpr int kPrepTile = 32;                  // keys per prepared tile
 constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
 
+// Block-sparse routing granularity and the longest kept-block list a query
+// block's workgroup stages in LDS (4 bytes an entry, beside 128 KB of K and V
+// rings: 8064 entries keep the kernel inside 160 KB).
+constexpr int kSparseKeyBlock = 128;    // keys per routing key block (4 tiles)
+constexpr int kSparseQueryBlock = 256;  // query rows per routing query block
+constexpr int kMaxSparseBlocks = 8064;  // key blocks per slab: N <= 1,032,192
+
 }  // namespace
 }  // namespace sol

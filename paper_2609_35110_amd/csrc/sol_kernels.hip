@@ -543,11 +543,16 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
 // issues no memory instruction of its own in the loop (the first pass: a
 // build test checks it); the second pass, whose spill code does, waits for
 // every copy (kAll).
-template <bool kAll>
+// kDeep (the block-sparse walk, whose scattered tiles miss L2 more often):
+// copies are issued one iteration earlier and the barrier leaves the last
+// eight -- this iteration's and the previous one's -- in flight.
+template <bool kAll, bool kDeep>
 __device__ __forceinline__ void dma_barrier() {
   asm volatile("" ::: "memory");
   if (kAll)
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt 0, expcnt 7, lgkmcnt 15
+  else if (kDeep)
+    __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt 8, expcnt 7, lgkmcnt 15 (no LDS wait)
   else
     __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt 4, expcnt 7, lgkmcnt 15 (no LDS wait)
   __builtin_amdgcn_s_barrier();
@@ -601,9 +606,7 @@ constexpr int kBufferDword3 = 0x00020000;
 // copies (walk positions i + 3 and i + 4 lie in one block or two neighbours);
 // masks need no lookup, since only the last listed block can hold keys past
 // N.
-constexpr int kSparseKeyBlock = 128;  // keys per routing key block
-constexpr int kSparseQueryBlock = 256;  // query rows per routing query block (= BM)
-constexpr int kMaxSparseBlocks = 8192;  // key blocks per slab the LDS list holds (N <= 2^20)
+static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's rows");
 
 template <bool kRope, bool kRobust, bool kSparse>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
@@ -614,7 +617,11 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
                           const uint16_t* __restrict__ blocks, const int* __restrict__ counts,
                           int nkb) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVBufs * kPrepTileElems];
+  // The sparse walk copies K 5 and V 4 walk positions ahead (the dense walk
+  // 4 and 3), with a V ring of 8: 64 + 64 + 32 KB, the whole 160 KB of LDS.
+  constexpr int kVB = kSparse ? 8 : kVBufs;
+  constexpr int kKAhead = kSparse ? 5 : 4, kVAhead = kSparse ? 4 : 3;
+  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVB * kPrepTileElems];
   __shared__ uint32_t blist[kSparse ? kMaxSparseBlocks : 1];  // entry e | entry e + 1 << 16
 
   // pin() in the first pass only.  The second pass spills, and with the empty
@@ -762,14 +769,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     dma_blk(rsrc_k, k_lds + (t & (kKBufs - 1)) * kPrepTileElems, tile, u);
   };
   auto dma_v = [&](int t, int tile, int u) __attribute__((always_inline)) {
-    dma_blk(rsrc_v, v_lds + (t & (kVBufs - 1)) * kPrepTileElems, tile, u);
+    dma_blk(rsrc_v, v_lds + (t & (kVB - 1)) * kPrepTileElems, tile, u);
   };
   // Fragment kk of K tile `tile` / fragment j = 4 kst + db of V tile `tile`.
   auto kfrag = [&](int tile, int kk) __attribute__((always_inline)) {
     return *reinterpret_cast<const f16x8*>(k_lds + (tile & (kKBufs - 1)) * kPrepTileElems + kk * 512 + lane * 8);
   };
   auto vfrag = [&](int tile, int j) __attribute__((always_inline)) {
-    return *reinterpret_cast<const f16x8*>(v_lds + (tile & (kVBufs - 1)) * kPrepTileElems + j * 512 + lane * 8);
+    return *reinterpret_cast<const f16x8*>(v_lds + (tile & (kVB - 1)) * kPrepTileElems + j * 512 + lane * 8);
   };
 
   f32x16 o[2][4];
@@ -819,15 +826,17 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   //     P(i+1) qb0 word j
   auto iteration = [&](int i, f32x16* cs, f32x16* ns, uint32_t* p0_cur, uint32_t* p0_next,
                        float& l0_cur, float& l0_next) __attribute__((always_inline)) {
-    // K tile t sits in buffer t % 8 from its copy (iteration t-4, or the
-    // prologue) to iteration t+4, read in iteration t-2 (and by the second
-    // pass's rare path in iteration t); V tile t in buffer t % 4 from its copy
-    // (iteration t-3) to iteration t+1, read in iteration t-1.
-    // Sparse walk: list entries of the tiles this iteration copies (i + 4,
-    // i + 3), masks (i + 1) and may recompute (i), read from LDS now and made
-    // scalar where they are used.
-    uint32_t pair = 0;  // list word of walk position i + 3 (and the next entry)
-    if (kSparse) pair = blist[min(i + 3, n_kv - 1) >> 2];
+    // K tile t sits in buffer t % 8 from its copy (iteration t - kKAhead, or
+    // the prologue) until the copy of tile t + 8 overwrites it, and is read in
+    // iteration t-2 (and by the second pass's rare path in iteration t); V
+    // tile t sits in buffer t % kVB from its copy (iteration t - kVAhead) until
+    // tile t + kVB's, and is read in iteration t-1.  Every overwrite comes at
+    // least two barriers after the last wave consumed the reads of the tile
+    // it replaces.
+    // Sparse walk: the list word of the tiles this iteration copies, read
+    // from LDS now and made scalar at the start of phase B.
+    uint32_t pair = 0;  // list word of walk position i + kVAhead (and the next entry)
+    if (kSparse) pair = blist[min(i + kVAhead, n_kv - 1) >> 2];
     // ---- phase A
     uint32_t p1[8];
     float l1;
@@ -959,13 +968,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // ---- phase B
     pa = pb = 0.0f;
     t01 = t23 = t03 = t45 = 0;
-    int tile_k4 = i + 4, tile_v3 = i + 3;
+    // slab tiles of this iteration's copies: K(i + kKAhead), V(i + kVAhead)
+    int tile_k = i + kKAhead, tile_v = i + kVAhead;
     if (kSparse) {
       const uint32_t w = __builtin_amdgcn_readfirstlane(pair);
-      const int t3 = min(i + 3, n_kv - 1), t4 = min(i + 4, n_kv - 1);
+      const int tv = min(i + kVAhead, n_kv - 1), tk = min(i + kKAhead, n_kv - 1);
       const int lo = (int)(w & 0xFFFFu), hi = (int)(w >> 16);
-      tile_v3 = 4 * lo + (t3 & 3);
-      tile_k4 = 4 * ((t4 >> 2) == (t3 >> 2) ? lo : hi) + (t4 & 3);
+      tile_v = 4 * lo + (tv & 3);
+      tile_k = 4 * ((tk >> 2) == (tv >> 2) ? lo : hi) + (tk & 3);
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -980,10 +990,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
         p0_next[j - 1] = pack_f16x2(pa, pb);
         keep(p0_next[j - 1]);
       }
-      if (j == 1) dma_k(i + 4, tile_k4, 0);  // over K(i-4)
-      if (j == 2) dma_v(i + 3, tile_v3, 0);  // over V(i-1), read in iteration i-2
-      if (j == 3) dma_k(i + 4, tile_k4, 1);
-      if (j == 5) dma_v(i + 3, tile_v3, 1);
+      // over K(i + kKAhead - 8), read in iteration i - 6 at the latest; over
+      // V(i + kVAhead - kVB), whose fragments every wave read two barriers ago
+      if (j == 1) dma_k(i + kKAhead, tile_k, 0);
+      if (j == 2) dma_v(i + kVAhead, tile_v, 0);
+      if (j == 3) dma_k(i + kKAhead, tile_k, 1);
+      if (j == 5) dma_v(i + kVAhead, tile_v, 1);
       __builtin_amdgcn_sched_barrier(0);
       // slot 2: PV MFMA of block 1; fragment j of V(i+1) into the register
       // just used; exponential of register 2j + 1; a step of the word-sum tree.
@@ -1004,15 +1016,19 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     l0_next = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p0_next[6], p0_next[7]))));
     keep(p0_next[7]);
     keep(l0_next);
-    // The copies issued in the previous iteration (K(i+3), V(i+2)) must have
-    // landed: only this iteration's four may still be in flight.
-    dma_barrier<kRobust>();
+    // The copies the next iteration reads must have landed: those issued
+    // kKAhead - 2 iterations ago (K) and kVAhead - 1 ago (V) -- so only this
+    // iteration's four copies (dense walk) or this and the previous
+    // iteration's eight (sparse walk) may still be in flight.
+    dma_barrier<kRobust, kSparse>();
   };
 
-  // ---- prologue: K(0..2) and V(0..1) in LDS, K(3) and V(2) on their way;
-  // S(0) against m = its own max; the qb0 words of P(0); the fragment
-  // registers loaded with K(1) and V(0).
+  // ---- prologue: K(0 .. kKAhead - 2) and V(0 .. kVAhead - 2) in LDS,
+  // K(kKAhead - 1) and V(kVAhead - 1) on their way; S(0) against m = its own
+  // max; the qb0 words of P(0); the fragment registers loaded with K(1) and
+  // V(0).
   const int w0 = walk_tile(0), w1 = walk_tile(1), w2 = walk_tile(2), w3 = walk_tile(3);
+  const int w4 = kSparse ? walk_tile(4) : 0;
   dma_k(0, w0, 0);
   dma_k(0, w0, 1);
   dma_v(0, w0, 0);
@@ -1023,12 +1039,25 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   dma_k(2, w2, 1);
   dma_v(1, w1, 0);
   dma_v(1, w1, 1);
+  if (kSparse) {
+    dma_k(3, w3, 0);
+    dma_k(3, w3, 1);
+    dma_v(2, w2, 0);
+    dma_v(2, w2, 1);
+  }
   __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
-  dma_k(3, w3, 0);
-  dma_k(3, w3, 1);
-  dma_v(2, w2, 0);
-  dma_v(2, w2, 1);
+  if (kSparse) {
+    dma_k(4, w4, 0);
+    dma_k(4, w4, 1);
+    dma_v(3, w3, 0);
+    dma_v(3, w3, 1);
+  } else {
+    dma_k(3, w3, 0);
+    dma_k(3, w3, 1);
+    dma_v(2, w2, 0);
+    dma_v(2, w2, 1);
+  }
   // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
   // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
   // such copies.

@@ -24,9 +24,9 @@
 namespace sol {
 namespace {
 
-constexpr int kQB = 256;             // query rows per routing query block
-constexpr int kKB = 128;             // keys per routing key block (4 prepared tiles)
-constexpr int kMaxKeyBlocks = 8192;  // key blocks per slab (N <= 2^20)
+constexpr int kQB = kSparseQueryBlock;
+constexpr int kKB = kSparseKeyBlock;
+constexpr int kMaxKeyBlocks = kMaxSparseBlocks;
 
 // Mean of q^ over each query block.  Grid (nqb, slabs); 256 threads = 16 rows
 // x 16 chunks per step, 16 steps over the block's rows: each thread sums its

@@ -223,7 +223,8 @@ def test_sparse_workspace_size(L):
     o2 = up(o1 + 40 * nqb * nkb * 2)
     o3 = up(o2 + 40 * nqb * 128 * 4)
     assert sol.sol_sparse_workspace_bytes(1, 40, 111600, 128) == up(o3 + 40 * nkb * 128 * 4)
-    assert sol.sol_sparse_workspace_bytes(1, 1, (1 << 20) + 1, 128) == 0
+    assert sol.sol_sparse_workspace_bytes(1, 1, 8064 * 128 + 1, 128) == 0
+    assert sol.sol_sparse_workspace_bytes(1, 1, 8064 * 128, 128) > 0
     assert sol.sol_sparse_workspace_bytes(1, 1, 100, 64) == 0
 
 
@@ -231,7 +232,7 @@ WSS = P(0x30000000)
 
 
 @pytest.mark.parametrize("kw,status,fragment", [
-    (dict(N=(1 << 20) + 1, T=1, Hl=1, Wl=1), -2, "N <= "),
+    (dict(N=8064 * 128 + 1, T=1, Hl=1, Wl=1), -2, "N <= "),
     (dict(ws=None), -1, "workspace is NULL"),
     (dict(ws_bytes=100), -1, "workspace needs"),
     (dict(ws=P(0x30000004)), -1, "aligned"),
