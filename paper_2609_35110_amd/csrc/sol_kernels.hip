@@ -184,10 +184,8 @@ __device__ __forceinline__ int tab_pair_hi(int c, const Pos& p, const SeqGrid& g
 // written over V(i-1); the barrier ending each iteration orders every reuse.
 // Loads past the last tile re-read row N-1 and land in buffers nobody reads,
 // so phases A and B are branch-free.
-// kRope: rotate Q (and K unless kPre) with the table; kTabLds: the table is
-// staged in LDS; kPre: k is already rotated and v already fp16 (workspace
-// path), so staging is a plain copy.
-template <bool kRope, bool kTabLds, bool kPre>
+// kRope: rotate Q and K with the table; kTabLds: the table is staged in LDS.
+template <bool kRope, bool kTabLds>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
@@ -248,7 +246,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     vreg[1] = sv[c0 + 8];
   };
   auto fetch_k_rotation = [&](int kv0) {
-    if (kRope && !kPre) {
+    if (kRope) {
       const Pos p = token_pos(min(kv0 + rr, N - 1), g);
       const int a0 = tab_pair_lo(c0, p, g), a1 = tab_pair_hi(c0, p, g);
       kcs[0] = *reinterpret_cast<const float4*>(tab + a0);
@@ -259,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   };
   auto store_k = [&](int buf) {
     uint4 x0 = kreg[0], x1 = kreg[1];
-    if (kRope && !kPre) {
+    if (kRope) {
       x0 = rope_rotate(x0, kcs[0], kcs[1]);
       x1 = rope_rotate(x1, kcs[2], kcs[3]);
     }
@@ -267,8 +265,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     *reinterpret_cast<uint4*>(&k_lds[buf][rr * KS + c0 * 8 + 64]) = x1;
   };
   auto store_v = [&](int buf) {
-    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8]) = kPre ? vreg[0] : bf16x8_to_f16x8(vreg[0]);
-    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8 + 64]) = kPre ? vreg[1] : bf16x8_to_f16x8(vreg[1]);
+    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8]) = bf16x8_to_f16x8(vreg[0]);
+    *reinterpret_cast<uint4*>(&v_lds[buf][rr * VS + c0 * 8 + 64]) = bf16x8_to_f16x8(vreg[1]);
   };
 
   // K fragment (A operand) of key block kb (0/1), dims [16kk + 8hh, +8).
@@ -1216,13 +1214,13 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   const int tab_pairs = g.tab_w + g.Wl * (3 * D / 16);
   if (tab == nullptr)
-    hipLaunchKernelGGL((attn_fwd_kernel<false, false, false>), grid, dim3(kThreads), 0, stream, q,
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false>), grid, dim3(kThreads), 0, stream, q,
                        k, v, out, g, tab, 0, n_qtiles, c_log2);
   else if (tab_pairs <= kTabLdsPairs)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, true, false>), grid, dim3(kThreads), 0, stream, q,
+    hipLaunchKernelGGL((attn_fwd_kernel<true, true>), grid, dim3(kThreads), 0, stream, q,
                        k, v, out, g, tab, tab_pairs, n_qtiles, c_log2);
   else
-    hipLaunchKernelGGL((attn_fwd_kernel<true, false, false>), grid, dim3(kThreads), 0, stream, q,
+    hipLaunchKernelGGL((attn_fwd_kernel<true, false>), grid, dim3(kThreads), 0, stream, q,
                        k, v, out, g, tab, tab_pairs, n_qtiles, c_log2);
   return hipGetLastError();
 }

@@ -205,3 +205,26 @@ def test_sparse_p720_sampled_parity(tau):
     _log("p720s tau=%g: density %.4f, %d/%d decisions at rounding distance; %s"
          % (tau, mask.mean(), n_diff, n_tot, st))
     assert_parity(st, "p720s")
+
+
+def test_sparse_maximum_tokens():
+    """The largest sequence the sparse path takes: 8064 key blocks (N =
+    1,032,192, grid 63 x 128 x 128), so each query block's kept-block list can
+    reach the full LDS list; tau = -1 keeps most blocks.  Routing of the slab
+    against the oracle, sampled rows (first, last, random) under the kernel's
+    routing."""
+    w = W.custom(1, 1, 63, 128, 128, seed_index=1100, shared_dir=1.0)
+    assert w.N == 8064 * KB
+    _log("generating %s" % w.describe())
+    q, k, v = W.make_inputs(w)
+    out, mask = _run_sparse(w, q, k, v, -1.0)
+    _log("max tokens: density %.3f, longest list %d of %d" % (mask.mean(), mask.sum(-1).max(), mask.shape[-1]))
+    check_routing(mask, q, k, w, -1.0)
+    gen = torch.Generator().manual_seed(5)
+    rows = np.unique(np.concatenate([np.arange(32), np.arange(w.N - 80, w.N),
+                                     torch.randint(0, w.N, (160,), generator=gen).numpy()]))
+    ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rows=rows, block_mask=mask,
+                           qblk=QB, kblk=KB)
+    st = compare(_bits(out).reshape(-1, w.D)[rows], ref, rows)
+    _log("max tokens: %s" % st)
+    assert_parity(st, "sparse max tokens")
