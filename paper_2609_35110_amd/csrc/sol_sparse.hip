@@ -16,9 +16,9 @@
 // the block-sparse attention kernel to walk.
 //
 // Three launches, all small next to the attention: pool_q_kernel (reads q
-// once), pool_k_kernel (reads the prepared K once), route_kernel (one
-// workgroup per query block: the scores go to LDS, mean and spread are fixed-
-// order tree reductions, and the kept blocks are compacted with wave ballots).
+// once), pool_k_kernel (reads the prepared K once), route_kernel (four query
+// blocks per workgroup: the scores go to LDS, mean and spread are fixed-order
+// tree reductions, and the kept blocks are compacted with wave ballots).
 #include "sol_device.h"
 
 namespace sol {
@@ -146,88 +146,118 @@ __device__ __forceinline__ float block_sum(float x, float* red) {
   return r;
 }
 
-// Routing of one query block per workgroup.  Grid (nqb, slabs).
+// Routing of kRouteQB consecutive query blocks per workgroup (each pooled key
+// block read from L2 serves all of them).  Grid (ceil(nqb / kRouteQB),
+// slabs).  Scores go to LDS; per query block the mean and the spread are
+// fixed-order tree reductions, the best block a (score, lowest index)
+// reduction, and the kept blocks are compacted in ascending order with wave
+// ballots -- the same arithmetic, in the same order, for every block of a
+// workgroup.
+constexpr int kRouteQB = 4;
+
 __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ qbar,
                                                     const float* __restrict__ kbar,
                                                     uint16_t* __restrict__ blocks,
                                                     int* __restrict__ counts, int64_t bh_count,
                                                     int nqb, int nkb, int n_prefix, float tau,
                                                     float scale) {
-  __shared__ float qs[D];
-  __shared__ float sc[kMaxKeyBlocks];
+  __shared__ float qs[kRouteQB][D];
+  __shared__ float sc[kRouteQB][kMaxKeyBlocks];
   __shared__ float red[256];
   __shared__ int redi[256];
   __shared__ int wcount[4];
-  const int I = blockIdx.x;
+  const int I0 = blockIdx.x * kRouteQB;
+  const int nq = min(kRouteQB, nqb - I0);
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const bool dense = I * kQB < n_prefix;  // the block holds a prefix row
   for (int64_t bh = blockIdx.y; bh < bh_count; bh += gridDim.y) {
-    const size_t qi = (size_t)bh * nqb + I;
-    if (t < D) qs[t] = qbar[qi * D + t];
+    for (int e = t; e < kRouteQB * D; e += 256) {
+      const int u = e / D, d = e % D;
+      qs[u][d] = u < nq ? qbar[((size_t)bh * nqb + I0 + u) * D + d] : 0.0f;
+    }
     __syncthreads();
-    // scores, this thread's share of their sum, its first best block
-    float psum = 0.0f, best_v = -__builtin_inff();
-    int best_j = nkb;
+    // scores of every query block, this thread's share of their sums, its
+    // first best block
+    float psum[kRouteQB], best_v[kRouteQB];
+    int best_j[kRouteQB];
+#pragma unroll
+    for (int u = 0; u < kRouteQB; ++u) {
+      psum[u] = 0.0f;
+      best_v[u] = -__builtin_inff();
+      best_j[u] = nkb;
+    }
     for (int J = t; J < nkb; J += 256) {
       const float4* kr = reinterpret_cast<const float4*>(kbar + ((size_t)bh * nkb + J) * D);
-      float dot = 0.0f;
+      float dot[kRouteQB];
+#pragma unroll
+      for (int u = 0; u < kRouteQB; ++u) dot[u] = 0.0f;
       for (int d4 = 0; d4 < D / 4; ++d4) {
         const float4 kv = kr[d4];
-        dot = __builtin_fmaf(qs[4 * d4], kv.x, dot);
-        dot = __builtin_fmaf(qs[4 * d4 + 1], kv.y, dot);
-        dot = __builtin_fmaf(qs[4 * d4 + 2], kv.z, dot);
-        dot = __builtin_fmaf(qs[4 * d4 + 3], kv.w, dot);
-      }
-      const float s = dot * scale;
-      sc[J] = s;
-      psum += s;
-      if (s > best_v) {
-        best_v = s;
-        best_j = J;
-      }
-    }
-    const float mu = block_sum(psum, red) / (float)nkb;
-    float pvar = 0.0f;
-    for (int J = t; J < nkb; J += 256) {
-      const float d = sc[J] - mu;
-      pvar = __builtin_fmaf(d, d, pvar);
-    }
-    const float var = block_sum(pvar, red) / (float)nkb;
-    const float thr = mu + tau * __builtin_sqrtf(var);
-    // first best block: largest score, lowest index among equals
-    red[t] = best_v;
-    redi[t] = best_j;
-    __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-      if (t < s) {
-        const float ov = red[t + s];
-        const int oi = redi[t + s];
-        if (ov > red[t] || (ov == red[t] && oi < redi[t])) {
-          red[t] = ov;
-          redi[t] = oi;
+#pragma unroll
+        for (int u = 0; u < kRouteQB; ++u) {
+          dot[u] = __builtin_fmaf(qs[u][4 * d4], kv.x, dot[u]);
+          dot[u] = __builtin_fmaf(qs[u][4 * d4 + 1], kv.y, dot[u]);
+          dot[u] = __builtin_fmaf(qs[u][4 * d4 + 2], kv.z, dot[u]);
+          dot[u] = __builtin_fmaf(qs[u][4 * d4 + 3], kv.w, dot[u]);
         }
       }
-      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kRouteQB; ++u) {
+        const float sv = dot[u] * scale;
+        sc[u][J] = sv;
+        psum[u] += sv;
+        if (sv > best_v[u]) {
+          best_v[u] = sv;
+          best_j[u] = J;
+        }
+      }
     }
-    const int best = redi[0];
-    __syncthreads();
-    // kept blocks, compacted in ascending order
-    int base = 0;
-    uint16_t* out = blocks + qi * nkb;
-    for (int c0 = 0; c0 < nkb; c0 += 256) {
-      const int J = c0 + t;
-      const bool keep = J < nkb && (dense || J * kKB < n_prefix || J == best || sc[J] > thr);
-      const uint64_t m = __ballot(keep);
-      const int before = __popcll(m & ((1ull << lane) - 1ull));
-      if (lane == 0) wcount[wave] = __popcll(m);
+    for (int u = 0; u < nq; ++u) {  // uniform
+      const int I = I0 + u;
+      const size_t qi = (size_t)bh * nqb + I;
+      const bool dense = I * kQB < n_prefix;  // the block holds a prefix row
+      const float mu = block_sum(psum[u], red) / (float)nkb;
+      float pvar = 0.0f;
+      for (int J = t; J < nkb; J += 256) {
+        const float d = sc[u][J] - mu;
+        pvar = __builtin_fmaf(d, d, pvar);
+      }
+      const float var = block_sum(pvar, red) / (float)nkb;
+      const float thr = mu + tau * __builtin_sqrtf(var);
+      // first best block: largest score, lowest index among equals
+      red[t] = best_v[u];
+      redi[t] = best_j[u];
       __syncthreads();
-      int off = base;
-      for (int w = 0; w < wave; ++w) off += wcount[w];
-      if (keep) out[off + before] = (uint16_t)J;
-      base += wcount[0] + wcount[1] + wcount[2] + wcount[3];
+      for (int s = 128; s > 0; s >>= 1) {
+        if (t < s) {
+          const float ov = red[t + s];
+          const int oi = redi[t + s];
+          if (ov > red[t] || (ov == red[t] && oi < redi[t])) {
+            red[t] = ov;
+            redi[t] = oi;
+          }
+        }
+        __syncthreads();
+      }
+      const int best = redi[0];
       __syncthreads();
+      // kept blocks, compacted in ascending order
+      int base = 0;
+      uint16_t* out = blocks + qi * nkb;
+      for (int c0 = 0; c0 < nkb; c0 += 256) {
+        const int J = c0 + t;
+        const bool keep = J < nkb && (dense || J * kKB < n_prefix || J == best || sc[u][J] > thr);
+        const uint64_t m = __ballot(keep);
+        const int before = __popcll(m & ((1ull << lane) - 1ull));
+        if (lane == 0) wcount[wave] = __popcll(m);
+        __syncthreads();
+        int off = base;
+        for (int w = 0; w < wave; ++w) off += wcount[w];
+        if (keep) out[off + before] = (uint16_t)J;
+        base += wcount[0] + wcount[1] + wcount[2] + wcount[3];
+        __syncthreads();
+      }
+      if (t == 0) counts[qi] = base;
     }
-    if (t == 0) counts[qi] = base;
   }
 }
 
@@ -266,7 +296,8 @@ hipError_t launch_sparse_route(const uint16_t* q, const uint16_t* k_prep, int BH
                      reinterpret_cast<const uint4*>(k_prep), kbar, (int64_t)BH, N, nkb);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(route_kernel, dim3(nqb, gy), dim3(256), 0, stream, qbar, kbar, blocks, counts,
+  hipLaunchKernelGGL(route_kernel, dim3((nqb + kRouteQB - 1) / kRouteQB, gy), dim3(256), 0, stream, qbar,
+                     kbar, blocks, counts,
                      (int64_t)BH, nqb, nkb, g.nt, tau, (float)(1.0 / 11.313708498984761));
   return hipGetLastError();
 }
