@@ -63,3 +63,24 @@ def passes(stats):
 
 def assert_parity(stats, label=""):
     assert passes(stats), "parity failed %s: %s" % (label, stats)
+
+
+def sparse_mask(ws, B, H, N):
+    """The kept-block mask [B, H, nqb, nkb] (uint8) of the block-sparse routing
+    a sol_sparse_route call left in the device workspace ws; checks that each
+    query block's list is non-empty, strictly ascending and in range."""
+    from paper_2609_35110_amd import sol
+
+    counts, blocks = sol.sparse_routing(ws, B, H, N)
+    counts, blocks = counts.cpu().numpy(), blocks.cpu().numpy().astype(np.int64)
+    nqb, nkb = blocks.shape[2], blocks.shape[3]
+    mask = np.zeros((B, H, nqb, nkb), dtype=np.uint8)
+    for b in range(B):
+        for h in range(H):
+            for I in range(nqb):
+                c = counts[b, h, I]
+                assert 1 <= c <= nkb
+                lst = blocks[b, h, I, :c]
+                assert (np.diff(lst) > 0).all() and lst[0] >= 0 and lst[-1] < nkb
+                mask[b, h, I, lst] = 1
+    return mask

@@ -25,7 +25,7 @@ import oracle
 from paper_2609_35110_amd import sol
 from paper_2609_35110_amd import workloads as W
 
-from parity import assert_parity, compare
+from parity import assert_parity, compare, sparse_mask as gpu_mask
 
 pytestmark = pytest.mark.gpu
 
@@ -65,24 +65,6 @@ def _run_sparse(w, q, k, v, tau, gq=None, gk=None, fp8=False):
     out = sol.attn_fwd_sparse(qd, kp, vp, w.T, w.Hl, w.Wl, tab, ws, gamma=gqd, eps=EPS, fp8=fp8)
     torch.cuda.synchronize()
     return out, gpu_mask(ws, w.B, w.H, w.N)
-
-
-def gpu_mask(ws, B, H, N):
-    """The kept-block mask [B, H, nqb, nkb] of the routing in the workspace;
-    checks each list is strictly ascending and in range."""
-    counts, blocks = sol.sparse_routing(ws, B, H, N)
-    counts, blocks = counts.cpu().numpy(), blocks.cpu().numpy().astype(np.int64)
-    nqb, nkb = blocks.shape[2], blocks.shape[3]
-    mask = np.zeros((B, H, nqb, nkb), dtype=np.uint8)
-    for b in range(B):
-        for h in range(H):
-            for I in range(nqb):
-                c = counts[b, h, I]
-                assert 1 <= c <= nkb
-                lst = blocks[b, h, I, :c]
-                assert (np.diff(lst) > 0).all() and lst[0] >= 0 and lst[-1] < nkb
-                mask[b, h, I, lst] = 1
-    return mask
 
 
 def check_routing(got, q, k, w, tau, gq=None, gk=None, slabs=None):
