@@ -541,18 +541,17 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
 // issues no memory instruction of its own in the loop (the first pass: a
 // build test checks it); the second pass, whose spill code does, waits for
 // every copy (kAll).
-// kDeep (the block-sparse walk, whose scattered tiles miss L2 more often):
-// copies are issued one iteration earlier and the barrier leaves the last
-// eight -- this iteration's and the previous one's -- in flight.
-template <bool kAll, bool kDeep>
+// kInflight: iterations whose copies may still be in flight (the dense walk
+// 1; the block-sparse walk, whose scattered tiles miss L2 more often, 2: its
+// copies are issued one iteration earlier).
+template <bool kAll, int kInflight>
 __device__ __forceinline__ void dma_barrier() {
+  static_assert(kInflight >= 1 && kInflight <= 3, "vmcnt holds at most 15 here");
   asm volatile("" ::: "memory");
   if (kAll)
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt 0, expcnt 7, lgkmcnt 15
-  else if (kDeep)
-    __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt 8, expcnt 7, lgkmcnt 15 (no LDS wait)
   else
-    __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt 4, expcnt 7, lgkmcnt 15 (no LDS wait)
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (4 * kInflight));  // vmcnt 4 kInflight, no LDS wait
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -617,8 +616,14 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   // The sparse walk copies K 5 and V 4 walk positions ahead (the dense walk
   // 4 and 3), with a V ring of 8: 64 + 64 + 32 KB, the whole 160 KB of LDS.
+  // K(t) is read in iteration t - 2 and V(t) in t - 1, so the copies of the
+  // last kInflight iterations may be in flight at an iteration's end.  (A
+  // third iteration in flight measured no better than two.)
   constexpr int kVB = kSparse ? 8 : kVBufs;
-  constexpr int kKAhead = kSparse ? 5 : 4, kVAhead = kSparse ? 4 : 3;
+  constexpr int kKAhead = kSparse ? 5 : 4, kVAhead = kKAhead - 1;
+  constexpr int kInflight = kKAhead - 3;
+  static_assert(kKAhead <= 7 && kVAhead <= 7 && (kSparse || kVAhead <= 3),
+                "a copy must land a barrier after the last read of the slot it overwrites");
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVB * kPrepTileElems];
   __shared__ uint32_t blist[kSparse ? kMaxSparseBlocks : 1];  // entry e | entry e + 1 << 16
 
@@ -1015,46 +1020,34 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     keep(p0_next[7]);
     keep(l0_next);
     // The copies the next iteration reads must have landed: those issued
-    // kKAhead - 2 iterations ago (K) and kVAhead - 1 ago (V) -- so only this
-    // iteration's four copies (dense walk) or this and the previous
-    // iteration's eight (sparse walk) may still be in flight.
-    dma_barrier<kRobust, kSparse>();
+    // kKAhead - 2 iterations ago (K) and kVAhead - 1 ago (V) -- so only the
+    // copies of this and the kInflight - 1 previous iterations (4 each) may
+    // still be in flight.
+    dma_barrier<kRobust, kInflight>();
   };
 
   // ---- prologue: K(0 .. kKAhead - 2) and V(0 .. kVAhead - 2) in LDS,
   // K(kKAhead - 1) and V(kVAhead - 1) on their way; S(0) against m = its own
   // max; the qb0 words of P(0); the fragment registers loaded with K(1) and
   // V(0).
-  const int w0 = walk_tile(0), w1 = walk_tile(1), w2 = walk_tile(2), w3 = walk_tile(3);
-  const int w4 = kSparse ? walk_tile(4) : 0;
-  dma_k(0, w0, 0);
-  dma_k(0, w0, 1);
-  dma_v(0, w0, 0);
-  dma_v(0, w0, 1);
-  dma_k(1, w1, 0);
-  dma_k(1, w1, 1);
-  dma_k(2, w2, 0);
-  dma_k(2, w2, 1);
-  dma_v(1, w1, 0);
-  dma_v(1, w1, 1);
-  if (kSparse) {
-    dma_k(3, w3, 0);
-    dma_k(3, w3, 1);
-    dma_v(2, w2, 0);
-    dma_v(2, w2, 1);
+#pragma unroll
+  for (int t = 0; t < kKAhead - 1; ++t) {
+    const int wt = walk_tile(t);
+    dma_k(t, wt, 0);
+    dma_k(t, wt, 1);
+    if (t < kVAhead - 1) {
+      dma_v(t, wt, 0);
+      dma_v(t, wt, 1);
+    }
   }
   __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
-  if (kSparse) {
-    dma_k(4, w4, 0);
-    dma_k(4, w4, 1);
-    dma_v(3, w3, 0);
-    dma_v(3, w3, 1);
-  } else {
-    dma_k(3, w3, 0);
-    dma_k(3, w3, 1);
-    dma_v(2, w2, 0);
-    dma_v(2, w2, 1);
+  {
+    const int wk = walk_tile(kKAhead - 1), wv = walk_tile(kVAhead - 1);
+    dma_k(kKAhead - 1, wk, 0);
+    dma_k(kKAhead - 1, wk, 1);
+    dma_v(kVAhead - 1, wv, 0);
+    dma_v(kVAhead - 1, wv, 1);
   }
   // S(0) with the builtin MFMA: outside the hot loop the compiler may stage
   // Q' through temporary AGPRs, and only MFMAs it can see are safe next to
