@@ -117,7 +117,7 @@ def calibrate_copy(mib):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="p720",
                     help="tiny | low | p480 | p720 | share | p720n (QK normalization) | "
