@@ -598,12 +598,13 @@ constexpr int kBufferDword3 = 0x00020000;
 // to the key blocks (kSparseKeyBlock keys = 4 tiles each) listed for it in
 // blocks[(bh * n_qtiles + qt) * nkb ..] (ascending, counts[bh * n_qtiles + qt]
 // of them).  The list is staged into LDS once, each word holding an entry and
-// the next one; the loop walks the listed tiles in order -- LDS ring slots
-// follow the walk, copies read the listed tile.  One LDS read per iteration,
+// the next one of the walk (which starts at the diagonal block and wraps);
+// the loop walks the listed tiles in that order -- LDS ring slots follow the
+// walk, copies read the listed tile.  One LDS read per iteration,
 // issued at its start and made scalar a phase later, gives the tiles of both
 // copies (walk positions i + 3 and i + 4 lie in one block or two neighbours);
 // masks need no lookup, since only the last listed block can hold keys past
-// N.
+// N and its walk position is known.
 static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's rows");
 
 template <bool kRope, bool kRobust, bool kSparse>
@@ -660,16 +661,33 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int qrow_first = qt * BM + wave * 64 + l32;
   // Tiles the workgroup walks: every tile of the slab, or the listed blocks'.
   int n_kv = (N + BN2 - 1) / BN2;
-  int last_blk = 0;  // sparse: the last listed key block
+  int last_blk = 0, last_pos = 0;  // sparse: the last key block and its walk position
   if (kSparse) {
     // counts and entries are clamped to the slab, whatever the list holds, so
     // every copy stays inside the slab's prepared tiles
     const size_t qb = (size_t)bh * n_qtiles + qt;
     const int cnt = min(max(counts[qb], 1), min(nkb, kMaxSparseBlocks));
-    auto entry = [&](int e) { return (uint32_t)min((int)blocks[qb * nkb + min(e, cnt - 1)], nkb - 1); };
+    auto listed = [&](int e) { return min((int)blocks[qb * nkb + e], nkb - 1); };
+    // Walk the ascending list from the first block at or past the rows' own
+    // keys (the diagonal), wrapping around: query blocks running side by side
+    // then fetch neighbouring key blocks at about the same time, so L2 serves
+    // more of them.  A full list keeps the plain order (the dense walk).
+    __shared__ int start_pos;
+    if (tid == 0) start_pos = 0;
+    __syncthreads();
+    const int diag = min((qt * BM + (N - Nq)) / kSparseKeyBlock, nkb - 1);
+    if (cnt < nkb)
+      for (int e = tid; e < cnt; e += 256)
+        if (listed(e) >= diag && (e == 0 || listed(e - 1) < diag)) start_pos = e;
+    __syncthreads();
+    const int pos0 = start_pos;
+    auto entry = [&](int e) { return (uint32_t)listed((pos0 + min(e, cnt - 1)) % cnt); };
     for (int e = tid; e < cnt; e += 256) blist[e] = entry(e) | entry(e + 1) << 16;
     n_kv = 4 * cnt;
-    last_blk = __builtin_amdgcn_readfirstlane((int)entry(cnt - 1));
+    // the list's last (largest) block -- the only one that can hold keys past
+    // N -- and where the walk meets it
+    last_blk = __builtin_amdgcn_readfirstlane(listed(cnt - 1));
+    last_pos = __builtin_amdgcn_readfirstlane((cnt - 1 - pos0 + cnt) % cnt);
     __syncthreads();
   }
   // Slab tile of walk position t (clamped to the walk; a listed block's
@@ -685,7 +703,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   // two blocks).
   auto mask_kv0 = [&](int t) __attribute__((always_inline)) {
     if (!kSparse) return t * BN2;
-    return t >= n_kv - 4 ? (4 * last_blk + (t & 3)) * BN2 : 0;
+    return (t >> 2) == last_pos ? (4 * last_blk + (t & 3)) * BN2 : 0;
   };
   if (kRobust) {
     // Second pass: only the row blocks the first pass marked (NaN rows) are
