@@ -142,8 +142,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the attention layer shards by heads; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(the attention layer would shard by heads, one GPU per head group). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -587,7 +587,6 @@ __device__ __forceinline__ void dma_barrier() {
 // LDS holds rings of eight K tiles and four V tiles (96 KB); the barrier that
 // ends an iteration waits only for the copies issued one iteration earlier.
 constexpr int BN2 = kPrepTile;         // keys per tile of the prepared-path kernel
-constexpr int kAbortCheck = 16;        // tiles after which the first pass may give up
 constexpr int kKBufs = 8;              // K tiles in LDS (a power of two: ring
 constexpr int kVBufs = 4;              // V tiles in LDS  offsets are masks)
 // Descriptor word 3 of a raw buffer resource (32-bit data, no format swizzle).
@@ -1145,33 +1144,18 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   }
   mfma_wait();
 
-  // First pass: after kAbortCheck tiles, a workgroup with any row block
-  // already outside the fp16 range (marked anyway) stops and hands all its
-  // rows to the second pass, instead of finishing a sweep whose result is
-  // thrown away -- as with keys far larger than the rest scattered through
-  // the sequence, which overflow nearly every row block early.
-  // (Two loops with the check between them: inside the loop it costs
-  // registers and the first pass would spill.)
   int i = 0;
-  for (; i + 1 < n_kv && (kRobust || i < kAbortCheck); i += 2) {
+  for (; i + 1 < n_kv; i += 2) {
     iteration(i, sa, sb, pA, pB, lA, lB);
     iteration(i + 1, sb, sa, pB, pA, lB, lA);
   }
-  // uniform over the workgroup
-  const bool aborted = !kRobust && i == kAbortCheck && __syncthreads_or(ovf > kP16SumLimit);
-  if (!aborted) {
-    for (; i + 1 < n_kv; i += 2) {
-      iteration(i, sa, sb, pA, pB, lA, lB);
-      iteration(i + 1, sb, sa, pB, pA, lB, lA);
-    }
-    if (i < n_kv) iteration(i, sa, sb, pA, pB, lA, lB);
-  }
+  if (i < n_kv) iteration(i, sa, sb, pA, pB, lA, lB);
 
   // ---- epilogue: out = O / l; register j of block (qb, db) is dim 32db + 8(j/4) + 4hh + j%4.
   // A first-pass wave whose probabilities left the fp16 range writes its rows
   // as NaN instead (bf16 0x7FC0, E4M3 0x7F): the second pass recomputes
   // exactly those.
-  const bool marked = !kRobust && (aborted || __any(ovf > kP16SumLimit));
+  const bool marked = !kRobust && __any(ovf > kP16SumLimit);
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int row = qrow0 + 32 * qb;
