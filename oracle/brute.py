@@ -196,3 +196,57 @@ def sparse_attention_np(qh, kh, v, mask, qblk, kblk):
     keys = np.repeat(np.repeat(mask, qblk, axis=-2), kblk, axis=-1)[..., :N, :kh.shape[-2]]
     s = np.where(keys, s, -np.inf)
     return np.matmul(softmax(s, axis=-1), v)
+
+
+def ue5m3_values():
+    """The value of every UE5M3 scale code 0..255 (unsigned, 5 exponent bits of
+    bias 15, 3 mantissa bits; exponent 31 infinity or NaN), float64 [256], from
+    the format's definition."""
+    vals = np.empty(256, dtype=np.float64)
+    for c in range(256):
+        e, m = c >> 3, c & 7
+        if e == 31:
+            vals[c] = np.inf if m == 0 else np.nan
+        elif e == 0:
+            vals[c] = m * 2.0 ** -17
+        else:
+            vals[c] = (1.0 + m / 8.0) * 2.0 ** (e - 15)
+    return vals
+
+
+def encode_records_np(qh_bits, kh_bits, v_bits):
+    """Block-INT8 QKV records (uint8 [B, N, H, 400]) of bf16 bits [B, H, N, 128],
+    vectorised: per 32-value group the smallest finite positive UE5M3 scale s
+    with 127 s >= max |x|, codes round(x / s) (numpy rounds half to even)
+    clipped to +-127; scales after the 384 code bytes, then 4 zero bytes."""
+    vals = ue5m3_values()
+    fin = vals[1:0xF8]                                       # codes 1..0xF7, increasing
+    parts = [bf16_bits_to_f64(x) for x in (qh_bits, kh_bits, v_bits)]
+    B, H, N, D = parts[0].shape
+    codes, scales = [], []
+    for x in parts:
+        g = x.reshape(B, H, N, D // 32, 32)
+        amax = np.abs(g).max(-1)
+        sc = 1 + np.searchsorted(127.0 * fin, amax, side="left")  # first with 127 s >= amax
+        sc = np.minimum(sc, 0xF7)
+        s = vals[sc][..., None]
+        c = np.clip(np.rint(g / s), -127, 127).astype(np.int8).reshape(B, H, N, D)
+        codes.append(c.view(np.uint8))
+        scales.append(sc.astype(np.uint8))
+    rec = np.zeros((B, N, H, 400), dtype=np.uint8)
+    for p in range(3):
+        rec[..., 128 * p:128 * (p + 1)] = np.transpose(codes[p], (0, 2, 1, 3))
+        rec[..., 384 + 4 * p:388 + 4 * p] = np.transpose(scales[p], (0, 2, 1, 3))
+    return rec
+
+
+def decode_records_np(rec):
+    """uint8 records [B, N, H, 400] -> float64 (q, k, v) [B, H, N, 128]: code
+    times its group's scale, before any rounding."""
+    vals = ue5m3_values()
+    out = []
+    for p in range(3):
+        c = rec[..., 128 * p:128 * (p + 1)].view(np.int8).astype(np.float64)
+        s = np.repeat(vals[rec[..., 384 + 4 * p:388 + 4 * p]], 32, axis=-1)
+        out.append(np.transpose(c * s, (0, 2, 1, 3)))
+    return tuple(out)

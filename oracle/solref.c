@@ -564,3 +564,104 @@ int solref_attn_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                              use_rope, use_rope, contract, NULL, NULL, 0.0, rows, nrows, out,
                              nthreads);
 }
+
+/* ------------------------------------------------- block-INT8 QKV records */
+
+/*
+ * The wire record of the quantized QKV exchange (Sec. 3.2, "Quantized
+ * communication"): one record per (token, head), 400 bytes -- 384 bytes of
+ * int8 codes, twelve scale codes (one per group of 32 values) and four zero
+ * bytes.  Readings where the paper gives only the sizes:
+ *   bytes   0..127  q codes, 128..255 k codes, 256..383 v codes (two's
+ *                   complement; dim d of a part at byte d of that part);
+ *   bytes 384..395  scale code of part p (0 q, 1 k, 2 v), dims [32g, 32g+32)
+ *                   at byte 384 + 4p + g;
+ *   bytes 396..399  zero.
+ * Records are token-major, (b, n, h) at byte ((b*N + n)*H + h)*400: the flat
+ * (tokens, heads, record) layout the exchange delivers.
+ *
+ * UE5M3 scale codes (reading): unsigned, 5 exponent bits of bias 15, 3
+ * mantissa bits; exponent 0 is subnormal (m * 2^-17), exponent 31 is not
+ * finite (m = 0 infinity, else NaN).  The finite positive codes 0x01..0xF7
+ * span 2^-17 .. 61440.
+ *
+ * Encoding (reading): a group's scale is the smallest finite positive code
+ * value s with 127 s >= max |x| (no value needs a code beyond +-127; a zero
+ * group takes 0x01, a group too large for any code 0xF7); each value's code
+ * is x / s rounded to the nearest integer, ties to even, clamped to
+ * [-127, 127].  The inputs are the bf16 q, k and v as attention consumes them
+ * (q and k normalised and rotated), finite.
+ * Decoding: code * s rounded once to bf16 (RNE), the rounding point at which
+ * a bf16 consumer receives them.
+ */
+#define REC_BYTES 400
+#define REC_SCALES 384
+
+static double ue5m3_value(uint8_t c) {
+  int e = c >> 3, m = c & 7;
+  if (e == 31) return m == 0 ? INFINITY : NAN;
+  if (e == 0) return ldexp((double)m, -17);
+  return ldexp(8.0 + m, e - 18); /* (1 + m/8) 2^(e-15) */
+}
+
+static uint8_t ue5m3_scale_for(double amax) {
+  for (int c = 1; c < 0xF7; ++c)
+    if (127.0 * ue5m3_value((uint8_t)c) >= amax) return (uint8_t)c;
+  return 0xF7;
+}
+
+static int8_t int8_code(double x, double s) {
+  double y = x / s;
+  double fl = floor(y);
+  double rem = y - fl;
+  if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;
+  if (fl > 127.0) fl = 127.0;
+  if (fl < -127.0) fl = -127.0;
+  return (int8_t)fl;
+}
+
+/* q, k, v: bf16 bits [B][H][N][D], D = 128; rec: [B][N][H][400]. */
+int solref_encode_qkv(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int H,
+                      int N, int D, uint8_t* rec) {
+  if (D != 128 || B < 1 || H < 1 || N < 1 || !q || !k || !v || !rec) return -1;
+  const uint16_t* part[3] = {q, k, v};
+  for (int b = 0; b < B; ++b)
+    for (int n = 0; n < N; ++n)
+      for (int h = 0; h < H; ++h) {
+        uint8_t* r = rec + (((int64_t)b * N + n) * H + h) * REC_BYTES;
+        for (int p = 0; p < 3; ++p) {
+          const uint16_t* x = part[p] + (((int64_t)b * H + h) * N + n) * D;
+          for (int g = 0; g < 4; ++g) {
+            double amax = 0.0;
+            for (int d = 32 * g; d < 32 * g + 32; ++d) amax = fmax(amax, fabs(bf16_to_double(x[d])));
+            const uint8_t sc = ue5m3_scale_for(amax);
+            const double s = ue5m3_value(sc);
+            r[REC_SCALES + 4 * p + g] = sc;
+            for (int d = 32 * g; d < 32 * g + 32; ++d)
+              r[128 * p + d] = (uint8_t)int8_code(bf16_to_double(x[d]), s);
+          }
+        }
+        for (int i = REC_SCALES + 12; i < REC_BYTES; ++i) r[i] = 0;
+      }
+  return 0;
+}
+
+/* rec: [B][N][H][400] -> q, k, v bf16 bits [B][H][N][D], D = 128. */
+int solref_decode_qkv(const uint8_t* rec, int B, int H, int N, int D, uint16_t* q, uint16_t* k,
+                      uint16_t* v) {
+  if (D != 128 || B < 1 || H < 1 || N < 1 || !rec || !q || !k || !v) return -1;
+  uint16_t* part[3] = {q, k, v};
+  for (int b = 0; b < B; ++b)
+    for (int n = 0; n < N; ++n)
+      for (int h = 0; h < H; ++h) {
+        const uint8_t* r = rec + (((int64_t)b * N + n) * H + h) * REC_BYTES;
+        for (int p = 0; p < 3; ++p) {
+          uint16_t* x = part[p] + (((int64_t)b * H + h) * N + n) * D;
+          for (int d = 0; d < D; ++d) {
+            const double s = ue5m3_value(r[REC_SCALES + 4 * p + d / 32]);
+            x[d] = double_to_bf16((double)(int8_t)r[128 * p + d] * s);
+          }
+        }
+      }
+  return 0;
+}

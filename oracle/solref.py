@@ -60,6 +60,10 @@ class Oracle:
         lib.solref_qknorm_rope3d.argtypes = [P, P, P, i64, i32, i32, i32, i32, i32, i32, i32,
                                              i32, f64, i32, P, f64, i32]
         lib.solref_qknorm_rope3d.restype = None
+        lib.solref_encode_qkv.argtypes = [P, P, P, i32, i32, i32, i32, P]
+        lib.solref_encode_qkv.restype = ctypes.c_int
+        lib.solref_decode_qkv.argtypes = [P, i32, i32, i32, i32, P, P, P]
+        lib.solref_decode_qkv.restype = ctypes.c_int
         lib.solref_num_threads.argtypes = []
         lib.solref_num_threads.restype = ctypes.c_int
         self.lib = lib
@@ -82,6 +86,29 @@ class Oracle:
         y = np.empty(x.shape, dtype=np.uint8)
         self.lib.solref_round_e4m3(_ptr(x), _ptr(y), x.size)
         return y
+
+    def encode_qkv(self, q, k, v) -> np.ndarray:
+        """Block-INT8 QKV records of bf16 bits q, k, v [B, H, N, 128] (q and k
+        as attention consumes them): uint8 [B, N, H, 400]."""
+        q, k, v = _u16(q), _u16(k), _u16(v)
+        if q.ndim != 4 or q.shape != k.shape or q.shape != v.shape:
+            raise ValueError("q, k, v must share one [B, H, N, D] shape")
+        B, H, N, D = q.shape
+        rec = np.empty((B, N, H, 400), dtype=np.uint8)
+        if self.lib.solref_encode_qkv(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, _ptr(rec)) != 0:
+            raise ValueError("oracle rejected the arguments")
+        return rec
+
+    def decode_qkv(self, rec):
+        """uint8 records [B, N, H, 400] -> (q, k, v) bf16 bits [B, H, N, 128]."""
+        rec = np.ascontiguousarray(rec)
+        if rec.dtype != np.uint8 or rec.ndim != 4 or rec.shape[3] != 400:
+            raise ValueError("records must be uint8 [B, N, H, 400]")
+        B, N, H = rec.shape[:3]
+        q, k, v = (np.empty((B, H, N, 128), dtype=np.uint16) for _ in range(3))
+        if self.lib.solref_decode_qkv(_ptr(rec), B, H, N, 128, _ptr(q), _ptr(k), _ptr(v)) != 0:
+            raise ValueError("oracle rejected the arguments")
+        return q, k, v
 
     def rope3d_f64(self, x, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE) -> np.ndarray:
         """Exact-arithmetic (double) 3D rotary embedding of x[..., N, D] (float64)."""
@@ -225,6 +252,14 @@ def round_bf16(x):
 
 def round_e4m3(x):
     return default().round_e4m3(x)
+
+
+def encode_qkv(q, k, v):
+    return default().encode_qkv(q, k, v)
+
+
+def decode_qkv(rec):
+    return default().decode_qkv(rec)
 
 
 def rope3d_f64(x, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE):

@@ -12,6 +12,7 @@ computed (3D rotary embedding on q and k, then exact softmax attention, with
 the text prefix unrotated); the pins below check that meaning.
 """
 import math
+import os
 
 import numpy as np
 import torch
@@ -669,6 +670,159 @@ def pin_sparse_attention_vs_numpy_twin(o):
     want = brute.sparse_attention_np(qh, kh, _f(v), m.astype(bool), 16, 8)
     assert np.allclose(got, want, atol=2e-6, rtol=1e-6)
     assert not np.allclose(got, o.attn_rows(q, k, v, T, Hl, Wl), atol=1e-3), "mask had no effect"
+
+
+# ------------------------------------------------ block-INT8 QKV records
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _record_format():
+    """The record sizes the paper prints (tests/golden/qkv_record_format.txt)."""
+    out = {}
+    for ln in open(os.path.join(GOLDEN, "qkv_record_format.txt")):
+        ln = ln.split("#")[0].strip()
+        if ln:
+            key, val = (x.strip() for x in ln.split("="))
+            out[key] = int(val)
+    return out
+
+
+def _float16_of_code(c):
+    """UE5M3 code c read as the IEEE half-precision number with the same
+    exponent field and the top three mantissa bits (numpy's float16)."""
+    return np.array([int(c) << 7], dtype=np.uint16).view(np.float16).astype(np.float64)[0]
+
+
+def _one_record(q, k, v):
+    return [_bits(x).reshape(1, 1, 1, 128) for x in (q, k, v)]
+
+
+def pin_records_sizes_are_the_papers(o):
+    """Record of 400 bytes: 3 x 128 code bytes, twelve scale codes each
+    covering 32 values (a value moved across a 32-dim boundary moves to the
+    next scale), four zero bytes (the paper's printed sizes)."""
+    fmt = _record_format()
+    rng = np.random.default_rng(70)
+    q, k, v = (_rand_bits(rng, (2, 3, 5, 128)) for _ in range(3))
+    rec = o.encode_qkv(q, k, v)
+    assert rec.shape == (2, 5, 3, fmt["record_bytes"])
+    assert 3 * 128 == fmt["value_bytes"]
+    assert fmt["value_bytes"] + fmt["scale_codes"] + fmt["padding_bytes"] == fmt["record_bytes"]
+    assert (rec[..., fmt["record_bytes"] - fmt["padding_bytes"]:] == 0).all()
+    sc = rec[..., fmt["value_bytes"]:fmt["value_bytes"] + fmt["scale_codes"]]
+    assert ((sc >= 1) & (sc <= 0xF7)).all()  # finite positive codes only
+    G = fmt["group_size"]
+    base = o.encode_qkv(*_one_record(np.ones(128), np.ones(128), np.ones(128)))[0, 0, 0]
+    for p in range(3):
+        for d in (0, G - 1, G, 2 * G + 5, 4 * G - 1):
+            xs = [np.ones(128), np.ones(128), np.ones(128)]
+            xs[p][d] = 100.0
+            r = o.encode_qkv(*_one_record(*xs))[0, 0, 0]
+            changed = {i for i in range(fmt["scale_codes"]) if r[384 + i] != base[384 + i]}
+            assert changed == {4 * p + d // G}, (p, d, changed)
+
+
+def pin_records_scale_values_are_float16(o):
+    """A scale code's value is the half-precision number with the same
+    exponent field and leading mantissa bits (numpy float16, library): every
+    finite positive code, read through the decoder with a unit code."""
+    codes = np.arange(1, 0xF8)
+    rec = np.zeros((1, codes.size, 1, 400), dtype=np.uint8)
+    rec[0, :, 0, 0] = 1                 # q dim 0: code +1
+    rec[0, :, 0, 128 + 40] = 0xFF       # k dim 40: code -1
+    rec[0, :, 0, 384] = codes           # q group 0
+    rec[0, :, 0, 384 + 5] = codes       # k group 1
+    rec[0, :, 0, 384 + 8:384 + 12] = 0x78  # v groups: scale 1.0
+    dq, dk, _ = o.decode_qkv(rec)
+    want = np.array([_float16_of_code(c) for c in codes])
+    assert np.array_equal(_f(dq[0, 0, :, 0]), want)
+    assert np.array_equal(_f(dk[0, 0, :, 40]), -want)
+    assert _float16_of_code(0xF7) == 61440.0 and _float16_of_code(1) == 2.0 ** -17
+
+
+def pin_records_hand_worked_example(o):
+    """One record worked by hand from the format's definition: scale = the
+    smallest code value s with 127 s >= max|x|, code = round-half-even(x/s)
+    clamped to +-127 -- including exact ties, a zero group, subnormal scales,
+    a group too large for any scale, and 127 s equal to max|x|."""
+    q, k, v = np.zeros(128), np.zeros(128), np.zeros(128)
+    q[0:32] = 1.0        # 127 * 2^-7 < 1 <= 127 * 1.125 * 2^-7: scale 0x41, 1 / 0.00878... -> 114
+    q[32:64] = -2.5      # 127 * 0.01953125 < 2.5 <= 127 * 0.021484375: 0x4B, -116.36 -> -116
+    q[96:102] = [15.875, 0.1875, 0.3125, -0.4375, 0.0625, -0.0625]  # 127 * 0.125 = 15.875: 0x60
+    k[0], k[1:32] = 999424.0, 1.0    # 127 * 7680 < 999424 <= 127 * 8192: 0xE0, 122 exactly
+    k[32], k[33] = 1e8, -1e8         # beyond 127 * 61440: 0xF7, clamped to +-127
+    k[64:96] = 2.0 ** -20            # smallest code 0x01 (2^-17); 0.125 -> 0
+    k[96:128] = 2.0 ** -10           # subnormal 0x02 (2^-16); 64 exactly
+    v[0:32] = np.arange(32) - 16.0   # 127 * 0.125 < 16 <= 127 * 0.140625: 0x61
+    v[32:] = 3.0                     # 127 * 0.0234375 < 3 <= 127 * 0.025390625: 0x4D, 118.15 -> 118
+    r = o.encode_qkv(*_one_record(q, k, v))[0, 0, 0]
+    assert r[384:400].tolist() == [0x41, 0x4B, 0x01, 0x60, 0xE0, 0xF7, 0x01, 0x02,
+                                   0x61, 0x4D, 0x4D, 0x4D, 0, 0, 0, 0]
+    c = r[:384].view(np.int8).astype(int)
+    assert (c[0:32] == 114).all() and (c[32:64] == -116).all() and (c[64:96] == 0).all()
+    assert c[96:102].tolist() == [127, 2, 2, -4, 0, 0]  # 1.5 -> 2, 2.5 -> 2, -3.5 -> -4, +-0.5 -> 0
+    assert c[128] == 122 and (c[129:160] == 0).all()
+    assert c[160:164].tolist() == [127, -127, 0, 0]
+    assert (c[192:224] == 0).all() and (c[224:256] == 64).all()
+    assert c[256] == -114 and c[257] == -107 and c[272] == 0 and c[273] == 7 and c[287] == 107
+    assert (c[288:384] == 118).all()
+    # decoding: code times scale, rounded once to bf16
+    dq, dk, dv = o.decode_qkv(r.reshape(1, 1, 1, 400))
+    assert _f(dq[0, 0, 0, 0]) == float(torch.tensor(114 * 0.0087890625).to(torch.bfloat16))
+    assert _f(dk[0, 0, 0, 0]) == 999424.0 and _f(dk[0, 0, 0, 96]) == 2.0 ** -10
+    assert _f(dk[0, 0, 0, 32]) == 7798784.0  # 127 * 61440 = 7802880, rounded to 8 bits
+
+
+def pin_records_round_trip_bounds(o):
+    """Random groups over 40 binades: every code within +-127, each value
+    within half a scale of code * scale (unsaturated groups), the scale the
+    smallest that fits (127 s(c-1) < max|x| <= 127 s(c)), multiples of the
+    scale reproduced exactly, and decoding = bf16(code * scale) (torch)."""
+    rng = np.random.default_rng(71)
+    B, H, N = 1, 2, 64
+    mag = np.exp2(rng.uniform(-20, 20, (B, H, N, 4, 1)))
+    xs = [_bits((rng.standard_normal((B, H, N, 4, 32)) * mag).reshape(B, H, N, 128)) for _ in range(3)]
+    rec = o.encode_qkv(*xs)
+    dec = o.decode_qkv(rec)
+    h16 = np.array([_float16_of_code(c) for c in range(0xF8)])
+    for p in range(3):
+        x = _f(xs[p]).transpose(0, 2, 1, 3).reshape(B, N, H, 4, 32)
+        sc = rec[..., 384 + 4 * p:388 + 4 * p]
+        s = h16[sc][..., None]
+        c = rec[..., 128 * p:128 * (p + 1)].view(np.int8).astype(np.float64).reshape(B, N, H, 4, 32)
+        amax = np.abs(x).max(-1)
+        assert (np.abs(c) <= 127).all()
+        assert (amax <= 127 * s[..., 0]).all()
+        assert ((sc == 1) | (127 * h16[np.maximum(sc, 1) - 1] < amax)).all()
+        assert (np.abs(c * s - x) <= s / 2).all()
+        want = torch.from_numpy((c * s).astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+        got = _f(dec[p]).transpose(0, 2, 1, 3).reshape(B, N, H, 4, 32)
+        assert np.array_equal(got, want)
+    # exact multiples of the scale survive the round trip
+    s = 2.0 ** -5  # code 0x50
+    ints = rng.integers(-127, 128, (1, 1, 8, 128)).astype(np.float64)
+    ints[..., ::32] = 127  # every group's max is 127 s, so its scale is s
+    x = _bits(ints * s)
+    assert np.array_equal(_f(x), ints * s)  # bf16-exact inputs
+    rec = o.encode_qkv(x, x, x)
+    assert (rec[..., 384:396] == 0x50).all()
+    assert np.array_equal(o.decode_qkv(rec)[1], x)
+
+
+def pin_records_vs_numpy_twin(o):
+    """Encoding and decoding equal the vectorised numpy twin, ties included."""
+    rng = np.random.default_rng(72)
+    B, H, N = 2, 3, 7
+    xs = []
+    for _ in range(3):
+        x = rng.standard_normal((B, H, N, 128)) * np.exp2(rng.uniform(-18, 18, (B, H, N, 1)))
+        x[..., 5] = rng.integers(-60, 60, (B, H, N)) + 0.5  # half-way cases where the scale allows
+        xs.append(_bits(x))
+    rec = o.encode_qkv(*xs)
+    assert np.array_equal(rec, brute.encode_records_np(*xs))
+    for got, want in zip(o.decode_qkv(rec), brute.decode_records_np(rec)):
+        assert np.array_equal(got, _bits(want.astype(np.float32)))  # code * scale is float32-exact
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -132,6 +132,26 @@ MUTANTS = [
     ("sparse: key blocks summed, not averaged", "kbar[J * D + d] /= (double)keys;", "(void)keys;"),
     ("sparse: mask ignored", "if (keep && !keep[j / J->kblk]) s[j] = -INFINITY;", "(void)keep;"),
     # queries and keys of different lengths
+    ("records: scale needs 127 s > max", "if (127.0 * ue5m3_value((uint8_t)c) >= amax) return",
+     "if (127.0 * ue5m3_value((uint8_t)c) > amax) return"),
+    ("records: scale rounded down", "if (127.0 * ue5m3_value((uint8_t)c) >= amax) return",
+     "if (127.0 * ue5m3_value((uint8_t)(c + 1)) > amax) return"),
+    ("records: codes tie away from zero",
+     "if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;\n  if (fl > 127.0)",
+     "if (rem >= 0.5) fl += 1.0;\n  if (fl > 127.0)"),
+    ("records: codes truncated", "double y = x / s;", "double y = trunc(x / s);"),
+    ("records: codes reach -128", "if (fl < -127.0) fl = -127.0;", "if (fl < -128.0) fl = -128.0;"),
+    ("records: scale slots group-major", "r[REC_SCALES + 4 * p + g] = sc;", "r[REC_SCALES + 3 * g + p] = sc;"),
+    ("records: head-major record order",
+     "        uint8_t* r = rec + (((int64_t)b * N + n) * H + h) * REC_BYTES;",
+     "        uint8_t* r = rec + (((int64_t)b * H + h) * N + n) * REC_BYTES;"),
+    ("records: decode truncated to bf16",
+     "x[d] = double_to_bf16((double)(int8_t)r[128 * p + d] * s);",
+     "{ float f = (float)((double)(int8_t)r[128 * p + d] * s); uint32_t u; memcpy(&u, &f, 4);"
+     " x[d] = (uint16_t)(u >> 16); }"),
+    ("ue5m3: exponent bias 16", "return ldexp(8.0 + m, e - 18);", "return ldexp(8.0 + m, e - 19);"),
+    ("ue5m3: subnormals read as normals", "if (e == 0) return ldexp((double)m, -17);",
+     "if (e == 0) return ldexp(8.0 + m, -18);"),
     ("key count taken from the queries", "for (int j = 0; j < Nkv; ++j) {\n    const double* kj",
      "for (int j = 0; j < Nkv && j < J->qs.N; ++j) {\n    const double* kj"),
 ]
