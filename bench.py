@@ -6,8 +6,10 @@ converted to fp16 tiles, one pass) then sol_attn_fwd_prepared_ex (q rotated in
 its tile load, softmax(q^ k^T / sqrt(D)) v, bf16 out); --path fused times
 sol_attn_fwd (q and k rotated in every tile load).  The p720n workload adds
 the QK normalization ahead of the rotation; ref720 attends to a cached
-reference segment prepared once, before the timed steps.  Inputs are resident
-in HBM before the timed region starts.
+reference segment prepared once, before the timed steps; --tau runs the
+block-sparse attention, --records the block-INT8 QKV wire records (encoded,
+then decoded in the prepare pass and the query tile load).  Inputs are
+resident in HBM before the timed region starts.
 
 Prints ONE JSON line: throughput in TFLOP/s (4 Nq Nkv D H B algorithmic flops
 per layer), ms per layer, the fraction of the dense bf16 MFMA peak measured
@@ -55,9 +57,11 @@ def measured_traffic(workload_name, kernel):
     return entry.get("bytes_per_launch")
 
 
-def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread, ref_kv=None):
+def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread, ref_kv=None, records=False):
     """Time the oracle on a bounded, seeded sample of query rows of slab (0, 0)
-    against all keys; check those rows of the GPU output against it."""
+    against all keys; check those rows of the GPU output against it.  records:
+    the oracle first rotates (and normalises) q and k of the slab, encodes the
+    slab's block-INT8 records and decodes them, then attends without rotation."""
     import numpy as np
     import torch
 
@@ -76,6 +80,14 @@ def cpu_baseline(w, q, k, v, out_gpu, rows_per_thread, ref_kv=None):
         gq, gk = W.norm_weights(w)
         kw = dict(q_gamma=gq.numpy(), k_gamma=gk.numpy(), eps=W.QK_NORM_EPS)
     t0 = time.perf_counter()
+    if records:
+        if w.qk_norm:
+            qh = oracle.qknorm_rope3d(qb, w.T, w.Hl, w.Wl, kw["q_gamma"], kw["eps"])
+            kh = oracle.qknorm_rope3d(kb, w.T, w.Hl, w.Wl, kw["k_gamma"], kw["eps"])
+        else:
+            qh, kh = oracle.rope3d_bf16(qb, w.T, w.Hl, w.Wl), oracle.rope3d_bf16(kb, w.T, w.Hl, w.Wl)
+        qb, kb, vb = oracle.decode_qkv(oracle.encode_qkv(qh, kh, vb))
+        kw = dict(rope=False)
     if ref_kv is not None:
         # keys: the cached reference segment (its own grid), then the own tokens
         krb, vrb = (W.as_bits(t[:1, :1].contiguous()) for t in ref_kv)
@@ -130,6 +142,10 @@ def main():
                     help="block-sparse attention with this threshold parameter (the paper's "
                          "refinement steps use 1.0, 1.25, 1.5); the step is then sol_prepare_kv_ex + "
                          "sol_sparse_route + sol_attn_fwd_sparse")
+    ap.add_argument("--records", action="store_true",
+                    help="block-INT8 QKV records (the quantized exchange format): the step is "
+                         "sol_qkv_encode (normalise, rotate, quantise) + sol_prepare_kv_records + "
+                         "sol_attn_fwd_records (q decoded in the tile load)")
     ap.add_argument("--cpu-rows-per-thread", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -178,7 +194,11 @@ def main():
                           key0=0, n_kv=w.n_kv)
         torch.cuda.synchronize()
     sparse = args.tau is not None
-    special = w.qk_norm or w.n_ref or sparse
+    records = args.records
+    special = w.qk_norm or w.n_ref or sparse or records
+    if records and (sparse or w.n_ref):
+        print("--records runs the dense self-attention of one sequence", file=sys.stderr)
+        sys.exit(2)
     if special and args.path == "fused":
         print("the fused path has neither QK normalization, nor a key cache, nor block sparsity",
               file=sys.stderr)
@@ -188,9 +208,16 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     sws = sol.sparse_workspace(qd) if sparse else None
+    rec = (torch.empty((w.B, w.N, w.H, sol.QKV_RECORD_BYTES), dtype=torch.uint8, device=dev)
+           if records else None)
 
     def launches(path):
         """The launches of one step, in order: [(name, fn)]."""
+        if path == "prepared" and records:
+            return [("qkv_encode", lambda: sol.qkv_encode(qd, kd, vd, w.T, w.Hl, w.Wl, tab, gq, gk,
+                                                          W.QK_NORM_EPS, rec=rec)),
+                    ("prepare_kv", lambda: sol.prepare_kv_records(rec, k_prep, v_prep)),
+                    ("attn_fwd_records", lambda: sol.attn_fwd_records(rec, k_prep, v_prep, out=out))]
         if path == "prepared" and sparse:
             return [("prepare_kv", lambda: sol.prepare_kv_ex(kd, vd, w.T, w.Hl, w.Wl, tab, k_prep, v_prep,
                                                              gamma=gk, eps=W.QK_NORM_EPS)),
@@ -235,7 +262,8 @@ def main():
         return total / steps, per
 
     ms_step, per = timed(args.path, args.steps, args.warmup)
-    main_kernel = "attn_fwd" if args.path == "fused" else ("attn_fwd_sparse" if sparse else "attn_fwd_prepared")
+    main_kernel = ("attn_fwd" if args.path == "fused" else "attn_fwd_sparse" if sparse
+                   else "attn_fwd_records" if records else "attn_fwd_prepared")
     kern = per[main_kernel]
     ms_launch = sum(kern) / len(kern)
     ks = sorted(kern)
@@ -294,7 +322,10 @@ def main():
             "rope": ("3d (32/48/48, base 1e4) fused into the q and k tile loads" if args.path == "fused"
                      else "3d (32/48/48, base 1e4): q in the tile load, k in a one-pass prologue"),
             "path": ("sol_attn_fwd" if args.path == "fused"
+                     else "sol_qkv_encode + sol_prepare_kv_records + sol_attn_fwd_records" if records
+                     else "sol_prepare_kv_ex + sol_sparse_route + sol_attn_fwd_sparse" if sparse
                      else "sol_prepare_kv_ex + sol_attn_fwd_prepared_ex"),
+            "qkv_records": records,
         },
         "ms_per_layer": ms_step,
         "kernel_ms_median": ms_median,
@@ -317,7 +348,7 @@ def main():
         result["metric"] = METRIC + " (block-sparse: dense-equivalent flops)"
     if not args.no_cpu_baseline and not sparse:
         log("cpu baseline (oracle) ...")
-        cpu, par = cpu_baseline(w, q, k, v, out, args.cpu_rows_per_thread, ref_kv)
+        cpu, par = cpu_baseline(w, q, k, v, out, args.cpu_rows_per_thread, ref_kv, records)
         result["cpu_baseline"] = cpu
         result["parity"] = par
         from parity import passes

@@ -272,6 +272,65 @@ int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int 
                     int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,
                     size_t workspace_bytes, sol_stream_t stream);
 
+/*
+ * Block-INT8 QKV records (Sec. 3.2, "Quantized communication"): the wire
+ * format of the sequence-parallel QKV exchange.  One record per token and
+ * head, 400 bytes (SOL_QKV_RECORD_BYTES):
+ *   bytes   0..127  q codes, 128..255 k codes, 256..383 v codes: int8, two's
+ *                   complement, dim d of a part at byte d of that part;
+ *   bytes 384..395  scale codes, part p (0 q, 1 k, 2 v) dims [32g, 32g + 32)
+ *                   at byte 384 + 4p + g: UE5M3 (unsigned, 5 exponent bits of
+ *                   bias 15, 3 mantissa bits; exponent 0 subnormal, m 2^-17;
+ *                   the encoder writes only the finite positive codes
+ *                   0x01..0xF7 = 2^-17 .. 61440);
+ *   bytes 396..399  zero.
+ * Element value: bf16_RNE(code * scale).  Records are token-major: record
+ * (b, n, h) at byte ((b N + n) H + h) * 400 -- the flat (tokens, heads,
+ * record) layout the exchange delivers, heads being the receiver's head
+ * share.  q and k in a record are as attention consumes them (normalised and
+ * rotated): the records path applies no rotation of its own.
+ *
+ * sol_qkv_record_bytes: B * N * H * 400 (0 for invalid sizes).
+ *
+ * sol_qkv_encode: the sender's producer.  q, k, v: [B][H][N][D] bf16; q and k
+ * are first RMS-normalised (q_gamma_dev, k_gamma_dev, eps as in
+ * sol_qknorm_rope3d; NULL: not normalised) and rotated (rope_tab_dev, grid
+ * T x Hl x Wl, as sol_qknorm_rope3d: the same bits), then each group of 32
+ * values is quantised: scale s = the smallest finite positive UE5M3 value
+ * with 127 s >= max |x| (0x01 for an all-zero group, 0xF7 when no code is
+ * large enough), code = x / s rounded to nearest, ties to even, clamped to
+ * [-127, 127].  Finite inputs.  rec must not overlap q, k or v.
+ *
+ * sol_qkv_decode: rec -> q, k, v ([B][H][N][D] bf16, element values as
+ * above).  The outputs must not overlap rec or each other.
+ *
+ * sol_prepare_kv_records: sol_prepare_kv_ex with the keys and values taken
+ * from the records (k and v parts) instead of bf16 tensors: keys key0 ..
+ * key0 + N - 1 of a prepared sequence of n_kv keys, the same tile layout and
+ * buffer sizes (sol_prepared_kv_bytes(B, H, n_kv, D)), no rotation.
+ *
+ * sol_attn_fwd_records: sol_attn_fwd_prepared_ex with the queries decoded
+ * from the records (q parts) in the kernel's tile load: N query rows per
+ * (b, h) against the n_kv prepared keys, no rotation or normalisation,
+ * out [B][H][N][D] in out_format (SOL_OUT_BF16 or SOL_OUT_FP8_E4M3).  Equal,
+ * bit for bit, to sol_attn_fwd_prepared_ex on the decoded q (table NULL).
+ *
+ * All: D = 128; pointers 16-byte aligned device memory; 1 <= N <=
+ * SOL_MAX_TOKENS; errors as the prepared path.
+ */
+#define SOL_QKV_RECORD_BYTES 400
+size_t sol_qkv_record_bytes(int B, int H, int N);
+int sol_qkv_encode(const void* q, const void* k, const void* v, void* rec, int B, int H, int N,
+                   int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                   const float* q_gamma_dev, const float* k_gamma_dev, float eps,
+                   sol_stream_t stream);
+int sol_qkv_decode(const void* rec, void* q, void* k, void* v, int B, int H, int N, int D,
+                   sol_stream_t stream);
+int sol_prepare_kv_records(const void* rec, void* k_prep, void* v_prep, int B, int H, int N,
+                           int key0, int n_kv, int D, sol_stream_t stream);
+int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep, void* out, int B,
+                         int H, int N, int n_kv, int D, int out_format, sol_stream_t stream);
+
 /* Static description of a status code. */
 const char* sol_status_string(int status);
 

@@ -349,6 +349,113 @@ int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int 
   return sol_attn_fwd_prepared(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab_dev, stream);
 }
 
+size_t sol_qkv_record_bytes(int B, int H, int N) {
+  if (B < 1 || H < 1 || N < 1 || N > SOL_MAX_TOKENS) return 0;
+  const int64_t n_rec = (int64_t)B * N * H;
+  if ((n_rec + 3) / 4 > INT32_MAX) return 0;
+  return (size_t)n_rec * SOL_QKV_RECORD_BYTES;
+}
+
+int sol_qkv_encode(const void* q, const void* k, const void* v, void* rec, int B, int H, int N,
+                   int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                   const float* q_gamma_dev, const float* k_gamma_dev, float eps,
+                   sol_stream_t stream) {
+  if (!q || !k || !v || !rec) return fail(SOL_ERR_INVALID_ARG, "q, k, v, rec must not be NULL");
+  int st = check_shape(B, H, N, D, T, Hl, Wl);
+  if (st != SOL_OK) return st;
+  const size_t rbytes = sol_qkv_record_bytes(B, H, N);
+  if (rbytes == 0) return fail(SOL_ERR_UNSUPPORTED, "too many records");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(rec))
+    return fail(SOL_ERR_INVALID_ARG, "q, k, v, rec must be 16-byte aligned");
+  if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
+  if ((st = check_norm(q_gamma_dev, eps)) != SOL_OK || (st = check_norm(k_gamma_dev, eps)) != SOL_OK)
+    return st;
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(rec, rbytes, q, bytes) || overlaps(rec, rbytes, k, bytes) || overlaps(rec, rbytes, v, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "rec overlaps q, k or v");
+  const int64_t nv = (int64_t)T * Hl * Wl;
+  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+  hipError_t e = sol::launch_qkv_encode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                        static_cast<const uint16_t*>(v), static_cast<uint8_t*>(rec), B, H,
+                                        sol::make_grid(N, T, Hl, Wl), tab, q_gamma_dev, k_gamma_dev, eps,
+                                        reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "qkv_encode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int sol_qkv_decode(const void* rec, void* q, void* k, void* v, int B, int H, int N, int D,
+                   sol_stream_t stream) {
+  if (!q || !k || !v || !rec) return fail(SOL_ERR_INVALID_ARG, "rec, q, k, v must not be NULL");
+  int st = check_shape(B, H, N, D, 0, 0, 0);
+  if (st != SOL_OK) return st;
+  const size_t rbytes = sol_qkv_record_bytes(B, H, N);
+  if (rbytes == 0) return fail(SOL_ERR_UNSUPPORTED, "too many records");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(rec))
+    return fail(SOL_ERR_INVALID_ARG, "rec, q, k, v must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * N * D * 2;
+  if (overlaps(rec, rbytes, q, bytes) || overlaps(rec, rbytes, k, bytes) || overlaps(rec, rbytes, v, bytes) ||
+      overlaps(q, bytes, k, bytes) || overlaps(q, bytes, v, bytes) || overlaps(k, bytes, v, bytes))
+    return fail(SOL_ERR_INVALID_ARG, "q, k, v overlap rec or each other");
+  hipError_t e = sol::launch_qkv_decode(static_cast<const uint8_t*>(rec), static_cast<uint16_t*>(q),
+                                        static_cast<uint16_t*>(k), static_cast<uint16_t*>(v), B, H, N,
+                                        reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "qkv_decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int sol_prepare_kv_records(const void* rec, void* k_prep, void* v_prep, int B, int H, int N,
+                           int key0, int n_kv, int D, sol_stream_t stream) {
+  if (!rec || !k_prep || !v_prep) return fail(SOL_ERR_INVALID_ARG, "rec, k_prep, v_prep must not be NULL");
+  int st = check_shape(B, H, N, D, 0, 0, 0);
+  if (st != SOL_OK) return st;
+  const size_t rbytes = sol_qkv_record_bytes(B, H, N);
+  if (rbytes == 0) return fail(SOL_ERR_UNSUPPORTED, "too many records");
+  if (n_kv < 1 || n_kv > SOL_MAX_TOKENS)
+    return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
+  if (key0 < 0 || (int64_t)key0 + N > n_kv)
+    return fail(SOL_ERR_INVALID_ARG, "keys [%d, %lld) do not fit a sequence of n_kv=%d", key0,
+                (long long)key0 + N, n_kv);
+  if (!aligned16(rec) || !aligned16(k_prep) || !aligned16(v_prep))
+    return fail(SOL_ERR_INVALID_ARG, "rec, k_prep, v_prep must be 16-byte aligned");
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
+  if (overlaps(k_prep, pbytes, rec, rbytes) || overlaps(v_prep, pbytes, rec, rbytes) ||
+      overlaps(k_prep, pbytes, v_prep, pbytes))
+    return fail(SOL_ERR_INVALID_ARG, "k_prep / v_prep overlap each other or rec");
+  hipError_t e = sol::launch_prepare_kv_records(static_cast<const uint8_t*>(rec), static_cast<uint16_t*>(k_prep),
+                                                static_cast<uint16_t*>(v_prep), B, H, N, key0, n_kv,
+                                                reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "prepare_kv_records launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep, void* out, int B,
+                         int H, int N, int n_kv, int D, int out_format, sol_stream_t stream) {
+  if (!rec || !k_prep || !v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "rec, k_prep, v_prep, out must not be NULL");
+  int st = check_shape(B, H, N, D, 0, 0, 0);
+  if (st != SOL_OK) return st;
+  const size_t rbytes = sol_qkv_record_bytes(B, H, N);
+  if (rbytes == 0) return fail(SOL_ERR_UNSUPPORTED, "too many records");
+  if (n_kv < 1 || n_kv > SOL_MAX_TOKENS)
+    return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
+  if (!aligned16(rec) || !aligned16(k_prep) || !aligned16(v_prep) || !aligned16(out))
+    return fail(SOL_ERR_INVALID_ARG, "rec, k_prep, v_prep, out must be 16-byte aligned");
+  if (out_format != SOL_OUT_BF16 && out_format != SOL_OUT_FP8_E4M3)
+    return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
+  const size_t obytes = (size_t)B * H * N * D * (out_format == SOL_OUT_BF16 ? 2 : 1);
+  const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
+  if (overlaps(out, obytes, rec, rbytes) || overlaps(out, obytes, k_prep, pbytes) || overlaps(out, obytes, v_prep, pbytes))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps rec, k_prep or v_prep");
+  if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
+  hipError_t e = sol::launch_attn_fwd_prepared(nullptr, static_cast<const uint16_t*>(k_prep),
+                                               static_cast<const uint16_t*>(v_prep), out, B * H,
+                                               sol::make_grid(N, 0, 0, 0), n_kv, nullptr, nullptr, 0.0f,
+                                               out_format == SOL_OUT_FP8_E4M3, nullptr, nullptr, 0,
+                                               reinterpret_cast<hipStream_t>(stream),
+                                               static_cast<const uint8_t*>(rec), H);
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_records launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 const char* sol_status_string(int status) {
   switch (status) {
     case SOL_OK: return "ok";
@@ -361,6 +468,6 @@ const char* sol_status_string(int status) {
 
 const char* sol_last_error(void) { return g_last_error; }
 
-int sol_version(void) { return 101; }
+int sol_version(void) { return 102; }
 
 }  // extern "C"

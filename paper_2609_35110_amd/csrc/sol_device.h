@@ -1,7 +1,8 @@
-// Device helpers shared by the HIP kernels (sol_kernels.hip, sol_sparse.hip):
-// token positions on the latent grid, bf16/fp16 conversions, the 3D rotary
-// embedding of one 16-byte chunk, the QK normalisation, and the prepared-path
-// tile size.  Every rotation and normalisation in the library goes through
+// Device helpers shared by the HIP kernels (sol_kernels.hip, sol_sparse.hip,
+// sol_records.hip): token positions on the latent grid, bf16/fp16
+// conversions, the 3D rotary embedding of one 16-byte chunk, the QK
+// normalisation, the prepared-path tile size and the block-INT8 record
+// decoding.  Every rotation and normalisation in the library goes through
 // these functions, so all kernels produce the same bits for the same row.
 #pragma once
 
@@ -195,6 +196,44 @@ constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
 constexpr int kSparseKeyBlock = 128;    // keys per routing key block (4 tiles)
 constexpr int kSparseQueryBlock = 256;  // query rows per routing query block
 constexpr int kMaxSparseBlocks = 8064;  // key blocks per slab: N <= 1,032,192
+
+// ------------------------------------------------ block-INT8 QKV records
+
+// The wire record of the quantized QKV exchange (Sec. 3.2, "Quantized
+// communication"): per (token, head) 400 bytes -- int8 codes of q (bytes
+// 0..127), k (128..255) and v (256..383), then one UE5M3 scale code per group
+// of 32 values (byte 384 + 4 part + group), then 4 zero bytes.  Records are
+// token-major: (b, n, h) at ((b N + n) H + h) 400.  An element is its code
+// times its group's scale, rounded once to bf16.
+constexpr int kRecBytes = 400;
+constexpr int kRecScales = 384;  // first scale byte; part p group g at 384 + 4p + g
+
+// UE5M3 code -> value: unsigned, 5 exponent bits of bias 15, 3 mantissa bits;
+// exponent 0 subnormal (m 2^-17), exponent 31 infinity (m = 0) or NaN.  Exact.
+__device__ __forceinline__ float ue5m3_value(uint32_t c) {
+  if (c >= 0xF8u) return __uint_as_float(c == 0xF8u ? 0x7F800000u : 0x7FC00000u);
+  if (c < 8u) return (float)c * 0x1p-17f;
+  return __uint_as_float((c << 20) + (112u << 23));  // exponent e - 15 + 127, mantissa m
+}
+
+// Eight int8 codes (one 8-byte word of a record) times their scale, to bf16
+// (the product is exact in fp32; one RNE rounding).
+__device__ __forceinline__ uint4 decode_rec_chunk(uint2 codes, float s) {
+  float f[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f[e] = (float)(int8_t)(codes.x >> (8 * e)) * s;
+    f[4 + e] = (float)(int8_t)(codes.y >> (8 * e)) * s;
+  }
+  return pack_bf16x8(f);
+}
+
+// Chunk cc (dims 8cc..8cc+7) of part p (0 q, 1 k, 2 v) of the record at r,
+// decoded to bf16.
+__device__ __forceinline__ uint4 rec_chunk(const uint8_t* __restrict__ r, int p, int cc) {
+  const uint2 codes = *reinterpret_cast<const uint2*>(r + 128 * p + 8 * cc);
+  return decode_rec_chunk(codes, ue5m3_value(r[kRecScales + 4 * p + (cc >> 2)]));
+}
 
 }  // namespace
 }  // namespace sol

@@ -48,12 +48,29 @@ hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_p
 // blocks != nullptr: block-sparse, each 256-row query block attends only to
 // the counts[...] key blocks of 128 keys listed for it in blocks (nkb entries
 // per query block, ascending).
+// qrec != nullptr: the queries come from block-INT8 QKV records instead of q
+// (token-major, `heads` records per token: already normalised and rotated, so
+// tab and q_gamma are null; dense).
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, void* out, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
                                     const float* q_gamma, float eps, bool out_fp8,
                                     const uint16_t* blocks, const int* counts, int nkb,
-                                    hipStream_t stream);
+                                    hipStream_t stream, const uint8_t* qrec = nullptr,
+                                    int heads = 1);
+// Block-INT8 QKV records (sol_records.hip and the prepare pass), records
+// [B][N][H][400]: the encoder (q and k normalised with their gammas and
+// rotated with grid g first when tab != nullptr), the standalone decoder
+// (bf16 [B][H][N][D] out), and the prepare pass reading k and v from records
+// into keys key0 .. key0 + N - 1 of a prepared sequence of n_kv keys.
+hipError_t launch_qkv_encode(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint8_t* rec,
+                             int B, int H, const SeqGrid& g, const float2* tab,
+                             const float* q_gamma, const float* k_gamma, float eps,
+                             hipStream_t stream);
+hipError_t launch_qkv_decode(const uint8_t* rec, uint16_t* q, uint16_t* k, uint16_t* v, int B, int H,
+                             int N, hipStream_t stream);
+hipError_t launch_prepare_kv_records(const uint8_t* rec, uint16_t* k_prep, uint16_t* v_prep,
+                                     int B, int H, int N, int key0, int n_kv, hipStream_t stream);
 // fp16 elements of one (b, h) slab of prepared K (or V).
 int64_t prepared_tile_elems(int N);
 

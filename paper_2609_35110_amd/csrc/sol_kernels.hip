@@ -72,14 +72,15 @@ __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x
 // written element by element, only where this call owns the key.  One
 // workgroup per tile (from tile0 on); grid.y walks the slabs.
 
-template <bool kRope>
+template <bool kRope, bool kRec>
 __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ k,
                                                       const uint4* __restrict__ v,
                                                       uint4* __restrict__ kp, uint4* __restrict__ vp,
                                                       int64_t bh_count, SeqGrid g,
                                                       const float2* __restrict__ tab, int key0,
                                                       int n_kv, int tile0,
-                                                      const float* __restrict__ gamma, float eps) {
+                                                      const float* __restrict__ gamma, float eps,
+                                                      const uint8_t* __restrict__ rec, int heads) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPrepTile * (D + 8)];
   const int n_src = g.n;
   const int n_tiles = (n_kv + kPrepTile - 1) / kPrepTile;  // tiles per prepared slab
@@ -110,14 +111,27 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
     const size_t row0 = (size_t)bh * n_src;
     uint4* kt = kp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
     uint4* vtile = vp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
+    // kRec: the keys and values come decoded from the block-INT8 records of
+    // the (b, h) slab, token-major with `heads` records per token
+    const int64_t rb = kRec ? bh / heads : 0;
+    const size_t rslab = kRec ? (size_t)rb * n_src * heads + (size_t)(bh - rb * heads) : 0;
+    auto rec_of = [&](int u) { return rec + (rslab + (size_t)src[u] * heads) * kRecBytes; };
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const uint4 x = valid[u] ? k[(row0 + src[u]) * kChunks + cc[u]] : zero;
-      // every lane takes part in the row sums (rows sit in 16 aligned lanes)
-      const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(x)), eps) : 1.0f;
-      const uint4 xr = valid[u] ? qk_chunk(x, gamma, inv, cc[u], rot[u], tab, pair0[u]) : zero;
-      if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(xr);
-      const uint4 y = valid[u] ? v[(row0 + src[u]) * kChunks + cc[u]] : zero;
+      if (kRec) {
+        // records carry k as attention consumes it (normalised and rotated)
+        const uint4 xr = valid[u] ? rec_chunk(rec_of(u), 1, cc[u]) : zero;
+        if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(xr);
+      } else {
+        const uint4 x = valid[u] ? k[(row0 + src[u]) * kChunks + cc[u]] : zero;
+        // every lane takes part in the row sums (rows sit in 16 aligned lanes)
+        const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(x)), eps) : 1.0f;
+        const uint4 xr = valid[u] ? qk_chunk(x, gamma, inv, cc[u], rot[u], tab, pair0[u]) : zero;
+        if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(xr);
+      }
+      const uint4 y = !valid[u] ? zero
+                      : kRec    ? rec_chunk(rec_of(u), 2, cc[u])
+                                : v[(row0 + src[u]) * kChunks + cc[u]];
       *reinterpret_cast<uint4*>(&vt[r[u] * (D + 8) + cc[u] * 8]) = bf16x8_to_f16x8(y);
     }
     __syncthreads();
@@ -606,14 +620,14 @@ constexpr int kBufferDword3 = 0x00020000;
 // N and its walk position is known.
 static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's rows");
 
-template <bool kRope, bool kRobust, bool kSparse>
+template <bool kRope, bool kRobust, bool kSparse, bool kRec>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
                           const float2* __restrict__ tab, int n_qtiles, float c_log2, int n_keys,
                           const float* __restrict__ q_gamma, float eps, int out_fp8,
                           const uint16_t* __restrict__ blocks, const int* __restrict__ counts,
-                          int nkb) {
+                          int nkb, const uint8_t* __restrict__ qrec, int heads) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
   // The sparse walk copies K 5 and V 4 walk positions ahead (the dense walk
   // 4 and 3), with a V ring of 8: 64 + 64 + 32 KB, the whole 160 KB of LDS.
@@ -727,12 +741,21 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int row = min(qrow0 + 32 * qb, Nq - 1);
-    const uint4* src = reinterpret_cast<const uint4*>(qs + (size_t)row * D);
     Pos p{0, 0, 0, false};
     if (kRope) p = token_pos(row, g);
     uint4 x[8];
+    if (kRec) {
+      // q decoded from the row's block-INT8 record (token-major, `heads`
+      // records per token), already normalised and rotated
+      const int b = bh / heads;
+      const uint8_t* r = qrec + (((size_t)b * Nq + row) * heads + (bh - b * heads)) * kRecBytes;
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) x[kk] = src[2 * kk + hh];
+      for (int kk = 0; kk < 8; ++kk) x[kk] = rec_chunk(r, 0, 2 * kk + hh);
+    } else {
+      const uint4* src = reinterpret_cast<const uint4*>(qs + (size_t)row * D);
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) x[kk] = src[2 * kk + hh];
+    }
     float inv = 1.0f;
     if (q_gamma != nullptr) {
       float s1[8];
@@ -1244,15 +1267,28 @@ hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_p
   const int tile1 = (key0 + g.n - 1) / kPrepTile;  // last tile holding one of these keys
   const dim3 pgrid((unsigned)(tile1 - tile0 + 1), (unsigned)(BH < 65535 ? BH : 65535));
   if (tab != nullptr)
-    hipLaunchKernelGGL(prep_kv_kernel<true>, pgrid, dim3(256), 0, stream,
+    hipLaunchKernelGGL((prep_kv_kernel<true, false>), pgrid, dim3(256), 0, stream,
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
                        reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
-                       (int64_t)BH, g, tab, key0, n_kv, tile0, gamma, eps);
+                       (int64_t)BH, g, tab, key0, n_kv, tile0, gamma, eps, nullptr, 1);
   else
-    hipLaunchKernelGGL(prep_kv_kernel<false>, pgrid, dim3(256), 0, stream,
+    hipLaunchKernelGGL((prep_kv_kernel<false, false>), pgrid, dim3(256), 0, stream,
                        reinterpret_cast<const uint4*>(k), reinterpret_cast<const uint4*>(v),
                        reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
-                       (int64_t)BH, g, tab, key0, n_kv, tile0, gamma, eps);
+                       (int64_t)BH, g, tab, key0, n_kv, tile0, gamma, eps, nullptr, 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_prepare_kv_records(const uint8_t* rec, uint16_t* k_prep, uint16_t* v_prep,
+                                     int B, int H, int N, int key0, int n_kv, hipStream_t stream) {
+  const int BH = B * H;
+  const SeqGrid g = make_grid(N, 0, 0, 0);
+  const int tile0 = key0 / kPrepTile;
+  const int tile1 = (key0 + N - 1) / kPrepTile;
+  const dim3 pgrid((unsigned)(tile1 - tile0 + 1), (unsigned)(BH < 65535 ? BH : 65535));
+  hipLaunchKernelGGL((prep_kv_kernel<false, true>), pgrid, dim3(256), 0, stream, nullptr, nullptr,
+                     reinterpret_cast<uint4*>(k_prep), reinterpret_cast<uint4*>(v_prep),
+                     (int64_t)BH, g, nullptr, key0, n_kv, tile0, nullptr, 0.0f, rec, H);
   return hipGetLastError();
 }
 
@@ -1265,7 +1301,7 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const SeqGrid& g, int n_kv, const float2* tab,
                                     const float* q_gamma, float eps, bool out_fp8,
                                     const uint16_t* blocks, const int* counts, int nkb,
-                                    hipStream_t stream) {
+                                    hipStream_t stream, const uint8_t* qrec, int heads) {
   uint16_t* out = static_cast<uint16_t*>(out_v);
   const int fp8 = out_fp8 ? 1 : 0;
   const int n_qtiles = (g.n + BM - 1) / BM;
@@ -1275,19 +1311,23 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   // First pass, then the second over the row blocks whose probabilities left
   // the fp16 range.
   for (int pass = 0; pass < 2; ++pass) {
-    const int sel = (tab != nullptr) * 4 + pass * 2 + sparse;
-#define SOL_LAUNCH_PREPARED(R, P, S)                                                            \
-  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S>), grid, dim3(256), 0, stream, q, k_prep, v_prep, \
-                     out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8, blocks, counts, nkb)
+    // queries from records: no rotation, no normalisation, dense
+    const int sel = qrec != nullptr ? 8 + pass : (tab != nullptr) * 4 + pass * 2 + sparse;
+#define SOL_LAUNCH_PREPARED(R, P, S, Q)                                                         \
+  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S, Q>), grid, dim3(256), 0, stream, q, k_prep,  \
+                     v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8, blocks,     \
+                     counts, nkb, qrec, heads)
     switch (sel) {
-      case 0: SOL_LAUNCH_PREPARED(false, false, false); break;
-      case 1: SOL_LAUNCH_PREPARED(false, false, true); break;
-      case 2: SOL_LAUNCH_PREPARED(false, true, false); break;
-      case 3: SOL_LAUNCH_PREPARED(false, true, true); break;
-      case 4: SOL_LAUNCH_PREPARED(true, false, false); break;
-      case 5: SOL_LAUNCH_PREPARED(true, false, true); break;
-      case 6: SOL_LAUNCH_PREPARED(true, true, false); break;
-      default: SOL_LAUNCH_PREPARED(true, true, true); break;
+      case 0: SOL_LAUNCH_PREPARED(false, false, false, false); break;
+      case 1: SOL_LAUNCH_PREPARED(false, false, true, false); break;
+      case 2: SOL_LAUNCH_PREPARED(false, true, false, false); break;
+      case 3: SOL_LAUNCH_PREPARED(false, true, true, false); break;
+      case 4: SOL_LAUNCH_PREPARED(true, false, false, false); break;
+      case 5: SOL_LAUNCH_PREPARED(true, false, true, false); break;
+      case 6: SOL_LAUNCH_PREPARED(true, true, false, false); break;
+      case 7: SOL_LAUNCH_PREPARED(true, true, true, false); break;
+      case 8: SOL_LAUNCH_PREPARED(false, false, false, true); break;
+      default: SOL_LAUNCH_PREPARED(false, true, false, true); break;
     }
 #undef SOL_LAUNCH_PREPARED
     const hipError_t e = hipGetLastError();

@@ -2,8 +2,8 @@
 
 The ``sol_*`` functions mirror the C ABI one to one (device pointers and
 streams as integers).  The other functions (``rope3d_table``, ``rope3d``,
-``qknorm_rope3d``, ``attn_fwd``, ``prepare_kv[_ex]``, ``attn_fwd_prepared[_ex]``
-...) take torch tensors and pass their device pointers and the current HIP
+``qknorm_rope3d``, ``attn_fwd``, ``prepare_kv[_ex]``, ``attn_fwd_prepared[_ex]``,
+``qkv_encode``, ``attn_fwd_records`` ...) take torch tensors and pass their device pointers and the current HIP
 stream.  Every
 step of the computation runs in the HIP library; there is no fallback: if
 libsol.so is missing or fails to load, every call raises.
@@ -78,6 +78,16 @@ def lib():
         L.sol_attn_fwd_sparse.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32,
                                           P, sz, i32, P]
         L.sol_attn_fwd_sparse.restype = i32
+        L.sol_qkv_record_bytes.argtypes = [i32, i32, i32]
+        L.sol_qkv_record_bytes.restype = sz
+        L.sol_qkv_encode.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, P, f32, P]
+        L.sol_qkv_encode.restype = i32
+        L.sol_qkv_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, P]
+        L.sol_qkv_decode.restype = i32
+        L.sol_prepare_kv_records.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, P]
+        L.sol_prepare_kv_records.restype = i32
+        L.sol_attn_fwd_records.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, P]
+        L.sol_attn_fwd_records.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
         L.sol_last_error.argtypes = []
@@ -157,6 +167,27 @@ def sol_attn_workspace_bytes(B, H, N, D):
 def sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, workspace, workspace_bytes, stream):
     return lib().sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, workspace,
                                  workspace_bytes, stream)
+
+
+def sol_qkv_record_bytes(B, H, N):
+    return lib().sol_qkv_record_bytes(B, H, N)
+
+
+def sol_qkv_encode(q, k, v, rec, B, H, N, D, T, Hl, Wl, rope_tab, q_gamma, k_gamma, eps, stream):
+    return lib().sol_qkv_encode(q, k, v, rec, B, H, N, D, T, Hl, Wl, rope_tab, q_gamma, k_gamma, eps,
+                                stream)
+
+
+def sol_qkv_decode(rec, q, k, v, B, H, N, D, stream):
+    return lib().sol_qkv_decode(rec, q, k, v, B, H, N, D, stream)
+
+
+def sol_prepare_kv_records(rec, k_prep, v_prep, B, H, N, key0, n_kv, D, stream):
+    return lib().sol_prepare_kv_records(rec, k_prep, v_prep, B, H, N, key0, n_kv, D, stream)
+
+
+def sol_attn_fwd_records(rec, k_prep, v_prep, out, B, H, N, n_kv, D, out_format, stream):
+    return lib().sol_attn_fwd_records(rec, k_prep, v_prep, out, B, H, N, n_kv, D, out_format, stream)
 
 
 def sol_status_string(status):
@@ -470,4 +501,86 @@ def attn_fwd_sparse(q, k_prep, v_prep, T, Hl, Wl, table, workspace, gamma=None, 
                               float(eps), ctypes.c_void_p(workspace.data_ptr()),
                               workspace.numel() * workspace.element_size(),
                               SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16, _stream(q)))
+    return out
+
+
+# ------------------------------------------------------ block-INT8 QKV records
+
+QKV_RECORD_BYTES = 400
+
+
+def _check_records(rec, B, H, N, device):
+    if (not isinstance(rec, torch.Tensor) or rec.dtype != torch.uint8 or not rec.is_cuda
+            or rec.device != device or not rec.is_contiguous()
+            or tuple(rec.shape) != (B, N, H, QKV_RECORD_BYTES)):
+        raise ValueError("records must be a contiguous uint8 [B, N, H, 400] tensor on %s" % device)
+
+
+def qkv_encode(q, k, v, T=0, Hl=0, Wl=0, table=None, q_gamma=None, k_gamma=None, eps=1e-6,
+               rec=None):
+    """Block-INT8 QKV records (uint8 [B, N, H, 400]) of q, k, v [B, H, N, D]
+    bf16: q and k normalised (gammas) and rotated (table, grid T x Hl x Wl)
+    first, then every group of 32 values quantised to int8 codes and a UE5M3
+    scale."""
+    _check_tensor("q", q)
+    _check_tensor("k", k, q.shape)
+    _check_tensor("v", v, q.shape)
+    B, H, N, D = q.shape
+    if rec is None:
+        rec = torch.empty((B, N, H, QKV_RECORD_BYTES), dtype=torch.uint8, device=q.device)
+    _check_records(rec, B, H, N, q.device)
+    check(sol_qkv_encode(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                         ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(rec.data_ptr()), B, H, N, D,
+                         T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(q_gamma, q.device),
+                         _gamma_ptr(k_gamma, q.device), float(eps), _stream(q)))
+    return rec
+
+
+def qkv_decode(rec):
+    """(q, k, v) bf16 [B, H, N, D] decoded from records [B, N, H, 400]."""
+    B, N, H = rec.shape[:3]
+    _check_records(rec, B, H, N, rec.device)
+    q, k, v = (torch.empty((B, H, N, HEAD_DIM), dtype=torch.bfloat16, device=rec.device)
+               for _ in range(3))
+    check(sol_qkv_decode(ctypes.c_void_p(rec.data_ptr()), ctypes.c_void_p(q.data_ptr()),
+                         ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()), B, H, N,
+                         HEAD_DIM, _stream(rec)))
+    return q, k, v
+
+
+def prepare_kv_records(rec, k_prep, v_prep, key0=0, n_kv=None):
+    """Write the k and v of records [B, N, H, 400] as keys key0 .. key0 + N - 1
+    of the prepared sequence of n_kv keys held by k_prep, v_prep."""
+    B, N, H = rec.shape[:3]
+    _check_records(rec, B, H, N, rec.device)
+    n_kv = N if n_kv is None else n_kv
+    nbytes = sol_prepared_kv_bytes(B, H, n_kv, HEAD_DIM)
+    _check_prepared("k_prep", k_prep, nbytes, rec.device)
+    _check_prepared("v_prep", v_prep, nbytes, rec.device)
+    check(sol_prepare_kv_records(ctypes.c_void_p(rec.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
+                                 ctypes.c_void_p(v_prep.data_ptr()), B, H, N, key0, n_kv, HEAD_DIM,
+                                 _stream(rec)))
+    return k_prep, v_prep
+
+
+def attn_fwd_records(rec, k_prep, v_prep, n_kv=None, out=None, fp8=False):
+    """The queries of records [B, N, H, 400] against n_kv prepared keys; out
+    bf16 [B, H, N, D] (or E4M3 codes, uint8, with fp8)."""
+    B, N, H = rec.shape[:3]
+    _check_records(rec, B, H, N, rec.device)
+    n_kv = N if n_kv is None else n_kv
+    nbytes = sol_prepared_kv_bytes(B, H, n_kv, HEAD_DIM)
+    _check_prepared("k_prep", k_prep, nbytes, rec.device)
+    _check_prepared("v_prep", v_prep, nbytes, rec.device)
+    shape = (B, H, N, HEAD_DIM)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.uint8 if fp8 else torch.bfloat16, device=rec.device)
+    if (out.dtype != (torch.uint8 if fp8 else torch.bfloat16) or tuple(out.shape) != shape
+            or not out.is_contiguous() or out.device != rec.device):
+        raise ValueError("out must be a contiguous %s tensor of shape %s on %s"
+                         % ("uint8" if fp8 else "bfloat16", shape, rec.device))
+    check(sol_attn_fwd_records(ctypes.c_void_p(rec.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
+                               ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                               B, H, N, n_kv, HEAD_DIM, SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16,
+                               _stream(rec)))
     return out

@@ -231,6 +231,18 @@ def make_ref_inputs(w: Workload, seed: int = None, threads: int = None):
     return tuple(out)
 
 
+def random_records(B: int, H: int, N: int, seed: int):
+    """Random block-INT8 QKV records, uint8 [B, N, H, 400] (CPU): codes uniform
+    in [-127, 127], scale codes uniform in 0x30..0x97 (2^-9 .. 7.5), the four
+    trailing bytes zero -- wire records as an encoder could write them."""
+    gen = torch.Generator().manual_seed(seed)
+    rec = torch.zeros((B, N, H, 400), dtype=torch.uint8)
+    codes = torch.randint(-127, 128, (B, N, H, 384), generator=gen, dtype=torch.int16)
+    rec[..., :384] = (codes & 0xFF).to(torch.uint8)
+    rec[..., 384:396] = torch.randint(0x30, 0x98, (B, N, H, 12), generator=gen).to(torch.uint8)
+    return rec
+
+
 def as_bits(t: torch.Tensor):
     """bf16 tensor -> numpy uint16 view of its bit patterns (CPU, no copy when possible)."""
     import numpy as np

@@ -39,7 +39,7 @@ def test_status_strings(L):
     assert sol.sol_status_string(0) == "ok"
     for s in (-1, -2, -3):
         assert sol.sol_status_string(s) not in ("ok", "unknown status")
-    assert sol.sol_version() == 101
+    assert sol.sol_version() == 102
 
 
 # Fake, 16-byte aligned device addresses: every call below is rejected on the
@@ -271,6 +271,90 @@ def test_attn_fwd_sparse_rejects_before_any_hip_call(L, kw, status, fragment):
                                  args["H"], args["N"], args["D"], args["T"], args["Hl"], args["Wl"],
                                  args["tab"], args["gamma"], args["eps"], args["ws"], args["ws_bytes"],
                                  args["fmt"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+def test_qkv_record_bytes(L):
+    assert sol.sol_qkv_record_bytes(1, 2, 192) == 192 * 2 * 400
+    assert sol.sol_qkv_record_bytes(2, 40, 111600) == 2 * 40 * 111600 * 400
+    assert sol.sol_qkv_record_bytes(0, 2, 192) == 0
+    assert sol.sol_qkv_record_bytes(1, 2, (1 << 23) + 1) == 0
+
+
+# records of B=1, H=2, N=192: 153,600 bytes
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(q=None), -1, "NULL"),
+    (dict(D=64), -2, "head dim"),
+    (dict(rec=P(0x1000008)), -1, "aligned"),
+    (dict(rec=P(0x100000 + 512)), -1, "overlaps"),   # records over q
+    (dict(qg=P(0x20000004)), -1, "gamma"),
+    (dict(kg=P(0x20000004)), -1, "gamma"),
+    (dict(eps=-1.0), -1, "eps"),
+    (dict(T=9), -1, "more tokens"),
+    (dict(tab=P(0x500008)), -1, "aligned"),
+])
+def test_qkv_encode_rejects_before_any_hip_call(L, kw, status, fragment):
+    a = dict(q=A, k=Bp, v=C, rec=P(0x1000000), B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB,
+             qg=G, kg=G, eps=1e-6)
+    a.update(kw)
+    st = sol.sol_qkv_encode(a["q"], a["k"], a["v"], a["rec"], a["B"], a["H"], a["N"], a["D"], a["T"],
+                            a["Hl"], a["Wl"], a["tab"], a["qg"], a["kg"], a["eps"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(rec=None), -1, "NULL"),
+    (dict(D=64), -2, "head dim"),
+    (dict(N=0), -1, ">= 1"),
+    (dict(k=P(0x400000 - 64)), -1, "overlap"),        # k (96 KB) runs into v
+    (dict(q=P(0x100000 + 1024)), -1, "overlap"),      # q inside the records
+    (dict(v=P(0x300008)), -1, "aligned"),
+])
+def test_qkv_decode_rejects_before_any_hip_call(L, kw, status, fragment):
+    a = dict(rec=A, q=Bp, k=C, v=Dp, B=1, H=2, N=192, D=128)
+    a.update(kw)
+    st = sol.sol_qkv_decode(a["rec"], a["q"], a["k"], a["v"], a["B"], a["H"], a["N"], a["D"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(rec=None), -1, "NULL"),
+    (dict(key0=-1), -1, "do not fit"),
+    (dict(key0=100, n_kv=291), -1, "do not fit"),
+    (dict(n_kv=0), -1, "n_kv"),
+    (dict(n_kv=(1 << 23) + 1), -2, "n_kv"),
+    (dict(k_prep=P(0x1000008)), -1, "aligned"),
+    (dict(k_prep=P(0x100000 + 4096)), -1, "overlap"),  # k_prep over the records
+    (dict(D=256), -2, "head dim"),
+])
+def test_prepare_kv_records_rejects_before_any_hip_call(L, kw, status, fragment):
+    a = dict(rec=A, k_prep=P(0x1000000), v_prep=P(0x2000000), B=1, H=2, N=192, key0=0, n_kv=192,
+             D=128)
+    a.update(kw)
+    st = sol.sol_prepare_kv_records(a["rec"], a["k_prep"], a["v_prep"], a["B"], a["H"], a["N"],
+                                    a["key0"], a["n_kv"], a["D"], None)
+    assert st == status, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
+@pytest.mark.parametrize("kw,status,fragment", [
+    (dict(out=None), -1, "NULL"),
+    (dict(n_kv=0), -1, "n_kv"),
+    (dict(fmt=2), -1, "out_format"),
+    (dict(out=P(0x100000 + 2048)), -1, "overlaps"),    # out over the records
+    (dict(out=P(0x1000000 + 256)), -1, "overlaps"),    # out inside k_prep
+    (dict(D=64), -2, "head dim"),
+    (dict(out=P(0x400004)), -1, "aligned"),
+])
+def test_attn_fwd_records_rejects_before_any_hip_call(L, kw, status, fragment):
+    a = dict(rec=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=192, n_kv=1000,
+             D=128, fmt=0)
+    a.update(kw)
+    st = sol.sol_attn_fwd_records(a["rec"], a["k_prep"], a["v_prep"], a["out"], a["B"], a["H"], a["N"],
+                                  a["n_kv"], a["D"], a["fmt"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
 

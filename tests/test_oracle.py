@@ -100,8 +100,8 @@ MUTANTS = [
     ("keys used as values", "const double* vj = J->vd + (int64_t)j * D;",
      "const double* vj = J->khat + (int64_t)j * D;"),
     ("ties rounded away from zero",
-     "if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;",
-     "if (rem >= 0.5) fl += 1.0;"),
+     "if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;\n  double r = fl * quantum;",
+     "if (rem >= 0.5) fl += 1.0;\n  double r = fl * quantum;"),
     ("rotated q/k not rounded to bf16", "  if (contract && changed)\n", "  if (0)\n"),
     ("dot product skips the last dim", "for (int d = 0; d < D; ++d) dot += qhat[d] * kj[d];",
      "for (int d = 0; d < D - 1; ++d) dot += qhat[d] * kj[d];"),
@@ -131,11 +131,11 @@ MUTANTS = [
     ("sparse: best block not kept", "dense || sink || J == best || s[J] > t", "dense || sink || s[J] > t"),
     ("sparse: key blocks summed, not averaged", "kbar[J * D + d] /= (double)keys;", "(void)keys;"),
     ("sparse: mask ignored", "if (keep && !keep[j / J->kblk]) s[j] = -INFINITY;", "(void)keep;"),
-    # queries and keys of different lengths
-    ("records: scale needs 127 s > max", "if (127.0 * ue5m3_value((uint8_t)c) >= amax) return",
-     "if (127.0 * ue5m3_value((uint8_t)c) > amax) return"),
-    ("records: scale rounded down", "if (127.0 * ue5m3_value((uint8_t)c) >= amax) return",
-     "if (127.0 * ue5m3_value((uint8_t)(c + 1)) > amax) return"),
+    # block-INT8 QKV records
+    ("records: scale needs 127 s > max", "if (127.0 * ue5m3_value((uint8_t)mid) >= amax) past = mid;",
+     "if (127.0 * ue5m3_value((uint8_t)mid) > amax) past = mid;"),
+    ("records: scale rounded down", "if (127.0 * ue5m3_value((uint8_t)mid) >= amax) past = mid;",
+     "if (127.0 * ue5m3_value((uint8_t)(mid + 1)) > amax) past = mid;"),
     ("records: codes tie away from zero",
      "if (rem > 0.5 || (rem == 0.5 && fmod(fl, 2.0) != 0.0)) fl += 1.0;\n  if (fl > 127.0)",
      "if (rem >= 0.5) fl += 1.0;\n  if (fl > 127.0)"),
@@ -152,6 +152,7 @@ MUTANTS = [
     ("ue5m3: exponent bias 16", "return ldexp(8.0 + m, e - 18);", "return ldexp(8.0 + m, e - 19);"),
     ("ue5m3: subnormals read as normals", "if (e == 0) return ldexp((double)m, -17);",
      "if (e == 0) return ldexp(8.0 + m, -18);"),
+    # queries and keys of different lengths
     ("key count taken from the queries", "for (int j = 0; j < Nkv; ++j) {\n    const double* kj",
      "for (int j = 0; j < Nkv && j < J->qs.N; ++j) {\n    const double* kj"),
 ]
