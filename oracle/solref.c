@@ -604,10 +604,17 @@ static double ue5m3_value(uint8_t c) {
   return ldexp(8.0 + m, e - 18); /* (1 + m/8) 2^(e-15) */
 }
 
+/* The first code c in 1..0xF7 with 127 value(c) >= amax (0xF7 if none):
+ * value() increases with the code, so the codes that pass form a suffix of
+ * 1..0xF7 and halving the interval finds its start. */
 static uint8_t ue5m3_scale_for(double amax) {
-  for (int c = 1; c < 0xF7; ++c)
-    if (127.0 * ue5m3_value((uint8_t)c) >= amax) return (uint8_t)c;
-  return 0xF7;
+  int first = 1, past = 0xF7; /* the answer lies in [first, past] */
+  while (first < past) {
+    int mid = (first + past) / 2;
+    if (127.0 * ue5m3_value((uint8_t)mid) >= amax) past = mid;
+    else first = mid + 1;
+  }
+  return (uint8_t)first;
 }
 
 static int8_t int8_code(double x, double s) {
