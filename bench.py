@@ -299,6 +299,24 @@ def main():
         ms_other, _ = timed(other, min(3, args.steps), 1)
         log("other path (%s): %.3f ms/step" % (other, ms_other))
 
+    # the dense fp16 MFMA rate this machine sustains at the attention kernels'
+    # launch shape (one wave per SIMD), with seeded operands
+    gen = torch.Generator().manual_seed(w.seed + 4242)
+    ops = torch.randn(8192, generator=gen).to(torch.float16).to(dev)
+    probe_wg, probe_iters = 2048, 25000
+    sol.mfma_probe(ops, probe_wg, 1000)
+    probe_ms = []
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        sol.mfma_probe(ops, probe_wg, probe_iters)
+        e1.record()
+        torch.cuda.synchronize()
+        probe_ms.append(e0.elapsed_time(e1))
+    probe_tflops = sol.mfma_probe_flops(probe_wg, probe_iters) / (min(probe_ms) * 1e-3) / 1e12
+    log("mfma probe: %.1f TFLOP/s (%.2f GHz equivalent); the step reaches %.1f %% of it"
+        % (probe_tflops, 2.4 * probe_tflops / PEAK_BF16_TFLOPS, 100.0 * tflops / probe_tflops))
+
     traffic = measured_traffic(w.name, main_kernel)
     result = {
         "metric": METRIC,
@@ -332,6 +350,13 @@ def main():
         "pct_peak_bf16": 100.0 * tflops / PEAK_BF16_TFLOPS,
         "kernel_ms": {name: sum(v) / len(v) for name, v in per.items()},
         "block_sparse": sparsity,
+        "mfma_probe": {
+            "what": "fp16 32x32x16 MFMAs only, one wave per SIMD, seeded operands (sol_mfma_probe)",
+            "tflops": probe_tflops,
+            "ghz_equivalent": 2.4 * probe_tflops / PEAK_BF16_TFLOPS,
+            "pct_of_probe": 100.0 * tflops / probe_tflops,
+            "kernel_frac_of_probe": achieved / probe_tflops,
+        },
         "other_path": None if ms_other is None else {
             "path": other, "ms_per_step": ms_other, "tflops": w.flops / (ms_other * 1e-3) / 1e12},
         "roofline": {

@@ -331,6 +331,21 @@ int sol_prepare_kv_records(const void* rec, void* k_prep, void* v_prep, int B, i
 int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep, void* out, int B,
                          int H, int N, int n_kv, int D, int out_format, sol_stream_t stream);
 
+/*
+ * Measurement aid: the dense matrix rate of this GPU at the attention
+ * kernels' launch shape.  Launches `workgroups` workgroups of four waves (one
+ * per SIMD, as the attention kernels run), each wave issuing iters * 16 fp16
+ * MFMAs of 32 x 32 x 16 with fp32 accumulation on operands read once from
+ * `operands` (8192 fp16 values, 16 KB, device memory): flops = workgroups *
+ * 4 * iters * 16 * 32768.  `out` (workgroups * 256 floats, device) receives
+ * per-thread sums so no product is skipped.  Time it with events on
+ * `stream`: the datasheet peak assumes 2.4 GHz, while a long dense launch runs
+ * at the clock the chip's power limit allows for such operands.
+ * 1 <= workgroups <= 1 << 20, 1 <= iters <= 1 << 24; pointers 16-byte aligned.
+ */
+int sol_mfma_probe(const void* operands, float* out, int workgroups, int iters,
+                   sol_stream_t stream);
+
 /* Static description of a status code. */
 const char* sol_status_string(int status);
 

@@ -456,6 +456,19 @@ int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep
   return ok();
 }
 
+int sol_mfma_probe(const void* operands, float* out, int workgroups, int iters, sol_stream_t stream) {
+  if (!operands || !out) return fail(SOL_ERR_INVALID_ARG, "operands, out must not be NULL");
+  if (workgroups < 1 || workgroups > (1 << 20) || iters < 1 || iters > (1 << 24))
+    return fail(SOL_ERR_INVALID_ARG, "workgroups %d or iters %d out of range", workgroups, iters);
+  if (!aligned16(operands) || !aligned16(out)) return fail(SOL_ERR_INVALID_ARG, "operands, out must be 16-byte aligned");
+  if (overlaps(out, (size_t)workgroups * 256 * 4, operands, 16384))
+    return fail(SOL_ERR_INVALID_ARG, "out overlaps operands");
+  hipError_t e = sol::launch_mfma_probe(static_cast<const uint16_t*>(operands), out, workgroups, iters,
+                                        reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "mfma_probe launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 const char* sol_status_string(int status) {
   switch (status) {
     case SOL_OK: return "ok";

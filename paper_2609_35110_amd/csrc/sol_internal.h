@@ -87,6 +87,12 @@ hipError_t launch_sparse_route(const uint16_t* q, const uint16_t* k_prep, int BH
                                const float2* tab, const float* q_gamma, float eps, float tau,
                                void* workspace, hipStream_t stream);
 
+// Dense fp16 MFMA rate probe (sol_probe.hip): `workgroups` of four waves,
+// each issuing 16 MFMAs of 32x32x16 per iteration; operands: 8192 fp16
+// values (16 KB); out: one float per thread (workgroups * 256).
+hipError_t launch_mfma_probe(const uint16_t* operands, float* out, int workgroups, int iters,
+                             hipStream_t stream);
+
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
 int64_t attn_max_workgroups(int N, int BH);
 

@@ -88,6 +88,8 @@ def lib():
         L.sol_prepare_kv_records.restype = i32
         L.sol_attn_fwd_records.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, P]
         L.sol_attn_fwd_records.restype = i32
+        L.sol_mfma_probe.argtypes = [P, P, i32, i32, P]
+        L.sol_mfma_probe.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
         L.sol_last_error.argtypes = []
@@ -188,6 +190,10 @@ def sol_prepare_kv_records(rec, k_prep, v_prep, B, H, N, key0, n_kv, D, stream):
 
 def sol_attn_fwd_records(rec, k_prep, v_prep, out, B, H, N, n_kv, D, out_format, stream):
     return lib().sol_attn_fwd_records(rec, k_prep, v_prep, out, B, H, N, n_kv, D, out_format, stream)
+
+
+def sol_mfma_probe(operands, out, workgroups, iters, stream):
+    return lib().sol_mfma_probe(operands, out, workgroups, iters, stream)
 
 
 def sol_status_string(status):
@@ -583,4 +589,24 @@ def attn_fwd_records(rec, k_prep, v_prep, n_kv=None, out=None, fp8=False):
                                ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                                B, H, N, n_kv, HEAD_DIM, SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16,
                                _stream(rec)))
+    return out
+
+
+# ------------------------------------------------------------ measurement aid
+
+def mfma_probe_flops(workgroups, iters):
+    """Flops of one sol_mfma_probe launch."""
+    return float(workgroups) * 4 * iters * 16 * 32768
+
+
+def mfma_probe(operands, workgroups, iters, out=None):
+    """Launch the dense fp16 MFMA probe on the current stream; operands: a
+    float16 device tensor of 8192 values.  Returns `out` (per-thread sums)."""
+    if (operands.dtype != torch.float16 or operands.numel() != 8192 or not operands.is_cuda
+            or not operands.is_contiguous()):
+        raise ValueError("operands must be a contiguous float16 device tensor of 8192 values")
+    if out is None:
+        out = torch.empty(workgroups * 256, dtype=torch.float32, device=operands.device)
+    check(sol_mfma_probe(ctypes.c_void_p(operands.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                         workgroups, iters, _stream(operands)))
     return out

@@ -359,6 +359,22 @@ def test_attn_fwd_records_rejects_before_any_hip_call(L, kw, status, fragment):
     assert fragment in sol.sol_last_error()
 
 
+@pytest.mark.parametrize("kw,fragment", [
+    (dict(ops=None), "NULL"),
+    (dict(wg=0), "out of range"),
+    (dict(iters=0), "out of range"),
+    (dict(iters=(1 << 24) + 1), "out of range"),
+    (dict(out=P(0x100008)), "aligned"),
+    (dict(out=P(0x200000 - 1024)), "overlaps"),   # 256 floats per workgroup reach the operands
+])
+def test_mfma_probe_rejects_before_any_hip_call(L, kw, fragment):
+    a = dict(ops=P(0x200000), out=P(0x100000), wg=4, iters=10)
+    a.update(kw)
+    st = sol.sol_mfma_probe(a["ops"], a["out"], a["wg"], a["iters"], None)
+    assert st == -1, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
 def test_binding_rejects_wrong_dtype_and_device():
     import torch
     x = torch.zeros(1, 1, 4, 128, dtype=torch.float32)

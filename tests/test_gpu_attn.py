@@ -79,6 +79,19 @@ def test_library_is_the_in_tree_build():
     assert sol.sol_version() == 102
 
 
+def test_mfma_probe_runs_every_product():
+    """The rate probe's per-thread sums: every MFMA of every wave happened
+    (iters * 4 copies of a fixed product per chain, so the sums scale exactly
+    with iters for power-of-two operands)."""
+    ops = torch.full((8192,), 0.5, dtype=torch.float16, device="cuda:0")
+    one = sol.mfma_probe(ops, 8, 1)
+    four = sol.mfma_probe(ops, 8, 4)
+    torch.cuda.synchronize()
+    # each accumulator element gets 4 MFMAs per iteration of 16 products 0.25
+    # per chain: 16 elements x 4 chains x 4 x 16 x 0.25 = 1024 per iteration
+    assert torch.all(one == 1024.0) and torch.all(four == 4096.0)
+
+
 def test_tiny_full_parity():
     w = W.WORKLOADS["tiny"]
     q, k, v = W.make_inputs(w)
