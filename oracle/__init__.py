@@ -20,7 +20,7 @@ Two independent implementations, both in IEEE double:
 """
 from .solref import (  # noqa: F401
     Oracle, default,
-    DEFAULT_SPLIT, ROPE_BASE, attn_rows, decode_qkv, encode_qkv, num_threads, qknorm_rope3d,
-    rope3d_bf16, rope3d_f64, round_bf16, round_e4m3, sparse_route,
+    DEFAULT_SPLIT, ROPE_BASE, attn_rows, decode_qkv, encode_out_records, encode_qkv, num_threads,
+    qknorm_rope3d, rope3d_bf16, rope3d_f64, round_bf16, round_e4m3, sparse_route,
 )
 from . import brute  # noqa: F401

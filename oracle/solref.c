@@ -672,3 +672,29 @@ int solref_decode_qkv(const uint8_t* rec, int B, int H, int N, int D, uint16_t* 
       }
   return 0;
 }
+
+/*
+ * Block-INT8 output records (Sec. 3.2, "Quantized communication": the
+ * attention output's block-INT8 wire format, 128 value bytes and four scale
+ * codes, padded from 132 to 144 bytes).  Reading: bytes 0..127 the int8
+ * codes of the 128 output dims, bytes 128..131 the UE5M3 scale codes of dims
+ * [32g, 32g + 32), bytes 132..143 zero; the codes and scales follow the QKV
+ * records' rule, applied to the exact (double) attention output.
+ * x: double [rows][128]; rec: [rows][144].
+ */
+#define OUT_REC_BYTES 144
+void solref_encode_out_records(const double* x, int64_t rows, uint8_t* rec) {
+  for (int64_t r = 0; r < rows; ++r) {
+    const double* xr = x + r * 128;
+    uint8_t* o = rec + r * OUT_REC_BYTES;
+    for (int g = 0; g < 4; ++g) {
+      double amax = 0.0;
+      for (int d = 32 * g; d < 32 * g + 32; ++d) amax = fmax(amax, fabs(xr[d]));
+      const uint8_t sc = ue5m3_scale_for(amax);
+      const double s = ue5m3_value(sc);
+      o[128 + g] = sc;
+      for (int d = 32 * g; d < 32 * g + 32; ++d) o[d] = (uint8_t)int8_code(xr[d], s);
+    }
+    for (int i = 132; i < OUT_REC_BYTES; ++i) o[i] = 0;
+  }
+}

@@ -64,6 +64,8 @@ class Oracle:
         lib.solref_encode_qkv.restype = ctypes.c_int
         lib.solref_decode_qkv.argtypes = [P, i32, i32, i32, i32, P, P, P]
         lib.solref_decode_qkv.restype = ctypes.c_int
+        lib.solref_encode_out_records.argtypes = [P, i64, P]
+        lib.solref_encode_out_records.restype = None
         lib.solref_num_threads.argtypes = []
         lib.solref_num_threads.restype = ctypes.c_int
         self.lib = lib
@@ -97,6 +99,16 @@ class Oracle:
         rec = np.empty((B, N, H, 400), dtype=np.uint8)
         if self.lib.solref_encode_qkv(_ptr(q), _ptr(k), _ptr(v), B, H, N, D, _ptr(rec)) != 0:
             raise ValueError("oracle rejected the arguments")
+        return rec
+
+    def encode_out_records(self, x) -> np.ndarray:
+        """Block-INT8 output records of float64 rows x [..., 128]: uint8 [..., 144]
+        (128 codes, four UE5M3 scales, twelve zero bytes)."""
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        if x.shape[-1] != 128:
+            raise ValueError("rows of 128 values")
+        rec = np.empty(x.shape[:-1] + (144,), dtype=np.uint8)
+        self.lib.solref_encode_out_records(_ptr(x), x.size // 128, _ptr(rec))
         return rec
 
     def decode_qkv(self, rec):
@@ -260,6 +272,10 @@ def encode_qkv(q, k, v):
 
 def decode_qkv(rec):
     return default().decode_qkv(rec)
+
+
+def encode_out_records(x):
+    return default().encode_out_records(x)
 
 
 def rope3d_f64(x, T, Hl, Wl, split=DEFAULT_SPLIT, base=ROPE_BASE):

@@ -825,4 +825,46 @@ def pin_records_vs_numpy_twin(o):
         assert np.array_equal(got, _bits(want.astype(np.float32)))  # code * scale is float32-exact
 
 
+def pin_out_records_sizes_are_the_papers(o):
+    """Output records of 144 bytes: 128 code bytes and four scale codes (132),
+    padded with zeros to the next multiple of 16 (the paper's printed sizes);
+    one scale per 32 dims."""
+    fmt = _record_format()
+    assert fmt["out_value_bytes"] + fmt["out_scale_codes"] == fmt["out_unpadded_bytes"]
+    assert fmt["out_record_bytes"] % 16 == 0 and fmt["out_record_bytes"] - fmt["out_unpadded_bytes"] < 16
+    rng = np.random.default_rng(73)
+    rec = o.encode_out_records(rng.standard_normal((2, 5, 128)) * 1e-3)
+    assert rec.shape == (2, 5, fmt["out_record_bytes"])
+    assert (rec[..., fmt["out_unpadded_bytes"]:] == 0).all()
+    base = o.encode_out_records(np.ones(128))
+    for d in (0, 31, 32, 70, 127):
+        x = np.ones(128)
+        x[d] = 100.0
+        r = o.encode_out_records(x)
+        changed = {i for i in range(4) if r[128 + i] != base[128 + i]}
+        assert changed == {d // fmt["group_size"]}, (d, changed)
+
+
+def pin_out_records_quantise_like_qkv_records(o):
+    """The output records follow the QKV records' rule: on bf16 values their
+    codes and scales equal those of a record's q part; on double values the
+    round-trip bound |code s - x| <= s/2 and the scale's minimality hold."""
+    rng = np.random.default_rng(74)
+    xb = _bits(rng.standard_normal((1, 2, 9, 128)) * np.exp2(rng.uniform(-15, 15, (1, 2, 9, 1))))
+    q_rec = o.encode_qkv(xb, xb, xb)                       # [1, 9, 2, 400]
+    out = o.encode_out_records(_f(xb))                     # [1, 2, 9, 144]
+    q_rec = np.transpose(q_rec, (0, 2, 1, 3))
+    assert np.array_equal(out[..., :128], q_rec[..., :128])
+    assert np.array_equal(out[..., 128:132], q_rec[..., 384:388])
+    x = rng.standard_normal((64, 4, 32)) * np.exp2(rng.uniform(-30, 10, (64, 4, 1)))
+    rec = o.encode_out_records(x.reshape(64, 128))
+    h16 = np.array([_float16_of_code(c) for c in range(0xF8)])
+    sc = rec[:, 128:132]
+    s = h16[sc][..., None]
+    c = rec[:, :128].view(np.int8).astype(np.float64).reshape(64, 4, 32)
+    amax = np.abs(x).max(-1)
+    assert (amax <= 127 * s[..., 0]).all() and ((sc == 1) | (127 * h16[np.maximum(sc, 1) - 1] < amax)).all()
+    assert (np.abs(c * s - x) <= s / 2).all()
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

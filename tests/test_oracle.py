@@ -152,6 +152,10 @@ MUTANTS = [
     ("ue5m3: exponent bias 16", "return ldexp(8.0 + m, e - 18);", "return ldexp(8.0 + m, e - 19);"),
     ("ue5m3: subnormals read as normals", "if (e == 0) return ldexp((double)m, -17);",
      "if (e == 0) return ldexp(8.0 + m, -18);"),
+    ("out records: group max over 16 values",
+     "for (int d = 32 * g; d < 32 * g + 32; ++d) amax = fmax(amax, fabs(xr[d]));",
+     "for (int d = 32 * g; d < 32 * g + 16; ++d) amax = fmax(amax, fabs(xr[d]));"),
+    ("out records: scales one slot late", "o[128 + g] = sc;", "o[129 + g] = sc;"),
     # queries and keys of different lengths
     ("key count taken from the queries", "for (int j = 0; j < Nkv; ++j) {\n    const double* kj",
      "for (int j = 0; j < Nkv && j < J->qs.N; ++j) {\n    const double* kj"),
