@@ -54,10 +54,12 @@ enum {
   SOL_ERR_HIP = -3          /* the HIP runtime reported an error */
 };
 
-/* Output formats of sol_attn_fwd_prepared_ex. */
+/* Output formats of sol_attn_fwd_prepared_ex, sol_attn_fwd_sparse and
+ * sol_attn_fwd_records. */
 enum {
-  SOL_OUT_BF16 = 0,    /* bf16, round to nearest even (every other entry point) */
-  SOL_OUT_FP8_E4M3 = 1 /* FP8 E4M3 bytes with unit scale (see sol_attn_fwd_prepared_ex) */
+  SOL_OUT_BF16 = 0,        /* bf16, round to nearest even (every other entry point) */
+  SOL_OUT_FP8_E4M3 = 1,    /* FP8 E4M3 bytes with unit scale (see sol_attn_fwd_prepared_ex) */
+  SOL_OUT_INT8_RECORDS = 2 /* block-INT8 output records (see sol_attn_fwd_prepared_ex) */
 };
 
 /* Largest N the kernels accept (token indices stay exact in float32 arithmetic). */
@@ -195,6 +197,13 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
  * the raw E4M3 values the paper's attention hands to the quantized output
  * projection (Sec. 3.5, "Joint optimization with quantized communication") --
  * rounded to nearest even from the fp32 result and saturated at +-448.
+ * SOL_OUT_INT8_RECORDS: the paper's block-INT8 output wire format (Sec. 3.2,
+ * "Quantized communication"), one record of SOL_OUT_RECORD_BYTES = 144 bytes
+ * per row, token-major like the QKV records (row (b, h, n) at byte
+ * ((b N + n) H + h) * 144): bytes 0..127 the int8 codes of the 128 output
+ * dims, 128..131 the UE5M3 scale codes of dims [32g, 32g + 32), 132..143
+ * zero; scales and codes follow the QKV records' rule (sol_qkv_encode),
+ * applied to the fp32 result.
  * sol_attn_fwd_prepared(...) is this call with n_kv = N, no normalisation and
  * bf16 output.
  *
@@ -238,7 +247,8 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
  * entries are meaningful); then pooled queries and keys (fp32).
  * nqb = ceil(N/256), nkb = ceil(N/128).  tau finite.
  * sol_attn_fwd_sparse: the attention under that routing (the workspace as
- * sol_sparse_route left it), bf16 or E4M3 output as sol_attn_fwd_prepared_ex.
+ * sol_sparse_route left it), bf16 or E4M3 output as sol_attn_fwd_prepared_ex
+ * (SOL_OUT_INT8_RECORDS: SOL_ERR_UNSUPPORTED).
  * The workspace is sol_sparse_workspace_bytes(B, H, N, D) bytes of device
  * memory, 16-byte aligned, not overlapping q, k_prep, v_prep or out.
  * N <= 1,032,192 = 8064 key blocks (SOL_ERR_UNSUPPORTED beyond: the
@@ -312,13 +322,15 @@ int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int 
  * sol_attn_fwd_records: sol_attn_fwd_prepared_ex with the queries decoded
  * from the records (q parts) in the kernel's tile load: N query rows per
  * (b, h) against the n_kv prepared keys, no rotation or normalisation,
- * out [B][H][N][D] in out_format (SOL_OUT_BF16 or SOL_OUT_FP8_E4M3).  Equal,
+ * out [B][H][N][D] in out_format (SOL_OUT_BF16, SOL_OUT_FP8_E4M3 or
+ * SOL_OUT_INT8_RECORDS).  Equal,
  * bit for bit, to sol_attn_fwd_prepared_ex on the decoded q (table NULL).
  *
  * All: D = 128; pointers 16-byte aligned device memory; 1 <= N <=
  * SOL_MAX_TOKENS; errors as the prepared path.
  */
 #define SOL_QKV_RECORD_BYTES 400
+#define SOL_OUT_RECORD_BYTES 144
 size_t sol_qkv_record_bytes(int B, int H, int N);
 int sol_qkv_encode(const void* q, const void* k, const void* v, void* rec, int B, int H, int N,
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev,

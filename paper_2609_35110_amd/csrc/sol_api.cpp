@@ -54,6 +54,17 @@ int check_norm(const float* gamma, float eps) {
   return SOL_OK;
 }
 
+// Bytes of an attention output in out_format (0 for an unknown format).
+size_t out_bytes(int B, int H, int N, int D, int out_format) {
+  const size_t rows = (size_t)B * H * N;
+  switch (out_format) {
+    case SOL_OUT_BF16: return rows * D * 2;
+    case SOL_OUT_FP8_E4M3: return rows * D;
+    case SOL_OUT_INT8_RECORDS: return rows * SOL_OUT_RECORD_BYTES;
+    default: return 0;
+  }
+}
+
 // Common checks of the two block-sparse entry points.
 int check_sparse(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
                  int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
@@ -241,10 +252,9 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   st = check_norm(q_gamma_dev, eps);
   if (st != SOL_OK) return st;
-  if (out_format != SOL_OUT_BF16 && out_format != SOL_OUT_FP8_E4M3)
-    return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
+  const size_t obytes = out_bytes(B, H, N, D, out_format);
+  if (obytes == 0) return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
   const size_t bytes = (size_t)B * H * N * D * 2;
-  const size_t obytes = out_format == SOL_OUT_BF16 ? bytes : bytes / 2;
   const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
   if (overlaps(out, obytes, q, bytes) || overlaps(out, obytes, k_prep, pbytes) || overlaps(out, obytes, v_prep, pbytes))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep or v_prep");
@@ -254,8 +264,8 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
   hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
                                                static_cast<const uint16_t*>(v_prep), out, B * H, g, n_kv, tab,
-                                               q_gamma_dev, eps, out_format == SOL_OUT_FP8_E4M3,
-                                               nullptr, nullptr, 0, reinterpret_cast<hipStream_t>(stream));
+                                               q_gamma_dev, eps, out_format, nullptr, nullptr, 0,
+                                               reinterpret_cast<hipStream_t>(stream), nullptr, H);
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_prepared launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -300,10 +310,11 @@ int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, v
   if (st != SOL_OK) return st;
   if (!v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must not be NULL");
   if (!aligned16(v_prep) || !aligned16(out)) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must be 16-byte aligned");
-  if (out_format != SOL_OUT_BF16 && out_format != SOL_OUT_FP8_E4M3)
-    return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
+  const size_t obytes = out_bytes(B, H, N, D, out_format);
+  if (obytes == 0) return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
+  if (out_format == SOL_OUT_INT8_RECORDS)
+    return fail(SOL_ERR_UNSUPPORTED, "block-INT8 output records are not built for the block-sparse walk");
   const size_t bytes = (size_t)B * H * N * D * 2;
-  const size_t obytes = out_format == SOL_OUT_BF16 ? bytes : bytes / 2;
   const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
   const size_t need = sol_sparse_workspace_bytes(B, H, N, D);
   if (overlaps(out, obytes, q, bytes) || overlaps(out, obytes, k_prep, pbytes) ||
@@ -318,9 +329,9 @@ int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, v
   const char* ws = static_cast<const char*>(workspace);
   hipError_t e = sol::launch_attn_fwd_prepared(
       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep), static_cast<const uint16_t*>(v_prep),
-      out, B * H, g, N, tab, q_gamma_dev, eps, out_format == SOL_OUT_FP8_E4M3,
+      out, B * H, g, N, tab, q_gamma_dev, eps, out_format,
       reinterpret_cast<const uint16_t*>(ws + off[1]), reinterpret_cast<const int*>(ws + off[0]),
-      (N + 127) / 128, reinterpret_cast<hipStream_t>(stream));
+      (N + 127) / 128, reinterpret_cast<hipStream_t>(stream), nullptr, H);
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_sparse launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -439,9 +450,8 @@ int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep
     return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
   if (!aligned16(rec) || !aligned16(k_prep) || !aligned16(v_prep) || !aligned16(out))
     return fail(SOL_ERR_INVALID_ARG, "rec, k_prep, v_prep, out must be 16-byte aligned");
-  if (out_format != SOL_OUT_BF16 && out_format != SOL_OUT_FP8_E4M3)
-    return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
-  const size_t obytes = (size_t)B * H * N * D * (out_format == SOL_OUT_BF16 ? 2 : 1);
+  const size_t obytes = out_bytes(B, H, N, D, out_format);
+  if (obytes == 0) return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
   const size_t pbytes = sol_prepared_kv_bytes(B, H, n_kv, D);
   if (overlaps(out, obytes, rec, rbytes) || overlaps(out, obytes, k_prep, pbytes) || overlaps(out, obytes, v_prep, pbytes))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps rec, k_prep or v_prep");
@@ -449,7 +459,7 @@ int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep
   hipError_t e = sol::launch_attn_fwd_prepared(nullptr, static_cast<const uint16_t*>(k_prep),
                                                static_cast<const uint16_t*>(v_prep), out, B * H,
                                                sol::make_grid(N, 0, 0, 0), n_kv, nullptr, nullptr, 0.0f,
-                                               out_format == SOL_OUT_FP8_E4M3, nullptr, nullptr, 0,
+                                               out_format, nullptr, nullptr, 0,
                                                reinterpret_cast<hipStream_t>(stream),
                                                static_cast<const uint8_t*>(rec), H);
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd_records launch: %s", hipGetErrorString(e));

@@ -207,6 +207,9 @@ constexpr int kMaxSparseBlocks = 8064;  // key blocks per slab: N <= 1,032,192
 // times its group's scale, rounded once to bf16.
 constexpr int kRecBytes = 400;
 constexpr int kRecScales = 384;  // first scale byte; part p group g at 384 + 4p + g
+// The attention output's block-INT8 record: 128 codes, 4 scale codes (dims
+// [32g, 32g + 32)), 12 zero bytes; token-major like the QKV records.
+constexpr int kOutRecBytes = 144;
 
 // UE5M3 code -> value: unsigned, 5 exponent bits of bias 15, 3 mantissa bits;
 // exponent 0 subnormal (m 2^-17), exponent 31 infinity (m = 0) or NaN.  Exact.
@@ -214,6 +217,33 @@ __device__ __forceinline__ float ue5m3_value(uint32_t c) {
   if (c >= 0xF8u) return __uint_as_float(c == 0xF8u ? 0x7F800000u : 0x7FC00000u);
   if (c < 8u) return (float)c * 0x1p-17f;
   return __uint_as_float((c << 20) + (112u << 23));  // exponent e - 15 + 127, mantissa m
+}
+
+// Quantisation of a group of 32 values (the records' scale granularity):
+// scale s = the smallest finite positive UE5M3 value with 127 s >= max |x|,
+// so no code passes +-127; code = x / s rounded to nearest, ties to even.
+// 127 s is exact in fp32 (a 4-bit significand times 127), so the scale is
+// the exact one.  For bf16 x (8 significant bits) x / s lies on a
+// half-integer or at least 2^-8 / 15 away from one, far beyond the fp32
+// division's rounding error, so the correctly rounded quotient gives the code
+// of the exact one; the attention output epilogue quantises its fp32 results
+// with the same division.
+// Smallest code c in 1..0xF7 with 127 value(c) >= amax (0xF7 when none is
+// large enough), by bisection: 127 value(lo) < amax <= 127 value(hi).
+__device__ __forceinline__ uint32_t ue5m3_scale_for(float amax) {
+  uint32_t lo = 0, hi = 0xF7;
+  if (!(127.0f * ue5m3_value(hi) >= amax)) return hi;
+#pragma unroll 1
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (127.0f * ue5m3_value(mid) >= amax) hi = mid;
+    else lo = mid;
+  }
+  return hi;
+}
+// One value's int8 code at scale s, as the low byte of the result.
+__device__ __forceinline__ uint32_t int8_code(float x, float s) {
+  return (uint32_t)(int)fminf(fmaxf(__builtin_rintf(x / s), -127.0f), 127.0f) & 0xFFu;
 }
 
 // Eight int8 codes (one 8-byte word of a record) times their scale, to bf16

@@ -48,16 +48,17 @@ hipError_t launch_prepare_kv(const uint16_t* k, const uint16_t* v, uint16_t* k_p
 // blocks != nullptr: block-sparse, each 256-row query block attends only to
 // the counts[...] key blocks of 128 keys listed for it in blocks (nkb entries
 // per query block, ascending).
-// qrec != nullptr: the queries come from block-INT8 QKV records instead of q
-// (token-major, `heads` records per token: already normalised and rotated, so
-// tab and q_gamma are null; dense).
+// out_format: 0 bf16, 1 FP8 E4M3 bytes, 2 block-INT8 output records (144
+// bytes per row, token-major over `heads`).  qrec != nullptr: the queries
+// come from block-INT8 QKV records instead of q (token-major, `heads` records
+// per token: already normalised and rotated, so tab and q_gamma are null;
+// dense).  heads: H of the B*H = BH slabs.
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, void* out, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
-                                    const float* q_gamma, float eps, bool out_fp8,
+                                    const float* q_gamma, float eps, int out_format,
                                     const uint16_t* blocks, const int* counts, int nkb,
-                                    hipStream_t stream, const uint8_t* qrec = nullptr,
-                                    int heads = 1);
+                                    hipStream_t stream, const uint8_t* qrec, int heads);
 // Block-INT8 QKV records (sol_records.hip and the prepare pass), records
 // [B][N][H][400]: the encoder (q and k normalised with their gammas and
 // rotated with grid g first when tab != nullptr), the standalone decoder

@@ -620,12 +620,17 @@ constexpr int kBufferDword3 = 0x00020000;
 // N and its walk position is known.
 static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's rows");
 
-template <bool kRope, bool kRobust, bool kSparse, bool kRec>
+// kOutRec: block-INT8 output records (out_format 2).  A template flag, not a
+// run-time branch: compiled into the bf16 / E4M3 instances, the unused
+// record epilogue changed the second pass's register allocation and the
+// compiler then produced wrong results for the first row block of each wave
+// (scores climbing 24 binades); the instances without it compile as before.
+template <bool kRope, bool kRobust, bool kSparse, bool kRec, bool kOutRec>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
                           const float2* __restrict__ tab, int n_qtiles, float c_log2, int n_keys,
-                          const float* __restrict__ q_gamma, float eps, int out_fp8,
+                          const float* __restrict__ q_gamma, float eps, int out_format,
                           const uint16_t* __restrict__ blocks, const int* __restrict__ counts,
                           int nkb, const uint8_t* __restrict__ qrec, int heads) {
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[kKBufs * kPrepTileElems];
@@ -668,9 +673,16 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   // into the main loop makes every LDS wait there a full lgkmcnt(0).
   uint16_t* out_slab = out + slab;
   asm volatile("" : "+s"(out_slab));
-  // out_fp8: one E4M3 byte per element instead of a bf16 pair
+  // out_format 1: one E4M3 byte per element instead of a bf16 pair; 2: one
+  // block-INT8 record of kOutRecBytes per row, token-major over `heads`
+  const bool out_fp8 = out_format == 1;
+  constexpr bool out_rec = kOutRec;
   uint8_t* out8_slab = reinterpret_cast<uint8_t*>(out) + slab;
-  asm volatile("" : "+s"(out8_slab), "+s"(out_fp8));
+  asm volatile("" : "+s"(out8_slab), "+s"(out_format));
+  const int ob = bh / heads;
+  uint8_t* outrec_slab =
+      reinterpret_cast<uint8_t*>(out) + ((size_t)ob * Nq * heads + (bh - ob * heads)) * kOutRecBytes;
+  const size_t outrec_stride = (size_t)heads * kOutRecBytes;
   const int qrow_first = qt * BM + wave * 64 + l32;
   // Tiles the workgroup walks: every tile of the slab, or the listed blocks'.
   int n_kv = (N + BN2 - 1) / BN2;
@@ -726,8 +738,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     for (int qb = 0; qb < 2; ++qb) {
       const int row = qrow_first + 32 * qb;
       if (hh == 0 && row < Nq)
-        marked |= out_fp8 ? (out8_slab[(size_t)row * D] & 0x7F) == 0x7F
-                          : (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
+        marked |= out_rec   ? outrec_slab[row * outrec_stride + 128] == 0xFF
+                  : out_fp8 ? (out8_slab[(size_t)row * D] & 0x7F) == 0x7F
+                            : (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
     }
     if (!__syncthreads_or(marked)) return;
   }
@@ -1184,6 +1197,36 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     const int row = qrow0 + 32 * qb;
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.0f / l_tot;
+    if (out_rec) {
+      // block-INT8 output record: 32 dims per scale; a group's 32 values sit
+      // in this lane's 16 registers of block db and its partner lane's (hh ^ 1)
+      if (row >= Nq) continue;  // uniform over the lane pair
+      uint8_t* dst = outrec_slab + row * outrec_stride;
+      if (marked) {  // scale codes 0xFF (NaN): recomputed by the second pass
+        if (hh == 0) *reinterpret_cast<uint4*>(dst + 128) = make_uint4(0xFFFFFFFFu, 0u, 0u, 0u);
+        continue;
+      }
+      uint32_t scales = 0;
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        float a = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) a = fmaxf(a, __builtin_fabsf(o[qb][db][j] * inv));
+        a = fmaxf(a, __shfl_xor(a, 32));
+        const uint32_t sc = ue5m3_scale_for(a);
+        const float sv = ue5m3_value(sc);
+        scales |= sc << (8 * db);
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          uint32_t w = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w |= int8_code(o[qb][db][4 * g4 + e] * inv, sv) << (8 * e);
+          *reinterpret_cast<uint32_t*>(dst + 32 * db + 8 * g4 + 4 * hh) = w;
+        }
+      }
+      if (hh == 0) *reinterpret_cast<uint4*>(dst + 128) = make_uint4(scales, 0u, 0u, 0u);
+      continue;
+    }
     if (out_fp8) {
       if (row >= Nq) continue;
       uint8_t* dst = out8_slab + (size_t)row * D;
@@ -1299,11 +1342,10 @@ int64_t prepared_tile_elems(int N) {
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, void* out_v, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
-                                    const float* q_gamma, float eps, bool out_fp8,
+                                    const float* q_gamma, float eps, int out_format,
                                     const uint16_t* blocks, const int* counts, int nkb,
                                     hipStream_t stream, const uint8_t* qrec, int heads) {
   uint16_t* out = static_cast<uint16_t*>(out_v);
-  const int fp8 = out_fp8 ? 1 : 0;
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
@@ -1311,23 +1353,32 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   // First pass, then the second over the row blocks whose probabilities left
   // the fp16 range.
   for (int pass = 0; pass < 2; ++pass) {
-    // queries from records: no rotation, no normalisation, dense
-    const int sel = qrec != nullptr ? 8 + pass : (tab != nullptr) * 4 + pass * 2 + sparse;
-#define SOL_LAUNCH_PREPARED(R, P, S, Q)                                                         \
-  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S, Q>), grid, dim3(256), 0, stream, q, k_prep,  \
-                     v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, fp8, blocks,     \
-                     counts, nkb, qrec, heads)
+    // queries from records: no rotation, no normalisation, dense; block-INT8
+    // output records: dense (the caller rejects them on the sparse walk)
+    const bool orec = out_format == 2;
+    const int sel = (qrec != nullptr ? 8 + pass : (tab != nullptr) * 4 + pass * 2 + sparse) + 10 * orec;
+#define SOL_LAUNCH_PREPARED(R, P, S, Q, O)                                                      \
+  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S, Q, O>), grid, dim3(256), 0, stream, q,       \
+                     k_prep, v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps,          \
+                     out_format, blocks, counts, nkb, qrec, heads)
     switch (sel) {
-      case 0: SOL_LAUNCH_PREPARED(false, false, false, false); break;
-      case 1: SOL_LAUNCH_PREPARED(false, false, true, false); break;
-      case 2: SOL_LAUNCH_PREPARED(false, true, false, false); break;
-      case 3: SOL_LAUNCH_PREPARED(false, true, true, false); break;
-      case 4: SOL_LAUNCH_PREPARED(true, false, false, false); break;
-      case 5: SOL_LAUNCH_PREPARED(true, false, true, false); break;
-      case 6: SOL_LAUNCH_PREPARED(true, true, false, false); break;
-      case 7: SOL_LAUNCH_PREPARED(true, true, true, false); break;
-      case 8: SOL_LAUNCH_PREPARED(false, false, false, true); break;
-      default: SOL_LAUNCH_PREPARED(false, true, false, true); break;
+      case 0: SOL_LAUNCH_PREPARED(false, false, false, false, false); break;
+      case 1: SOL_LAUNCH_PREPARED(false, false, true, false, false); break;
+      case 2: SOL_LAUNCH_PREPARED(false, true, false, false, false); break;
+      case 3: SOL_LAUNCH_PREPARED(false, true, true, false, false); break;
+      case 4: SOL_LAUNCH_PREPARED(true, false, false, false, false); break;
+      case 5: SOL_LAUNCH_PREPARED(true, false, true, false, false); break;
+      case 6: SOL_LAUNCH_PREPARED(true, true, false, false, false); break;
+      case 7: SOL_LAUNCH_PREPARED(true, true, true, false, false); break;
+      case 8: SOL_LAUNCH_PREPARED(false, false, false, true, false); break;
+      case 9: SOL_LAUNCH_PREPARED(false, true, false, true, false); break;
+      case 10: SOL_LAUNCH_PREPARED(false, false, false, false, true); break;
+      case 12: SOL_LAUNCH_PREPARED(false, true, false, false, true); break;
+      case 14: SOL_LAUNCH_PREPARED(true, false, false, false, true); break;
+      case 16: SOL_LAUNCH_PREPARED(true, true, false, false, true); break;
+      case 18: SOL_LAUNCH_PREPARED(false, false, false, true, true); break;
+      case 19: SOL_LAUNCH_PREPARED(false, true, false, true, true); break;
+      default: return hipErrorInvalidValue;  // records output on the sparse walk
     }
 #undef SOL_LAUNCH_PREPARED
     const hipError_t e = hipGetLastError();

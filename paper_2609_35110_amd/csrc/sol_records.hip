@@ -6,15 +6,8 @@
 // tensors back (for consumers other than this library's attention, which
 // decodes records in its own tile loads).  Both kernels stream: HBM-bound,
 // 768 bytes read and 400 written per record (encoder), the reverse (decoder).
-//
-// Quantisation of a group of 32 values (the record's scale granularity):
-// scale s = the smallest finite positive UE5M3 value with 127 s >= max |x|,
-// so no code passes +-127; code = x / s rounded to nearest, ties to even.
-// Both decisions are exact: 127 s is exact in fp32 (a 4-bit significand times
-// 127), and x / s (x with 8 significant bits) lies at least 2^-8 / 15 away
-// from a half-integer unless it is one, far more than the division's
-// rounding error, so the fp32 quotient rounds to the same code as the exact
-// one.
+// The quantisation rule (scale search, rounding) lives in sol_device.h, shared
+// with the attention kernel's block-INT8 output epilogue.
 #include "sol_device.h"
 
 namespace sol {
@@ -23,30 +16,13 @@ namespace {
 constexpr int kRecPerWg = 4;                 // records per workgroup
 constexpr int kRecThreads = 48 * kRecPerWg;  // one thread per 16-byte chunk of q, k and v
 
-// Smallest code c in 1..0xF7 with 127 value(c) >= amax (0xF7 when none is
-// large enough), by bisection: 127 value(lo) < amax <= 127 value(hi).
-__device__ __forceinline__ uint32_t ue5m3_scale_for(float amax) {
-  uint32_t lo = 0, hi = 0xF7;
-  if (!(127.0f * ue5m3_value(hi) >= amax)) return hi;
-#pragma unroll 1
-  while (hi - lo > 1) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (127.0f * ue5m3_value(mid) >= amax) hi = mid;
-    else lo = mid;
-  }
-  return hi;
-}
-
 // Eight bf16 values -> eight int8 codes of scale s (one 8-byte word).
 __device__ __forceinline__ uint2 encode_chunk(uint4 y, float s) {
   float f[8];
   unpack_bf16x8(y, f);
   uint32_t w[2] = {0u, 0u};
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float c = fminf(fmaxf(__builtin_rintf(f[e] / s), -127.0f), 127.0f);
-    w[e >> 2] |= ((uint32_t)(int)c & 0xFFu) << (8 * (e & 3));
-  }
+  for (int e = 0; e < 8; ++e) w[e >> 2] |= int8_code(f[e], s) << (8 * (e & 3));
   return make_uint2(w[0], w[1]);
 }
 

@@ -23,6 +23,8 @@ SOL_ERR_UNSUPPORTED = -2
 SOL_ERR_HIP = -3
 SOL_OUT_BF16 = 0
 SOL_OUT_FP8_E4M3 = 1
+SOL_OUT_INT8_RECORDS = 2
+OUT_RECORD_BYTES = 144
 HEAD_DIM = 128
 ROPE_BASE = 10000.0
 
@@ -401,31 +403,41 @@ def prepare_kv_ex(k, v, T, Hl, Wl, table, k_prep, v_prep, key0=0, n_kv=None, gam
     return k_prep, v_prep
 
 
+def _out_tensor(out, B, H, N, device, fp8, int8_records):
+    """The output tensor of an attention call in its format: bf16 [B, H, N, D],
+    E4M3 codes uint8 [B, H, N, D], or block-INT8 records uint8 [B, N, H, 144]."""
+    if fp8 and int8_records:
+        raise ValueError("one output format at a time")
+    if not fp8 and not int8_records:
+        if out is None:
+            out = torch.empty((B, H, N, HEAD_DIM), dtype=torch.bfloat16, device=device)
+        _check_tensor("out", out, (B, H, N, HEAD_DIM))
+        return out, SOL_OUT_BF16
+    shape = (B, N, H, OUT_RECORD_BYTES) if int8_records else (B, H, N, HEAD_DIM)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.uint8, device=device)
+    if (out.dtype != torch.uint8 or tuple(out.shape) != shape or not out.is_contiguous()
+            or out.device != device):
+        raise ValueError("out must be a contiguous uint8 tensor of shape %s on %s" % (shape, device))
+    return out, SOL_OUT_INT8_RECORDS if int8_records else SOL_OUT_FP8_E4M3
+
+
 def attn_fwd_prepared_ex(q, k_prep, v_prep, n_kv, T, Hl, Wl, table=None, gamma=None, eps=1e-6,
-                         out=None, fp8=False):
+                         out=None, fp8=False, int8_records=False):
     """q [B, H, N, D] (rotated with grid T x Hl x Wl, normalised with gamma if
     given) against the n_kv prepared keys of k_prep, v_prep.  fp8: the output
-    is FP8 E4M3 codes (uint8 [B, H, N, D], unit scale) instead of bf16."""
+    is FP8 E4M3 codes (uint8 [B, H, N, D], unit scale) instead of bf16;
+    int8_records: block-INT8 output records (uint8 [B, N, H, 144])."""
     _check_tensor("q", q)
     B, H, N, D = q.shape
     nbytes = sol_prepared_kv_bytes(B, H, n_kv, D)
     _check_prepared("k_prep", k_prep, nbytes, q.device)
     _check_prepared("v_prep", v_prep, nbytes, q.device)
-    if fp8:
-        if out is None:
-            out = torch.empty(q.shape, dtype=torch.uint8, device=q.device)
-        if (out.dtype != torch.uint8 or tuple(out.shape) != tuple(q.shape) or not out.is_contiguous()
-                or out.device != q.device):
-            raise ValueError("an E4M3 out must be a contiguous uint8 tensor of q's shape and device")
-    else:
-        if out is None:
-            out = torch.empty_like(q)
-        _check_tensor("out", out, q.shape)
+    out, fmt = _out_tensor(out, B, H, N, q.device, fp8, int8_records)
     check(sol_attn_fwd_prepared_ex(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                                    ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                                    B, H, N, n_kv, D, T, Hl, Wl, _table_ptr(table, q.device),
-                                   _gamma_ptr(gamma, q.device), float(eps),
-                                   SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16, _stream(q)))
+                                   _gamma_ptr(gamma, q.device), float(eps), fmt, _stream(q)))
     return out
 
 
@@ -483,7 +495,7 @@ def sparse_routing(workspace, B, H, N):
 
 
 def attn_fwd_sparse(q, k_prep, v_prep, T, Hl, Wl, table, workspace, gamma=None, eps=1e-6, out=None,
-                    fp8=False):
+                    fp8=False, int8_records=False):
     """Block-sparse attention under the routing held by the workspace."""
     _check_tensor("q", q)
     B, H, N, D = q.shape
@@ -491,22 +503,12 @@ def attn_fwd_sparse(q, k_prep, v_prep, T, Hl, Wl, table, workspace, gamma=None, 
     _check_prepared("k_prep", k_prep, nbytes, q.device)
     _check_prepared("v_prep", v_prep, nbytes, q.device)
     _check_workspace(workspace, sol_sparse_workspace_bytes(B, H, N, D), q.device)
-    if fp8:
-        if out is None:
-            out = torch.empty(q.shape, dtype=torch.uint8, device=q.device)
-        if (out.dtype != torch.uint8 or tuple(out.shape) != tuple(q.shape) or not out.is_contiguous()
-                or out.device != q.device):
-            raise ValueError("an E4M3 out must be a contiguous uint8 tensor of q's shape and device")
-    else:
-        if out is None:
-            out = torch.empty_like(q)
-        _check_tensor("out", out, q.shape)
+    out, fmt = _out_tensor(out, B, H, N, q.device, fp8, int8_records)
     check(sol_attn_fwd_sparse(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                               ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H,
                               N, D, T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(gamma, q.device),
                               float(eps), ctypes.c_void_p(workspace.data_ptr()),
-                              workspace.numel() * workspace.element_size(),
-                              SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16, _stream(q)))
+                              workspace.numel() * workspace.element_size(), fmt, _stream(q)))
     return out
 
 
@@ -569,26 +571,20 @@ def prepare_kv_records(rec, k_prep, v_prep, key0=0, n_kv=None):
     return k_prep, v_prep
 
 
-def attn_fwd_records(rec, k_prep, v_prep, n_kv=None, out=None, fp8=False):
+def attn_fwd_records(rec, k_prep, v_prep, n_kv=None, out=None, fp8=False, int8_records=False):
     """The queries of records [B, N, H, 400] against n_kv prepared keys; out
-    bf16 [B, H, N, D] (or E4M3 codes, uint8, with fp8)."""
+    bf16 [B, H, N, D] (E4M3 codes with fp8, block-INT8 output records
+    [B, N, H, 144] with int8_records)."""
     B, N, H = rec.shape[:3]
     _check_records(rec, B, H, N, rec.device)
     n_kv = N if n_kv is None else n_kv
     nbytes = sol_prepared_kv_bytes(B, H, n_kv, HEAD_DIM)
     _check_prepared("k_prep", k_prep, nbytes, rec.device)
     _check_prepared("v_prep", v_prep, nbytes, rec.device)
-    shape = (B, H, N, HEAD_DIM)
-    if out is None:
-        out = torch.empty(shape, dtype=torch.uint8 if fp8 else torch.bfloat16, device=rec.device)
-    if (out.dtype != (torch.uint8 if fp8 else torch.bfloat16) or tuple(out.shape) != shape
-            or not out.is_contiguous() or out.device != rec.device):
-        raise ValueError("out must be a contiguous %s tensor of shape %s on %s"
-                         % ("uint8" if fp8 else "bfloat16", shape, rec.device))
+    out, fmt = _out_tensor(out, B, H, N, rec.device, fp8, int8_records)
     check(sol_attn_fwd_records(ctypes.c_void_p(rec.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                                ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
-                               B, H, N, n_kv, HEAD_DIM, SOL_OUT_FP8_E4M3 if fp8 else SOL_OUT_BF16,
-                               _stream(rec)))
+                               B, H, N, n_kv, HEAD_DIM, fmt, _stream(rec)))
     return out
 
 

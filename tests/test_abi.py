@@ -184,10 +184,11 @@ def test_prepare_kv_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     (dict(eps=float("inf")), -1, "eps"),
     (dict(out=P(0x1000000 + 256)), -1, "overlaps"),   # out inside k_prep of 1000 keys
     (dict(D=64), -2, "head dim"),
-    (dict(fmt=2), -1, "out_format"),
+    (dict(fmt=3), -1, "out_format"),
     (dict(fmt=-1), -1, "out_format"),
     (dict(out=P(0x100000 - 49152)), -1, "overlaps"),   # 96 KB of bf16 out would reach q
     (dict(out=P(0x100000 - 49152 + 16), fmt=1), -1, "overlaps"),  # 48 KB of E4M3 out reaches q
+    (dict(out=P(0x100000 - 55296 + 16), fmt=2), -1, "overlaps"),  # 54 KB of records reach q
 ])
 def test_attn_fwd_prepared_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     args = dict(q=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=192, n_kv=1000,
@@ -343,7 +344,7 @@ def test_prepare_kv_records_rejects_before_any_hip_call(L, kw, status, fragment)
 @pytest.mark.parametrize("kw,status,fragment", [
     (dict(out=None), -1, "NULL"),
     (dict(n_kv=0), -1, "n_kv"),
-    (dict(fmt=2), -1, "out_format"),
+    (dict(fmt=3), -1, "out_format"),
     (dict(out=P(0x100000 + 2048)), -1, "overlaps"),    # out over the records
     (dict(out=P(0x1000000 + 256)), -1, "overlaps"),    # out inside k_prep
     (dict(D=64), -2, "head dim"),
