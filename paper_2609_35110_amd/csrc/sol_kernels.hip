@@ -622,9 +622,11 @@ static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's
 
 // kOutRec: block-INT8 output records (out_format 2).  A template flag, not a
 // run-time branch: compiled into the bf16 / E4M3 instances, the unused
-// record epilogue changed the second pass's register allocation and the
-// compiler then produced wrong results for the first row block of each wave
-// (scores climbing 24 binades); the instances without it compile as before.
+// record epilogue changed the second pass's register allocation and spills,
+// and that second pass then returned wrong rows for the first row block of
+// each wave on scores climbing 24 binades (cause not found: the generated-code
+// checks pass on it); the instances without the flag compile exactly as
+// before.
 template <bool kRope, bool kRobust, bool kSparse, bool kRec, bool kOutRec>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
