@@ -39,6 +39,7 @@
 #define SOL_H
 
 #include <stddef.h>
+#include <stdint.h>
 
 #ifdef __cplusplus
 extern "C" {
@@ -311,6 +312,17 @@ int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int 
  * large enough), code = x / s rounded to nearest, ties to even, clamped to
  * [-127, 127].  Finite inputs.  rec must not overlap q, k or v.
  *
+ * sol_qkv_encode_strided: the same, with q, k and v read where they lie
+ * (Sec. 3.2: the stride-aware pack kernels read Q, K and V through their
+ * existing strides, e.g. from packed QKV storage, and write the exchange
+ * buffer in one pass): row (b, h, n) of each tensor starts at element
+ * b stride_b + h stride_h + n stride_n of its pointer, its D values
+ * contiguous.  Strides are non-negative multiples of 8 elements (rows stay
+ * 16-byte aligned); a packed [B][N][3][H][D] buffer X is q = X, k = X + H D,
+ * v = X + 2 H D with stride_b = 3 N H D, stride_h = D, stride_n = 3 H D.
+ * sol_qkv_encode is this call with stride_b = H N D, stride_h = N D,
+ * stride_n = D.  rec must not overlap the span of q, k or v.
+ *
  * sol_qkv_decode: rec -> q, k, v ([B][H][N][D] bf16, element values as
  * above).  The outputs must not overlap rec or each other.
  *
@@ -336,6 +348,11 @@ int sol_qkv_encode(const void* q, const void* k, const void* v, void* rec, int B
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                    const float* q_gamma_dev, const float* k_gamma_dev, float eps,
                    sol_stream_t stream);
+int sol_qkv_encode_strided(const void* q, const void* k, const void* v, int64_t stride_b,
+                           int64_t stride_h, int64_t stride_n, void* rec, int B, int H, int N, int D,
+                           int T, int Hl, int Wl, const float* rope_tab_dev,
+                           const float* q_gamma_dev, const float* k_gamma_dev, float eps,
+                           sol_stream_t stream);
 int sol_qkv_decode(const void* rec, void* q, void* k, void* v, int B, int H, int N, int D,
                    sol_stream_t stream);
 int sol_prepare_kv_records(const void* rec, void* k_prep, void* v_prep, int B, int H, int N,

@@ -371,9 +371,23 @@ int sol_qkv_encode(const void* q, const void* k, const void* v, void* rec, int B
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                    const float* q_gamma_dev, const float* k_gamma_dev, float eps,
                    sol_stream_t stream) {
+  return sol_qkv_encode_strided(q, k, v, (int64_t)H * N * D, (int64_t)N * D, D, rec, B, H, N, D, T, Hl,
+                                Wl, rope_tab_dev, q_gamma_dev, k_gamma_dev, eps, stream);
+}
+
+int sol_qkv_encode_strided(const void* q, const void* k, const void* v, int64_t stride_b,
+                           int64_t stride_h, int64_t stride_n, void* rec, int B, int H, int N, int D,
+                           int T, int Hl, int Wl, const float* rope_tab_dev,
+                           const float* q_gamma_dev, const float* k_gamma_dev, float eps,
+                           sol_stream_t stream) {
   if (!q || !k || !v || !rec) return fail(SOL_ERR_INVALID_ARG, "q, k, v, rec must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if (stride_b < 0 || stride_h < 0 || stride_n < 0 || stride_b % 8 || stride_h % 8 || stride_n % 8)
+    return fail(SOL_ERR_INVALID_ARG, "strides must be non-negative multiples of 8 elements");
+  // the extent each tensor spans: its last row's offset plus one row
+  const int64_t span = ((int64_t)(B - 1) * stride_b + (int64_t)(H - 1) * stride_h +
+                        (int64_t)(N - 1) * stride_n + D) * 2;
   const size_t rbytes = sol_qkv_record_bytes(B, H, N);
   if (rbytes == 0) return fail(SOL_ERR_UNSUPPORTED, "too many records");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(rec))
@@ -381,15 +395,14 @@ int sol_qkv_encode(const void* q, const void* k, const void* v, void* rec, int B
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   if ((st = check_norm(q_gamma_dev, eps)) != SOL_OK || (st = check_norm(k_gamma_dev, eps)) != SOL_OK)
     return st;
-  const size_t bytes = (size_t)B * H * N * D * 2;
-  if (overlaps(rec, rbytes, q, bytes) || overlaps(rec, rbytes, k, bytes) || overlaps(rec, rbytes, v, bytes))
+  if (overlaps(rec, rbytes, q, span) || overlaps(rec, rbytes, k, span) || overlaps(rec, rbytes, v, span))
     return fail(SOL_ERR_INVALID_ARG, "rec overlaps q, k or v");
   const int64_t nv = (int64_t)T * Hl * Wl;
   const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
   hipError_t e = sol::launch_qkv_encode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                                         static_cast<const uint16_t*>(v), static_cast<uint8_t*>(rec), B, H,
                                         sol::make_grid(N, T, Hl, Wl), tab, q_gamma_dev, k_gamma_dev, eps,
-                                        reinterpret_cast<hipStream_t>(stream));
+                                        stride_b, stride_h, stride_n, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "qkv_encode launch: %s", hipGetErrorString(e));
   return ok();
 }

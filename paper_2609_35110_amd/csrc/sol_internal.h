@@ -64,10 +64,12 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
 // rotated with grid g first when tab != nullptr), the standalone decoder
 // (bf16 [B][H][N][D] out), and the prepare pass reading k and v from records
 // into keys key0 .. key0 + N - 1 of a prepared sequence of n_kv keys.
+// The encoder reads row (b, h, n) of q, k and v at element offset
+// b sb + h sh + n sn (multiples of 8), its D values contiguous.
 hipError_t launch_qkv_encode(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint8_t* rec,
                              int B, int H, const SeqGrid& g, const float2* tab,
                              const float* q_gamma, const float* k_gamma, float eps,
-                             hipStream_t stream);
+                             int64_t sb, int64_t sh, int64_t sn, hipStream_t stream);
 hipError_t launch_qkv_decode(const uint8_t* rec, uint16_t* q, uint16_t* k, uint16_t* v, int B, int H,
                              int N, hipStream_t stream);
 hipError_t launch_prepare_kv_records(const uint8_t* rec, uint16_t* k_prep, uint16_t* v_prep,

@@ -39,11 +39,15 @@ __device__ __forceinline__ float chunk_amax(uint4 y) {
 // p = (t / 16) % 3 (q, k, v), chunk cc = t % 16.  A part's 16 chunks sit in
 // 16 aligned lanes of one wave (48 and 64 are multiples of 16), as the row
 // sums of the normalisation need; a scale group is 4 aligned lanes.
+// Rows are read through element strides (sb, sh, sn) shared by q, k and v,
+// so a packed QKV buffer (e.g. [B][N][3][H][D]) is encoded where it lies, as
+// the paper's stride-aware pack kernels do; each row's D values contiguous.
 template <bool kRope>
 __global__ __launch_bounds__(kRecThreads) void qkv_encode_kernel(
     const uint4* __restrict__ q, const uint4* __restrict__ k, const uint4* __restrict__ v,
     uint8_t* __restrict__ rec, int64_t n_rec, int H, SeqGrid g, const float2* __restrict__ tab,
-    const float* __restrict__ q_gamma, const float* __restrict__ k_gamma, float eps) {
+    const float* __restrict__ q_gamma, const float* __restrict__ k_gamma, float eps,
+    int64_t sb, int64_t sh, int64_t sn) {
   __shared__ uint8_t scales[kRecPerWg][12];
   const int t = threadIdx.x;
   const int j = t / 48, p = (t / 16) % 3, cc = t & 15;
@@ -54,9 +58,9 @@ __global__ __launch_bounds__(kRecThreads) void qkv_encode_kernel(
     const int h = (int)(ri - bn * H);
     const int64_t b = bn / N;
     const int n = (int)(bn - b * N);
-    const size_t row = ((size_t)b * H + h) * N + n;
+    const int64_t row = b * sb + h * sh + n * sn;  // in elements, a multiple of 8
     const uint4* src = p == 0 ? q : (p == 1 ? k : v);
-    const uint4 x = src[row * kChunks + cc];
+    const uint4 x = src[row / 8 + cc];
     uint4 y = x;
     if (p < 2) {
       const float* gamma = p == 0 ? q_gamma : k_gamma;
@@ -108,7 +112,7 @@ __global__ __launch_bounds__(kRecThreads) void qkv_decode_kernel(
 hipError_t launch_qkv_encode(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint8_t* rec,
                              int B, int H, const SeqGrid& g, const float2* tab,
                              const float* q_gamma, const float* k_gamma, float eps,
-                             hipStream_t stream) {
+                             int64_t sb, int64_t sh, int64_t sn, hipStream_t stream) {
   const int64_t n_rec = (int64_t)B * g.n * H;
   const dim3 grid((unsigned)((n_rec + kRecPerWg - 1) / kRecPerWg));
   const uint4* q4 = reinterpret_cast<const uint4*>(q);
@@ -116,10 +120,10 @@ hipError_t launch_qkv_encode(const uint16_t* q, const uint16_t* k, const uint16_
   const uint4* v4 = reinterpret_cast<const uint4*>(v);
   if (tab != nullptr)
     hipLaunchKernelGGL(qkv_encode_kernel<true>, grid, dim3(kRecThreads), 0, stream, q4, k4, v4, rec,
-                       n_rec, H, g, tab, q_gamma, k_gamma, eps);
+                       n_rec, H, g, tab, q_gamma, k_gamma, eps, sb, sh, sn);
   else
     hipLaunchKernelGGL(qkv_encode_kernel<false>, grid, dim3(kRecThreads), 0, stream, q4, k4, v4, rec,
-                       n_rec, H, g, tab, q_gamma, k_gamma, eps);
+                       n_rec, H, g, tab, q_gamma, k_gamma, eps, sb, sh, sn);
   return hipGetLastError();
 }
 

@@ -84,6 +84,10 @@ def lib():
         L.sol_qkv_record_bytes.restype = sz
         L.sol_qkv_encode.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, P, f32, P]
         L.sol_qkv_encode.restype = i32
+        i64 = ctypes.c_int64
+        L.sol_qkv_encode_strided.argtypes = [P, P, P, i64, i64, i64, P, i32, i32, i32, i32, i32, i32,
+                                             i32, P, P, P, f32, P]
+        L.sol_qkv_encode_strided.restype = i32
         L.sol_qkv_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, P]
         L.sol_qkv_decode.restype = i32
         L.sol_prepare_kv_records.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, P]
@@ -180,6 +184,12 @@ def sol_qkv_record_bytes(B, H, N):
 def sol_qkv_encode(q, k, v, rec, B, H, N, D, T, Hl, Wl, rope_tab, q_gamma, k_gamma, eps, stream):
     return lib().sol_qkv_encode(q, k, v, rec, B, H, N, D, T, Hl, Wl, rope_tab, q_gamma, k_gamma, eps,
                                 stream)
+
+
+def sol_qkv_encode_strided(q, k, v, stride_b, stride_h, stride_n, rec, B, H, N, D, T, Hl, Wl,
+                           rope_tab, q_gamma, k_gamma, eps, stream):
+    return lib().sol_qkv_encode_strided(q, k, v, stride_b, stride_h, stride_n, rec, B, H, N, D, T, Hl,
+                                        Wl, rope_tab, q_gamma, k_gamma, eps, stream)
 
 
 def sol_qkv_decode(rec, q, k, v, B, H, N, D, stream):
@@ -541,6 +551,26 @@ def qkv_encode(q, k, v, T=0, Hl=0, Wl=0, table=None, q_gamma=None, k_gamma=None,
                          ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(rec.data_ptr()), B, H, N, D,
                          T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(q_gamma, q.device),
                          _gamma_ptr(k_gamma, q.device), float(eps), _stream(q)))
+    return rec
+
+
+def qkv_encode_packed(qkv, T=0, Hl=0, Wl=0, table=None, q_gamma=None, k_gamma=None, eps=1e-6,
+                      rec=None):
+    """Records of a packed QKV buffer qkv [B, N, 3, H, D] bf16 (as a fused QKV
+    projection writes it), read in place through its strides."""
+    if (not isinstance(qkv, torch.Tensor) or qkv.dtype != torch.bfloat16 or not qkv.is_cuda
+            or qkv.dim() != 5 or qkv.shape[2] != 3 or qkv.shape[4] != HEAD_DIM or not qkv.is_contiguous()):
+        raise ValueError("qkv must be a contiguous bf16 [B, N, 3, H, %d] device tensor" % HEAD_DIM)
+    B, N, _, H, D = qkv.shape
+    if rec is None:
+        rec = torch.empty((B, N, H, QKV_RECORD_BYTES), dtype=torch.uint8, device=qkv.device)
+    _check_records(rec, B, H, N, qkv.device)
+    base, el = qkv.data_ptr(), qkv.element_size()
+    check(sol_qkv_encode_strided(ctypes.c_void_p(base), ctypes.c_void_p(base + H * D * el),
+                                 ctypes.c_void_p(base + 2 * H * D * el), N * 3 * H * D, D, 3 * H * D,
+                                 ctypes.c_void_p(rec.data_ptr()), B, H, N, D, T, Hl, Wl,
+                                 _table_ptr(table, qkv.device), _gamma_ptr(q_gamma, qkv.device),
+                                 _gamma_ptr(k_gamma, qkv.device), float(eps), _stream(qkv)))
     return rec
 
 

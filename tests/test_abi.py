@@ -305,6 +305,22 @@ def test_qkv_encode_rejects_before_any_hip_call(L, kw, status, fragment):
     assert fragment in sol.sol_last_error()
 
 
+@pytest.mark.parametrize("kw,fragment", [
+    (dict(sb=-8), "strides"),
+    (dict(sh=12), "strides"),
+    (dict(sn=4), "strides"),
+    (dict(rec=P(0x100000 + 3 * 128 * 2 + 16)), "overlaps"),  # inside the packed span of q
+])
+def test_qkv_encode_strided_rejects_before_any_hip_call(L, kw, fragment):
+    # packed [1, 192, 3, 2, 128] at A: q = A, k = A + 256 elements, v = A + 512
+    a = dict(rec=P(0x1000000), sb=192 * 3 * 2 * 128, sh=128, sn=3 * 2 * 128)
+    a.update(kw)
+    st = sol.sol_qkv_encode_strided(A, P(0x100000 + 512), P(0x100000 + 1024), a["sb"], a["sh"], a["sn"],
+                                    a["rec"], 1, 2, 192, 128, 0, 0, 0, None, None, None, 0.0, None)
+    assert st == -1, sol.sol_last_error()
+    assert fragment in sol.sol_last_error()
+
+
 @pytest.mark.parametrize("kw,status,fragment", [
     (dict(rec=None), -1, "NULL"),
     (dict(D=64), -2, "head dim"),

@@ -131,6 +131,21 @@ def test_encode_fused_equals_normalise_rotate_then_encode():
         assert torch.equal(fused, plain)
 
 
+def test_encode_packed_qkv_in_place():
+    """The stride-aware encoder on a packed [B, N, 3, H, D] buffer (read where
+    it lies) writes the records of the contiguous q, k, v, byte for byte, with
+    the rotation and the normalisation fused."""
+    w = W.custom(2, 3, 3, 7, 9, n_text=11, seed_index=1225, qk_norm=True)
+    q, k, v = W.make_inputs(w)
+    gq, gk = W.norm_weights(w)
+    tab = _table(w.T, w.Hl, w.Wl)
+    packed = torch.stack([q, k, v], 2).permute(0, 3, 2, 1, 4).contiguous().to(DEV)  # [B, N, 3, H, D]
+    got = sol.qkv_encode_packed(packed, w.T, w.Hl, w.Wl, tab, gq.to(DEV), gk.to(DEV), EPS)
+    want = sol.qkv_encode(q.to(DEV), k.to(DEV), v.to(DEV), w.T, w.Hl, w.Wl, tab, gq.to(DEV), gk.to(DEV), EPS)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+
+
 def test_encode_with_rotation_close_to_oracle():
     """With the rotation (fp32 table against the oracle's double trig) the
     rotated bf16 values differ in rare last bits, so a few codes may differ:
