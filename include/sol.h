@@ -248,8 +248,7 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
  * entries are meaningful); then pooled queries and keys (fp32).
  * nqb = ceil(N/256), nkb = ceil(N/128).  tau finite.
  * sol_attn_fwd_sparse: the attention under that routing (the workspace as
- * sol_sparse_route left it), bf16 or E4M3 output as sol_attn_fwd_prepared_ex
- * (SOL_OUT_INT8_RECORDS: SOL_ERR_UNSUPPORTED).
+ * sol_sparse_route left it), in any output format of sol_attn_fwd_prepared_ex.
  * The workspace is sol_sparse_workspace_bytes(B, H, N, D) bytes of device
  * memory, 16-byte aligned, not overlapping q, k_prep, v_prep or out.
  * N <= 1,032,192 = 8064 key blocks (SOL_ERR_UNSUPPORTED beyond: the

@@ -312,8 +312,6 @@ int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, v
   if (!aligned16(v_prep) || !aligned16(out)) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must be 16-byte aligned");
   const size_t obytes = out_bytes(B, H, N, D, out_format);
   if (obytes == 0) return fail(SOL_ERR_INVALID_ARG, "unknown out_format %d", out_format);
-  if (out_format == SOL_OUT_INT8_RECORDS)
-    return fail(SOL_ERR_UNSUPPORTED, "block-INT8 output records are not built for the block-sparse walk");
   const size_t bytes = (size_t)B * H * N * D * 2;
   const size_t pbytes = sol_prepared_kv_bytes(B, H, N, D);
   const size_t need = sol_sparse_workspace_bytes(B, H, N, D);

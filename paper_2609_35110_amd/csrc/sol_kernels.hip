@@ -1355,8 +1355,7 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   // First pass, then the second over the row blocks whose probabilities left
   // the fp16 range.
   for (int pass = 0; pass < 2; ++pass) {
-    // queries from records: no rotation, no normalisation, dense; block-INT8
-    // output records: dense (the caller rejects them on the sparse walk)
+    // queries from records: no rotation, no normalisation, dense
     const bool orec = out_format == 2;
     const int sel = (qrec != nullptr ? 8 + pass : (tab != nullptr) * 4 + pass * 2 + sparse) + 10 * orec;
 #define SOL_LAUNCH_PREPARED(R, P, S, Q, O)                                                      \
@@ -1375,12 +1374,15 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
       case 8: SOL_LAUNCH_PREPARED(false, false, false, true, false); break;
       case 9: SOL_LAUNCH_PREPARED(false, true, false, true, false); break;
       case 10: SOL_LAUNCH_PREPARED(false, false, false, false, true); break;
+      case 11: SOL_LAUNCH_PREPARED(false, false, true, false, true); break;
       case 12: SOL_LAUNCH_PREPARED(false, true, false, false, true); break;
+      case 13: SOL_LAUNCH_PREPARED(false, true, true, false, true); break;
       case 14: SOL_LAUNCH_PREPARED(true, false, false, false, true); break;
+      case 15: SOL_LAUNCH_PREPARED(true, false, true, false, true); break;
       case 16: SOL_LAUNCH_PREPARED(true, true, false, false, true); break;
+      case 17: SOL_LAUNCH_PREPARED(true, true, true, false, true); break;
       case 18: SOL_LAUNCH_PREPARED(false, false, false, true, true); break;
-      case 19: SOL_LAUNCH_PREPARED(false, true, false, true, true); break;
-      default: return hipErrorInvalidValue;  // records output on the sparse walk
+      default: SOL_LAUNCH_PREPARED(false, true, false, true, true); break;
     }
 #undef SOL_LAUNCH_PREPARED
     const hipError_t e = hipGetLastError();

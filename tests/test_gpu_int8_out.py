@@ -26,6 +26,8 @@ import oracle
 from paper_2609_35110_amd import sol
 from paper_2609_35110_amd import workloads as W
 
+from parity import sparse_mask
+
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
@@ -154,9 +156,9 @@ def test_int8_records_second_pass():
 
 
 def test_int8_records_from_qkv_records_and_sparse():
-    """The same epilogue behind the records path, against its own bf16 output
-    and the oracle's decoded-records attention; the block-sparse walk rejects
-    the format (not built there)."""
+    """The same epilogue behind the records path and the block-sparse walk,
+    each against its own bf16 output and the oracle (decoded records; the
+    kernel's own routing)."""
     w = W.custom(1, 2, 3, 9, 11, n_text=20, seed_index=1330, shared_dir=1.0)
     q, k, v = W.make_inputs(w)
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
@@ -168,10 +170,17 @@ def test_int8_records_from_qkv_records_and_sparse():
     b1 = sol.attn_fwd_records(qrec, kp, vp)
     kp2, vp2 = sol.prepare_kv(kd, vd, w.T, w.Hl, w.Wl, tab)
     ws = sol.sparse_route(qd, kp2, w.T, w.Hl, w.Wl, tab, 1.0)
-    with pytest.raises(sol.SolError) as e:
-        sol.attn_fwd_sparse(qd, kp2, vp2, w.T, w.Hl, w.Wl, tab, ws, int8_records=True)
-    assert e.value.status == sol.SOL_ERR_UNSUPPORTED
+    r2 = sol.attn_fwd_sparse(qd, kp2, vp2, w.T, w.Hl, w.Wl, tab, ws, int8_records=True)
+    b2 = sol.attn_fwd_sparse(qd, kp2, vp2, w.T, w.Hl, w.Wl, tab, ws)
     torch.cuda.synchronize()
+    rows2 = r2.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, 144)
+    check_against_bf16(rows2, _bits(b2).reshape(-1, 128))
+    mask = sparse_mask(ws, w.B, w.H, w.N)
+    ref2 = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, block_mask=mask,
+                            qblk=sol.SPARSE_QUERY_BLOCK, kblk=sol.SPARSE_KEY_BLOCK)
+    st2 = check_against_oracle(rows2, ref2.reshape(-1, 128), np.arange(w.B * w.H * w.N))
+    _log("int8 records, block-sparse: %s" % st2)
+    assert st2["worst_excess"] <= MIDPOINT_TOL and st2["exact_codes"] >= MIN_EXACT
     rows = r1.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, 144)
     check_against_bf16(rows, _bits(b1).reshape(-1, 128))
     dq, dk, dv = oracle.decode_qkv(oracle.encode_qkv(oracle.rope3d_bf16(_bits(q), w.T, w.Hl, w.Wl),

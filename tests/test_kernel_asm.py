@@ -92,13 +92,13 @@ def first_pass(name):
 
 
 def test_mfma_latency_respected(asm_text):
-    """Every MFMA of the sixteen kernels (rotary or not, first or second pass,
+    """Every MFMA of the twenty kernels (rotary or not, first or second pass,
     dense or block-sparse, queries from bf16 or from records, output records
     or not), inline or not: the compiler's own hazard handling
     is checked too (it once let a spill reload overwrite an accumulator still
     being read)."""
     kernels = functions(asm_text, "attn_prepared_kernel")
-    assert len(kernels) == 16
+    assert len(kernels) == 20
     for name, body in kernels:
         ins = instructions(body)
         n_asm = 0
@@ -143,14 +143,14 @@ def test_mfma_latency_respected(asm_text):
 
 def test_second_pass_has_no_inline_asm_mfma(asm_text):
     kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if not first_pass(f[0])]
-    assert len(kernels) == 8
+    assert len(kernels) == 10
     for name, body in kernels:
         assert not any(in_asm and t.startswith("v_mfma") for t, in_asm in instructions(body)), name
 
 
 def test_m0_used_only_by_tile_copies(asm_text):
     kernels = functions(asm_text, "attn_prepared_kernel")
-    assert len(kernels) == 16
+    assert len(kernels) == 20
     implicit_m0 = ("s_movrel", "v_movrel", "s_sendmsg", "ds_gws", "v_interp", "ds_append", "ds_consume",
                    "ds_ordered", "s_setreg")
     for name, body in kernels:
@@ -175,7 +175,7 @@ def test_first_pass_copy_count_waits_see_only_copies(asm_text):
     vmcnt waits for its own loads, e.g. in the prologue, wait for at least as
     much as they need: the counter retires in order.)"""
     kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if first_pass(f[0])]
-    assert len(kernels) == 8
+    assert len(kernels) == 10
     for name, body in kernels:
         ins = instructions(body)
         assert not any(t.startswith("scratch_") for t, _ in ins), "%s spills" % name
