@@ -229,17 +229,27 @@ __device__ __forceinline__ float ue5m3_value(uint32_t c) {
 // of the exact one; the attention output epilogue quantises its fp32 results
 // with the same division.
 // Smallest code c in 1..0xF7 with 127 value(c) >= amax (0xF7 when none is
-// large enough), by bisection: 127 value(lo) < amax <= 127 value(hi).
+// large enough).  The candidate is the code at or just above t = amax / 127
+// read off t's fp32 bits (exponent and top three mantissa bits, rounded up);
+// t's two roundings move it by under 2^-22 of itself while neighbouring codes
+// differ by at least 1/16 (2^-17 absolute among the subnormal codes), so the
+// candidate is the answer or one code off, and one exact comparison each way
+// settles it.
 __device__ __forceinline__ uint32_t ue5m3_scale_for(float amax) {
-  uint32_t lo = 0, hi = 0xF7;
-  if (!(127.0f * ue5m3_value(hi) >= amax)) return hi;
-#pragma unroll 1
-  while (hi - lo > 1) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (127.0f * ue5m3_value(mid) >= amax) hi = mid;
-    else lo = mid;
+  const float t = amax * (1.0f / 127.0f);
+  uint32_t c;
+  if (!(t < 61440.0f)) {
+    c = 0xF7u;
+  } else if (t < 0x1p-14f) {
+    c = (uint32_t)__builtin_ceilf(t * 0x1p17f);  // subnormal codes: m 2^-17, m = 0..8
+  } else {
+    const uint32_t u = __float_as_uint(t);
+    c = (u >> 20) - (112u << 3) + ((u & 0xFFFFFu) != 0u);  // (e + 15) << 3 | m, rounded up
   }
-  return hi;
+  c = c < 1u ? 1u : (c > 0xF7u ? 0xF7u : c);
+  if (c > 1u && 127.0f * ue5m3_value(c - 1u) >= amax) --c;
+  else if (c < 0xF7u && 127.0f * ue5m3_value(c) < amax) ++c;
+  return c;
 }
 // One value's int8 code at scale s, as the low byte of the result.
 __device__ __forceinline__ uint32_t int8_code(float x, float s) {

@@ -6,7 +6,7 @@
 // tensors back (for consumers other than this library's attention, which
 // decodes records in its own tile loads).  Both kernels stream: HBM-bound,
 // 768 bytes read and 400 written per record (encoder), the reverse (decoder).
-// The quantisation rule (scale search, rounding) lives in sol_device.h, shared
+// The quantisation rule (scale choice, rounding) lives in sol_device.h, shared
 // with the attention kernel's block-INT8 output epilogue.
 #include "sol_device.h"
 

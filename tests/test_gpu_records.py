@@ -48,11 +48,14 @@ def _table(T, Hl, Wl):
 
 
 def _spread(x, seed):
-    """Rows scaled by 2^e, e in [-12, 12] (exact), and a few all-zero rows and
-    32-value groups: inputs whose groups span many scale codes."""
+    """Rows scaled by 2^e, e in [-12, 12] (exact), a few all-zero rows and
+    32-value groups, and rows scaled by 2^23, too large for any scale code:
+    inputs whose groups span every kind of scale (subnormal, normal,
+    saturated)."""
     gen = torch.Generator().manual_seed(seed)
     B, H, N, D = x.shape
     e = torch.randint(-12, 13, (B, H, N, 1), generator=gen).to(torch.float32)
+    e[:, :, 3::11] = 23
     y = (x.to(torch.float32) * torch.exp2(e)).to(torch.bfloat16)
     y[:, :, ::7] = 0
     y[:, :, 1::5, 32:64] = 0
