@@ -223,11 +223,8 @@ __device__ __forceinline__ float ue5m3_value(uint32_t c) {
 // scale s = the smallest finite positive UE5M3 value with 127 s >= max |x|,
 // so no code passes +-127; code = x / s rounded to nearest, ties to even.
 // 127 s is exact in fp32 (a 4-bit significand times 127), so the scale is
-// the exact one.  For bf16 x (8 significant bits) x / s lies on a
-// half-integer or at least 2^-8 / 15 away from one, far beyond the fp32
-// division's rounding error, so the correctly rounded quotient gives the code
-// of the exact one; the attention output epilogue quantises its fp32 results
-// with the same division.
+// the exact one, and int8_code rounds the exact quotient x / s, for bf16
+// inputs (the QKV records) and fp32 ones (the output epilogue) alike.
 // Smallest code c in 1..0xF7 with 127 value(c) >= amax (0xF7 when none is
 // large enough).  The candidate is the code at or just above t = amax / 127
 // read off t's fp32 bits (exponent and top three mantissa bits, rounded up);
@@ -251,9 +248,17 @@ __device__ __forceinline__ uint32_t ue5m3_scale_for(float amax) {
   else if (c < 0xF7u && 127.0f * ue5m3_value(c) < amax) ++c;
   return c;
 }
-// One value's int8 code at scale s, as the low byte of the result.
+// One value's int8 code at scale s, as the low byte of the result: x / s
+// rounded to nearest, ties to even, exactly.  r = rint(x rcp(s)) is the
+// answer or one off (the hardware reciprocal's error moves the quotient by
+// under 2^-15 here); the residual x - r s is exact (r s lies within a factor
+// two of x unless r = 0), so comparing it with s / 2 settles the rounding.
 __device__ __forceinline__ uint32_t int8_code(float x, float s) {
-  return (uint32_t)(int)fminf(fmaxf(__builtin_rintf(x / s), -127.0f), 127.0f) & 0xFFu;
+  float r = __builtin_rintf(x * __builtin_amdgcn_rcpf(s));
+  const float e = __builtin_fmaf(-r, s, x);
+  const float h = 0.5f * s, ae = __builtin_fabsf(e);
+  if (ae > h || (ae == h && ((int)r & 1) != 0)) r += e > 0.0f ? 1.0f : -1.0f;
+  return (uint32_t)(int)fminf(fmaxf(r, -127.0f), 127.0f) & 0xFFu;
 }
 
 // Eight int8 codes (one 8-byte word of a record) times their scale, to bf16
