@@ -146,7 +146,8 @@ def main():
                     help="block-INT8 QKV records (the quantized exchange format): the step is "
                          "sol_qkv_encode (normalise, rotate, quantise) + sol_prepare_kv_records + "
                          "sol_attn_fwd_records (q decoded in the tile load)")
-    ap.add_argument("--cpu-rows-per-thread", type=int, default=1024)
+    ap.add_argument("--cpu-rows-per-thread", type=int, default=1536,
+                    help="oracle rows per host thread for the CPU baseline (p720: about 14 s on 16 cores)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times), the "
