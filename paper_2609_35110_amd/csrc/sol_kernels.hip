@@ -551,21 +551,17 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
 // then the workgroup barrier -- after which every wave's completed copies are
 // visible.  No LDS read needs to complete first: the next iteration's copies
 // overwrite tiles whose fragments every wave read (and waited for) at least
-// one iteration earlier.  The count of four holds only where the compiler
-// issues no memory instruction of its own in the loop (the first pass: a
-// build test checks it); the second pass, whose spill code does, waits for
-// every copy (kAll).
+// one iteration earlier.  The count of four holds only because the compiler
+// issues no memory instruction of its own in the loop (no loads, stores or
+// spills: a build test checks the generated code).
 // kInflight: iterations whose copies may still be in flight (the dense walk
 // 1; the block-sparse walk, whose scattered tiles miss L2 more often, 2: its
 // copies are issued one iteration earlier).
-template <bool kAll, int kInflight>
+template <int kInflight>
 __device__ __forceinline__ void dma_barrier() {
   static_assert(kInflight >= 1 && kInflight <= 3, "vmcnt holds at most 15 here");
   asm volatile("" ::: "memory");
-  if (kAll)
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt 0, expcnt 7, lgkmcnt 15
-  else
-    __builtin_amdgcn_s_waitcnt(0x0F70 | (4 * kInflight));  // vmcnt 4 kInflight, no LDS wait
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (4 * kInflight));  // vmcnt 4 kInflight, no LDS wait
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -620,14 +616,16 @@ constexpr int kBufferDword3 = 0x00020000;
 // N and its walk position is known.
 static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's rows");
 
-// kOutRec: block-INT8 output records (out_format 2).  A template flag, not a
-// run-time branch: compiled into the bf16 / E4M3 instances, the unused
-// record epilogue changed the second pass's register allocation and spills,
-// and that second pass then returned wrong rows for the first row block of
-// each wave on scores climbing 24 binades (cause not found: the generated-code
-// checks pass on it); the instances without the flag compile exactly as
-// before.
-template <bool kRope, bool kRobust, bool kSparse, bool kRec, bool kOutRec>
+// kOutRec: block-INT8 output records (out_format 2), a template flag so that
+// the bf16 and E4M3 instances do not carry the record epilogue's registers.
+//
+// One launch, one pass: each row's reference max m starts at the largest
+// score of the walk's first key tile and of the rows' diagonal tile, and a
+// tile whose probabilities would leave the fp16 range against it (a score
+// more than 15 above m) raises m in place -- the tile's scores are
+// recomputed, the accumulated O and l rescaled -- before its probabilities
+// are used.  Exact softmax whatever the score distribution.
+template <bool kRope, bool kSparse, bool kRec, bool kOutRec>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
@@ -649,14 +647,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVB * kPrepTileElems];
   __shared__ uint32_t blist[kSparse ? kMaxSparseBlocks : 1];  // entry e | entry e + 1 << 16
 
-  // pin() in the first pass only.  The second pass spills, and with the empty
-  // asm statements in place the compiler put a spill reload of an MFMA's
-  // accumulator registers inside that MFMA's latency (seen in the generated
-  // code: the second pass then got whole query blocks wrong); without them its
-  // hazard handling is complete.  A build test checks every MFMA.
-  auto keep = [&](auto& x) __attribute__((always_inline)) {
-    if (!kRobust) pin(x);
-  };
+  auto keep = [&](auto& x) __attribute__((always_inline)) { pin(x); };
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -732,21 +723,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     if (!kSparse) return t * BN2;
     return (t >> 2) == last_pos ? (4 * last_blk + (t & 3)) * BN2 : 0;
   };
-  if (kRobust) {
-    // Second pass: only the row blocks the first pass marked (NaN rows) are
-    // recomputed; every other workgroup leaves at once.
-    bool marked = false;
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int row = qrow_first + 32 * qb;
-      if (hh == 0 && row < Nq)
-        marked |= out_rec   ? outrec_slab[row * outrec_stride + 128] == 0xFF
-                  : out_fp8 ? (out8_slab[(size_t)row * D] & 0x7F) == 0x7F
-                            : (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
-    }
-    if (!__syncthreads_or(marked)) return;
-  }
-
   // ---- Q' fragments of the wave's two 32-row blocks, normalised (q_gamma)
   // and rotated in the load.  A lane holds the even (hh = 0) or odd chunks of
   // its row; the sum of squares pairs them across the lane halves first, then
@@ -846,7 +822,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   float m_ref[2];   // reference max of each query row (units of c q.k)
   f32x16 bias[2];   // -m_ref, the first addend of every score chain
   float l_run[2] = {0.0f, 0.0f};
-  float ovf = 0.0f;  // first pass: largest per-lane tile sum (above 2^15: rows marked)
 
   // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of the tile;
   // the tile's first key is kv0.
@@ -871,6 +846,37 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     for (int j = 2; j < 16; j += 2) mx = fmaxf(fmaxf(mx, s[j]), s[j + 1]);
     return fmaxf(mx, __shfl_xor(mx, 32));
   };
+  // Raise the reference max of query block qb to the largest score of tile
+  // s (scores held against the current m, keys past N at -inf) where that
+  // is larger: O and l are rescaled, s (and s_next, the block's scores of the
+  // next tile when they exist) move to the new m, and the tile's fp16 words
+  // and their sum are redone.  Exact: numerator and denominator keep one
+  // reference.
+  auto raise_max = [&](int qb, f32x16& s, f32x16* s_next, uint32_t* words, float& lsum)
+      __attribute__((always_inline)) {
+    const float delta = fmaxf(tile_max(s), 0.0f);
+    const float alpha = __builtin_amdgcn_exp2f(-delta);
+    m_ref[qb] += delta;
+    l_run[qb] *= alpha;
+#pragma unroll
+    for (int db = 0; db < 4; ++db) o[qb][db] *= alpha;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      s[j] -= delta;
+      if (s_next) (*s_next)[j] -= delta;
+      bias[qb][j] -= delta;
+    }
+    float la = 0.0f, lb = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const float ea = __builtin_amdgcn_exp2f(s[2 * w]);
+      const float eb = __builtin_amdgcn_exp2f(s[2 * w + 1]);
+      words[w] = pack_f16x2(ea, eb);
+      la += ea;
+      lb += eb;
+    }
+    lsum = la + lb;
+  };
   // Fragment registers, a whole tile ahead: kr[kk] holds fragment kk of the K
   // tile being multiplied (then of the next one), vr[j] fragment j of the V
   // tile (then of the next one).
@@ -887,7 +893,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
                        float& l0_cur, float& l0_next) __attribute__((always_inline)) {
     // K tile t sits in buffer t % 8 from its copy (iteration t - kKAhead, or
     // the prologue) until the copy of tile t + 8 overwrites it, and is read in
-    // iteration t-2 (and by the second pass's rare path in iteration t); V
+    // iteration t-2 (and by the rare path below in iteration t); V
     // tile t sits in buffer t % kVB from its copy (iteration t - kVAhead) until
     // tile t + kVB's, and is read in iteration t-1.  Every overwrite comes at
     // least two barriers after the last wave consumed the reads of the tile
@@ -905,11 +911,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     for (int j = 0; j < 8; ++j) {
       // slot 1: S MFMA of block 0; exponential of register 2j; pack of
       // word j-1.
-      if (kRobust) {
-        // The second pass spills; only MFMAs the compiler sees are safe next
-        // to its spill code.
-        ns[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j], qf[0][j], j == 0 ? bias[0] : ns[0], 0, 0, 0);
-      } else if (j == 0) {
+      if (j == 0) {
         mfma_s_first(ns[0], kr[0], qf[0][0], bias[0]);
       } else {
         mfma_s_next(ns[0], kr[j], qf[0][j]);
@@ -924,9 +926,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       __builtin_amdgcn_sched_barrier(0);
       // slot 2: S MFMA of block 1; fragment kk = j of K(i+2) into the register
       // just used; exponential of register 2j + 1; a step of the word-sum tree.
-      if (kRobust) {
-        ns[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j], qf[1][j], j == 0 ? bias[1] : ns[1], 0, 0, 0);
-      } else if (j == 0) {
+      if (j == 0) {
         mfma_s_first(ns[1], kr[0], qf[1][0], bias[1]);
       } else {
         mfma_s_next(ns[1], kr[j], qf[1][j]);
@@ -945,58 +945,18 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
     p1[7] = pack_f16x2(pa, pb);
     l1 = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p1[6], p1[7]))));
-    {
-      const float s0 = l0_cur, s1 = l1;
-      if (!kRobust) ovf = fmaxf(ovf, fmaxf(s0, s1));
-      if (kRobust && __any(fmaxf(s0, s1) > kP16SumLimit)) {
-        // Rare: a score of tile i exceeds m by more than 15.  Per query block:
-        // S(i) again from K(i) (its buffer is not reused for four iterations),
-        // m raised to its max where it exceeds m, O and l rescaled, the next
-        // tile's scores moved to the new m, and the words of P(i) redone.
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          mfma_wait();  // ns was just written by the score MFMAs
-          f32x16 t = bias[qb];
-#pragma unroll
-          for (int kk = 0; kk < 8; ++kk)
-            t = __builtin_amdgcn_mfma_f32_32x32x16_f16(kfrag(i, kk), qf[qb][kk], t, 0, 0, 0);
-          const int kv0 = mask_kv0(i);
-          if (kv0 + BN2 > N) mask_block(kv0, t);
-          const float delta = fmaxf(tile_max(t), 0.0f);
-          const float alpha = __builtin_amdgcn_exp2f(-delta);
-          m_ref[qb] += delta;
-          l_run[qb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < 4; ++db) o[qb][db] *= alpha;
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            ns[qb][j] -= delta;
-            bias[qb][j] = -m_ref[qb];
-          }
-          float la = 0.0f, lb = 0.0f;
-#pragma unroll
-          for (int w = 0; w < 8; ++w) {
-            const float ea = __builtin_amdgcn_exp2f(t[2 * w] - delta);
-            const float eb = __builtin_amdgcn_exp2f(t[2 * w + 1] - delta);
-            f16x2 h;
-            h[0] = (_Float16)ea;
-            h[1] = (_Float16)eb;
-            if (qb == 0) p0_cur[w] = __builtin_bit_cast(uint32_t, h);
-            else p1[w] = __builtin_bit_cast(uint32_t, h);
-            la += ea;
-            lb += eb;
-          }
-          if (qb == 0) l0_cur = la + lb;
-          else l1 = la + lb;
-          mfma_wait();
-        }
-      }
-      l_run[0] += l0_cur;
-      l_run[1] += l1;
-      keep(l_run[0]);
-      keep(l_run[1]);
-      if (!kRobust) keep(ovf);
+    // Rare: a score of this block's tile exceeds m by more than 15, so its
+    // fp16 words (or their sums) overflowed: raise m while S(i) is still in
+    // registers (S(i+1) of the block, just computed against the old m, moves
+    // with it).
+    if (__builtin_expect(__any(l1 > kP16SumLimit), 0)) {
+      mfma_wait();  // the inline score MFMAs of S(i+1) have landed
+      raise_max(1, cs[1], &ns[1], p1, l1);
     }
+    l_run[0] += l0_cur;
+    l_run[1] += l1;
+    keep(l_run[0]);
+    keep(l_run[1]);
     // The tail above runs in the shadow of the last score MFMAs and counts
     // toward their latency (pinned here: the compiler would otherwise sink it
     // past the branch below).
@@ -1017,7 +977,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // otherwise reuse their registers while the MFMAs, invisible to it, still
     // write or read them.
     mfma_wait_tail();
-    if (!kRobust) asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
+    asm volatile("" ::"v"(ns[0]), "v"(ns[1]), "v"(bias[0]), "v"(bias[1]));
     const int kv_next = mask_kv0(i + 1);  // first key of walk tile i + 1
     if (__builtin_expect(i + 1 < n_kv && kv_next + BN2 > N, 0)) {
       mfma_wait();
@@ -1073,13 +1033,16 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
     p0_next[7] = pack_f16x2(pa, pb);
     l0_next = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p0_next[6], p0_next[7]))));
+    // Block 0's words of P(i+1) are checked here, where S(i+1) is still in
+    // registers (its next scores are computed with the raised m).
+    if (__builtin_expect(__any(l0_next > kP16SumLimit), 0)) raise_max(0, ns[0], nullptr, p0_next, l0_next);
     keep(p0_next[7]);
     keep(l0_next);
     // The copies the next iteration reads must have landed: those issued
     // kKAhead - 2 iterations ago (K) and kVAhead - 1 ago (V) -- so only the
     // copies of this and the kInflight - 1 previous iterations (4 each) may
     // still be in flight.
-    dma_barrier<kRobust, kInflight>();
+    dma_barrier<kInflight>();
   };
 
   // ---- prologue: K(0 .. kKAhead - 2) and V(0 .. kVAhead - 2) in LDS,
@@ -1118,17 +1081,17 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     sa[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[1][kk], sa[1], 0, 0, 0);
   }
   if (mask_kv0(0) + BN2 > N) mask_tile(mask_kv0(0), sa);
-  // The first pass also takes the reference max over each 32-row block's
-  // "diagonal" tile -- the keys at the rows' own positions (offset by n_keys -
-  // Nq, the layout of a cached prefix of keys) -- where a video DiT's local
-  // attention peaks: with the first tile alone, rows whose scores climb 11 or
-  // more binades above it overflow the fp16 word sums and are recomputed by
-  // the slower second pass.  The tile must be one the walk attends (always
-  // in the dense walk; looked up in the list for the sparse one), so the
-  // reference never exceeds the attended maximum.  Fragments are read
-  // straight from the prepared tile in global memory.
+  // The reference max also covers each 32-row block's "diagonal" tile -- the
+  // keys at the rows' own positions (offset by n_keys - Nq, the layout of a
+  // cached prefix of keys) -- where a video DiT's local attention peaks: with
+  // the first tile alone, rows whose scores climb 11 or more binades above it
+  // would overflow the fp16 word sums and take the rare path again and again.
+  // The tile must be one the walk attends (always in the dense walk; looked
+  // up in the list for the sparse one), so the reference never exceeds the
+  // attended maximum.  Fragments are read straight from the prepared tile in
+  // global memory.
   float m_diag[2] = {-__builtin_inff(), -__builtin_inff()};
-  if (!kRobust) {
+  {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const int key = min(max(qt * BM + wave * 64 + 32 * qb + (N - Nq), 0), N - 1);
@@ -1190,10 +1153,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   if (i < n_kv) iteration(i, sa, sb, pA, pB, lA, lB);
 
   // ---- epilogue: out = O / l; register j of block (qb, db) is dim 32db + 8(j/4) + 4hh + j%4.
-  // A first-pass wave whose probabilities left the fp16 range writes its rows
-  // as NaN instead (bf16 0x7FC0, E4M3 0x7F): the second pass recomputes
-  // exactly those.
-  const bool marked = !kRobust && __any(ovf > kP16SumLimit);
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int row = qrow0 + 32 * qb;
@@ -1204,10 +1163,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       // in this lane's 16 registers of block db and its partner lane's (hh ^ 1)
       if (row >= Nq) continue;  // uniform over the lane pair
       uint8_t* dst = outrec_slab + row * outrec_stride;
-      if (marked) {  // scale codes 0xFF (NaN): recomputed by the second pass
-        if (hh == 0) *reinterpret_cast<uint4*>(dst + 128) = make_uint4(0xFFFFFFFFu, 0u, 0u, 0u);
-        continue;
-      }
       uint32_t scales = 0;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
@@ -1232,12 +1187,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     if (out_fp8) {
       if (row >= Nq) continue;
       uint8_t* dst = out8_slab + (size_t)row * D;
-      if (marked) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-          *reinterpret_cast<uint4*>(dst + 64 * hh + 16 * c) = make_uint4(0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu);
-        continue;
-      }
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -1250,12 +1199,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       }
       continue;
     }
-    if (row < Nq && marked) {
-      uint16_t* dst = out_slab + (size_t)row * D;
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        *reinterpret_cast<uint4*>(dst + 64 * hh + 8 * c) = make_uint4(0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u);
-    } else if (row < Nq) {
+    if (row < Nq) {
       uint16_t* dst = out_slab + (size_t)row * D;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
@@ -1352,43 +1296,27 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   const bool sparse = blocks != nullptr;
-  // First pass, then the second over the row blocks whose probabilities left
-  // the fp16 range.
-  for (int pass = 0; pass < 2; ++pass) {
-    // queries from records: no rotation, no normalisation, dense
-    const bool orec = out_format == 2;
-    const int sel = (qrec != nullptr ? 8 + pass : (tab != nullptr) * 4 + pass * 2 + sparse) + 10 * orec;
-#define SOL_LAUNCH_PREPARED(R, P, S, Q, O)                                                      \
-  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S, Q, O>), grid, dim3(256), 0, stream, q,       \
-                     k_prep, v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps,          \
-                     out_format, blocks, counts, nkb, qrec, heads)
-    switch (sel) {
-      case 0: SOL_LAUNCH_PREPARED(false, false, false, false, false); break;
-      case 1: SOL_LAUNCH_PREPARED(false, false, true, false, false); break;
-      case 2: SOL_LAUNCH_PREPARED(false, true, false, false, false); break;
-      case 3: SOL_LAUNCH_PREPARED(false, true, true, false, false); break;
-      case 4: SOL_LAUNCH_PREPARED(true, false, false, false, false); break;
-      case 5: SOL_LAUNCH_PREPARED(true, false, true, false, false); break;
-      case 6: SOL_LAUNCH_PREPARED(true, true, false, false, false); break;
-      case 7: SOL_LAUNCH_PREPARED(true, true, true, false, false); break;
-      case 8: SOL_LAUNCH_PREPARED(false, false, false, true, false); break;
-      case 9: SOL_LAUNCH_PREPARED(false, true, false, true, false); break;
-      case 10: SOL_LAUNCH_PREPARED(false, false, false, false, true); break;
-      case 11: SOL_LAUNCH_PREPARED(false, false, true, false, true); break;
-      case 12: SOL_LAUNCH_PREPARED(false, true, false, false, true); break;
-      case 13: SOL_LAUNCH_PREPARED(false, true, true, false, true); break;
-      case 14: SOL_LAUNCH_PREPARED(true, false, false, false, true); break;
-      case 15: SOL_LAUNCH_PREPARED(true, false, true, false, true); break;
-      case 16: SOL_LAUNCH_PREPARED(true, true, false, false, true); break;
-      case 17: SOL_LAUNCH_PREPARED(true, true, true, false, true); break;
-      case 18: SOL_LAUNCH_PREPARED(false, false, false, true, true); break;
-      default: SOL_LAUNCH_PREPARED(false, true, false, true, true); break;
-    }
-#undef SOL_LAUNCH_PREPARED
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+  // queries from records: no rotation, no normalisation, dense
+  const bool orec = out_format == 2;
+  const int sel = (qrec != nullptr ? 4 : (tab != nullptr) * 2 + sparse) + 5 * orec;
+#define SOL_LAUNCH_PREPARED(R, S, Q, O)                                                          \
+  hipLaunchKernelGGL((attn_prepared_kernel<R, S, Q, O>), grid, dim3(256), 0, stream, q, k_prep,  \
+                     v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, out_format,      \
+                     blocks, counts, nkb, qrec, heads)
+  switch (sel) {
+    case 0: SOL_LAUNCH_PREPARED(false, false, false, false); break;
+    case 1: SOL_LAUNCH_PREPARED(false, true, false, false); break;
+    case 2: SOL_LAUNCH_PREPARED(true, false, false, false); break;
+    case 3: SOL_LAUNCH_PREPARED(true, true, false, false); break;
+    case 4: SOL_LAUNCH_PREPARED(false, false, true, false); break;
+    case 5: SOL_LAUNCH_PREPARED(false, false, false, true); break;
+    case 6: SOL_LAUNCH_PREPARED(false, true, false, true); break;
+    case 7: SOL_LAUNCH_PREPARED(true, false, false, true); break;
+    case 8: SOL_LAUNCH_PREPARED(true, true, false, true); break;
+    default: SOL_LAUNCH_PREPARED(false, false, true, true); break;
   }
-  return hipSuccess;
+#undef SOL_LAUNCH_PREPARED
+  return hipGetLastError();
 }
 
 int64_t attn_max_workgroups(int N, int BH) { return (int64_t)((N + BM - 1) / BM) * BH; }

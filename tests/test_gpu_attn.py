@@ -245,11 +245,12 @@ def test_workspace_path_is_the_two_prepared_calls(shape):
 
 
 @pytest.mark.parametrize("growth", [24.0, 300.0])
-def test_second_pass_recomputes_rows_that_leave_fp16(growth):
+def test_rising_scores_raise_the_reference_in_place(growth):
     """Scores that climb along the key sequence far above the first key
-    tile's max (by ~growth binades): the prepared path's first pass marks
-    those row blocks and the second recomputes them with a rising reference.
-    Text-only, one direction u for every token: logit_j = a_j |u|^2 / sqrt(D)."""
+    tile's max (by ~growth binades): on the prepared path nearly every tile's
+    fp16 probabilities would overflow against the reference max, which is
+    raised in place (O and l rescaled) before they are used.  Text-only, one
+    direction u for every token: logit_j = a_j |u|^2 / sqrt(D)."""
     w = W.custom(1, 2, 0, 0, 0, n_text=700, seed_index=603)
     q, k, v = W.make_inputs(w)
     g = torch.Generator().manual_seed(9)

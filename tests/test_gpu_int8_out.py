@@ -132,9 +132,9 @@ def test_int8_records_parity(shape):
     assert st["worst_excess"] <= MIDPOINT_TOL and st["exact_codes"] >= MIN_EXACT
 
 
-def test_int8_records_second_pass():
-    """Rows the first pass marks (scores 24 binades above the first tile) are
-    recomputed by the second pass in the record format too: no marker left."""
+def test_int8_records_rising_scores():
+    """Scores climbing 24 binades above the first tile: the reference max is
+    raised in place, with the record epilogue too."""
     w = W.custom(1, 2, 0, 0, 0, n_text=700, seed_index=1320)
     q, k, v = W.make_inputs(w)
     g = torch.Generator().manual_seed(9)
@@ -151,7 +151,7 @@ def test_int8_records_second_pass():
     check_against_bf16(rows, _bits(bf).reshape(-1, 128))
     ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), 0, 0, 0, rope=False)
     st = check_against_oracle(rows, ref.reshape(-1, 128), np.repeat(np.arange(w.B * w.H), w.N))
-    _log("int8 records second pass: %s" % st)
+    _log("int8 records rising scores: %s" % st)
     assert st["worst_excess"] <= MIDPOINT_TOL and st["exact_codes"] >= MIN_EXACT
 
 

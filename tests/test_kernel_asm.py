@@ -1,14 +1,17 @@
 """Checks on the generated gfx950 code of the prepared-path attention kernel
 (CPU only: hipcc cross-compiles the kernels to assembly).
 
-The first-pass kernel issues its score MFMAs and its LDS tile copies as inline
-assembly, which the compiler's hazard recognizer and register allocator do not
-see.  These tests check the properties that make that safe on the code the
+The kernel issues its score MFMAs and its LDS tile copies as inline assembly,
+which the compiler's hazard recognizer and register allocator do not see.
+These tests check the properties that make that safe on the code the
 compiler actually produced:
   * no instruction reads or overwrites an MFMA's result registers, or
     overwrites its accumulator input, within the 12 wait states an 8-pass
     MFMA needs -- for the inline MFMAs and the compiler's own alike;
-  * the second-pass kernels contain no inline-assembly MFMA at all;
+  * no instance spills (no scratch memory instruction anywhere), so the
+    copy-count waits see only the copies;
+  * no VALU instruction writes an SGPR that a tile copy reads within the 5
+    wait states such a read needs;
   * M0, which the copies set without saving it, is used by nothing else.
 """
 import os
@@ -79,26 +82,24 @@ def operands(t):
 STORE_PREFIXES = ("ds_write", "global_store", "buffer_store", "scratch_store", "flat_store")
 
 
+N_INSTANCES = 10  # (rope, sparse, records, output records) combinations launched
+
+
 def template_args(name):
-    """(kRope, kRobust, kSparse, kRec, kOutRec) of an attn_prepared_kernel instance from its
+    """(kRope, kSparse, kRec, kOutRec) of an attn_prepared_kernel instance from its
     mangled name."""
-    m = re.search(r"attn_prepared_kernelILb(\d)ELb(\d)ELb(\d)ELb(\d)ELb(\d)EE", name)
+    m = re.search(r"attn_prepared_kernelILb(\d)ELb(\d)ELb(\d)ELb(\d)EE", name)
     assert m, name
     return tuple(bool(int(x)) for x in m.groups())
 
 
-def first_pass(name):
-    return not template_args(name)[1]
-
-
 def test_mfma_latency_respected(asm_text):
-    """Every MFMA of the twenty kernels (rotary or not, first or second pass,
-    dense or block-sparse, queries from bf16 or from records, output records
-    or not), inline or not: the compiler's own hazard handling
-    is checked too (it once let a spill reload overwrite an accumulator still
-    being read)."""
+    """Every MFMA of the ten kernels (rotary or not, dense or block-sparse,
+    queries from bf16 or from records, output records or not), inline or not:
+    the compiler's own hazard handling is checked too (it once let a spill
+    reload overwrite an accumulator still being read)."""
     kernels = functions(asm_text, "attn_prepared_kernel")
-    assert len(kernels) == 20
+    assert len(kernels) == N_INSTANCES
     for name, body in kernels:
         ins = instructions(body)
         n_asm = 0
@@ -137,20 +138,56 @@ def test_mfma_latency_respected(asm_text):
                     written, read = regs(ops2[0]), set().union(set(), *(regs(x) for x in ops2[1:]))
                 assert not (written & (dst | srcc)), "%s: %r overwrites registers of %r" % (name, t2, t)
                 assert not (read & dst), "%s: %r reads the result of %r too early" % (name, t2, t)
-        if first_pass(name):
-            assert n_asm >= 32, "%s: expected the score MFMAs as inline assembly" % name
+        assert n_asm >= 32, "%s: expected the score MFMAs as inline assembly" % name
 
 
-def test_second_pass_has_no_inline_asm_mfma(asm_text):
-    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if not first_pass(f[0])]
-    assert len(kernels) == 10
+def test_no_instance_spills(asm_text):
+    """No scratch memory anywhere in the attention kernels.  A kernel that
+    spills issues memory instructions the inline copies' waits do not count,
+    and spill code beside the inline MFMAs is where generated-code hazards
+    have appeared (a build whose instance spilled 41 reloads returned wrong
+    row blocks); the register budget is checked here instead of trusted."""
+    kernels = functions(asm_text, "attn_prepared_kernel")
+    assert len(kernels) == N_INSTANCES
     for name, body in kernels:
-        assert not any(in_asm and t.startswith("v_mfma") for t, in_asm in instructions(body)), name
+        ins = instructions(body)
+        assert not any(t.startswith("scratch_") for t, _ in ins), "%s spills" % name
+        assert not any(re.match(r"(buffer|global)_(load|store)\S* .*\boff, s\[0:3\]", t) for t, _ in ins), name
+
+
+def sregs(tok):
+    m = re.match(r"s\[(\d+):(\d+)\]$", tok.strip())
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"s(\d+)$", tok.strip())
+    return {int(m.group(1))} if m else set()
+
+
+def test_copy_sgprs_not_written_by_valu_just_before(asm_text):
+    """A vector-memory instruction reading an SGPR that a VALU instruction
+    (v_readfirstlane, a compare) wrote needs 5 wait states between them; the
+    compiler inserts them for its own instructions, not for the tile copies
+    written as inline assembly, whose offset and resource operands it
+    computes."""
+    for name, body in functions(asm_text, "attn_prepared_kernel"):
+        ins = instructions(body)
+        for i, (t, in_asm) in enumerate(ins):
+            if not (t.startswith("buffer_load") and t.endswith(" lds")):
+                continue
+            used = set().union(*(sregs(o) for o in operands(t)))
+            ws = 0
+            for t2, _ in reversed(ins[max(0, i - 40):i]):
+                m = re.match(r"s_nop (\d+)", t2)
+                ws += int(m.group(1)) + 1 if m else 1
+                if ws > 5:
+                    break
+                if t2.startswith("v_") and operands(t2):
+                    assert not (sregs(operands(t2)[0]) & used), "%s: %r then %r" % (name, t2, t)
 
 
 def test_m0_used_only_by_tile_copies(asm_text):
     kernels = functions(asm_text, "attn_prepared_kernel")
-    assert len(kernels) == 20
+    assert len(kernels) == N_INSTANCES
     implicit_m0 = ("s_movrel", "v_movrel", "s_sendmsg", "ds_gws", "v_interp", "ds_append", "ds_consume",
                    "ds_ordered", "s_setreg")
     for name, body in kernels:
@@ -174,18 +211,17 @@ def test_first_pass_copy_count_waits_see_only_copies(asm_text):
     the compiler must issue no load, store or spill of its own.  (Its own
     vmcnt waits for its own loads, e.g. in the prologue, wait for at least as
     much as they need: the counter retires in order.)"""
-    kernels = [f for f in functions(asm_text, "attn_prepared_kernel") if first_pass(f[0])]
-    assert len(kernels) == 10
+    kernels = functions(asm_text, "attn_prepared_kernel")
+    assert len(kernels) == N_INSTANCES
     for name, body in kernels:
         ins = instructions(body)
-        assert not any(t.startswith("scratch_") for t, _ in ins), "%s spills" % name
         since, n_waits = [], 0
         for i, (t, in_asm) in enumerate(ins):
             if t.startswith(("buffer_", "global_", "flat_")):
                 since.append((t, in_asm))
             if t.startswith("s_waitcnt") and "vmcnt" in t:
                 # the dense walk leaves its four copies in flight, the sparse walk eight
-                want = "vmcnt(8)" if template_args(name)[2] else "vmcnt(4)"
+                want = "vmcnt(8)" if template_args(name)[1] else "vmcnt(4)"
                 if want in t and i + 1 < len(ins) and ins[i + 1][0] == "s_barrier":
                     n_waits += 1
                     others = [x for x, a in since if not (a and x.endswith(" lds"))]
