@@ -597,6 +597,7 @@ __device__ __forceinline__ void dma_barrier() {
 // LDS holds rings of eight K tiles and four V tiles (96 KB); the barrier that
 // ends an iteration waits only for the copies issued one iteration earlier.
 constexpr int BN2 = kPrepTile;         // keys per tile of the prepared-path kernel
+constexpr int kWaves2 = 4;             // waves per workgroup of the prepared-path kernel
 constexpr int kKBufs = 8;              // K tiles in LDS (a power of two: ring
 constexpr int kVBufs = 4;              // V tiles in LDS  offsets are masks)
 // Descriptor word 3 of a raw buffer resource (32-bit data, no format swizzle).
@@ -619,13 +620,18 @@ static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's
 // kOutRec: block-INT8 output records (out_format 2), a template flag so that
 // the bf16 and E4M3 instances do not carry the record epilogue's registers.
 //
-// One launch, one pass: each row's reference max m starts at the largest
-// score of the walk's first key tile and of the rows' diagonal tile, and a
-// tile whose probabilities would leave the fp16 range against it (a score
-// more than 15 above m) raises m in place -- the tile's scores are
-// recomputed, the accumulated O and l rescaled -- before its probabilities
-// are used.  Exact softmax whatever the score distribution.
-template <bool kRope, bool kSparse, bool kRec, bool kOutRec>
+// Two launches.  Each row's reference max m starts at the largest score of
+// the walk's first key tile and of the rows' diagonal tile.  The first launch
+// (kRobust false) keeps m fixed: its loop carries no per-tile branch.  A wave
+// whose probabilities leave the fp16 range against m (a score more than 15
+// above it) stops computing at the end of that loop trip -- it keeps issuing
+// its share of the tile copies and barriers for the other waves -- and writes
+// its rows as NaN.  The second launch (kRobust true) recomputes exactly the
+// row blocks so marked (every other workgroup leaves at once): there a tile
+// whose probabilities would overflow raises m in place, while its scores are
+// still in registers -- O and l rescaled -- before its probabilities are used.
+// Neither kernel spills.  Exact softmax whatever the score distribution.
+template <bool kRope, bool kRobust, bool kSparse, bool kRec, bool kOutRec>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                           const uint16_t* __restrict__ v, uint16_t* __restrict__ out, SeqGrid g,
@@ -646,6 +652,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
                 "a copy must land a barrier after the last read of the slot it overwrites");
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVB * kPrepTileElems];
   __shared__ uint32_t blist[kSparse ? kMaxSparseBlocks : 1];  // entry e | entry e + 1 << 16
+  __shared__ int n_gave_up;  // first pass: waves of the workgroup that stopped computing
 
   auto keep = [&](auto& x) __attribute__((always_inline)) { pin(x); };
   const int tid = threadIdx.x;
@@ -723,6 +730,21 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     if (!kSparse) return t * BN2;
     return (t >> 2) == last_pos ? (4 * last_blk + (t & 3)) * BN2 : 0;
   };
+  if (kRobust) {
+    // Second pass: only the row blocks the first pass marked (NaN rows) are
+    // recomputed; every other workgroup leaves at once.
+    bool marked = false;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int row = qrow_first + 32 * qb;
+      if (hh == 0 && row < Nq)
+        marked |= out_rec   ? outrec_slab[row * outrec_stride + 128] == 0xFF
+                  : out_fp8 ? (out8_slab[(size_t)row * D] & 0x7F) == 0x7F
+                            : (out_slab[(size_t)row * D] & 0x7FFF) > 0x7F80;
+    }
+    if (!__syncthreads_or(marked)) return;
+  }
+
   // ---- Q' fragments of the wave's two 32-row blocks, normalised (q_gamma)
   // and rotated in the load.  A lane holds the even (hh = 0) or odd chunks of
   // its row; the sum of squares pairs them across the lane halves first, then
@@ -822,6 +844,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   float m_ref[2];   // reference max of each query row (units of c q.k)
   f32x16 bias[2];   // -m_ref, the first addend of every score chain
   float l_run[2] = {0.0f, 0.0f};
+  float ovf = 0.0f;  // first pass: largest per-lane tile sum (above 2^15: rows marked)
 
   // Register j of a score block holds key 8(j/4) + 4hh + (j%4) of the tile;
   // the tile's first key is kv0.
@@ -845,6 +868,20 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
 #pragma unroll
     for (int j = 2; j < 16; j += 2) mx = fmaxf(fmaxf(mx, s[j]), s[j + 1]);
     return fmaxf(mx, __shfl_xor(mx, 32));
+  };
+  // Slab tiles of iteration i's copies, K(i + kKAhead) and V(i + kVAhead);
+  // pair: the sparse walk's list word of walk position i + kVAhead (and the
+  // next entry).
+  auto copy_tiles = [&](int i, uint32_t pair, int& tile_k, int& tile_v) __attribute__((always_inline)) {
+    tile_k = i + kKAhead;
+    tile_v = i + kVAhead;
+    if (kSparse) {
+      const uint32_t w = __builtin_amdgcn_readfirstlane(pair);
+      const int tv = min(i + kVAhead, n_kv - 1), tk = min(i + kKAhead, n_kv - 1);
+      const int lo = (int)(w & 0xFFFFu), hi = (int)(w >> 16);
+      tile_v = 4 * lo + (tv & 3);
+      tile_k = 4 * ((tk >> 2) == (tv >> 2) ? lo : hi) + (tk & 3);
+    }
   };
   // Raise the reference max of query block qb to the largest score of tile
   // s (scores held against the current m, keys past N at -inf) where that
@@ -888,7 +925,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   //   phase A (8 slot pairs): S(i+1) MFMAs (qb0, then qb1, per K fragment) +
   //     P(i) qb1 word j
   //   phase B (8 slot pairs): PV(i) MFMAs (qb0, then qb1, per V fragment) +
-  //     P(i+1) qb0 word j
+  //     P(i+1) qb0 word j; the overflow check of P(i) qb1 between the first
+  //     two, that of P(i+1) qb0 at the end
   auto iteration = [&](int i, f32x16* cs, f32x16* ns, uint32_t* p0_cur, uint32_t* p0_next,
                        float& l0_cur, float& l0_next) __attribute__((always_inline)) {
     // K tile t sits in buffer t % 8 from its copy (iteration t - kKAhead, or
@@ -945,30 +983,36 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
     p1[7] = pack_f16x2(pa, pb);
     l1 = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p1[6], p1[7]))));
-    // Rare: a score of this block's tile exceeds m by more than 15, so its
-    // fp16 words (or their sums) overflowed: raise m while S(i) is still in
-    // registers (S(i+1) of the block, just computed against the old m, moves
-    // with it).
-    if (__builtin_expect(__any(l1 > kP16SumLimit), 0)) {
-      mfma_wait();  // the inline score MFMAs of S(i+1) have landed
-      raise_max(1, cs[1], &ns[1], p1, l1);
+    if (kRobust) {
+      // Rare: a score of block 1's tile exceeds m by more than 15, so its
+      // fp16 words (or their sums) overflowed: raise m while S(i) is still in
+      // registers (S(i+1) of the block, computed against the old m, moves
+      // with it).
+      if (__builtin_expect(__any(l1 > kP16SumLimit), 0)) {
+        mfma_wait();  // the inline score MFMAs of S(i+1) have landed
+        raise_max(1, cs[1], &ns[1], p1, l1);
+      }
+    } else {
+      ovf = fmaxf(ovf, fmaxf(l0_cur, l1));
     }
     l_run[0] += l0_cur;
     l_run[1] += l1;
     keep(l_run[0]);
     keep(l_run[1]);
+    if (!kRobust) keep(ovf);
     // The tail above runs in the shadow of the last score MFMAs and counts
     // toward their latency (pinned here: the compiler would otherwise sink it
     // past the branch below).
     __builtin_amdgcn_sched_barrier(0);
     f16x8 pf[2][2];
+    auto words_to_operands = [&](int qb, const uint32_t* w) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kst = 0; kst < 2; ++kst) {
-      pf[0][kst] = __builtin_bit_cast(f16x8, make_uint4(p0_cur[4 * kst], p0_cur[4 * kst + 1],
-                                                        p0_cur[4 * kst + 2], p0_cur[4 * kst + 3]));
-      pf[1][kst] = __builtin_bit_cast(f16x8, make_uint4(p1[4 * kst], p1[4 * kst + 1],
-                                                        p1[4 * kst + 2], p1[4 * kst + 3]));
-    }
+      for (int kst = 0; kst < 2; ++kst)
+        pf[qb][kst] = __builtin_bit_cast(f16x8, make_uint4(w[4 * kst], w[4 * kst + 1], w[4 * kst + 2],
+                                                           w[4 * kst + 3]));
+    };
+    words_to_operands(0, p0_cur);
+    words_to_operands(1, p1);
     // S(i+1) is read by the VALU from here on: its MFMAs must have landed (the
     // tail above and these wait states make the 12 an 8-pass result needs; a
     // build test checks the count), and a ragged last tile is masked first.
@@ -987,15 +1031,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // ---- phase B
     pa = pb = 0.0f;
     t01 = t23 = t03 = t45 = 0;
-    // slab tiles of this iteration's copies: K(i + kKAhead), V(i + kVAhead)
-    int tile_k = i + kKAhead, tile_v = i + kVAhead;
-    if (kSparse) {
-      const uint32_t w = __builtin_amdgcn_readfirstlane(pair);
-      const int tv = min(i + kVAhead, n_kv - 1), tk = min(i + kKAhead, n_kv - 1);
-      const int lo = (int)(w & 0xFFFFu), hi = (int)(w >> 16);
-      tile_v = 4 * lo + (tv & 3);
-      tile_k = 4 * ((tk >> 2) == (tv >> 2) ? lo : hi) + (tk & 3);
-    }
+    int tile_k, tile_v;
+    copy_tiles(i, pair, tile_k, tile_v);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
@@ -1033,16 +1070,24 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     }
     p0_next[7] = pack_f16x2(pa, pb);
     l0_next = sum_f16x2(add_f16x2(t03, add_f16x2(t45, add_f16x2(p0_next[6], p0_next[7]))));
-    // Block 0's words of P(i+1) are checked here, where S(i+1) is still in
-    // registers (its next scores are computed with the raised m).
-    if (__builtin_expect(__any(l0_next > kP16SumLimit), 0)) raise_max(0, ns[0], nullptr, p0_next, l0_next);
     keep(p0_next[7]);
-    keep(l0_next);
+    // Second pass: block 0's words of P(i+1) are compared here and branched
+    // on after the barrier (not after the last tile: S(n_kv) is a re-read of
+    // a real tile, unmasked, whose words are never used).
+    uint64_t ovf0 = 0;
+    if (kRobust && i + 1 < n_kv) {
+      ovf0 = __ballot(l0_next > kP16SumLimit);
+      asm volatile("" : "+s"(ovf0));
+    }
     // The copies the next iteration reads must have landed: those issued
     // kKAhead - 2 iterations ago (K) and kVAhead - 1 ago (V) -- so only the
     // copies of this and the kInflight - 1 previous iterations (4 each) may
     // still be in flight.
     dma_barrier<kInflight>();
+    // Raise block 0's m while S(i+1) is still in registers (the block's next
+    // scores are computed with the raised m).
+    if (kRobust && __builtin_expect(ovf0 != 0, 0)) raise_max(0, ns[0], nullptr, p0_next, l0_next);
+    keep(l0_next);
   };
 
   // ---- prologue: K(0 .. kKAhead - 2) and V(0 .. kVAhead - 2) in LDS,
@@ -1059,6 +1104,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       dma_v(t, wt, 1);
     }
   }
+  if (!kRobust && tid == 0) n_gave_up = 0;
   __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt 0, lgkmcnt 0: every copy so far has landed
   __syncthreads();
   {
@@ -1146,13 +1192,46 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   mfma_wait();
 
   int i = 0;
+  bool gave_up = false;
   for (; i + 1 < n_kv; i += 2) {
     iteration(i, sa, sb, pA, pB, lA, lB);
     iteration(i + 1, sb, sa, pB, pA, lB, lA);
+    // First pass: a wave whose probabilities left the fp16 range stops here
+    // (its rows are recomputed by the second pass).  Checked once per loop
+    // trip, beside the loop's own branch.
+    if (!kRobust && __builtin_expect(__any(ovf > kP16SumLimit), 0)) {
+      gave_up = true;
+      i += 2;
+      break;
+    }
   }
-  if (i < n_kv) iteration(i, sa, sb, pA, pB, lA, lB);
+  if (gave_up) {
+    // The other waves still need this wave's share of every tile copy, and
+    // the barriers: one per remaining tile, as their loop does -- until every
+    // wave of the workgroup has stopped (the count is raised before a barrier
+    // and read after it, so all four see the last raise after the same one).
+    if (lane == 0) atomicAdd(&n_gave_up, 1);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt 0: the raise is done before the barrier
+    for (; i < n_kv; ++i) {
+      const uint32_t pair = kSparse ? blist[min(i + kVAhead, n_kv - 1) >> 2] : 0u;
+      int tile_k, tile_v;
+      copy_tiles(i, pair, tile_k, tile_v);
+      dma_k(i + kKAhead, tile_k, 0);
+      dma_v(i + kVAhead, tile_v, 0);
+      dma_k(i + kKAhead, tile_k, 1);
+      dma_v(i + kVAhead, tile_v, 1);
+      dma_barrier<kInflight>();
+      if (__builtin_amdgcn_readfirstlane(n_gave_up) == kWaves2) break;
+    }
+  } else if (i < n_kv) {
+    iteration(i, sa, sb, pA, pB, lA, lB);
+  }
 
   // ---- epilogue: out = O / l; register j of block (qb, db) is dim 32db + 8(j/4) + 4hh + j%4.
+  // A first-pass wave whose probabilities left the fp16 range writes its rows
+  // as NaN instead (bf16 0x7FC0, E4M3 0x7F, records with scale codes 0xFF):
+  // the second pass recomputes exactly those.
+  const bool marked = !kRobust && __any(ovf > kP16SumLimit);
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int row = qrow0 + 32 * qb;
@@ -1163,6 +1242,10 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       // in this lane's 16 registers of block db and its partner lane's (hh ^ 1)
       if (row >= Nq) continue;  // uniform over the lane pair
       uint8_t* dst = outrec_slab + row * outrec_stride;
+      if (marked) {
+        if (hh == 0) *reinterpret_cast<uint4*>(dst + 128) = make_uint4(0xFFFFFFFFu, 0u, 0u, 0u);
+        continue;
+      }
       uint32_t scales = 0;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
@@ -1187,6 +1270,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     if (out_fp8) {
       if (row >= Nq) continue;
       uint8_t* dst = out8_slab + (size_t)row * D;
+      if (marked) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          *reinterpret_cast<uint4*>(dst + 64 * hh + 16 * c) = make_uint4(0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu);
+        continue;
+      }
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -1199,7 +1288,12 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       }
       continue;
     }
-    if (row < Nq) {
+    if (row < Nq && marked) {
+      uint16_t* dst = out_slab + (size_t)row * D;
+#pragma unroll
+      for (int c = 0; c < 8; ++c)
+        *reinterpret_cast<uint4*>(dst + 64 * hh + 8 * c) = make_uint4(0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u);
+    } else if (row < Nq) {
       uint16_t* dst = out_slab + (size_t)row * D;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
@@ -1296,27 +1390,43 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   const bool sparse = blocks != nullptr;
-  // queries from records: no rotation, no normalisation, dense
-  const bool orec = out_format == 2;
-  const int sel = (qrec != nullptr ? 4 : (tab != nullptr) * 2 + sparse) + 5 * orec;
-#define SOL_LAUNCH_PREPARED(R, S, Q, O)                                                          \
-  hipLaunchKernelGGL((attn_prepared_kernel<R, S, Q, O>), grid, dim3(256), 0, stream, q, k_prep,  \
-                     v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps, out_format,      \
-                     blocks, counts, nkb, qrec, heads)
-  switch (sel) {
-    case 0: SOL_LAUNCH_PREPARED(false, false, false, false); break;
-    case 1: SOL_LAUNCH_PREPARED(false, true, false, false); break;
-    case 2: SOL_LAUNCH_PREPARED(true, false, false, false); break;
-    case 3: SOL_LAUNCH_PREPARED(true, true, false, false); break;
-    case 4: SOL_LAUNCH_PREPARED(false, false, true, false); break;
-    case 5: SOL_LAUNCH_PREPARED(false, false, false, true); break;
-    case 6: SOL_LAUNCH_PREPARED(false, true, false, true); break;
-    case 7: SOL_LAUNCH_PREPARED(true, false, false, true); break;
-    case 8: SOL_LAUNCH_PREPARED(true, true, false, true); break;
-    default: SOL_LAUNCH_PREPARED(false, false, true, true); break;
-  }
+  // First pass, then the second over the row blocks whose probabilities left
+  // the fp16 range.
+  for (int pass = 0; pass < 2; ++pass) {
+    // queries from records: no rotation, no normalisation, dense
+    const bool orec = out_format == 2;
+    const int sel = (qrec != nullptr ? 8 + pass : (tab != nullptr) * 4 + pass * 2 + sparse) + 10 * orec;
+#define SOL_LAUNCH_PREPARED(R, P, S, Q, O)                                                      \
+  hipLaunchKernelGGL((attn_prepared_kernel<R, P, S, Q, O>), grid, dim3(256), 0, stream, q,       \
+                     k_prep, v_prep, out, g, tab, n_qtiles, c_log2, n_kv, q_gamma, eps,          \
+                     out_format, blocks, counts, nkb, qrec, heads)
+    switch (sel) {
+      case 0: SOL_LAUNCH_PREPARED(false, false, false, false, false); break;
+      case 1: SOL_LAUNCH_PREPARED(false, false, true, false, false); break;
+      case 2: SOL_LAUNCH_PREPARED(false, true, false, false, false); break;
+      case 3: SOL_LAUNCH_PREPARED(false, true, true, false, false); break;
+      case 4: SOL_LAUNCH_PREPARED(true, false, false, false, false); break;
+      case 5: SOL_LAUNCH_PREPARED(true, false, true, false, false); break;
+      case 6: SOL_LAUNCH_PREPARED(true, true, false, false, false); break;
+      case 7: SOL_LAUNCH_PREPARED(true, true, true, false, false); break;
+      case 8: SOL_LAUNCH_PREPARED(false, false, false, true, false); break;
+      case 9: SOL_LAUNCH_PREPARED(false, true, false, true, false); break;
+      case 10: SOL_LAUNCH_PREPARED(false, false, false, false, true); break;
+      case 11: SOL_LAUNCH_PREPARED(false, false, true, false, true); break;
+      case 12: SOL_LAUNCH_PREPARED(false, true, false, false, true); break;
+      case 13: SOL_LAUNCH_PREPARED(false, true, true, false, true); break;
+      case 14: SOL_LAUNCH_PREPARED(true, false, false, false, true); break;
+      case 15: SOL_LAUNCH_PREPARED(true, false, true, false, true); break;
+      case 16: SOL_LAUNCH_PREPARED(true, true, false, false, true); break;
+      case 17: SOL_LAUNCH_PREPARED(true, true, true, false, true); break;
+      case 18: SOL_LAUNCH_PREPARED(false, false, false, true, true); break;
+      default: SOL_LAUNCH_PREPARED(false, true, false, true, true); break;
+    }
 #undef SOL_LAUNCH_PREPARED
-  return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 int64_t attn_max_workgroups(int N, int BH) { return (int64_t)((N + BM - 1) / BM) * BH; }

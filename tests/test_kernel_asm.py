@@ -82,20 +82,21 @@ def operands(t):
 STORE_PREFIXES = ("ds_write", "global_store", "buffer_store", "scratch_store", "flat_store")
 
 
-N_INSTANCES = 10  # (rope, sparse, records, output records) combinations launched
+N_INSTANCES = 20  # (rope, pass, sparse, records, output records) combinations launched
 
 
 def template_args(name):
-    """(kRope, kSparse, kRec, kOutRec) of an attn_prepared_kernel instance from its
-    mangled name."""
-    m = re.search(r"attn_prepared_kernelILb(\d)ELb(\d)ELb(\d)ELb(\d)EE", name)
+    """(kRope, kRobust, kSparse, kRec, kOutRec) of an attn_prepared_kernel instance
+    from its mangled name."""
+    m = re.search(r"attn_prepared_kernelILb(\d)ELb(\d)ELb(\d)ELb(\d)ELb(\d)EE", name)
     assert m, name
     return tuple(bool(int(x)) for x in m.groups())
 
 
 def test_mfma_latency_respected(asm_text):
-    """Every MFMA of the ten kernels (rotary or not, dense or block-sparse,
-    queries from bf16 or from records, output records or not), inline or not:
+    """Every MFMA of the twenty kernels (rotary or not, first or second pass,
+    dense or block-sparse, queries from bf16 or from records, output records
+    or not), inline or not:
     the compiler's own hazard handling is checked too (it once let a spill
     reload overwrite an accumulator still being read)."""
     kernels = functions(asm_text, "attn_prepared_kernel")
@@ -221,7 +222,7 @@ def test_first_pass_copy_count_waits_see_only_copies(asm_text):
                 since.append((t, in_asm))
             if t.startswith("s_waitcnt") and "vmcnt" in t:
                 # the dense walk leaves its four copies in flight, the sparse walk eight
-                want = "vmcnt(8)" if template_args(name)[1] else "vmcnt(4)"
+                want = "vmcnt(8)" if template_args(name)[2] else "vmcnt(4)"
                 if want in t and i + 1 < len(ins) and ins[i + 1][0] == "s_barrier":
                     n_waits += 1
                     others = [x for x, a in since if not (a and x.endswith(" lds"))]
