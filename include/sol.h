@@ -28,7 +28,8 @@
  *  - The caller owns every buffer (tensors and the rotary table) and keeps
  *    them alive until the work on `stream` completes.  The library never
  *    allocates, frees or synchronises, and keeps no state across calls except
- *    a thread-local error message.
+ *    a thread-local error message (and the static per-GPU workspace of
+ *    sol_attn_fwd_noalloc).
  *  - Arguments are validated on the host before any HIP call; a rejected call
  *    returns a negative status and launches nothing.  Launch failures return
  *    SOL_ERR_HIP.  Work is asynchronous on `stream` (NULL = the null stream);
@@ -281,6 +282,28 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int D);
 int sol_attn_fwd_ws(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
                     int D, int T, int Hl, int Wl, const float* rope_tab_dev, void* workspace,
                     size_t workspace_bytes, sol_stream_t stream);
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * computation as sol_attn_fwd_ws (the same kernels, the same bits), on a
+ * workspace the library holds itself instead of the caller's.  The workspace
+ * is a static device array of SOL_NOALLOC_MAX_BYTES (256 MiB) on every GPU the
+ * library runs on, held until the process ends; a call whose
+ * sol_attn_workspace_bytes(B, H, N, D) exceeds it returns SOL_ERR_UNSUPPORTED
+ * and launches nothing (e.g. B = 1, D = 128: H * ceil(N/32) * 32 <= 524,288,
+ * such as 24 heads of 12,480 tokens).  The call allocates and frees nothing
+ * (no hipMalloc, no allocating library routine).  Every call on one GPU uses
+ * that GPU's one array: calls that overlap in time on one GPU (other streams,
+ * other threads) race and must be serialised by the caller; calls in order on
+ * one stream are safe.  Its contents between calls are unspecified (the
+ * computation needs none cleared).  Other arguments, validation and errors as
+ * sol_attn_fwd.
+ */
+#define SOL_NOALLOC_MAX_BYTES ((size_t)256 << 20)
+int sol_attn_fwd_noalloc(const void* q, const void* k, const void* v, void* out, int B, int H,
+                         int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
+                         sol_stream_t stream);
 
 /*
  * Block-INT8 QKV records (Sec. 3.2, "Quantized communication"): the wire

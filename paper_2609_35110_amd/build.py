@@ -9,7 +9,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsol.so")
-SOURCES = ["sol_kernels.hip", "sol_sparse.hip", "sol_records.hip", "sol_probe.hip", "sol_api.cpp"]
+SOURCES = ["sol_kernels.hip", "sol_sparse.hip", "sol_records.hip", "sol_probe.hip", "sol_noalloc.hip",
+           "sol_api.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -91,6 +91,8 @@ int check_sparse(const void* q, const void* k_prep, int B, int H, int N, int D, 
 
 }  // namespace
 
+int sol::set_error(int status, const char* msg) { return fail(status, "%s", msg); }
+
 sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl) {
   SeqGrid g;
   const int64_t nv = (int64_t)T * Hl * Wl;

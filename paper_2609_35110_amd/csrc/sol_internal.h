@@ -99,4 +99,8 @@ hipError_t launch_mfma_probe(const uint16_t* operands, float* out, int workgroup
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
 int64_t attn_max_workgroups(int N, int BH);
 
+// Record msg as the calling thread's last error (sol_last_error) and return
+// status: the front end's error path, for entry points in other sources.
+int set_error(int status, const char* msg);
+
 }  // namespace sol

@@ -63,6 +63,8 @@ def lib():
         L.sol_attn_workspace_bytes.restype = sz
         L.sol_attn_fwd_ws.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, sz, P]
         L.sol_attn_fwd_ws.restype = i32
+        L.sol_attn_fwd_noalloc.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
+        L.sol_attn_fwd_noalloc.restype = i32
         f32 = ctypes.c_float
         L.sol_qknorm_rope3d.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32, P]
         L.sol_qknorm_rope3d.restype = i32
@@ -175,6 +177,10 @@ def sol_attn_workspace_bytes(B, H, N, D):
 def sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, workspace, workspace_bytes, stream):
     return lib().sol_attn_fwd_ws(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, workspace,
                                  workspace_bytes, stream)
+
+
+def sol_attn_fwd_noalloc(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
+    return lib().sol_attn_fwd_noalloc(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
 
 
 def sol_qkv_record_bytes(B, H, N):
@@ -341,6 +347,22 @@ def attn_fwd_ws(q, k, v, T, Hl, Wl, table=None, workspace=None, out=None):
                           ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N,
                           D, T, Hl, Wl, _table_ptr(table, q.device),
                           ctypes.c_void_p(workspace.data_ptr()), nbytes, _stream(q)))
+    return out
+
+
+def attn_fwd_noalloc(q, k, v, T, Hl, Wl, table=None, out=None):
+    """attn_fwd_ws on the library's own static workspace (no device allocation
+    by the library; out is allocated here when not given)."""
+    _check_tensor("q", q)
+    _check_tensor("k", k, q.shape)
+    _check_tensor("v", v, q.shape)
+    B, H, N, D = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensor("out", out, q.shape)
+    check(sol_attn_fwd_noalloc(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                               ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N,
+                               D, T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
     return out
 
 
