@@ -9,11 +9,15 @@
  *     q^ = bf16(R(pos) q),  k^ = bf16(R(pos) k)      (3D rotary embedding)
  *     out = softmax(q^ k^T / sqrt(D)) v               (no mask, bidirectional)
  *
- * R is the rotary embedding of Sec. 3.5 (fusion group 2, "partial RoPE"),
- * extended to three axes: head dims [0, D/4) rotate with the latent frame t,
- * [D/4, 5D/8) with the latent row h, [5D/8, D) with the latent column w (the
- * 32/48/48 split at D = 128).  Within an axis chunk of width d, the
- * interleaved pair (2i, 2i+1) is turned by the angle pos * base^(-2i/d).
+ * R is the rotary embedding of Sec. 3.5 (fusion group 2, "QK normalization
+ * with partial RoPE"), extended to three axes: head dims [0, dt) rotate with
+ * the latent frame t, [dt, dt+dh) with the latent row h, [dt+dh, dt+dh+dw)
+ * with the latent column w, and any dims past dt+dh+dw pass through unrotated
+ * (partial RoPE).  The default split is D/4, 3D/8, 3D/8 (32/48/48 at D = 128,
+ * every dim rotated); the entry points with dt, dh, dw arguments take any
+ * split of non-negative multiples of 8 with dt+dh+dw <= D.  Within an axis
+ * chunk of width d, the interleaved pair (2i, 2i+1) is turned by the angle
+ * pos * base^(-2i/d).
  *
  * Sequence packing follows Sec. 3.4 "Safety rails" (prefix before the target
  * video): of the N tokens, the first Nt = N - T*Hl*Wl form an unrotated
@@ -68,21 +72,30 @@ enum {
 #define SOL_MAX_TOKENS (1 << 23)
 
 /*
- * Number of floats in the rotary table for head dim D and latent grid
- * T x Hl x Wl: 2 * (T*D/8 + Hl*3D/16 + Wl*3D/16).  Returns 0 for invalid
- * arguments (D not a positive multiple of 16, a negative extent).
+ * Number of floats in the rotary table for head dim D, latent grid
+ * T x Hl x Wl and split dt/dh/dw: 2 * (T*dt/2 + Hl*dh/2 + Wl*dw/2).  Returns 0
+ * for invalid arguments (D not a positive multiple of 16, a negative extent,
+ * a split that is not three non-negative multiples of 8 summing to at most
+ * D).  sol_rope3d_table_floats is the default split D/4, 3D/8, 3D/8.
  */
+size_t sol_rope3d_table_floats_ex(int D, int T, int Hl, int Wl, int dt, int dh, int dw);
 size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl);
 
 /*
  * Fill a HOST buffer with the rotary table (caller copies it to the device).
  * Layout (float pairs (cos, sin), computed in double and rounded to float):
- *   [T  rows x D/8  pairs]  frame axis:  angle t * base^(-2i/(D/4))
- *   [Hl rows x 3D/16 pairs] row axis:    angle h * base^(-2i/(3D/8))
- *   [Wl rows x 3D/16 pairs] column axis: angle w * base^(-2i/(3D/8))
- * host_tab must hold n_floats >= sol_rope3d_table_floats(D, T, Hl, Wl).
- * base > 1 (10000 for the workloads here).  Host-only: no HIP call.
+ *   [T  rows x dt/2 pairs]  frame axis:  angle t * base^(-2i/dt)
+ *   [Hl rows x dh/2 pairs]  row axis:    angle h * base^(-2i/dh)
+ *   [Wl rows x dw/2 pairs]  column axis: angle w * base^(-2i/dw)
+ * (an axis of width 0 has no section).  host_tab must hold n_floats >=
+ * sol_rope3d_table_floats_ex(D, T, Hl, Wl, dt, dh, dw) floats.  base > 1
+ * (10000 for the workloads here).  Host-only: no HIP call.  A device copy is
+ * valid only for calls with the same grid and split.  sol_rope3d_table is the
+ * default split D/4, 3D/8, 3D/8: the table of every entry point without
+ * dt, dh, dw arguments.
  */
+int sol_rope3d_table_ex(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, int dt,
+                        int dh, int dw, double base);
 int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, double base);
 
 /*
@@ -98,7 +111,8 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
 
 /*
  * QK normalization ahead of the rotation (Sec. 3.5, fusion group 2, "QK
- * normalization with partial RoPE"), standalone:
+ * normalization with partial RoPE"), standalone, under the split dt/dh/dw
+ * (dims past dt+dh+dw are normalised, not rotated):
  *   y = bf16(R(pos) (x * gamma / sqrt(mean_d(x_d^2) + eps)))
  * per token and head: the root mean square is taken over the head's D entries
  * of the bf16 input (the rounding point the paper keeps ahead of QK
@@ -107,13 +121,16 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
  * prefix tokens are not rotated.  gamma_dev: D fp32 weights in device memory,
  * 16-byte aligned, or NULL (no normalisation: exactly sol_rope3d).  eps >= 0
  * and finite (an all-zero row with eps = 0 gives NaN, as the formula does).
- * Other arguments as sol_rope3d.  The same normalisation runs in the
+ * rope_tab_dev: the table of this grid and split (NULL only when nothing
+ * rotates: an empty grid or dt+dh+dw = 0).  Other arguments as sol_rope3d;
+ * sol_rope3d is this call with the default split and no normalisation.  The
+ * same normalisation runs in the
  * prepared path below (sol_prepare_kv_ex, sol_attn_fwd_prepared_ex), to the
  * same bits: the sum of squares follows one fixed order in every kernel.
  */
 int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
-                      const float* rope_tab_dev, const float* gamma_dev, float eps,
-                      sol_stream_t stream);
+                      int dt, int dh, int dw, const float* rope_tab_dev, const float* gamma_dev,
+                      float eps, sol_stream_t stream);
 
 /*
  * out = softmax(q^ k^T / sqrt(D)) v with q^, k^ rotated and rounded to bf16
@@ -177,8 +194,9 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
  * ([B][H][N][D] bf16) become keys key0 .. key0 + N - 1 of a prepared sequence
  * of n_kv keys (buffers of sol_prepared_kv_bytes(B, H, n_kv, D) bytes, the
  * layout of sol_prepare_kv).  The rotation uses this call's own grid T x Hl x
- * Wl (its first N - T*Hl*Wl keys are an unrotated prefix); with k_gamma_dev
- * the keys are RMS-normalised first, as in sol_qknorm_rope3d.  Several calls
+ * Wl and split dt/dh/dw (its first N - T*Hl*Wl keys are an unrotated prefix;
+ * rope_tab_dev the table of that grid and split); with k_gamma_dev the keys
+ * are RMS-normalised first, as in sol_qknorm_rope3d.  Several calls
  * fill one prepared sequence from several sources -- the paper's reference-KV
  * cache (Sec. 5, "Reference KV caching mechanism"): the reference tokens'
  * keys and values are prepared once, at the first denoising step, and later
@@ -186,11 +204,12 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
  * write only their own keys (a tile shared with another call's keys is
  * written element by element) and the zero padding past n_kv, so their order
  * does not matter.  0 <= key0, key0 + N <= n_kv <= SOL_MAX_TOKENS.
- * sol_prepare_kv(...) is sol_prepare_kv_ex with key0 = 0, n_kv = N and no
- * normalisation.
+ * sol_prepare_kv(...) is sol_prepare_kv_ex with key0 = 0, n_kv = N, the
+ * default split and no normalisation.
  *
  * sol_attn_fwd_prepared_ex: N query rows per slab (q, out: [B][H][N][D],
- * rotated with the grid T x Hl x Wl, RMS-normalised first with q_gamma_dev)
+ * rotated with the grid T x Hl x Wl and split dt/dh/dw, RMS-normalised first
+ * with q_gamma_dev)
  * against the n_kv prepared keys: out = softmax(q^ k^T / sqrt(D)) v over all
  * of them (n_kv may differ from N).  Every key must have been written by a
  * sol_prepare_kv_ex call.  out_format SOL_OUT_BF16: out is bf16 (2 bytes per
@@ -206,21 +225,21 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
  * dims, 128..131 the UE5M3 scale codes of dims [32g, 32g + 32), 132..143
  * zero; scales and codes follow the QKV records' rule (sol_qkv_encode),
  * applied to the fp32 result.
- * sol_attn_fwd_prepared(...) is this call with n_kv = N, no normalisation and
- * bf16 output.
+ * sol_attn_fwd_prepared(...) is this call with n_kv = N, the default split,
+ * no normalisation and bf16 output.
  *
  * gamma pointers: D fp32 device weights, 16-byte aligned, or NULL; eps as in
  * sol_qknorm_rope3d (ignored when the pointer is NULL).  Other arguments,
  * ownership and errors as sol_prepare_kv / sol_attn_fwd_prepared.
  */
 int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H,
-                      int N, int key0, int n_kv, int D, int T, int Hl, int Wl,
-                      const float* rope_tab_dev, const float* k_gamma_dev, float eps,
+                      int N, int key0, int n_kv, int D, int T, int Hl, int Wl, int dt, int dh,
+                      int dw, const float* rope_tab_dev, const float* k_gamma_dev, float eps,
                       sol_stream_t stream);
 int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_prep, void* out,
-                             int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl,
-                             const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                             int out_format, sol_stream_t stream);
+                             int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl, int dt,
+                             int dh, int dw, const float* rope_tab_dev, const float* q_gamma_dev,
+                             float eps, int out_format, sol_stream_t stream);
 
 /*
  * Block-sparse attention (Sec. 3.4, "Per-step dynamic sparsity" and "Safety
@@ -258,12 +277,14 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
  */
 size_t sol_sparse_workspace_bytes(int B, int H, int N, int D);
 int sol_sparse_route(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
-                     int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                     float tau, void* workspace, size_t workspace_bytes, sol_stream_t stream);
+                     int Wl, int dt, int dh, int dw, const float* rope_tab_dev,
+                     const float* q_gamma_dev, float eps, float tau, void* workspace,
+                     size_t workspace_bytes, sol_stream_t stream);
 int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
-                        int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
-                        const float* q_gamma_dev, float eps, const void* workspace,
-                        size_t workspace_bytes, int out_format, sol_stream_t stream);
+                        int H, int N, int D, int T, int Hl, int Wl, int dt, int dh, int dw,
+                        const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                        const void* workspace, size_t workspace_bytes, int out_format,
+                        sol_stream_t stream);
 
 /*
  * Bytes of device workspace sol_attn_fwd_ws needs: room for k_prep then

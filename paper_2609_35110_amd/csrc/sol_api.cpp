@@ -54,6 +54,24 @@ int check_norm(const float* gamma, float eps) {
   return SOL_OK;
 }
 
+// The rotary split: dt, dh, dw head dims turn with t, h, w; each a
+// non-negative multiple of 8 (whole 16-byte chunks), together at most D; the
+// remaining dims pass through.
+int check_split(int D, int dt, int dh, int dw) {
+  if (dt < 0 || dh < 0 || dw < 0 || dt % 8 || dh % 8 || dw % 8)
+    return fail(SOL_ERR_INVALID_ARG, "rotary split %d/%d/%d: each must be a non-negative multiple of 8", dt, dh, dw);
+  if ((int64_t)dt + dh + dw > D)
+    return fail(SOL_ERR_INVALID_ARG, "rotary split %d/%d/%d exceeds the head dim %d", dt, dh, dw, D);
+  return SOL_OK;
+}
+
+// The device table of a call: NULL when nothing rotates (an empty grid, or an
+// empty split).
+const float2* table_of(const float* rope_tab_dev, int T, int Hl, int Wl, int dt, int dh, int dw) {
+  const bool rotates = (int64_t)T * Hl * Wl > 0 && dt + dh + dw > 0;
+  return rotates ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
+}
+
 // Bytes of an attention output in out_format (0 for an unknown format).
 size_t out_bytes(int B, int H, int N, int D, int out_format) {
   const size_t rows = (size_t)B * H * N;
@@ -67,11 +85,12 @@ size_t out_bytes(int B, int H, int N, int D, int out_format) {
 
 // Common checks of the two block-sparse entry points.
 int check_sparse(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
-                 int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                 const void* workspace, size_t workspace_bytes) {
+                 int Wl, int dt, int dh, int dw, const float* rope_tab_dev, const float* q_gamma_dev,
+                 float eps, const void* workspace, size_t workspace_bytes) {
   if (!q || !k_prep) return fail(SOL_ERR_INVALID_ARG, "q and k_prep must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if ((st = check_split(D, dt, dh, dw)) != SOL_OK) return st;
   if (N > sol::sparse_max_tokens())
     return fail(SOL_ERR_UNSUPPORTED, "block-sparse attention takes N <= %d (got %d)", sol::sparse_max_tokens(), N);
   if (!aligned16(q) || !aligned16(k_prep)) return fail(SOL_ERR_INVALID_ARG, "q and k_prep must be 16-byte aligned");
@@ -93,7 +112,7 @@ int check_sparse(const void* q, const void* k_prep, int B, int H, int N, int D, 
 
 int sol::set_error(int status, const char* msg) { return fail(status, "%s", msg); }
 
-sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl) {
+sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl, int dt, int dh, int dw) {
   SeqGrid g;
   const int64_t nv = (int64_t)T * Hl * Wl;
   g.n = N;
@@ -105,22 +124,39 @@ sol::SeqGrid sol::make_grid(int N, int T, int Hl, int Wl) {
   g.hw = g.Hl * g.Wl;
   g.inv_hw = 1.0f / (float)g.hw;
   g.inv_wl = 1.0f / (float)g.Wl;
-  g.tab_h = g.T * (kHeadDim / 8);
-  g.tab_w = g.tab_h + g.Hl * (3 * kHeadDim / 16);
+  g.c_t = dt / 8;
+  g.c_h = g.c_t + dh / 8;
+  g.c_w = g.c_h + dw / 8;
+  g.s_t = dt / 2;
+  g.s_h = dh / 2;
+  g.s_w = dw / 2;
+  g.tab_h = g.T * g.s_t;
+  g.tab_w = g.tab_h + g.Hl * g.s_h;
+  g.tab_pairs = g.tab_w + g.Wl * g.s_w;
+  // row 0 of the first axis section that has one: angle 0 in every pair
+  g.id_pair = dt ? 0 : dh ? g.tab_h : g.tab_w;
   return g;
 }
 
 extern "C" {
 
-size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl) {
+size_t sol_rope3d_table_floats_ex(int D, int T, int Hl, int Wl, int dt, int dh, int dw) {
   if (D <= 0 || D % 16 != 0 || T < 0 || Hl < 0 || Wl < 0) return 0;
-  return 2 * ((size_t)T * (D / 8) + (size_t)Hl * (3 * D / 16) + (size_t)Wl * (3 * D / 16));
+  if (dt < 0 || dh < 0 || dw < 0 || dt % 8 || dh % 8 || dw % 8 || (int64_t)dt + dh + dw > D) return 0;
+  return 2 * ((size_t)T * (dt / 2) + (size_t)Hl * (dh / 2) + (size_t)Wl * (dw / 2));
 }
 
-int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, double base) {
-  const size_t need = sol_rope3d_table_floats(D, T, Hl, Wl);
-  if (need == 0 && (D <= 0 || D % 16 != 0 || T < 0 || Hl < 0 || Wl < 0))
+size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl) {
+  return sol_rope3d_table_floats_ex(D, T, Hl, Wl, D / 4, 3 * D / 8, 3 * D / 8);
+}
+
+int sol_rope3d_table_ex(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, int dt,
+                        int dh, int dw, double base) {
+  if (D <= 0 || D % 16 != 0 || T < 0 || Hl < 0 || Wl < 0)
     return fail(SOL_ERR_INVALID_ARG, "bad table shape D=%d grid %dx%dx%d", D, T, Hl, Wl);
+  int st = check_split(D, dt, dh, dw);
+  if (st != SOL_OK) return st;
+  const size_t need = sol_rope3d_table_floats_ex(D, T, Hl, Wl, dt, dh, dw);
   if (!host_tab && need) return fail(SOL_ERR_INVALID_ARG, "host_tab is NULL");
   if (n_floats < need) return fail(SOL_ERR_INVALID_ARG, "table needs %zu floats, got %zu", need, n_floats);
   if (!(base > 1.0) || !std::isfinite(base)) return fail(SOL_ERR_INVALID_ARG, "base must be finite and > 1");
@@ -135,30 +171,35 @@ int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int
         *dst++ = (float)std::sin(phi);
       }
   };
-  section(T, D / 4);
-  section(Hl, 3 * D / 8);
-  section(Wl, 3 * D / 8);
+  section(T, dt);
+  section(Hl, dh);
+  section(Wl, dw);
   return ok();
 }
 
+int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int Wl, double base) {
+  return sol_rope3d_table_ex(host_tab, n_floats, D, T, Hl, Wl, D / 4, 3 * D / 8, 3 * D / 8, base);
+}
+
 int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
-                      const float* rope_tab_dev, const float* gamma_dev, float eps,
-                      sol_stream_t stream) {
+                      int dt, int dh, int dw, const float* rope_tab_dev, const float* gamma_dev,
+                      float eps, sol_stream_t stream) {
   if (!x || !y) return fail(SOL_ERR_INVALID_ARG, "x and y must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if ((st = check_split(D, dt, dh, dw)) != SOL_OK) return st;
   if (!aligned16(x) || !aligned16(y)) return fail(SOL_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
   const int64_t nv = (int64_t)T * Hl * Wl;
-  if (nv > 0 && !rope_tab_dev) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev is NULL for a non-empty grid");
+  if (nv > 0 && dt + dh + dw > 0 && !rope_tab_dev)
+    return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev is NULL for a non-empty grid and split");
   if (rope_tab_dev && !aligned16(rope_tab_dev)) return fail(SOL_ERR_INVALID_ARG, "rope_tab_dev must be 16-byte aligned");
   st = check_norm(gamma_dev, eps);
   if (st != SOL_OK) return st;
   const size_t bytes = (size_t)B * H * N * D * 2;
   if (x != y && overlaps(x, bytes, y, bytes)) return fail(SOL_ERR_INVALID_ARG, "x and y partially overlap");
-  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl, dt, dh, dw);
   hipError_t e = sol::launch_rope3d(static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y),
-                                    (int64_t)B * H * N, g,
-                                    nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr,
+                                    (int64_t)B * H * N, g, table_of(rope_tab_dev, T, Hl, Wl, dt, dh, dw),
                                     gamma_dev, eps, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SOL_ERR_HIP, "rope3d launch: %s", hipGetErrorString(e));
   return ok();
@@ -166,7 +207,8 @@ int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T,
 
 int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl, int Wl,
                const float* rope_tab_dev, sol_stream_t stream) {
-  return sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab_dev, nullptr, 0.0f, stream);
+  return sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, D / 4, 3 * D / 8, 3 * D / 8, rope_tab_dev,
+                           nullptr, 0.0f, stream);
 }
 
 int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int D,
@@ -201,12 +243,13 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int D) {
 }
 
 int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H,
-                      int N, int key0, int n_kv, int D, int T, int Hl, int Wl,
-                      const float* rope_tab_dev, const float* k_gamma_dev, float eps,
+                      int N, int key0, int n_kv, int D, int T, int Hl, int Wl, int dt, int dh,
+                      int dw, const float* rope_tab_dev, const float* k_gamma_dev, float eps,
                       sol_stream_t stream) {
   if (!k || !v || !k_prep || !v_prep) return fail(SOL_ERR_INVALID_ARG, "k, v, k_prep, v_prep must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if ((st = check_split(D, dt, dh, dw)) != SOL_OK) return st;
   if (n_kv < 1 || n_kv > SOL_MAX_TOKENS)
     return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
   if (key0 < 0 || (int64_t)key0 + N > n_kv)
@@ -223,9 +266,8 @@ int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, 
       overlaps(v_prep, pbytes, k, bytes) || overlaps(v_prep, pbytes, v, bytes) ||
       overlaps(k_prep, pbytes, v_prep, pbytes))
     return fail(SOL_ERR_INVALID_ARG, "k_prep / v_prep overlap each other or k, v");
-  const int64_t nv = (int64_t)T * Hl * Wl;
-  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
-  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  const float2* tab = table_of(rope_tab_dev, T, Hl, Wl, dt, dh, dw);
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl, dt, dh, dw);
   hipError_t e = sol::launch_prepare_kv(static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                                         static_cast<uint16_t*>(k_prep), static_cast<uint16_t*>(v_prep), B * H,
                                         g, tab, key0, n_kv, k_gamma_dev, eps,
@@ -236,17 +278,18 @@ int sol_prepare_kv_ex(const void* k, const void* v, void* k_prep, void* v_prep, 
 
 int sol_prepare_kv(const void* k, const void* v, void* k_prep, void* v_prep, int B, int H, int N,
                    int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
-  return sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, 0, N, D, T, Hl, Wl, rope_tab_dev, nullptr,
-                           0.0f, stream);
+  return sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, 0, N, D, T, Hl, Wl, D / 4, 3 * D / 8,
+                           3 * D / 8, rope_tab_dev, nullptr, 0.0f, stream);
 }
 
 int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_prep, void* out,
-                             int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl,
-                             const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                             int out_format, sol_stream_t stream) {
+                             int B, int H, int N, int n_kv, int D, int T, int Hl, int Wl, int dt,
+                             int dh, int dw, const float* rope_tab_dev, const float* q_gamma_dev,
+                             float eps, int out_format, sol_stream_t stream) {
   if (!q || !k_prep || !v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "q, k_prep, v_prep, out must not be NULL");
   int st = check_shape(B, H, N, D, T, Hl, Wl);
   if (st != SOL_OK) return st;
+  if ((st = check_split(D, dt, dh, dw)) != SOL_OK) return st;
   if (n_kv < 1 || n_kv > SOL_MAX_TOKENS)
     return fail(n_kv < 1 ? SOL_ERR_INVALID_ARG : SOL_ERR_UNSUPPORTED, "n_kv=%d out of range", n_kv);
   if (!aligned16(q) || !aligned16(k_prep) || !aligned16(v_prep) || !aligned16(out))
@@ -261,9 +304,8 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
   if (overlaps(out, obytes, q, bytes) || overlaps(out, obytes, k_prep, pbytes) || overlaps(out, obytes, v_prep, pbytes))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep or v_prep");
   if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
-  const int64_t nv = (int64_t)T * Hl * Wl;
-  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
-  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  const float2* tab = table_of(rope_tab_dev, T, Hl, Wl, dt, dh, dw);
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl, dt, dh, dw);
   hipError_t e = sol::launch_attn_fwd_prepared(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
                                                static_cast<const uint16_t*>(v_prep), out, B * H, g, n_kv, tab,
                                                q_gamma_dev, eps, out_format, nullptr, nullptr, 0,
@@ -275,8 +317,8 @@ int sol_attn_fwd_prepared_ex(const void* q, const void* k_prep, const void* v_pr
 int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
                           int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
                           sol_stream_t stream) {
-  return sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, N, D, T, Hl, Wl, rope_tab_dev,
-                                  nullptr, 0.0f, SOL_OUT_BF16, stream);
+  return sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, N, D, T, Hl, Wl, D / 4, 3 * D / 8,
+                                  3 * D / 8, rope_tab_dev, nullptr, 0.0f, SOL_OUT_BF16, stream);
 }
 
 size_t sol_sparse_workspace_bytes(int B, int H, int N, int D) {
@@ -287,15 +329,15 @@ size_t sol_sparse_workspace_bytes(int B, int H, int N, int D) {
 }
 
 int sol_sparse_route(const void* q, const void* k_prep, int B, int H, int N, int D, int T, int Hl,
-                     int Wl, const float* rope_tab_dev, const float* q_gamma_dev, float eps,
-                     float tau, void* workspace, size_t workspace_bytes, sol_stream_t stream) {
-  int st = check_sparse(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab_dev, q_gamma_dev, eps, workspace,
-                        workspace_bytes);
+                     int Wl, int dt, int dh, int dw, const float* rope_tab_dev,
+                     const float* q_gamma_dev, float eps, float tau, void* workspace,
+                     size_t workspace_bytes, sol_stream_t stream) {
+  int st = check_sparse(q, k_prep, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab_dev, q_gamma_dev, eps,
+                        workspace, workspace_bytes);
   if (st != SOL_OK) return st;
   if (!std::isfinite(tau)) return fail(SOL_ERR_INVALID_ARG, "tau must be finite");
-  const int64_t nv = (int64_t)T * Hl * Wl;
-  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
-  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  const float2* tab = table_of(rope_tab_dev, T, Hl, Wl, dt, dh, dw);
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl, dt, dh, dw);
   hipError_t e = sol::launch_sparse_route(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_prep),
                                           B * H, g, tab, q_gamma_dev, eps, tau, workspace,
                                           reinterpret_cast<hipStream_t>(stream));
@@ -304,11 +346,12 @@ int sol_sparse_route(const void* q, const void* k_prep, int B, int H, int N, int
 }
 
 int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, void* out, int B,
-                        int H, int N, int D, int T, int Hl, int Wl, const float* rope_tab_dev,
-                        const float* q_gamma_dev, float eps, const void* workspace,
-                        size_t workspace_bytes, int out_format, sol_stream_t stream) {
-  int st = check_sparse(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab_dev, q_gamma_dev, eps, workspace,
-                        workspace_bytes);
+                        int H, int N, int D, int T, int Hl, int Wl, int dt, int dh, int dw,
+                        const float* rope_tab_dev, const float* q_gamma_dev, float eps,
+                        const void* workspace, size_t workspace_bytes, int out_format,
+                        sol_stream_t stream) {
+  int st = check_sparse(q, k_prep, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab_dev, q_gamma_dev, eps,
+                        workspace, workspace_bytes);
   if (st != SOL_OK) return st;
   if (!v_prep || !out) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must not be NULL");
   if (!aligned16(v_prep) || !aligned16(out)) return fail(SOL_ERR_INVALID_ARG, "v_prep and out must be 16-byte aligned");
@@ -321,9 +364,8 @@ int sol_attn_fwd_sparse(const void* q, const void* k_prep, const void* v_prep, v
       overlaps(out, obytes, v_prep, pbytes) || overlaps(out, obytes, workspace, need))
     return fail(SOL_ERR_INVALID_ARG, "out overlaps q, k_prep, v_prep or the workspace");
   if (sol::attn_max_workgroups(N, B * H) > INT32_MAX) return fail(SOL_ERR_UNSUPPORTED, "grid too large");
-  const int64_t nv = (int64_t)T * Hl * Wl;
-  const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
-  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
+  const float2* tab = table_of(rope_tab_dev, T, Hl, Wl, dt, dh, dw);
+  const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl, dt, dh, dw);
   size_t off[4];
   sol::sparse_workspace_offsets(B * H, N, off);
   const char* ws = static_cast<const char*>(workspace);
@@ -504,6 +546,6 @@ const char* sol_status_string(int status) {
 
 const char* sol_last_error(void) { return g_last_error; }
 
-int sol_version(void) { return 102; }
+int sol_version(void) { return 200; }
 
 }  // extern "C"

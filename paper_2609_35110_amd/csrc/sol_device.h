@@ -24,8 +24,6 @@ constexpr int kChunks = D / 8;  // 16-byte chunks (8 bf16 = 4 rotary pairs) per 
 
 // ------------------------------------------------------------ rotary helpers
 
-// n / d for 0 <= n < 2^23, d >= 1: float reciprocal estimate (off by at most
-// one) and one integer correction.
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup w runs on
 // XCD w % 8), and each XCD has its own L2.  Renumber them so that XCD x gets
 // one contiguous range of work items: the workgroups an XCD runs at the same
@@ -38,6 +36,8 @@ __device__ __forceinline__ int xcd_local_id(int w, int n) {
   return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
+// n / d for 0 <= n < 2^23, d >= 1: float reciprocal estimate (off by at most
+// one) and one integer correction.
 __device__ __forceinline__ int div_exact(int n, int d, float inv) {
   int q = (int)((float)n * inv);
   int r = n - q * d;
@@ -62,12 +62,16 @@ __device__ __forceinline__ Pos token_pos(int n, const SeqGrid& g) {
   return p;
 }
 
-// First table pair of 16-byte chunk cc (head dims [8cc, 8cc+8)) at position p.
-// Chunks 0-3 carry t, 4-9 carry h, 10-15 carry w (the 32/48/48 split).
+// First table pair of 16-byte chunk cc (head dims [8cc, 8cc+8)) at position p,
+// under the grid's rotary split (32/48/48 by default: chunks 0-3 carry t, 4-9
+// h, 10-15 w).  A chunk past the split passes through: it turns by the pairs
+// of a position-0 row, angle 0, (cos, sin) = (1, 0), an exact identity (as
+// prefix tokens do, at position (0, 0, 0)).
 __device__ __forceinline__ int tab_pair(int cc, const Pos& p, const SeqGrid& g) {
-  if (cc < 4) return p.t * 16 + 4 * cc;
-  if (cc < 10) return g.tab_h + p.h * 24 + 4 * (cc - 4);
-  return g.tab_w + p.w * 24 + 4 * (cc - 10);
+  if (cc < g.c_t) return p.t * g.s_t + 4 * cc;
+  if (cc < g.c_h) return g.tab_h + p.h * g.s_h + 4 * (cc - g.c_t);
+  if (cc < g.c_w) return g.tab_w + p.w * g.s_w + 4 * (cc - g.c_h);
+  return g.id_pair;
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {

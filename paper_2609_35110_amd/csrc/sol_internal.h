@@ -10,7 +10,13 @@ namespace sol {
 
 constexpr int kHeadDim = 128;
 
-// Latent grid and packing of one sequence.  Derived on the host.
+// The default rotary split of the head dims across (t, h, w): D/4, 3D/8, 3D/8.
+constexpr int kSplitT = kHeadDim / 4, kSplitH = 3 * kHeadDim / 8, kSplitW = 3 * kHeadDim / 8;
+
+// Latent grid, packing and rotary split of one sequence.  Derived on the host.
+// The split is counted in 16-byte chunks of 8 head dims: chunks [0, c_t) turn
+// with the frame t, [c_t, c_h) with the row h, [c_h, c_w) with the column w,
+// and [c_w, D/8) pass through unrotated.
 struct SeqGrid {
   int n;        // tokens per sequence N
   int nt;       // prefix (unrotated) tokens: N - T*Hl*Wl
@@ -18,11 +24,17 @@ struct SeqGrid {
   int hw;       // Hl * Wl
   float inv_hw; // 1 / (Hl*Wl), for exact-after-correction division
   float inv_wl; // 1 / Wl
-  int tab_h;    // first pair of the row-axis section of the table  (T * D/8)
-  int tab_w;    // first pair of the column-axis section  (T*D/8 + Hl*3D/16)
+  int c_t, c_h, c_w;  // chunk boundaries of the split (dt/8, (dt+dh)/8, (dt+dh+dw)/8)
+  int s_t, s_h, s_w;  // table pairs per position of each axis (dt/2, dh/2, dw/2)
+  int tab_h;    // first pair of the row-axis section of the table  (T dt/2)
+  int tab_w;    // first pair of the column-axis section  (T dt/2 + Hl dh/2)
+  int tab_pairs;  // pairs in the whole table
+  int id_pair;  // first pair of a position-0 row: angle 0, (cos, sin) = (1, 0)
 };
 
-SeqGrid make_grid(int N, int T, int Hl, int Wl);
+// dt, dh, dw: multiples of 8 (validated by the caller), dt + dh + dw <= D.
+SeqGrid make_grid(int N, int T, int Hl, int Wl, int dt = kSplitT, int dh = kSplitH,
+                  int dw = kSplitW);
 
 // gamma != nullptr: RMS-normalise every row with these D weights first.
 hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int64_t rows, const SeqGrid& g,

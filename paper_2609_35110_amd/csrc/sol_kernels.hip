@@ -177,13 +177,17 @@ static_assert(kThreads == 8 * BN, "staging: one tile row per 8 threads, two 16-b
 // Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
 constexpr int kSgMfma = 0x008, kSgValu = 0x002, kSgDsRead = 0x100, kSgDsWrite = 0x200;
 
-// First table pair of chunk c (< 8: frame or row axis) and c + 8 (row or column axis).
+// First table pair of chunk c (< 8: frame or row axis) and c + 8 (row or column
+// axis) under the default 32/48/48 split -- the only one sol_attn_fwd, whose
+// signature carries no split, launches this kernel with -- in two selects
+// instead of tab_pair's three.
 __device__ __forceinline__ int tab_pair_lo(int c, const Pos& p, const SeqGrid& g) {
   return c < 4 ? p.t * 16 + 4 * c : g.tab_h + p.h * 24 + 4 * (c - 4);
 }
 __device__ __forceinline__ int tab_pair_hi(int c, const Pos& p, const SeqGrid& g) {
   return c < 2 ? g.tab_h + p.h * 24 + 4 * (c + 4) : g.tab_w + p.w * 24 + 4 * (c - 2);
 }
+static_assert(kSplitT == 32 && kSplitH == 48 && kSplitW == 48, "tab_pair_lo/hi assume 32/48/48");
 
 // Software pipeline, per wave, one barrier per 64-key tile.  Iteration i:
 //   phase A (one scheduling region): S(i+1) = K^(i+1) Q^^T on the matrix
@@ -1329,7 +1333,7 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
-  const int tab_pairs = g.tab_w + g.Wl * (3 * D / 16);
+  const int tab_pairs = g.tab_pairs;
   if (tab == nullptr)
     hipLaunchKernelGGL((attn_fwd_kernel<false, false>), grid, dim3(kThreads), 0, stream, q,
                        k, v, out, g, tab, 0, n_qtiles, c_log2);

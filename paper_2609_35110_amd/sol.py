@@ -49,6 +49,10 @@ def lib():
         L.sol_rope3d_table_floats.restype = sz
         L.sol_rope3d_table.argtypes = [P, sz, i32, i32, i32, i32, f64]
         L.sol_rope3d_table.restype = i32
+        L.sol_rope3d_table_floats_ex.argtypes = [i32] * 7
+        L.sol_rope3d_table_floats_ex.restype = sz
+        L.sol_rope3d_table_ex.argtypes = [P, sz] + [i32] * 7 + [f64]
+        L.sol_rope3d_table_ex.restype = i32
         L.sol_rope3d.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_rope3d.restype = i32
         L.sol_attn_fwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
@@ -66,21 +70,17 @@ def lib():
         L.sol_attn_fwd_noalloc.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_attn_fwd_noalloc.restype = i32
         f32 = ctypes.c_float
-        L.sol_qknorm_rope3d.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32, P]
+        L.sol_qknorm_rope3d.argtypes = [P, P] + [i32] * 10 + [P, P, f32, P]
         L.sol_qknorm_rope3d.restype = i32
-        L.sol_prepare_kv_ex.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32,
-                                        P, P, f32, P]
+        L.sol_prepare_kv_ex.argtypes = [P, P, P, P] + [i32] * 12 + [P, P, f32, P]
         L.sol_prepare_kv_ex.restype = i32
-        L.sol_attn_fwd_prepared_ex.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
-                                               P, P, f32, i32, P]
+        L.sol_attn_fwd_prepared_ex.argtypes = [P, P, P, P] + [i32] * 11 + [P, P, f32, i32, P]
         L.sol_attn_fwd_prepared_ex.restype = i32
         L.sol_sparse_workspace_bytes.argtypes = [i32, i32, i32, i32]
         L.sol_sparse_workspace_bytes.restype = sz
-        L.sol_sparse_route.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32, f32, P,
-                                       sz, P]
+        L.sol_sparse_route.argtypes = [P, P] + [i32] * 10 + [P, P, f32, f32, P, sz, P]
         L.sol_sparse_route.restype = i32
-        L.sol_attn_fwd_sparse.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P, f32,
-                                          P, sz, i32, P]
+        L.sol_attn_fwd_sparse.argtypes = [P, P, P, P] + [i32] * 10 + [P, P, f32, P, sz, i32, P]
         L.sol_attn_fwd_sparse.restype = i32
         L.sol_qkv_record_bytes.argtypes = [i32, i32, i32]
         L.sol_qkv_record_bytes.restype = sz
@@ -118,40 +118,50 @@ def sol_rope3d_table(host_tab, n_floats, D, T, Hl, Wl, base):
     return lib().sol_rope3d_table(host_tab, n_floats, D, T, Hl, Wl, base)
 
 
+def sol_rope3d_table_floats_ex(D, T, Hl, Wl, dt, dh, dw):
+    return lib().sol_rope3d_table_floats_ex(D, T, Hl, Wl, dt, dh, dw)
+
+
+def sol_rope3d_table_ex(host_tab, n_floats, D, T, Hl, Wl, dt, dh, dw, base):
+    return lib().sol_rope3d_table_ex(host_tab, n_floats, D, T, Hl, Wl, dt, dh, dw, base)
+
+
 def sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream):
     return lib().sol_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, stream)
 
 
-def sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, stream):
-    return lib().sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, stream)
+def sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab, gamma, eps, stream):
+    return lib().sol_qknorm_rope3d(x, y, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab, gamma, eps,
+                                   stream)
 
 
-def sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl, rope_tab, gamma,
-                      eps, stream):
-    return lib().sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl,
-                                   rope_tab, gamma, eps, stream)
+def sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl, dt, dh, dw, rope_tab,
+                      gamma, eps, stream):
+    return lib().sol_prepare_kv_ex(k, v, k_prep, v_prep, B, H, N, key0, n_kv, D, T, Hl, Wl, dt, dh,
+                                   dw, rope_tab, gamma, eps, stream)
 
 
-def sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl, rope_tab, gamma,
-                             eps, out_format, stream):
-    return lib().sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl,
-                                          rope_tab, gamma, eps, out_format, stream)
+def sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl, dt, dh, dw,
+                             rope_tab, gamma, eps, out_format, stream):
+    return lib().sol_attn_fwd_prepared_ex(q, k_prep, v_prep, out, B, H, N, n_kv, D, T, Hl, Wl, dt,
+                                          dh, dw, rope_tab, gamma, eps, out_format, stream)
 
 
 def sol_sparse_workspace_bytes(B, H, N, D):
     return lib().sol_sparse_workspace_bytes(B, H, N, D)
 
 
-def sol_sparse_route(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, tau, workspace,
-                     workspace_bytes, stream):
-    return lib().sol_sparse_route(q, k_prep, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps, tau,
-                                  workspace, workspace_bytes, stream)
+def sol_sparse_route(q, k_prep, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab, gamma, eps, tau,
+                     workspace, workspace_bytes, stream):
+    return lib().sol_sparse_route(q, k_prep, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab, gamma, eps,
+                                  tau, workspace, workspace_bytes, stream)
 
 
-def sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab, gamma, eps,
-                        workspace, workspace_bytes, out_format, stream):
-    return lib().sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, rope_tab, gamma,
-                                     eps, workspace, workspace_bytes, out_format, stream)
+def sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, dt, dh, dw, rope_tab, gamma,
+                        eps, workspace, workspace_bytes, out_format, stream):
+    return lib().sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, dt, dh, dw,
+                                     rope_tab, gamma, eps, workspace, workspace_bytes, out_format,
+                                     stream)
 
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
@@ -234,17 +244,30 @@ def check(status):
 
 # ------------------------------------------------------- torch marshalling
 
-def rope3d_table_host(T, Hl, Wl, D=HEAD_DIM, base=ROPE_BASE) -> np.ndarray:
-    """The rotary table as a host float32 array (built by the library)."""
-    n = sol_rope3d_table_floats(D, T, Hl, Wl)
+DEFAULT_SPLIT = (HEAD_DIM // 4, 3 * HEAD_DIM // 8, 3 * HEAD_DIM // 8)
+
+
+def _split(split):
+    """(dt, dh, dw): the head dims turned by t, h, w (None: the default 32/48/48)."""
+    if split is None:
+        return DEFAULT_SPLIT
+    dt, dh, dw = (int(x) for x in split)
+    return dt, dh, dw
+
+
+def rope3d_table_host(T, Hl, Wl, D=HEAD_DIM, base=ROPE_BASE, split=None) -> np.ndarray:
+    """The rotary table of grid T x Hl x Wl and split (dt, dh, dw) as a host
+    float32 array (built by the library)."""
+    dt, dh, dw = _split(split)
+    n = sol_rope3d_table_floats_ex(D, T, Hl, Wl, dt, dh, dw)
     tab = np.zeros(max(n, 4), dtype=np.float32)
-    check(sol_rope3d_table(tab.ctypes.data_as(ctypes.c_void_p), n, D, T, Hl, Wl, base))
+    check(sol_rope3d_table_ex(tab.ctypes.data_as(ctypes.c_void_p), n, D, T, Hl, Wl, dt, dh, dw, base))
     return tab
 
 
-def rope3d_table(T, Hl, Wl, D=HEAD_DIM, base=ROPE_BASE, device="cuda") -> torch.Tensor:
+def rope3d_table(T, Hl, Wl, D=HEAD_DIM, base=ROPE_BASE, device="cuda", split=None) -> torch.Tensor:
     """The rotary table, copied to `device` (float32)."""
-    return torch.from_numpy(rope3d_table_host(T, Hl, Wl, D, base)).to(device)
+    return torch.from_numpy(rope3d_table_host(T, Hl, Wl, D, base, split)).to(device)
 
 
 def _stream(t):
@@ -264,11 +287,18 @@ def _check_tensor(name, t, shape=None):
         raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
 
 
-def _table_ptr(table, dev):
+def _table_ptr(table, dev, D, T, Hl, Wl, split=None):
+    """The device pointer of a rotary table, checked against the size the
+    kernels read for this grid and split (the C ABI receives only the
+    pointer, so a table built for another grid would be read past its end)."""
     if table is None:
         return None
     if table.dtype != torch.float32 or table.device != dev or not table.is_contiguous():
         raise ValueError("rope table must be a contiguous float32 tensor on %s" % dev)
+    need = sol_rope3d_table_floats_ex(D, T, Hl, Wl, *_split(split))
+    if T * Hl * Wl > 0 and table.numel() < need:
+        raise ValueError("rope table holds %d floats; grid %dx%dx%d and split %s need %d"
+                         % (table.numel(), T, Hl, Wl, _split(split), need))
     return ctypes.c_void_p(table.data_ptr())
 
 
@@ -280,7 +310,7 @@ def rope3d(x, T, Hl, Wl, table, out=None):
         out = torch.empty_like(x)
     _check_tensor("out", out, x.shape)
     check(sol_rope3d(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N, D,
-                     T, Hl, Wl, _table_ptr(table, x.device), _stream(x)))
+                     T, Hl, Wl, _table_ptr(table, x.device, D, T, Hl, Wl, None), _stream(x)))
     return out
 
 
@@ -294,7 +324,7 @@ def _gamma_ptr(gamma, dev):
     return ctypes.c_void_p(gamma.data_ptr())
 
 
-def qknorm_rope3d(x, T, Hl, Wl, table, gamma, eps=1e-6, out=None):
+def qknorm_rope3d(x, T, Hl, Wl, table, gamma, eps=1e-6, out=None, split=None):
     """out = bf16(R(pos) rms_norm(x; gamma, eps)) for x [B, H, N, D] bf16."""
     _check_tensor("x", x)
     B, H, N, D = x.shape
@@ -302,7 +332,7 @@ def qknorm_rope3d(x, T, Hl, Wl, table, gamma, eps=1e-6, out=None):
         out = torch.empty_like(x)
     _check_tensor("out", out, x.shape)
     check(sol_qknorm_rope3d(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H,
-                            N, D, T, Hl, Wl, _table_ptr(table, x.device),
+                            N, D, T, Hl, Wl, *_split(split), _table_ptr(table, x.device, D, T, Hl, Wl, split),
                             _gamma_ptr(gamma, x.device), float(eps), _stream(x)))
     return out
 
@@ -318,7 +348,7 @@ def attn_fwd(q, k, v, T, Hl, Wl, table=None, out=None):
     _check_tensor("out", out, q.shape)
     check(sol_attn_fwd(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
                        ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N, D,
-                       T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
+                       T, Hl, Wl, _table_ptr(table, q.device, D, T, Hl, Wl, None), _stream(q)))
     return out
 
 
@@ -345,7 +375,7 @@ def attn_fwd_ws(q, k, v, T, Hl, Wl, table=None, workspace=None, out=None):
     nbytes = workspace.numel() * workspace.element_size()
     check(sol_attn_fwd_ws(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
                           ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N,
-                          D, T, Hl, Wl, _table_ptr(table, q.device),
+                          D, T, Hl, Wl, _table_ptr(table, q.device, D, T, Hl, Wl, None),
                           ctypes.c_void_p(workspace.data_ptr()), nbytes, _stream(q)))
     return out
 
@@ -362,7 +392,7 @@ def attn_fwd_noalloc(q, k, v, T, Hl, Wl, table=None, out=None):
     _check_tensor("out", out, q.shape)
     check(sol_attn_fwd_noalloc(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
                                ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H, N,
-                               D, T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
+                               D, T, Hl, Wl, _table_ptr(table, q.device, D, T, Hl, Wl, None), _stream(q)))
     return out
 
 
@@ -390,7 +420,7 @@ def prepare_kv(k, v, T, Hl, Wl, table=None, k_prep=None, v_prep=None):
     _check_prepared("v_prep", v_prep, nbytes, k.device)
     check(sol_prepare_kv(ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
                          ctypes.c_void_p(k_prep.data_ptr()), ctypes.c_void_p(v_prep.data_ptr()),
-                         B, H, N, D, T, Hl, Wl, _table_ptr(table, k.device), _stream(k)))
+                         B, H, N, D, T, Hl, Wl, _table_ptr(table, k.device, D, T, Hl, Wl, None), _stream(k)))
     return k_prep, v_prep
 
 
@@ -406,7 +436,7 @@ def attn_fwd_prepared(q, k_prep, v_prep, T, Hl, Wl, table=None, out=None):
     _check_tensor("out", out, q.shape)
     check(sol_attn_fwd_prepared(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                                 ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
-                                B, H, N, D, T, Hl, Wl, _table_ptr(table, q.device), _stream(q)))
+                                B, H, N, D, T, Hl, Wl, _table_ptr(table, q.device, D, T, Hl, Wl, None), _stream(q)))
     return out
 
 
@@ -417,7 +447,8 @@ def prepared_kv_buffers(B, H, n_kv, device):
             torch.zeros(n, dtype=torch.float16, device=device))
 
 
-def prepare_kv_ex(k, v, T, Hl, Wl, table, k_prep, v_prep, key0=0, n_kv=None, gamma=None, eps=1e-6):
+def prepare_kv_ex(k, v, T, Hl, Wl, table, k_prep, v_prep, key0=0, n_kv=None, gamma=None, eps=1e-6,
+                  split=None):
     """Write k, v [B, H, N, D] (rotated with grid T x Hl x Wl, normalised with
     gamma if given) as keys key0 .. key0 + N - 1 of the prepared sequence of
     n_kv keys held by k_prep, v_prep."""
@@ -430,7 +461,7 @@ def prepare_kv_ex(k, v, T, Hl, Wl, table, k_prep, v_prep, key0=0, n_kv=None, gam
     _check_prepared("v_prep", v_prep, nbytes, k.device)
     check(sol_prepare_kv_ex(ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
                             ctypes.c_void_p(k_prep.data_ptr()), ctypes.c_void_p(v_prep.data_ptr()),
-                            B, H, N, key0, n_kv, D, T, Hl, Wl, _table_ptr(table, k.device),
+                            B, H, N, key0, n_kv, D, T, Hl, Wl, *_split(split), _table_ptr(table, k.device, D, T, Hl, Wl, split),
                             _gamma_ptr(gamma, k.device), float(eps), _stream(k)))
     return k_prep, v_prep
 
@@ -455,7 +486,7 @@ def _out_tensor(out, B, H, N, device, fp8, int8_records):
 
 
 def attn_fwd_prepared_ex(q, k_prep, v_prep, n_kv, T, Hl, Wl, table=None, gamma=None, eps=1e-6,
-                         out=None, fp8=False, int8_records=False):
+                         out=None, fp8=False, int8_records=False, split=None):
     """q [B, H, N, D] (rotated with grid T x Hl x Wl, normalised with gamma if
     given) against the n_kv prepared keys of k_prep, v_prep.  fp8: the output
     is FP8 E4M3 codes (uint8 [B, H, N, D], unit scale) instead of bf16;
@@ -468,7 +499,7 @@ def attn_fwd_prepared_ex(q, k_prep, v_prep, n_kv, T, Hl, Wl, table=None, gamma=N
     out, fmt = _out_tensor(out, B, H, N, q.device, fp8, int8_records)
     check(sol_attn_fwd_prepared_ex(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                                    ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()),
-                                   B, H, N, n_kv, D, T, Hl, Wl, _table_ptr(table, q.device),
+                                   B, H, N, n_kv, D, T, Hl, Wl, *_split(split), _table_ptr(table, q.device, D, T, Hl, Wl, split),
                                    _gamma_ptr(gamma, q.device), float(eps), fmt, _stream(q)))
     return out
 
@@ -495,7 +526,7 @@ def _check_workspace(ws, nbytes, device):
                          % (nbytes, device))
 
 
-def sparse_route(q, k_prep, T, Hl, Wl, table, tau, workspace=None, gamma=None, eps=1e-6):
+def sparse_route(q, k_prep, T, Hl, Wl, table, tau, workspace=None, gamma=None, eps=1e-6, split=None):
     """Route every 256-row query block of q [B, H, N, D] over the 128-key
     blocks of the prepared keys (threshold mean + tau * std, prefix sink).
     Returns the workspace holding the routing."""
@@ -507,7 +538,7 @@ def sparse_route(q, k_prep, T, Hl, Wl, table, tau, workspace=None, gamma=None, e
     nbytes = sol_sparse_workspace_bytes(B, H, N, D)
     _check_workspace(workspace, nbytes, q.device)
     check(sol_sparse_route(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()), B, H,
-                           N, D, T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(gamma, q.device),
+                           N, D, T, Hl, Wl, *_split(split), _table_ptr(table, q.device, D, T, Hl, Wl, split), _gamma_ptr(gamma, q.device),
                            float(eps), float(tau), ctypes.c_void_p(workspace.data_ptr()),
                            workspace.numel() * workspace.element_size(), _stream(q)))
     return workspace
@@ -527,7 +558,7 @@ def sparse_routing(workspace, B, H, N):
 
 
 def attn_fwd_sparse(q, k_prep, v_prep, T, Hl, Wl, table, workspace, gamma=None, eps=1e-6, out=None,
-                    fp8=False, int8_records=False):
+                    fp8=False, int8_records=False, split=None):
     """Block-sparse attention under the routing held by the workspace."""
     _check_tensor("q", q)
     B, H, N, D = q.shape
@@ -538,7 +569,8 @@ def attn_fwd_sparse(q, k_prep, v_prep, T, Hl, Wl, table, workspace, gamma=None, 
     out, fmt = _out_tensor(out, B, H, N, q.device, fp8, int8_records)
     check(sol_attn_fwd_sparse(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k_prep.data_ptr()),
                               ctypes.c_void_p(v_prep.data_ptr()), ctypes.c_void_p(out.data_ptr()), B, H,
-                              N, D, T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(gamma, q.device),
+                              N, D, T, Hl, Wl, *_split(split), _table_ptr(table, q.device, D, T, Hl, Wl, split),
+                              _gamma_ptr(gamma, q.device),
                               float(eps), ctypes.c_void_p(workspace.data_ptr()),
                               workspace.numel() * workspace.element_size(), fmt, _stream(q)))
     return out
@@ -571,7 +603,7 @@ def qkv_encode(q, k, v, T=0, Hl=0, Wl=0, table=None, q_gamma=None, k_gamma=None,
     _check_records(rec, B, H, N, q.device)
     check(sol_qkv_encode(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
                          ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(rec.data_ptr()), B, H, N, D,
-                         T, Hl, Wl, _table_ptr(table, q.device), _gamma_ptr(q_gamma, q.device),
+                         T, Hl, Wl, _table_ptr(table, q.device, D, T, Hl, Wl, None), _gamma_ptr(q_gamma, q.device),
                          _gamma_ptr(k_gamma, q.device), float(eps), _stream(q)))
     return rec
 
@@ -591,7 +623,7 @@ def qkv_encode_packed(qkv, T=0, Hl=0, Wl=0, table=None, q_gamma=None, k_gamma=No
     check(sol_qkv_encode_strided(ctypes.c_void_p(base), ctypes.c_void_p(base + H * D * el),
                                  ctypes.c_void_p(base + 2 * H * D * el), N * 3 * H * D, D, 3 * H * D,
                                  ctypes.c_void_p(rec.data_ptr()), B, H, N, D, T, Hl, Wl,
-                                 _table_ptr(table, qkv.device), _gamma_ptr(q_gamma, qkv.device),
+                                 _table_ptr(table, qkv.device, D, T, Hl, Wl, None), _gamma_ptr(q_gamma, qkv.device),
                                  _gamma_ptr(k_gamma, qkv.device), float(eps), _stream(qkv)))
     return rec
 

@@ -227,6 +227,35 @@ def pin_rope_numpy_twin(o):
     assert np.allclose(o.rope3d_f64(x, T, Hl, Wl, SPLIT, BASE), brute.rope_np(x, ang), atol=1e-12)
 
 
+def pin_rope_partial_split(o):
+    """Partial RoPE under a split (dt, dh, dw) with dt + dh + dw < D: the dims
+    past dt + dh + dw pass through bit for bit, every other pair is a
+    rotation, and at position 1 along axis a the pairs of that axis's section
+    turn by a geometric progression starting at 1 rad with ratio
+    base^(-2/d_a), d_a the split's own width (not the default one)."""
+    rng = np.random.default_rng(10)
+    for split in [(16, 24, 24), (0, 64, 64), (8, 0, 40)]:
+        tot = sum(split)
+        T, Hl, Wl = 3, 4, 5
+        N = T * Hl * Wl
+        x = rng.standard_normal((N, D))
+        y = o.rope3d_f64(x, T, Hl, Wl, split, BASE)
+        assert np.array_equal(y[:, tot:], x[:, tot:]), "pass-through dims changed under %s" % (split,)
+        assert np.allclose(np.hypot(y[:, 0::2], y[:, 1::2]), np.hypot(x[:, 0::2], x[:, 1::2]), atol=1e-12)
+        off = 0
+        for axis, d in enumerate(split):
+            if d:
+                dims = [1, 1, 1]
+                dims[axis] = 2
+                u = np.zeros((2, D))
+                u[:, 0::2] = 1.0  # every pair starts at angle 0
+                r = o.rope3d_f64(u, *dims, split, BASE)  # token 1 sits at position 1 on `axis`
+                ang = np.arctan2(r[1, off + 1:off + d:2], r[1, off:off + d:2])
+                want = BASE ** (-2.0 * np.arange(d // 2) / d)
+                assert np.allclose(ang, want, atol=1e-12), "axis %d of split %s" % (axis, split)
+            off += d
+
+
 def pin_rope_contract_rounding(o):
     """Contract mode is exactly: rotate in double, round once to nearest bf16."""
     rng = np.random.default_rng(9)

@@ -39,7 +39,7 @@ def test_status_strings(L):
     assert sol.sol_status_string(0) == "ok"
     for s in (-1, -2, -3):
         assert sol.sol_status_string(s) not in ("ok", "unknown status")
-    assert sol.sol_version() == 102
+    assert sol.sol_version() == 200
 
 
 # Fake, 16-byte aligned device addresses: every call below is rejected on the
@@ -166,14 +166,18 @@ G = P(0x20000000)  # fake, aligned device address of normalisation weights
     (dict(eps=float("nan")), -1, "eps"),
     (dict(k_prep=P(0x200000 + 4096)), -1, "overlap"),   # k_prep inside v
     (dict(T=9), -1, "more tokens"),
+    (dict(sp=(4, 48, 48)), -1, "multiple of 8"),
+    (dict(sp=(-8, 48, 48)), -1, "non-negative multiple of 8"),
+    (dict(sp=(32, 48, 56)), -1, "exceeds the head dim"),
 ])
 def test_prepare_kv_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     args = dict(k=A, v=Bp, k_prep=P(0x1000000), v_prep=P(0x2000000), B=1, H=2, N=192, key0=0,
-                n_kv=192, D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6)
+                n_kv=192, D=128, T=3, Hl=8, Wl=8, sp=(32, 48, 48), tab=TAB, gamma=G, eps=1e-6)
     args.update(kw)
     st = sol.sol_prepare_kv_ex(args["k"], args["v"], args["k_prep"], args["v_prep"], args["B"],
                                args["H"], args["N"], args["key0"], args["n_kv"], args["D"], args["T"],
-                               args["Hl"], args["Wl"], args["tab"], args["gamma"], args["eps"], None)
+                               args["Hl"], args["Wl"], *args["sp"], args["tab"], args["gamma"],
+                               args["eps"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
 
@@ -189,15 +193,18 @@ def test_prepare_kv_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     (dict(out=P(0x100000 - 49152)), -1, "overlaps"),   # 96 KB of bf16 out would reach q
     (dict(out=P(0x100000 - 49152 + 16), fmt=1), -1, "overlaps"),  # 48 KB of E4M3 out reaches q
     (dict(out=P(0x100000 - 55296 + 16), fmt=2), -1, "overlaps"),  # 54 KB of records reach q
+    (dict(sp=(4, 48, 48)), -1, "multiple of 8"),
+    (dict(sp=(-8, 48, 48)), -1, "non-negative multiple of 8"),
+    (dict(sp=(32, 48, 56)), -1, "exceeds the head dim"),
 ])
 def test_attn_fwd_prepared_ex_rejects_before_any_hip_call(L, kw, status, fragment):
     args = dict(q=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=192, n_kv=1000,
-                D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6, fmt=0)
+                D=128, T=3, Hl=8, Wl=8, sp=(32, 48, 48), tab=TAB, gamma=G, eps=1e-6, fmt=0)
     args.update(kw)
     st = sol.sol_attn_fwd_prepared_ex(args["q"], args["k_prep"], args["v_prep"], args["out"],
                                       args["B"], args["H"], args["N"], args["n_kv"], args["D"],
-                                      args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"],
-                                      args["eps"], args["fmt"], None)
+                                      args["T"], args["Hl"], args["Wl"], *args["sp"], args["tab"],
+                                      args["gamma"], args["eps"], args["fmt"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
 
@@ -207,13 +214,17 @@ def test_attn_fwd_prepared_ex_rejects_before_any_hip_call(L, kw, status, fragmen
     (dict(eps=-0.5), -1),
     (dict(tab=None), -1),
     (dict(D=96), -2),
+    (dict(sp=(4, 48, 48)), -1),
+    (dict(sp=(32, 48, -8)), -1),
+    (dict(sp=(64, 64, 8)), -1),
 ])
 def test_qknorm_rope3d_rejects_before_any_hip_call(L, kw, status):
-    args = dict(x=A, y=Bp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, tab=TAB, gamma=G, eps=1e-6)
+    args = dict(x=A, y=Bp, B=1, H=2, N=192, D=128, T=3, Hl=8, Wl=8, sp=(32, 48, 48), tab=TAB, gamma=G,
+                eps=1e-6)
     args.update(kw)
     st = sol.sol_qknorm_rope3d(args["x"], args["y"], args["B"], args["H"], args["N"], args["D"],
-                               args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"],
-                               args["eps"], None)
+                               args["T"], args["Hl"], args["Wl"], *args["sp"], args["tab"],
+                               args["gamma"], args["eps"], None)
     assert st == status, sol.sol_last_error()
 
 
@@ -242,16 +253,19 @@ WSS = P(0x30000000)
     (dict(tau=float("inf")), -1, "tau"),
     (dict(gamma=P(0x20000004)), -1, "gamma"),
     (dict(k_prep=None), -1, "NULL"),
+    (dict(sp=(4, 48, 48)), -1, "multiple of 8"),
+    (dict(sp=(-8, 48, 48)), -1, "non-negative multiple of 8"),
+    (dict(sp=(32, 48, 56)), -1, "exceeds the head dim"),
 ])
 def test_sparse_route_rejects_before_any_hip_call(L, kw, status, fragment):
-    args = dict(q=A, k_prep=P(0x1000000), B=1, H=2, N=1000, D=128, T=1, Hl=10, Wl=100, tab=TAB,
-                gamma=None, eps=1e-6, tau=1.0, ws=WSS, ws_bytes=None)
+    args = dict(q=A, k_prep=P(0x1000000), B=1, H=2, N=1000, D=128, T=1, Hl=10, Wl=100, sp=(32, 48, 48),
+                tab=TAB, gamma=None, eps=1e-6, tau=1.0, ws=WSS, ws_bytes=None)
     args.update(kw)
     if args["ws_bytes"] is None:
         args["ws_bytes"] = sol.sol_sparse_workspace_bytes(args["B"], args["H"], min(args["N"], 1 << 20), 128)
     st = sol.sol_sparse_route(args["q"], args["k_prep"], args["B"], args["H"], args["N"], args["D"],
-                              args["T"], args["Hl"], args["Wl"], args["tab"], args["gamma"], args["eps"],
-                              args["tau"], args["ws"], args["ws_bytes"], None)
+                              args["T"], args["Hl"], args["Wl"], *args["sp"], args["tab"], args["gamma"],
+                              args["eps"], args["tau"], args["ws"], args["ws_bytes"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
 
@@ -261,17 +275,21 @@ def test_sparse_route_rejects_before_any_hip_call(L, kw, status, fragment):
     (dict(fmt=3), -1, "out_format"),
     (dict(v_prep=None), -1, "NULL"),
     (dict(ws_bytes=10), -1, "workspace needs"),
+    (dict(sp=(4, 48, 48)), -1, "multiple of 8"),
+    (dict(sp=(-8, 48, 48)), -1, "non-negative multiple of 8"),
+    (dict(sp=(32, 48, 56)), -1, "exceeds the head dim"),
 ])
 def test_attn_fwd_sparse_rejects_before_any_hip_call(L, kw, status, fragment):
     args = dict(q=A, k_prep=P(0x1000000), v_prep=P(0x2000000), out=Dp, B=1, H=2, N=1000, D=128, T=1,
-                Hl=10, Wl=100, tab=TAB, gamma=None, eps=1e-6, ws=WSS, ws_bytes=None, fmt=0)
+                Hl=10, Wl=100, sp=(32, 48, 48), tab=TAB, gamma=None, eps=1e-6, ws=WSS, ws_bytes=None,
+                fmt=0)
     args.update(kw)
     if args["ws_bytes"] is None:
         args["ws_bytes"] = sol.sol_sparse_workspace_bytes(1, 2, 1000, 128)
     st = sol.sol_attn_fwd_sparse(args["q"], args["k_prep"], args["v_prep"], args["out"], args["B"],
                                  args["H"], args["N"], args["D"], args["T"], args["Hl"], args["Wl"],
-                                 args["tab"], args["gamma"], args["eps"], args["ws"], args["ws_bytes"],
-                                 args["fmt"], None)
+                                 *args["sp"], args["tab"], args["gamma"], args["eps"], args["ws"],
+                                 args["ws_bytes"], args["fmt"], None)
     assert st == status, sol.sol_last_error()
     assert fragment in sol.sol_last_error()
 
@@ -430,3 +448,56 @@ def test_table_matches_oracle_angles(L):
     ulps = np.abs(tab.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
     close = np.abs(tab - want) <= 1e-7
     assert np.all((ulps <= 1) | close)
+
+
+SPLITS = [(32, 48, 48), (16, 24, 24), (0, 64, 64), (8, 0, 0), (64, 0, 64)]
+
+
+@pytest.mark.parametrize("split", SPLITS)
+def test_split_table_matches_oracle_angles(L, split):
+    """The table of any rotary split (partial RoPE: dims past dt+dh+dw pass
+    through): one section per axis of width > 0, each (cos, sin) the float32
+    rounding of the numpy twin's angle for that position and pair."""
+    T, Hl, Wl = 4, 6, 5
+    dt, dh, dw = split
+    n = sol.sol_rope3d_table_floats_ex(128, T, Hl, Wl, dt, dh, dw)
+    assert n == 2 * (T * dt // 2 + Hl * dh // 2 + Wl * dw // 2)
+    tab = sol.rope3d_table_host(T, Hl, Wl, split=split)[:n].reshape(-1, 2)
+    sections, off = [], 0
+    for axis, (ext, width) in enumerate([(T, dt), (Hl, dh), (Wl, dw)]):
+        pos = np.zeros((ext, 3), np.int64)
+        pos[:, axis] = np.arange(ext)
+        ang = brute.rope_angles(pos, split=split)[:, off // 2:(off + width) // 2]
+        sections.append(ang.reshape(-1))
+        off += width
+    ang = np.concatenate(sections)
+    want = np.stack([np.cos(ang), np.sin(ang)], -1).astype(np.float32)
+    assert tab.shape == want.shape
+    ulps = np.abs(tab.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
+    assert np.all((ulps <= 1) | (np.abs(tab - want) <= 1e-7))
+    if split == (32, 48, 48):  # the default split is the table every other entry point takes
+        assert np.array_equal(tab.reshape(-1), sol.rope3d_table_host(T, Hl, Wl)[:n])
+
+
+@pytest.mark.parametrize("split", [(4, 48, 48), (32, 48, 56), (-8, 64, 64), (32, 12, 48)])
+def test_split_table_rejects_invalid_splits(L, split):
+    assert sol.sol_rope3d_table_floats_ex(128, 3, 8, 8, *split) == 0
+    tab = np.zeros(4096, np.float32)
+    st = sol.sol_rope3d_table_ex(tab.ctypes.data_as(P), tab.size, 128, 3, 8, 8, *split, 10000.0)
+    assert st == -1 and "split" in sol.sol_last_error()
+
+
+def test_binding_rejects_a_table_of_another_grid():
+    """The C ABI receives only the table's pointer; the binding checks its
+    length against the grid and split before any launch (a 720p call given the
+    low-resolution table would read past its end)."""
+    import torch
+    low = torch.from_numpy(sol.rope3d_table_host(8, 30, 52))
+    dev = low.device
+    assert sol._table_ptr(low, dev, 128, 8, 30, 52) is not None
+    with pytest.raises(ValueError, match="need"):
+        sol._table_ptr(low, dev, 128, 31, 45, 80)
+    part = torch.from_numpy(sol.rope3d_table_host(8, 30, 52, split=(16, 24, 24)))
+    with pytest.raises(ValueError, match="need"):
+        sol._table_ptr(part, dev, 128, 8, 30, 52)  # the default split needs twice as many floats
+    assert sol._table_ptr(part, dev, 128, 8, 30, 52, split=(16, 24, 24)) is not None

@@ -76,7 +76,7 @@ def _full_parity(w, q, k, v, label, rope=True):
 
 def test_library_is_the_in_tree_build():
     assert os.path.dirname(sol.lib()._name) == os.path.dirname(sol.__file__)
-    assert sol.sol_version() == 102
+    assert sol.sol_version() == 200
 
 
 def test_mfma_probe_runs_every_product():

@@ -92,6 +92,7 @@ MUTANTS = [
     ("frequency index off by one",
      "pow(base, -2.0 * i / (double)d)", "pow(base, -2.0 * (i + 1) / (double)d)"),
     ("axis chunks not advanced", "    off += d;\n", "\n"),
+    ("rotary split ignored (default widths)", "    int d = widths[a];", "    int d = a ? 3 * D / 8 : D / 4;"),
     ("h/w raster swapped", "*ph = (int)((r / Wl) % Hl);", "*ph = (int)(r % Hl);"),
     ("prefix tokens rotated", "if (n < nt) return 0;", "if (n < 0) return 0;"),
     ("softmax scale dropped", "s[j] = dot * scale;", "s[j] = dot;"),
