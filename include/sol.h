@@ -68,6 +68,27 @@ enum {
   SOL_OUT_INT8_RECORDS = 2 /* block-INT8 output records (see sol_attn_fwd_prepared_ex) */
 };
 
+/*
+ * Range status (sol_range_status): bits the kernels set, per device and
+ * sticky until cleared, when an input leaves the range the computation
+ * supports or an output is not finite.  The prepared path (sol_prepare_kv*,
+ * sol_attn_fwd_prepared*, sol_attn_fwd_ws, sol_attn_fwd_noalloc, the
+ * block-sparse and records paths) multiplies in fp16 with fp32 accumulation:
+ *   SOL_RANGE_Q: a query value q^ log2(e)/sqrt(D) is not finite in fp16
+ *     (|q^| >= about 513,000, or an inf/NaN input);
+ *   SOL_RANGE_K: a key value k^ (normalised, rotated, bf16) is not finite in
+ *     fp16 (|k^| >= 65520, or inf/NaN);
+ *   SOL_RANGE_V: a value v is not finite in fp16 (|v| >= 65520, or inf/NaN);
+ *   SOL_RANGE_OUT: an output element is inf or NaN (any attention entry
+ *     point: the fused sol_attn_fwd also converts v to fp16 for the second
+ *     product, so |v| >= 65520 lands here; inf or NaN inputs too).
+ * Such a call's outputs are not finite where the bad operand takes part --
+ * never a finite wrong value -- and the bits say why.  fp16's subnormal range
+ * keeps an absolute resolution of 2^-24: values below 2^-14 in magnitude lose
+ * relative precision but raise no bit.
+ */
+enum { SOL_RANGE_Q = 1, SOL_RANGE_K = 2, SOL_RANGE_V = 4, SOL_RANGE_OUT = 8 };
+
 /* Largest N the kernels accept (token indices stay exact in float32 arithmetic). */
 #define SOL_MAX_TOKENS (1 << 23)
 
@@ -137,8 +158,8 @@ int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T,
  * inside the kernel (fused into the tile loads).  fp32 logits, softmax
  * statistics and accumulators.  The second product takes the probabilities
  * rounded to fp16 and v converted to fp16 (exact for |v| < 65504; larger
- * values overflow to inf), so the output error stays at the bf16 rounding of
- * out (round to nearest even).
+ * values overflow to inf and raise SOL_RANGE_OUT), so the output error stays
+ * at the bf16 rounding of out (round to nearest even).
  * q, k, v, out: [B][H][N][D] bf16, 16-byte aligned; out must not overlap
  * q, k or v.  0 <= T*Hl*Wl <= N.  rope_tab_dev = NULL or T*Hl*Wl = 0 means
  * plain attention (nothing rotated); otherwise it is the device copy of
@@ -162,19 +183,21 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
  *     fp16(v)[key 16s + 8(i/4) + 4h + i%4][dim 32c + l].
  * Keys past N are zero.  The fp16 conversions are exact for 2^-14 <= |x| <
  * 65504; smaller values keep fp16's 2^-24 absolute resolution, larger ones
- * overflow to inf (outside what this path supports).  k_prep, v_prep: device
+ * overflow to inf and raise SOL_RANGE_K / SOL_RANGE_V (sol_range_status).  k_prep, v_prep: device
  * buffers of sol_prepared_kv_bytes(B, H, N, D) bytes each, 16-byte aligned,
  * not overlapping each other, k or v.  rope_tab_dev as in sol_attn_fwd.
  *
  * sol_attn_fwd_prepared: attention on prepared K/V; q is rotated and rounded
  * to bf16 in its tile load, then scaled by log2(e)/sqrt(D) and rounded to
  * fp16 so the score product runs in fp16 with the softmax scale folded in
- * (|q^| log2(e)/sqrt(D) must stay below 65504).  Two launches on the stream:
- * the first treats every query row with a reference max taken from the first
- * key tile; a row block whose probabilities would leave the fp16 range
- * (scores more than 15 binades above that reference) is written as NaN and
- * recomputed by the second, which raises the reference as it goes.  out must
- * not overlap q, k_prep or v_prep.
+ * (|q^| log2(e)/sqrt(D) must stay below 65504, else SOL_RANGE_Q).  Two
+ * launches on the stream: the first treats every query row with a reference
+ * max taken from the first key tile and the rows' diagonal tile, and stops a
+ * row block whose probabilities would leave the fp16 range (scores more than
+ * 15 binades above that reference), writing it as NaN; the second recomputes
+ * exactly those row blocks, raising the reference in place as it goes (any
+ * score distribution: p480's 1 % of keys x8 runs at the rate of the dense
+ * shapes).  out must not overlap q, k_prep or v_prep.
  *
  * The result differs from sol_attn_fwd's by rounding only (same contract and
  * error bound; the fp16 score operands and the reference max change the last
@@ -417,6 +440,15 @@ int sol_attn_fwd_records(const void* rec, const void* k_prep, const void* v_prep
  */
 int sol_mfma_probe(const void* operands, float* out, int workgroups, int iters,
                    sol_stream_t stream);
+
+/*
+ * The current device's range status (SOL_RANGE_* bits raised since the last
+ * clear) into *flags; clear != 0 resets it to 0.  The one call that
+ * synchronises: it waits for all work on the current device first.  The
+ * status is shared by every call on the device, whatever the stream or
+ * thread.
+ */
+int sol_range_status(unsigned* flags, int clear);
 
 /* Static description of a status code. */
 const char* sol_status_string(int status);

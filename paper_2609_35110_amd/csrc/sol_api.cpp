@@ -534,6 +534,13 @@ int sol_mfma_probe(const void* operands, float* out, int workgroups, int iters, 
   return ok();
 }
 
+int sol_range_status(unsigned* flags, int clear) {
+  if (!flags) return fail(SOL_ERR_INVALID_ARG, "flags must not be NULL");
+  hipError_t e = sol::range_status(flags, clear != 0);
+  if (e != hipSuccess) return fail(SOL_ERR_HIP, "range status: %s", hipGetErrorString(e));
+  return ok();
+}
+
 const char* sol_status_string(int status) {
   switch (status) {
     case SOL_OK: return "ok";

@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "sol.h"
+
 namespace sol {
 
 constexpr int kHeadDim = 128;
@@ -110,6 +112,10 @@ hipError_t launch_mfma_probe(const uint16_t* operands, float* out, int workgroup
 
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
 int64_t attn_max_workgroups(int N, int BH);
+
+// The current device's sticky range status (sol_range_status): waits for all
+// work on the device, copies the flags out, and clears them when asked.
+hipError_t range_status(unsigned* flags, bool clear);
 
 // Record msg as the calling thread's last error (sol_last_error) and return
 // status: the front end's error path, for entry points in other sources.

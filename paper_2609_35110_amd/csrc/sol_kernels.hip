@@ -24,10 +24,48 @@
 //     new tile max exceeds it by more than 2^8 in probability units, so the
 //     64-register output rescale is almost never executed.  Exact: numerator
 //     and denominator always share the same reference max.
+#include <mutex>
+
 #include "sol_device.h"
 
 namespace sol {
 namespace {
+
+// ------------------------------------------------------------ range status
+
+// Sticky range status of the device, read by sol_range_status: bits the
+// kernels set when a converted fp16 operand of the prepared path (q', k^, v)
+// or an output element is not finite.  Zero when the library is loaded.
+__device__ unsigned range_flags;
+
+// The tests below read the bits of floating-point values.  The library is
+// built with -fno-honor-nans, under which the compiler turns a test of the
+// exponent bits back into a floating-point compare with infinity that
+// assumes NaN away; the empty asm hides the bits' origin from it.
+__device__ __forceinline__ uint32_t opaque_bits(uint32_t u) {
+  asm volatile("" : "+v"(u));
+  return u;
+}
+// Any of the eight fp16 values of x is inf or NaN (exponent field all ones).
+__device__ __forceinline__ bool f16x8_nonfinite(uint4 x) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  bool bad = false;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t m = opaque_bits(w[u]) & 0x7C007C00u;
+    bad |= (m & 0xFFFFu) == 0x7C00u || (m >> 16) == 0x7C00u;
+  }
+  return bad;
+}
+// x is inf or NaN (exponent field all ones).
+__device__ __forceinline__ bool f32_nonfinite(float x) {
+  return (opaque_bits(__float_as_uint(x)) & 0x7F800000u) == 0x7F800000u;
+}
+// One atomic per wave in which some lane saw a bad value.
+__device__ __forceinline__ void note_range(bool bad, unsigned flag) {
+  const uint64_t m = __ballot(bad);
+  if (m != 0 && __lane_id() == (unsigned)__builtin_ctzll(m)) atomicOr(&range_flags, flag);
+}
 
 // --------------------------------------------------------- standalone rotary
 
@@ -107,6 +145,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
     pair0[u] = rot[u] ? tab_pair(cc[u], p, g) : 0;
   }
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+  bool bad_k = false, bad_v = false;  // an fp16 operand out of range (or not finite)
   for (int64_t bh = blockIdx.y; bh < bh_count; bh += gridDim.y) {
     const size_t row0 = (size_t)bh * n_src;
     uint4* kt = kp + ((size_t)bh * n_tiles + tile) * (kPrepTileElems / 8);
@@ -121,18 +160,24 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
       if (kRec) {
         // records carry k as attention consumes it (normalised and rotated)
         const uint4 xr = valid[u] ? rec_chunk(rec_of(u), 1, cc[u]) : zero;
-        if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(xr);
+        const uint4 xh = bf16x8_to_f16x8(xr);
+        bad_k |= f16x8_nonfinite(xh);
+        if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = xh;
       } else {
         const uint4 x = valid[u] ? k[(row0 + src[u]) * kChunks + cc[u]] : zero;
         // every lane takes part in the row sums (rows sit in 16 aligned lanes)
         const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(x)), eps) : 1.0f;
         const uint4 xr = valid[u] ? qk_chunk(x, gamma, inv, cc[u], rot[u], tab, pair0[u]) : zero;
-        if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = bf16x8_to_f16x8(xr);
+        const uint4 xh = bf16x8_to_f16x8(xr);
+        bad_k |= f16x8_nonfinite(xh);
+        if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = xh;
       }
       const uint4 y = !valid[u] ? zero
                       : kRec    ? rec_chunk(rec_of(u), 2, cc[u])
                                 : v[(row0 + src[u]) * kChunks + cc[u]];
-      *reinterpret_cast<uint4*>(&vt[r[u] * (D + 8) + cc[u] * 8]) = bf16x8_to_f16x8(y);
+      const uint4 yh = bf16x8_to_f16x8(y);
+      bad_v |= f16x8_nonfinite(yh);
+      *reinterpret_cast<uint4*>(&vt[r[u] * (D + 8) + cc[u] * 8]) = yh;
     }
     __syncthreads();
 #pragma unroll
@@ -155,6 +200,8 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
     }
     __syncthreads();
   }
+  note_range(bad_k, SOL_RANGE_K);
+  note_range(bad_v, SOL_RANGE_V);
 }
 
 // ------------------------------------------------------------ fused attention
@@ -463,6 +510,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   // ---- epilogue: out = O / l in bf16; register j of block db is dim 32db + 8(j/4) + 4hh + j%4.
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = 1.0f / l_tot;
+  {
+    // an output that is not finite is reported (|v| >= 65504 overflows the
+    // fp16 value operand; inf or NaN inputs): an inf or NaN accumulator, or
+    // 1/l, makes the lane's sum of them inf or NaN
+    float sum = inv;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sum += o[db][j];
+    note_range(f32_nonfinite(sum) && qrow < N, SOL_RANGE_OUT);
+  }
   if (qrow < N) {
     uint16_t* dst = out + slab + (size_t)qrow * D;
 #pragma unroll
@@ -755,6 +813,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   // runs the rest of the fixed tree in the lane.
   const int qrow0 = qrow_first;  // block qb holds row qrow0 + 32 qb
   f16x8 qf[2][8];
+  bool bad_q = false;  // |q^| log2(e)/sqrt(D) out of fp16's range (or not finite)
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int row = min(qrow0 + 32 * qb, Nq - 1);
@@ -791,8 +850,10 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       // kRope: prefix rows turn by the origin's table entries, an exact identity
       const uint4 y = qk_chunk(x[kk], q_gamma, inv, cc, kRope, tab, kRope ? tab_pair(cc, p, g) : 0);
       qf[qb][kk] = bf16x8_to_f16x8_scaled(y, c_log2);
+      bad_q |= f16x8_nonfinite(__builtin_bit_cast(uint4, qf[qb][kk]));
     }
   }
+  note_range(bad_q, SOL_RANGE_Q);
 
   // ---- staging: each prepared tile (8 KB) is copied into LDS by buffer loads
   // that write LDS directly: wave w moves the 1 KB blocks 2w and 2w + 1.  Tile
@@ -1241,6 +1302,17 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     const int row = qrow0 + 32 * qb;
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.0f / l_tot;
+    if (!marked) {
+      // an output that is not finite is reported (operands out of fp16's
+      // range, inf or NaN inputs; marked rows are the second pass's): an inf
+      // or NaN accumulator, or 1/l, makes the lane's sum of them inf or NaN
+      float sum = inv;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sum += o[qb][db][j];
+      note_range(f32_nonfinite(sum) && row < Nq, SOL_RANGE_OUT);
+    }
     if (out_rec) {
       // block-INT8 output record: 32 dims per scale; a group's 32 values sit
       // in this lane's 16 registers of block db and its partner lane's (hh ^ 1)
@@ -1434,5 +1506,33 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
 }
 
 int64_t attn_max_workgroups(int N, int BH) { return (int64_t)((N + BM - 1) / BM) * BH; }
+
+namespace {
+std::mutex g_flags_mutex;
+void* g_flags_ptr[64];  // per device, resolved on first use
+}  // namespace
+
+hipError_t range_status(unsigned* flags, bool clear) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  void* ptr;
+  {
+    std::lock_guard<std::mutex> lock(g_flags_mutex);
+    if (!g_flags_ptr[dev]) {
+      e = hipGetSymbolAddress(&g_flags_ptr[dev], HIP_SYMBOL(range_flags));
+      if (e != hipSuccess) return e;
+    }
+    ptr = g_flags_ptr[dev];
+  }
+  if ((e = hipDeviceSynchronize()) != hipSuccess) return e;
+  if ((e = hipMemcpy(flags, ptr, sizeof(unsigned), hipMemcpyDeviceToHost)) != hipSuccess) return e;
+  if (clear) {
+    const unsigned zero = 0;
+    e = hipMemcpy(ptr, &zero, sizeof(unsigned), hipMemcpyHostToDevice);
+  }
+  return e;
+}
 
 }  // namespace sol

@@ -21,6 +21,10 @@ SOL_OK = 0
 SOL_ERR_INVALID_ARG = -1
 SOL_ERR_UNSUPPORTED = -2
 SOL_ERR_HIP = -3
+SOL_RANGE_Q = 1
+SOL_RANGE_K = 2
+SOL_RANGE_V = 4
+SOL_RANGE_OUT = 8
 SOL_OUT_BF16 = 0
 SOL_OUT_FP8_E4M3 = 1
 SOL_OUT_INT8_RECORDS = 2
@@ -98,6 +102,8 @@ def lib():
         L.sol_attn_fwd_records.restype = i32
         L.sol_mfma_probe.argtypes = [P, P, i32, i32, P]
         L.sol_mfma_probe.restype = i32
+        L.sol_range_status.argtypes = [ctypes.POINTER(ctypes.c_uint), i32]
+        L.sol_range_status.restype = i32
         L.sol_status_string.argtypes = [i32]
         L.sol_status_string.restype = ctypes.c_char_p
         L.sol_last_error.argtypes = []
@@ -222,6 +228,10 @@ def sol_attn_fwd_records(rec, k_prep, v_prep, out, B, H, N, n_kv, D, out_format,
 
 def sol_mfma_probe(operands, out, workgroups, iters, stream):
     return lib().sol_mfma_probe(operands, out, workgroups, iters, stream)
+
+
+def sol_range_status(flags, clear):
+    return lib().sol_range_status(flags, clear)
 
 
 def sol_status_string(status):
@@ -690,3 +700,11 @@ def mfma_probe(operands, workgroups, iters, out=None):
     check(sol_mfma_probe(ctypes.c_void_p(operands.data_ptr()), ctypes.c_void_p(out.data_ptr()),
                          workgroups, iters, _stream(operands)))
     return out
+
+
+def range_status(clear=True):
+    """The current device's SOL_RANGE_* bits raised since the last clear (waits
+    for all work on the device); clears them unless clear=False."""
+    flags = ctypes.c_uint(0)
+    check(sol_range_status(ctypes.byref(flags), 1 if clear else 0))
+    return flags.value
