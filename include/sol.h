@@ -239,7 +239,7 @@ int sol_attn_fwd_prepared(const void* q, const void* k_prep, const void* v_prep,
  * element); SOL_OUT_FP8_E4M3: out holds one FP8 E4M3 byte per element (OCP
  * E4M3FN: bias 7, 3 mantissa bits, no infinities, 0x7F NaN) with unit scale --
  * the raw E4M3 values the paper's attention hands to the quantized output
- * projection (Sec. 3.5, "Joint optimization with quantized communication") --
+ * projection (Sec. 3.3, "Joint optimization with quantized communication") --
  * rounded to nearest even from the fp32 result and saturated at +-448.
  * SOL_OUT_INT8_RECORDS: the paper's block-INT8 output wire format (Sec. 3.2,
  * "Quantized communication"), one record of SOL_OUT_RECORD_BYTES = 144 bytes

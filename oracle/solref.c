@@ -94,7 +94,7 @@ void solref_round_bf16(const double* x, uint16_t* y, int64_t n) {
  * finite value 448, smallest subnormal 2^-9), round to nearest, ties to even,
  * saturating: every |x| >= 448 (infinities included) gives +-448.  This is the
  * raw E4M3 output the paper's attention hands to the next GEMM with unit
- * scales (Sec. 3.5, "Joint optimization with quantized communication"). */
+ * scales (Sec. 3.3, "Joint optimization with quantized communication"). */
 static uint8_t double_to_e4m3(double x) {
   if (isnan(x)) return 0x7f;
   uint8_t sign = signbit(x) ? 0x80 : 0;

@@ -592,7 +592,7 @@ __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 // fp32 -> FP8 E4M3 code (the OCP E4M3FN format: bias 7, 3 mantissa bits, no
 // infinities, 0x7F NaN), round to nearest even, saturating at +-448
 // (infinities too).  The raw E4M3 output the paper's attention hands to the
-// next GEMM with unit scales (Sec. 3.5, "Joint optimization with quantized
+// next GEMM with unit scales (Sec. 3.3, "Joint optimization with quantized
 // communication").  Normal results keep 3 of fp32's 23 mantissa bits by an
 // integer round-to-nearest-even on the bit pattern, then move the exponent
 // from fp32's bias 127 to 7; below 2^-6 the quantum is fixed at 2^-9.

@@ -2,7 +2,7 @@
 SOL_OUT_FP8_E4M3), through the C ABI, against the oracle's E4M3 codes.
 
 The paper's attention hands raw E4M3 values with unit scales to the quantized
-output projection (Sec. 3.5, "Joint optimization with quantized
+output projection (Sec. 3.3, "Joint optimization with quantized
 communication").  A code is an integer decided by floating point: the oracle
 rounds its own result, the kernel its fp32 result, so the two codes may differ
 only where the exact value lies within the kernel's error of the kernel code's
