@@ -717,6 +717,22 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   __shared__ int n_gave_up;  // first pass: waves of the workgroup that stopped computing
 
   auto keep = [&](auto& x) __attribute__((always_inline)) { pin(x); };
+  // Score units.  First pass: q' = fp16(q^ c), c = log2(e)/sqrt(D), so the
+  // score MFMAs return c q^.k^ and an exponential takes the accumulator as it
+  // is.  q^ c rounded to fp16 carries a relative error of 2^-12 per element,
+  // which moves a score by about 2^-12 of its size: negligible for the scores
+  // of diffuse rows, but the rows the second pass takes are the peaked ones,
+  // whose large scores would carry it into the output (p480: max error 0.0203
+  // of the RMS against the correctly rounded output's 0.0194).  Second pass:
+  // q'' = fp16(q^ / 8), exact (a power of two), so a score is the fp32 sum of
+  // exact products, q^.k^ / 8 (and m, the bias and the raises are in those
+  // units), and each exponential first multiplies by 8 c in fp32 -- one more
+  // VALU operation per score, in the pass that only peaked rows take.
+  const float q_scale = kRobust ? 0.125f : c_log2;
+  const float c_exp = c_log2 * 8.0f;
+  auto exp2_score = [&](float x) __attribute__((always_inline)) {
+    return __builtin_amdgcn_exp2f(kRobust ? x * c_exp : x);
+  };
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -849,7 +865,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       const int cc = 2 * kk + hh;
       // kRope: prefix rows turn by the origin's table entries, an exact identity
       const uint4 y = qk_chunk(x[kk], q_gamma, inv, cc, kRope, tab, kRope ? tab_pair(cc, p, g) : 0);
-      qf[qb][kk] = bf16x8_to_f16x8_scaled(y, c_log2);
+      qf[qb][kk] = bf16x8_to_f16x8_scaled(y, q_scale);
       bad_q |= f16x8_nonfinite(__builtin_bit_cast(uint4, qf[qb][kk]));
     }
   }
@@ -957,7 +973,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   auto raise_max = [&](int qb, f32x16& s, f32x16* s_next, uint32_t* words, float& lsum)
       __attribute__((always_inline)) {
     const float delta = fmaxf(tile_max(s), 0.0f);
-    const float alpha = __builtin_amdgcn_exp2f(-delta);
+    const float alpha = exp2_score(-delta);
     m_ref[qb] += delta;
     l_run[qb] *= alpha;
 #pragma unroll
@@ -971,8 +987,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     float la = 0.0f, lb = 0.0f;
 #pragma unroll
     for (int w = 0; w < 8; ++w) {
-      const float ea = __builtin_amdgcn_exp2f(s[2 * w]);
-      const float eb = __builtin_amdgcn_exp2f(s[2 * w + 1]);
+      const float ea = exp2_score(s[2 * w]);
+      const float eb = exp2_score(s[2 * w + 1]);
       words[w] = pack_f16x2(ea, eb);
       la += ea;
       lb += eb;
@@ -1020,7 +1036,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
         mfma_s_next(ns[0], kr[j], qf[0][j]);
       }
       __builtin_amdgcn_sched_barrier(0);
-      float ea = __builtin_amdgcn_exp2f(cs[1][2 * j]);
+      float ea = exp2_score(cs[1][2 * j]);
       keep(ea);
       if (j > 0) {
         p1[j - 1] = pack_f16x2(pa, pb);
@@ -1040,7 +1056,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       if (j == 4) { t23 = add_f16x2(p1[2], p1[3]); keep(t23); }
       if (j == 5) { t03 = add_f16x2(t01, t23); keep(t03); }
       if (j == 6) { t45 = add_f16x2(p1[4], p1[5]); keep(t45); }
-      float eb = __builtin_amdgcn_exp2f(cs[1][2 * j + 1]);
+      float eb = exp2_score(cs[1][2 * j + 1]);
       keep(eb);
       __builtin_amdgcn_sched_barrier(0);
       pa = ea;
@@ -1105,7 +1121,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       // block 0; pack of word j-1; a copy block in pairs 1, 2, 3 and 5.
       o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vr[j], pf[0][kst], o[0][db], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
-      float ea = __builtin_amdgcn_exp2f(ns[0][2 * j]);
+      float ea = exp2_score(ns[0][2 * j]);
       keep(ea);
       if (j > 0) {
         p0_next[j - 1] = pack_f16x2(pa, pb);
@@ -1127,7 +1143,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       if (j == 4) { t23 = add_f16x2(p0_next[2], p0_next[3]); keep(t23); }
       if (j == 5) { t03 = add_f16x2(t01, t23); keep(t03); }
       if (j == 6) { t45 = add_f16x2(p0_next[4], p0_next[5]); keep(t45); }
-      float eb = __builtin_amdgcn_exp2f(ns[0][2 * j + 1]);
+      float eb = exp2_score(ns[0][2 * j + 1]);
       keep(eb);
       __builtin_amdgcn_sched_barrier(0);
       pa = ea;
@@ -1241,8 +1257,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     float la = 0.0f, lb = 0.0f;
 #pragma unroll
     for (int w = 0; w < 8; ++w) {
-      const float ea = __builtin_amdgcn_exp2f(sa[0][2 * w]);
-      const float eb = __builtin_amdgcn_exp2f(sa[0][2 * w + 1]);
+      const float ea = exp2_score(sa[0][2 * w]);
+      const float eb = exp2_score(sa[0][2 * w + 1]);
       pA[w] = pack_f16x2(ea, eb);
       la += ea;
       lb += eb;

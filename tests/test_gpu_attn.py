@@ -130,10 +130,14 @@ def test_text_only_no_rotation():
 
 @pytest.mark.parametrize("name", ["low", "p480", "p720", "share"])
 def test_workload_sampled_parity(name):
+    """Full workload sizes, both paths, in the benchmark's launch
+    configuration: per (b, h) 1,024 seeded rows, the first 64, the last 512
+    (two 256-row tiles, the ragged one included) and the text/video boundary,
+    every row against all keys."""
     w = W.WORKLOADS[name]
     _log("generating %s" % w.describe())
     q, k, v = W.make_inputs(w)
-    rows = W.sample_rows(w, per_slab=16, head=32, tail=80).numpy()
+    rows = W.sample_rows(w, per_slab=1024, head=64, tail=512).numpy()
     _log("oracle on %d rows" % len(rows))
     ref = oracle.attn_rows(_bits(q), _bits(k), _bits(v), w.T, w.Hl, w.Wl, rows=rows)
     for path in PATHS:

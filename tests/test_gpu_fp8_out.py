@@ -35,6 +35,14 @@ MIDPOINT_TOL = 4e-3
 # (1.1 % measured on the tiny workload); every one of them must pass the
 # midpoint check above.
 MIN_EXACT = 0.97
+# Where neighbouring codes are more than twice the tolerance apart, a code
+# within the tolerance of its interval is the oracle's or one off.  Normal
+# E4M3 codes (|x| >= 2^-6) are 1/16 to 1/8 of the value apart, so that holds
+# for |x| >= 32 MIDPOINT_TOL x the group's RMS; smaller values (relative to
+# their row: local attention spreads row magnitudes) and subnormal codes (a
+# fixed 2^-9 apart) may be several codes off within the tolerance, where the
+# midpoint check alone bounds them.
+E4M3_MIN_NORMAL = 2.0 ** -6
 
 
 def _log(msg):
@@ -80,9 +88,12 @@ def e4m3_parity(got, ref, slab):
     hi = np.where(pos < len(fin) - 1, (fin[np.minimum(pos + 1, len(fin) - 1)] + x) / 2, np.inf)
     r = ref.astype(np.float64)
     outside = np.maximum(np.maximum(lo - r, r - hi), 0.0) / norm[:, None]
+    coarse = (np.abs(r) >= E4M3_MIN_NORMAL) & (np.abs(r) >= 32 * MIDPOINT_TOL * norm[:, None])
     return {
         "exact": float((dist == 0).mean()),
         "max_code_dist": int(dist.max()),
+        "max_code_dist_coarse": int(dist[coarse].max()) if coarse.any() else 0,
+        "coarse": float(coarse.mean()),
         "max_midpoint_dist": float(outside.max()),
         "nan": bool(np.isnan(x).any()),
         "elements": int(got.size),
@@ -90,8 +101,8 @@ def e4m3_parity(got, ref, slab):
 
 
 def assert_e4m3_parity(st, label):
-    assert not st["nan"] and st["max_midpoint_dist"] <= MIDPOINT_TOL and st["exact"] >= MIN_EXACT, \
-        "E4M3 parity failed %s: %s" % (label, st)
+    assert (not st["nan"] and st["max_midpoint_dist"] <= MIDPOINT_TOL and st["exact"] >= MIN_EXACT
+            and st["max_code_dist_coarse"] <= 1), "E4M3 parity failed %s: %s" % (label, st)
 
 
 def _fp8_attn(q, k, v, T, Hl, Wl):

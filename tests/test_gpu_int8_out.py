@@ -35,8 +35,10 @@ DEV = "cuda:0"
 # RMS (the bf16 parity shows a few 1e-4)
 MIDPOINT_TOL = 4e-3
 # codes equal to the oracle's: a code step is 1/127 to 1/113 of the group max
-# (~1/40 of the RMS), the kernel's error ~3e-4 of the RMS, so ~2 % may differ
-MIN_EXACT = 0.95
+# (~1/40 of the RMS) and the kernel's error ~3e-4 of the RMS, so a value lies
+# within that error of a rounding midpoint for ~1-2 % of the codes (1.0-1.6 %
+# measured across these tests, dense, sparse, from records and at p720)
+MIN_EXACT = 0.98
 
 
 def _log(msg):
