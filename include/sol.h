@@ -17,7 +17,11 @@
  * every dim rotated); the entry points with dt, dh, dw arguments take any
  * split of non-negative multiples of 8 with dt+dh+dw <= D.  Within an axis
  * chunk of width d, the interleaved pair (2i, 2i+1) is turned by the angle
- * pos * base^(-2i/d).
+ * pos * base^(-2i/d).  bf16(R(pos) x) is the nearest-even bf16 of the exact
+ * rotation: the kernels turn each pair in fp64 with cos and sin to 48 bits
+ * (the table's two planes) and round once, so they differ from the correctly
+ * rounded value only where it lies within about 2^-47 |pair| of a rounding
+ * midpoint.  (One exception, sol_attn_fwd's key tiles, is documented there.)
  *
  * Sequence packing follows Sec. 3.4 "Safety rails" (prefix before the target
  * video): of the N tokens, the first Nt = N - T*Hl*Wl form an unrotated
@@ -94,7 +98,7 @@ enum { SOL_RANGE_Q = 1, SOL_RANGE_K = 2, SOL_RANGE_V = 4, SOL_RANGE_OUT = 8 };
 
 /*
  * Number of floats in the rotary table for head dim D, latent grid
- * T x Hl x Wl and split dt/dh/dw: 2 * (T*dt/2 + Hl*dh/2 + Wl*dw/2).  Returns 0
+ * T x Hl x Wl and split dt/dh/dw: 4 * (T*dt/2 + Hl*dh/2 + Wl*dw/2).  Returns 0
  * for invalid arguments (D not a positive multiple of 16, a negative extent,
  * a split that is not three non-negative multiples of 8 summing to at most
  * D).  sol_rope3d_table_floats is the default split D/4, 3D/8, 3D/8.
@@ -104,12 +108,16 @@ size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl);
 
 /*
  * Fill a HOST buffer with the rotary table (caller copies it to the device).
- * Layout (float pairs (cos, sin), computed in double and rounded to float):
+ * Two planes of n/2 floats each, n = sol_rope3d_table_floats_ex(D, T, Hl,
+ * Wl, dt, dh, dw).  Plane 0 (hi) holds float pairs (cos, sin), computed in
+ * double and rounded to float:
  *   [T  rows x dt/2 pairs]  frame axis:  angle t * base^(-2i/dt)
  *   [Hl rows x dh/2 pairs]  row axis:    angle h * base^(-2i/dh)
  *   [Wl rows x dw/2 pairs]  column axis: angle w * base^(-2i/dw)
- * (an axis of width 0 has no section).  host_tab must hold n_floats >=
- * sol_rope3d_table_floats_ex(D, T, Hl, Wl, dt, dh, dw) floats.  base > 1
+ * (an axis of width 0 has no section); plane 1 (lo), in the same order, holds
+ * what that rounding lost, float(c - hi) for each double c, so that hi + lo
+ * carries c to 48 bits.  host_tab must hold n_floats >= n floats; every entry
+ * point reads exactly n (the lo plane starts n/2 floats in).  base > 1
  * (10000 for the workloads here).  Host-only: no HIP call.  A device copy is
  * valid only for calls with the same grid and split.  sol_rope3d_table is the
  * default split D/4, 3D/8, 3D/8: the table of every entry point without
@@ -121,7 +129,8 @@ int sol_rope3d_table(float* host_tab, size_t n_floats, int D, int T, int Hl, int
 
 /*
  * y = bf16(R(pos) x) for every token (prefix tokens copied unchanged).
- * Same rounding as the rotation fused into sol_attn_fwd, bit for bit.
+ * The same bits as the rotation of queries in every attention entry point and
+ * of keys in sol_prepare_kv, sol_sparse_route and the record encoder.
  * x, y: [B][H][N][D] bf16; y == x (in place) is allowed, any other overlap
  * is rejected.  0 <= T*Hl*Wl <= N.  rope_tab_dev: device copy of
  * sol_rope3d_table(D, T, Hl, Wl), 16-byte aligned; it may be NULL only when
@@ -155,7 +164,12 @@ int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T,
 
 /*
  * out = softmax(q^ k^T / sqrt(D)) v with q^, k^ rotated and rounded to bf16
- * inside the kernel (fused into the tile loads).  fp32 logits, softmax
+ * inside the kernel (fused into the tile loads): q^ as sol_rope3d, bit for
+ * bit; k^, rotated again in every query tile's pass over the keys, in fp32
+ * with the table's hi plane only (two operations an element against about
+ * ten), which is within one bf16 ulp of sol_rope3d's and equal to it except
+ * where the exact rotation lies within a few 2^-24 |pair| of a rounding
+ * midpoint (about 1 element in 10^4).  fp32 logits, softmax
  * statistics and accumulators.  The second product takes the probabilities
  * rounded to fp16 and v converted to fp16 (exact for |v| < 65504; larger
  * values overflow to inf and raise SOL_RANGE_OUT), so the output error stays

@@ -143,7 +143,8 @@ extern "C" {
 size_t sol_rope3d_table_floats_ex(int D, int T, int Hl, int Wl, int dt, int dh, int dw) {
   if (D <= 0 || D % 16 != 0 || T < 0 || Hl < 0 || Wl < 0) return 0;
   if (dt < 0 || dh < 0 || dw < 0 || dt % 8 || dh % 8 || dw % 8 || (int64_t)dt + dh + dw > D) return 0;
-  return 2 * ((size_t)T * (dt / 2) + (size_t)Hl * (dh / 2) + (size_t)Wl * (dw / 2));
+  // two planes (hi, then lo) of one (cos, sin) pair per rotary pair and position
+  return 4 * ((size_t)T * (dt / 2) + (size_t)Hl * (dh / 2) + (size_t)Wl * (dw / 2));
 }
 
 size_t sol_rope3d_table_floats(int D, int T, int Hl, int Wl) {
@@ -161,14 +162,22 @@ int sol_rope3d_table_ex(float* host_tab, size_t n_floats, int D, int T, int Hl, 
   if (n_floats < need) return fail(SOL_ERR_INVALID_ARG, "table needs %zu floats, got %zu", need, n_floats);
   if (!(base > 1.0) || !std::isfinite(base)) return fail(SOL_ERR_INVALID_ARG, "base must be finite and > 1");
   // Section for one axis of extent `len` whose chunk is `width` head dims wide:
-  // row pos, pair i holds (cos, sin) of pos * base^(-2i/width).
-  float* dst = host_tab;
+  // row pos, pair i holds (cos, sin) of pos * base^(-2i/width), rounded to
+  // fp32 in the hi plane; the lo plane, need / 2 floats on, holds what that
+  // rounding lost, so that hi + lo carries the double to 48 bits.
+  float* hi = host_tab;
+  float* lo = host_tab + need / 2;
+  auto put = [&](double x) {
+    const float h = (float)x;
+    *hi++ = h;
+    *lo++ = (float)(x - (double)h);  // exact difference, rounded once
+  };
   auto section = [&](int len, int width) {
     for (int pos = 0; pos < len; ++pos)
       for (int i = 0; i < width / 2; ++i) {
         const double phi = (double)pos * std::pow(base, -2.0 * i / (double)width);
-        *dst++ = (float)std::cos(phi);
-        *dst++ = (float)std::sin(phi);
+        put(std::cos(phi));
+        put(std::sin(phi));
       }
   };
   section(T, dt);

@@ -109,11 +109,70 @@ __device__ __forceinline__ uint4 pack_bf16x8(const float (&f)[8]) {
                     pack_bf16x2(f[6], f[7]));
 }
 
+// The rotary table (the 3D rotary embedding of Sec. 3.5) is two planes of
+// (cos, sin) pairs: plane 0 holds each value rounded to fp32 (hi), plane 1, g.tab_pairs
+// pairs on, what that rounding lost (lo = fp32(cos - hi)), so hi + lo carries each
+// to 48 bits.
+__device__ __forceinline__ const float2* tab_lo_plane(const float2* tab, const SeqGrid& g) {
+  return tab ? tab + g.tab_pairs : nullptr;
+}
+
+// fp64 -> fp32 rounded to odd: the truncation, its last bit set when inexact.
+// With 24 bits against bf16's 8, rounding that to bf16 (nearest even) gives
+// the nearest-even bf16 of the double itself: no double-rounding error.
+__device__ __forceinline__ float f32_round_odd(double d) {
+  const float f = (float)d;  // v_cvt_f32_f64, nearest even
+  uint32_t u = __float_as_uint(f);
+  const double back = (double)f;
+  // inexact and even: the neighbour on d's side (sign-magnitude: +1 is away from 0)
+  if (back != d && (u & 1u) == 0) u += fabs(back) < fabs(d) ? 1u : 0xffffffffu;
+  return __uint_as_float(u);
+}
+
 // Rotate the 4 interleaved pairs of one 16-byte chunk, held as fp32:
-//   (a, b) -> (a cos - b sin, a sin + b cos), fp32, then bf16 RNE.
-// The one function every rotation in this library goes through, so the
-// standalone rotation and the fused tile loads agree bit for bit.
-__device__ __forceinline__ uint4 rope_rotate_f32(const float (&f)[8], float4 cs01, float4 cs23) {
+//   (a, b) -> (a cos - b sin, a sin + b cos)
+// in fp64 with cos and sin taken as hi + lo (48 bits), then one rounding to
+// bf16.  The result is the nearest-even bf16 of the exact rotation unless that
+// lies within about 2^-47 |(a, b)| of a rounding midpoint.  Every rotation of
+// a query or key row in this library goes through this function, except the
+// fused kernel's key tiles (rope_rotate_fast below).
+__device__ __forceinline__ uint4 rope_rotate_exact(const float (&f)[8], const float2* __restrict__ hi,
+                                                   const float2* __restrict__ lo, int pair0) {
+  const float4 h01 = *reinterpret_cast<const float4*>(hi + pair0);
+  const float4 h23 = *reinterpret_cast<const float4*>(hi + pair0 + 2);
+  const float4 l01 = *reinterpret_cast<const float4*>(lo + pair0);
+  const float4 l23 = *reinterpret_cast<const float4*>(lo + pair0 + 2);
+  // hi + lo is exact in fp64 (|lo| <= half an fp32 ulp of hi)
+  const double c[4] = {(double)h01.x + (double)l01.x, (double)h01.z + (double)l01.z,
+                       (double)h23.x + (double)l23.x, (double)h23.z + (double)l23.z};
+  const double s[4] = {(double)h01.y + (double)l01.y, (double)h01.w + (double)l01.w,
+                       (double)h23.y + (double)l23.y, (double)h23.w + (double)l23.w};
+  uint32_t w[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const double a = f[2 * u], b = f[2 * u + 1];
+    const double ar = __builtin_fma(a, c[u], -(b * s[u]));
+    const double br = __builtin_fma(a, s[u], b * c[u]);
+    w[u] = pack_bf16x2(f32_round_odd(ar), f32_round_odd(br));
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+__device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ hi,
+                                            const float2* __restrict__ lo, int pair0) {
+  float f[8];
+  unpack_bf16x8(x, f);
+  return rope_rotate_exact(f, hi, lo, pair0);
+}
+
+// The fused kernel's key tiles: the same rotation in fp32 with the hi plane
+// alone (2 VALU operations an element, against about 10 for the exact form,
+// in a loop that rotates every key once per query tile).  Within one bf16 ulp
+// of rope_rotate_exact; the two differ where the exact result lies within a
+// few 2^-24 |(a, b)| of a rounding midpoint.
+__device__ __forceinline__ uint4 rope_rotate_fast(uint4 x, float4 cs01, float4 cs23) {
+  float f[8];
+  unpack_bf16x8(x, f);
   const float c[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
   const float s[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
   uint32_t w[4];
@@ -125,17 +184,6 @@ __device__ __forceinline__ uint4 rope_rotate_f32(const float (&f)[8], float4 cs0
     w[u] = pack_bf16x2(ar, br);
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-__device__ __forceinline__ uint4 rope_rotate(uint4 x, float4 cs01, float4 cs23) {
-  float f[8];
-  unpack_bf16x8(x, f);
-  return rope_rotate_f32(f, cs01, cs23);
-}
-
-__device__ __forceinline__ uint4 rope_chunk(uint4 x, const float2* __restrict__ tab, int pair0) {
-  return rope_rotate(x, *reinterpret_cast<const float4*>(tab + pair0),
-                     *reinterpret_cast<const float4*>(tab + pair0 + 2));
 }
 
 // ------------------------------------------------------- QK normalization
@@ -179,15 +227,15 @@ __device__ __forceinline__ void norm_chunk(uint4 x, float inv, const float* __re
 }
 // Chunk cc of a query or key row as it enters the products: normalised when
 // gamma is given (inv from the row's sum of squares), rotated when rot (table
-// pairs from pair0), rounded to bf16.
+// pairs from pair0 in planes hi and lo), rounded to bf16.
 __device__ __forceinline__ uint4 qk_chunk(uint4 x, const float* __restrict__ gamma, float inv, int cc,
-                                          bool rot, const float2* __restrict__ tab, int pair0) {
-  if (gamma == nullptr) return rot ? rope_chunk(x, tab, pair0) : x;
+                                          bool rot, const float2* __restrict__ hi,
+                                          const float2* __restrict__ lo, int pair0) {
+  if (gamma == nullptr) return rot ? rope_chunk(x, hi, lo, pair0) : x;
   float f[8];
   norm_chunk(x, inv, gamma, cc, f);
   if (!rot) return pack_bf16x8(f);
-  return rope_rotate_f32(f, *reinterpret_cast<const float4*>(tab + pair0),
-                         *reinterpret_cast<const float4*>(tab + pair0 + 2));
+  return rope_rotate_exact(f, hi, lo, pair0);
 }
 
 // Prepared K/V tiles: 32 keys, 8 KB of fp16 each for K and for V.

@@ -88,7 +88,7 @@ __global__ __launch_bounds__(256) void rope3d_kernel(const uint4* __restrict__ x
     const int64_t idx = bh * per_slab + i;
     const uint4 v = x[idx];
     const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(v)), eps) : 1.0f;
-    y[idx] = qk_chunk(v, gamma, inv, cc, rot, tab, pair0);
+    y[idx] = qk_chunk(v, gamma, inv, cc, rot, tab, tab_lo_plane(tab, g), pair0);
   }
 }
 
@@ -120,6 +120,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
                                                       const float* __restrict__ gamma, float eps,
                                                       const uint8_t* __restrict__ rec, int heads) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPrepTile * (D + 8)];
+  const float2* __restrict__ tab_lo = tab_lo_plane(tab, g);
   const int n_src = g.n;
   const int n_tiles = (n_kv + kPrepTile - 1) / kPrepTile;  // tiles per prepared slab
   const int tile = tile0 + blockIdx.x;
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
         const uint4 x = valid[u] ? k[(row0 + src[u]) * kChunks + cc[u]] : zero;
         // every lane takes part in the row sums (rows sit in 16 aligned lanes)
         const float inv = gamma ? rms_inv(row_sumsq_lanes16(chunk_sumsq(x)), eps) : 1.0f;
-        const uint4 xr = valid[u] ? qk_chunk(x, gamma, inv, cc[u], rot[u], tab, pair0[u]) : zero;
+        const uint4 xr = valid[u] ? qk_chunk(x, gamma, inv, cc[u], rot[u], tab, tab_lo, pair0[u]) : zero;
         const uint4 xh = bf16x8_to_f16x8(xr);
         bad_k |= f16x8_nonfinite(xh);
         if (owned(first + r[u])) kt[(cc[u] >> 1) * 64 + r[u] + 32 * (cc[u] & 1)] = xh;
@@ -273,6 +274,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   const uint16_t* __restrict__ vs = v + slab;
 
   const float2* tab = tab_g;
+  // queries turn exactly (both planes, from global memory: once per workgroup);
+  // key tiles turn in fp32 with the hi plane, staged in LDS when it fits
+  const float2* tab_lo = kRope ? tab_g + tab_pairs : nullptr;
   if (kRope && kTabLds) {
     for (int i = tid * 2; i < tab_pairs; i += 2 * kThreads)  // tab_pairs is a multiple of 4
       *reinterpret_cast<float4*>(&tab_lds[i]) = *reinterpret_cast<const float4*>(&tab_g[i]);
@@ -292,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
       const int cc = 2 * kk + hh;
       uint4 x = src[cc];
       // prefix tokens sit at (0, 0, 0): cos 0 = 1, sin 0 = 0, an exact identity
-      if (kRope) x = rope_chunk(x, tab, tab_pair(cc, p, g));
+      if (kRope) x = rope_chunk(x, tab, tab_lo, tab_pair(cc, p, g));
       qf[kk] = __builtin_bit_cast(bf16x8, x);
     }
   }
@@ -323,8 +327,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   auto store_k = [&](int buf) {
     uint4 x0 = kreg[0], x1 = kreg[1];
     if (kRope) {
-      x0 = rope_rotate(x0, kcs[0], kcs[1]);
-      x1 = rope_rotate(x1, kcs[2], kcs[3]);
+      x0 = rope_rotate_fast(x0, kcs[0], kcs[1]);
+      x1 = rope_rotate_fast(x1, kcs[2], kcs[3]);
     }
     *reinterpret_cast<uint4*>(&k_lds[buf][rr * KS + c0 * 8]) = x0;
     *reinterpret_cast<uint4*>(&k_lds[buf][rr * KS + c0 * 8 + 64]) = x1;
@@ -864,7 +868,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     for (int kk = 0; kk < 8; ++kk) {
       const int cc = 2 * kk + hh;
       // kRope: prefix rows turn by the origin's table entries, an exact identity
-      const uint4 y = qk_chunk(x[kk], q_gamma, inv, cc, kRope, tab, kRope ? tab_pair(cc, p, g) : 0);
+      const uint4 y = qk_chunk(x[kk], q_gamma, inv, cc, kRope, tab, tab_lo_plane(tab, g), kRope ? tab_pair(cc, p, g) : 0);
       qf[qb][kk] = bf16x8_to_f16x8_scaled(y, q_scale);
       bad_q |= f16x8_nonfinite(__builtin_bit_cast(uint4, qf[qb][kk]));
     }

@@ -68,7 +68,7 @@ __global__ __launch_bounds__(kRecThreads) void qkv_encode_kernel(
       Pos pos{0, 0, 0, false};
       if (kRope) pos = token_pos(n, g);
       const bool rot = kRope && pos.rot;
-      y = qk_chunk(x, gamma, inv, cc, rot, tab, rot ? tab_pair(cc, pos, g) : 0);
+      y = qk_chunk(x, gamma, inv, cc, rot, tab, tab_lo_plane(tab, g), rot ? tab_pair(cc, pos, g) : 0);
     }
     float a = chunk_amax(y);
     a = fmaxf(a, __shfl_xor(a, 1));

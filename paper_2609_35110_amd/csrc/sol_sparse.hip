@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void pool_q_kernel(const uint4* __restrict__ q
       Pos p{0, 0, 0, false};
       if (tab != nullptr && valid) p = token_pos(n, g);
       const bool rot = tab != nullptr && p.rot;
-      const uint4 y = valid ? qk_chunk(x, gamma, inv, cc, rot, tab, rot ? tab_pair(cc, p, g) : 0) : zero;
+      const uint4 y = valid ? qk_chunk(x, gamma, inv, cc, rot, tab, tab_lo_plane(tab, g), rot ? tab_pair(cc, p, g) : 0) : zero;
       float f[8];
       unpack_bf16x8(y, f);
 #pragma unroll

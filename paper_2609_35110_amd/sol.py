@@ -299,14 +299,15 @@ def _check_tensor(name, t, shape=None):
 
 def _table_ptr(table, dev, D, T, Hl, Wl, split=None):
     """The device pointer of a rotary table, checked against the size the
-    kernels read for this grid and split (the C ABI receives only the
-    pointer, so a table built for another grid would be read past its end)."""
+    grid and split give it (the C ABI takes a bare pointer and finds the
+    table's second plane half-way along it, so a table built for another grid
+    or split would be read in the wrong places)."""
     if table is None:
         return None
     if table.dtype != torch.float32 or table.device != dev or not table.is_contiguous():
         raise ValueError("rope table must be a contiguous float32 tensor on %s" % dev)
     need = sol_rope3d_table_floats_ex(D, T, Hl, Wl, *_split(split))
-    if T * Hl * Wl > 0 and table.numel() < need:
+    if T * Hl * Wl > 0 and table.numel() != need:
         raise ValueError("rope table holds %d floats; grid %dx%dx%d and split %s need %d"
                          % (table.numel(), T, Hl, Wl, _split(split), need))
     return ctypes.c_void_p(table.data_ptr())

@@ -423,18 +423,35 @@ def test_binding_rejects_wrong_dtype_and_device():
 # ------------------------------------------------------------ rotary table
 
 def test_table_size(L):
-    assert sol.sol_rope3d_table_floats(128, 31, 45, 80) == 2 * (31 * 16 + 45 * 24 + 80 * 24)
+    assert sol.sol_rope3d_table_floats(128, 31, 45, 80) == 4 * (31 * 16 + 45 * 24 + 80 * 24)
     assert sol.sol_rope3d_table_floats(100, 1, 1, 1) == 0
     tab = np.zeros(10, np.float32)
     st = sol.sol_rope3d_table(tab.ctypes.data_as(P), 10, 128, 3, 8, 8, 10000.0)
     assert st == -1 and "needs" in sol.sol_last_error()
 
 
+def _check_planes(tab, ang):
+    """Plane 0 of a table holds the float32 rounding of each (cos, sin) of
+    the numpy twin's angles (within 1 float32 ulp: libm vs numpy), plane 1
+    what that rounding lost: hi + lo within 2^-46 of numpy's double (two libm
+    results 1 ulp apart, plus lo's own rounding at 2^-48), |lo| at most half
+    an fp32 ulp of hi."""
+    hi, lo = tab.reshape(2, -1, 2)
+    exact = np.stack([np.cos(ang), np.sin(ang)], -1)
+    want = exact.astype(np.float32)
+    assert hi.shape == want.shape
+    ulps = np.abs(hi.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
+    assert np.all((ulps <= 1) | (np.abs(hi - want) <= 1e-7))
+    assert np.all(np.abs(hi.astype(np.float64) + lo - exact) <= 2.0 ** -46)
+    assert np.all(np.abs(lo.astype(np.float64)) <= np.spacing(np.abs(hi)) / 2)
+    assert np.abs(lo).max() > 0  # the second plane is not a copy of zeros
+
+
 def test_table_matches_oracle_angles(L):
-    """Each (cos, sin) entry is the float32 rounding of the oracle's angle for
-    that axis position and pair (within 1 float32 ulp: libm vs numpy)."""
+    """Both planes of the default table against the oracle's angle for each
+    axis position and pair."""
     T, Hl, Wl = 5, 7, 9
-    tab = sol.rope3d_table_host(T, Hl, Wl).reshape(-1, 2)
+    tab = sol.rope3d_table_host(T, Hl, Wl)
     # the oracle's angle of every pair at every position of each axis alone
     sections = []
     for axis, (ext, lo, width) in enumerate([(T, 0, 32), (Hl, 32, 48), (Wl, 80, 48)]):
@@ -442,12 +459,7 @@ def test_table_matches_oracle_angles(L):
         pos[:, axis] = np.arange(ext)
         ang = brute.rope_angles(pos)[:, lo // 2:(lo + width) // 2]
         sections.append(ang.reshape(-1))
-    ang = np.concatenate(sections)
-    want = np.stack([np.cos(ang), np.sin(ang)], -1).astype(np.float32)
-    assert tab.shape == want.shape
-    ulps = np.abs(tab.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
-    close = np.abs(tab - want) <= 1e-7
-    assert np.all((ulps <= 1) | close)
+    _check_planes(tab, np.concatenate(sections))
 
 
 SPLITS = [(32, 48, 48), (16, 24, 24), (0, 64, 64), (8, 0, 0), (64, 0, 64)]
@@ -456,13 +468,13 @@ SPLITS = [(32, 48, 48), (16, 24, 24), (0, 64, 64), (8, 0, 0), (64, 0, 64)]
 @pytest.mark.parametrize("split", SPLITS)
 def test_split_table_matches_oracle_angles(L, split):
     """The table of any rotary split (partial RoPE: dims past dt+dh+dw pass
-    through): one section per axis of width > 0, each (cos, sin) the float32
-    rounding of the numpy twin's angle for that position and pair."""
+    through): one section per axis of width > 0 in each plane, as above."""
     T, Hl, Wl = 4, 6, 5
     dt, dh, dw = split
     n = sol.sol_rope3d_table_floats_ex(128, T, Hl, Wl, dt, dh, dw)
-    assert n == 2 * (T * dt // 2 + Hl * dh // 2 + Wl * dw // 2)
-    tab = sol.rope3d_table_host(T, Hl, Wl, split=split)[:n].reshape(-1, 2)
+    assert n == 4 * (T * dt // 2 + Hl * dh // 2 + Wl * dw // 2)
+    tab = sol.rope3d_table_host(T, Hl, Wl, split=split)
+    assert tab.size == n
     sections, off = [], 0
     for axis, (ext, width) in enumerate([(T, dt), (Hl, dh), (Wl, dw)]):
         pos = np.zeros((ext, 3), np.int64)
@@ -470,13 +482,9 @@ def test_split_table_matches_oracle_angles(L, split):
         ang = brute.rope_angles(pos, split=split)[:, off // 2:(off + width) // 2]
         sections.append(ang.reshape(-1))
         off += width
-    ang = np.concatenate(sections)
-    want = np.stack([np.cos(ang), np.sin(ang)], -1).astype(np.float32)
-    assert tab.shape == want.shape
-    ulps = np.abs(tab.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
-    assert np.all((ulps <= 1) | (np.abs(tab - want) <= 1e-7))
+    _check_planes(tab, np.concatenate(sections))
     if split == (32, 48, 48):  # the default split is the table every other entry point takes
-        assert np.array_equal(tab.reshape(-1), sol.rope3d_table_host(T, Hl, Wl)[:n])
+        assert np.array_equal(tab, sol.rope3d_table_host(T, Hl, Wl))
 
 
 @pytest.mark.parametrize("split", [(4, 48, 48), (32, 48, 56), (-8, 64, 64), (32, 12, 48)])
@@ -490,13 +498,17 @@ def test_split_table_rejects_invalid_splits(L, split):
 def test_binding_rejects_a_table_of_another_grid():
     """The C ABI receives only the table's pointer; the binding checks its
     length against the grid and split before any launch (a 720p call given the
-    low-resolution table would read past its end)."""
+    low-resolution table would read past its end; the reverse would find its
+    second plane in the wrong place)."""
     import torch
     low = torch.from_numpy(sol.rope3d_table_host(8, 30, 52))
     dev = low.device
     assert sol._table_ptr(low, dev, 128, 8, 30, 52) is not None
     with pytest.raises(ValueError, match="need"):
         sol._table_ptr(low, dev, 128, 31, 45, 80)
+    big = torch.from_numpy(sol.rope3d_table_host(31, 45, 80))
+    with pytest.raises(ValueError, match="need"):
+        sol._table_ptr(big, dev, 128, 8, 30, 52)
     part = torch.from_numpy(sol.rope3d_table_host(8, 30, 52, split=(16, 24, 24)))
     with pytest.raises(ValueError, match="need"):
         sol._table_ptr(part, dev, 128, 8, 30, 52)  # the default split needs twice as many floats

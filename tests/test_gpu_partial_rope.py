@@ -50,9 +50,10 @@ def _ulps(got, want):
 @pytest.mark.parametrize("split", SPLITS, ids=[str(s) for s in SPLITS])
 @pytest.mark.parametrize("norm", [False, True], ids=["rope", "qknorm+rope"])
 def test_partial_rotation_matches_oracle(split, norm):
-    """Standalone rotation (and normalisation) under a split: within one bf16
-    ulp of the oracle, >= 99 % bit-exact; without normalisation the
-    pass-through dims are the input's bits."""
+    """Standalone rotation (and normalisation) under a split.  Rotation
+    alone: bit-identical to the oracle (exact rotation, one rounding), the
+    pass-through dims the input's bits.  With normalisation (fp32 against the
+    oracle's double): within one bf16 ulp, >= 99 % bit-exact."""
     w = W.custom(1, 3, 3, 11, 13, n_text=37, seed_index=1500 + sum(split), qk_norm=True)
     q, _, _ = W.make_inputs(w)
     gq, _ = W.norm_weights(w)
@@ -68,7 +69,7 @@ def test_partial_rotation_matches_oracle(split, norm):
         assert np.array_equal(got[..., tot:], _bits(q)[..., tot:]), "pass-through dims changed"
     ulp = _ulps(got, want)
     _log("partial rope %s norm=%s: max ulp %d, exact %.5f" % (split, norm, ulp.max(), (ulp == 0).mean()))
-    assert ulp.max() <= 1 and (ulp == 0).mean() >= 0.99
+    assert ulp.max() <= 1 and (ulp == 0).mean() >= (0.99 if norm else 1.0)
 
 
 SHAPES = [
