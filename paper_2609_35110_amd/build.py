@@ -9,6 +9,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsol.so")
+# debug build: LDS arrays that hold values are filled with NaN at kernel entry
+POISON_LIB = os.path.join(PKG, "libsol_poison.so")
 SOURCES = ["sol_kernels.hip", "sol_sparse.hip", "sol_records.hip", "sol_probe.hip", "sol_noalloc.hip",
            "sol_api.cpp"]
 ARCH = "gfx950"
@@ -38,11 +40,15 @@ def hipcc() -> str:
     return path
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP/C++ source into paper_2609_35110_amd/libsol.so (always rebuilds)."""
+def build(verbose: bool = False, poison: bool = False) -> str:
+    """Compile every HIP/C++ source into paper_2609_35110_amd/libsol.so (always
+    rebuilds).  poison: the LDS-poison debug build, libsol_poison.so (the same
+    sources with -DSOL_LDS_POISON)."""
+    out = POISON_LIB if poison else LIB
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE, "-I", CSRC, "-x", "hip"] + srcs + ["-o", tmp]
+    tmp = out + ".tmp%d" % os.getpid()
+    defs = ["-DSOL_LDS_POISON"] if poison else []
+    cmd = [hipcc()] + HIPCC_FLAGS + defs + ["-I", INCLUDE, "-I", CSRC, "-x", "hip"] + srcs + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -53,9 +59,9 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed (%d):\n%s" % (res.returncode, "\n".join(msgs)))
     if msgs and verbose:
         print("\n".join(msgs))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, poison="--poison" in sys.argv))

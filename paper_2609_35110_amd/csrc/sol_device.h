@@ -186,6 +186,29 @@ __device__ __forceinline__ uint4 rope_rotate_fast(uint4 x, float4 cs01, float4 c
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// ------------------------------------------------------- LDS poison (debug)
+
+// Debug build (-DSOL_LDS_POISON): a workgroup first fills the LDS arrays that
+// hold values -- never those holding indices, counts or flags -- with NaN bit
+// patterns and waits at a barrier, so a read that comes before the write it
+// needs (a missing barrier or wait) turns the output to NaN instead of
+// quietly reusing stale data.  Compiles to nothing in the normal build.
+template <typename T>
+__device__ __forceinline__ void lds_poison(T* p, size_t bytes) {
+#ifdef SOL_LDS_POISON
+  uint32_t* w = reinterpret_cast<uint32_t*>(p);
+  for (size_t i = threadIdx.x; i < bytes / 4; i += blockDim.x) w[i] = 0xFFFFFFFFu;
+#else
+  (void)p;
+  (void)bytes;
+#endif
+}
+__device__ __forceinline__ void lds_poison_done() {
+#ifdef SOL_LDS_POISON
+  __syncthreads();
+#endif
+}
+
 // ------------------------------------------------------- QK normalization
 
 // RMS normalisation of one head's row ahead of the rotation (Sec. 3.5, fusion
@@ -237,17 +260,6 @@ __device__ __forceinline__ uint4 qk_chunk(uint4 x, const float* __restrict__ gam
   if (!rot) return pack_bf16x8(f);
   return rope_rotate_exact(f, hi, lo, pair0);
 }
-
-// Prepared K/V tiles: 32 keys, 8 KB of fp16 each for K and for V.
-constexpr int kPrepTile = 32;                  // keys per prepared tile
-constexpr int kPrepTileElems = kPrepTile * D;  // 4096 fp16 = 8 KB
-
-// Block-sparse routing granularity and the longest kept-block list a query
-// block's workgroup stages in LDS (4 bytes an entry, beside 128 KB of K and V
-// rings: 8064 entries keep the kernel inside 160 KB).
-constexpr int kSparseKeyBlock = 128;    // keys per routing key block (4 tiles)
-constexpr int kSparseQueryBlock = 256;  // query rows per routing query block
-constexpr int kMaxSparseBlocks = 8064;  // key blocks per slab: N <= 1,032,192
 
 // ------------------------------------------------ block-INT8 QKV records
 

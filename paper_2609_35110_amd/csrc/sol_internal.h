@@ -88,16 +88,40 @@ hipError_t launch_qkv_decode(const uint8_t* rec, uint16_t* q, uint16_t* k, uint1
                              int N, hipStream_t stream);
 hipError_t launch_prepare_kv_records(const uint8_t* rec, uint16_t* k_prep, uint16_t* v_prep,
                                      int B, int H, int N, int key0, int n_kv, hipStream_t stream);
+// Tile and block sizes the host sizing below shares with the kernels.
+// Prepared K/V tiles: 32 keys, 8 KB of fp16 each for K and for V.
+constexpr int kPrepTile = 32;                         // keys per prepared tile
+constexpr int kPrepTileElems = kPrepTile * kHeadDim;  // 4096 fp16 = 8 KB
+// Block-sparse routing granularity and the longest kept-block list a query
+// block's workgroup stages in LDS (4 bytes an entry, beside 128 KB of K and V
+// rings: 8064 entries keep the kernel inside 160 KB).
+constexpr int kSparseKeyBlock = 128;    // keys per routing key block (4 tiles)
+constexpr int kSparseQueryBlock = 256;  // query rows per routing query block
+constexpr int kMaxSparseBlocks = 8064;  // key blocks per slab: N <= 1,032,192
+// Query rows per workgroup of the fused kernel (sol_attn_fwd).
+constexpr int kFusedRows = 256;
+
 // fp16 elements of one (b, h) slab of prepared K (or V).
-int64_t prepared_tile_elems(int N);
+inline int64_t prepared_tile_elems(int N) {
+  return (int64_t)((N + kPrepTile - 1) / kPrepTile) * kPrepTileElems;
+}
 
 // Block-sparse routing (sol_sparse.hip).  Workspace sections, byte offsets
 // off[0..3]: counts int32 [BH][nqb], blocks uint16 [BH][nqb][nkb], pooled
 // queries fp32 [BH][nqb][D], pooled keys fp32 [BH][nkb][D] (nqb = ceil(N/256),
 // nkb = ceil(N/128)); returns the total size.
-size_t sparse_workspace_offsets(int BH, int N, size_t off[4]);
+inline size_t sparse_workspace_offsets(int BH, int N, size_t off[4]) {
+  const size_t nqb = (size_t)(N + kSparseQueryBlock - 1) / kSparseQueryBlock;
+  const size_t nkb = (size_t)(N + kSparseKeyBlock - 1) / kSparseKeyBlock;
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  off[0] = 0;                                              // counts: int32 [BH][nqb]
+  off[1] = up(off[0] + (size_t)BH * nqb * 4);              // blocks: uint16 [BH][nqb][nkb]
+  off[2] = up(off[1] + (size_t)BH * nqb * nkb * 2);        // qbar: fp32 [BH][nqb][D]
+  off[3] = up(off[2] + (size_t)BH * nqb * kHeadDim * 4);   // kbar: fp32 [BH][nkb][D]
+  return up(off[3] + (size_t)BH * nkb * kHeadDim * 4);
+}
 // Largest N the block-sparse path takes (its key-block lists live in LDS).
-int sparse_max_tokens();
+inline int sparse_max_tokens() { return kMaxSparseBlocks * kSparseKeyBlock; }
 // Pools q (rotated with grid g, normalised with q_gamma) and the prepared
 // keys, then routes every query block with threshold parameter tau.
 hipError_t launch_sparse_route(const uint16_t* q, const uint16_t* k_prep, int BH, const SeqGrid& g,
@@ -111,7 +135,9 @@ hipError_t launch_mfma_probe(const uint16_t* operands, float* out, int workgroup
                              hipStream_t stream);
 
 // Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
-int64_t attn_max_workgroups(int N, int BH);
+inline int64_t attn_max_workgroups(int N, int BH) {
+  return (int64_t)((N + kFusedRows - 1) / kFusedRows) * BH;
+}
 
 // The current device's sticky range status (sol_range_status): waits for all
 // work on the device, copies the flags out, and clears them when asked.

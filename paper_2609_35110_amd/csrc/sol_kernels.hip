@@ -120,6 +120,8 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
                                                       const float* __restrict__ gamma, float eps,
                                                       const uint8_t* __restrict__ rec, int heads) {
   __shared__ __attribute__((aligned(16))) uint16_t vt[kPrepTile * (D + 8)];
+  lds_poison(vt, sizeof(vt));
+  lds_poison_done();
   const float2* __restrict__ tab_lo = tab_lo_plane(tab, g);
   const int n_src = g.n;
   const int n_tiles = (n_kv + kPrepTile - 1) / kPrepTile;  // tiles per prepared slab
@@ -210,6 +212,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint4* __restrict__ 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int BM = 32 * kWaves;  // query rows per workgroup (32 per wave)
+static_assert(BM == kFusedRows, "the host sizes the fused grid with kFusedRows");
 constexpr int BN = 64;           // keys per tile
 constexpr int KS = D + 8;        // K tile row stride in LDS (elements): 272 B
 constexpr int VS = D + 32;       // V tile row stride in LDS (elements): 320 B
@@ -259,6 +262,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][BN * KS];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][BN * VS];
   __shared__ __attribute__((aligned(16))) float2 tab_lds[kTabLds ? kTabLdsPairs : 2];
+  lds_poison(k_lds, sizeof(k_lds));
+  lds_poison(v_lds, sizeof(v_lds));
+  lds_poison(tab_lds, sizeof(tab_lds));
+  lds_poison_done();
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -719,6 +726,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[kVB * kPrepTileElems];
   __shared__ uint32_t blist[kSparse ? kMaxSparseBlocks : 1];  // entry e | entry e + 1 << 16
   __shared__ int n_gave_up;  // first pass: waves of the workgroup that stopped computing
+  lds_poison(k_lds, sizeof(k_lds));
+  lds_poison(v_lds, sizeof(v_lds));
+  lds_poison_done();
 
   auto keep = [&](auto& x) __attribute__((always_inline)) { pin(x); };
   // Score units.  First pass: q' = fp16(q^ c), c = log2(e)/sqrt(D), so the
@@ -1471,10 +1481,6 @@ hipError_t launch_prepare_kv_records(const uint8_t* rec, uint16_t* k_prep, uint1
   return hipGetLastError();
 }
 
-int64_t prepared_tile_elems(int N) {
-  return (int64_t)((N + kPrepTile - 1) / kPrepTile) * kPrepTileElems;
-}
-
 hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
                                     const uint16_t* v_prep, void* out_v, int BH,
                                     const SeqGrid& g, int n_kv, const float2* tab,
@@ -1524,8 +1530,6 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   }
   return hipSuccess;
 }
-
-int64_t attn_max_workgroups(int N, int BH) { return (int64_t)((N + BM - 1) / BM) * BH; }
 
 namespace {
 std::mutex g_flags_mutex;

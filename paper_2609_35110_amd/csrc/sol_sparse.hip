@@ -38,6 +38,8 @@ __global__ __launch_bounds__(256) void pool_q_kernel(const uint4* __restrict__ q
                                                      const float* __restrict__ gamma, float eps,
                                                      int nqb) {
   __shared__ float part[16][D + 4];
+  lds_poison(&part[0][0], sizeof(part));
+  lds_poison_done();
   const int N = g.n;
   const int I = blockIdx.x;
   const int t = threadIdx.x, cc = t & 15, rg = t >> 4;
@@ -166,6 +168,10 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ qb
   __shared__ float red[256];
   __shared__ int redi[256];
   __shared__ int wcount[4];
+  lds_poison(&qs[0][0], sizeof(qs));
+  lds_poison(&sc[0][0], sizeof(sc));
+  lds_poison(red, sizeof(red));
+  lds_poison_done();
   const int I0 = blockIdx.x * kRouteQB;
   const int nq = min(kRouteQB, nqb - I0);
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -262,18 +268,6 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ qb
 }
 
 }  // namespace
-
-size_t sparse_workspace_offsets(int BH, int N, size_t off[4]) {
-  const size_t nqb = (size_t)(N + kQB - 1) / kQB, nkb = (size_t)(N + kKB - 1) / kKB;
-  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  off[0] = 0;                                            // counts: int32 [BH][nqb]
-  off[1] = up(off[0] + (size_t)BH * nqb * 4);            // blocks: uint16 [BH][nqb][nkb]
-  off[2] = up(off[1] + (size_t)BH * nqb * nkb * 2);      // qbar: fp32 [BH][nqb][D]
-  off[3] = up(off[2] + (size_t)BH * nqb * D * 4);        // kbar: fp32 [BH][nkb][D]
-  return up(off[3] + (size_t)BH * nkb * D * 4);
-}
-
-int sparse_max_tokens() { return kMaxKeyBlocks * kKB; }
 
 hipError_t launch_sparse_route(const uint16_t* q, const uint16_t* k_prep, int BH, const SeqGrid& g,
                                const float2* tab, const float* q_gamma, float eps, float tau,

@@ -173,6 +173,24 @@ def boosted_tokens(w: Workload, seed: int = None):
     return torch.randperm(w.N, generator=gen)[: int(w.N * w.boost_frac)]
 
 
+def make_slab(w: Workload, tensor: int, bh: int, seed: int = None, boosted=None):
+    """One (tensor, b*H + h) slab of make_inputs, bf16 [N, D] (CPU): tensor
+    0/1/2 = q/k/v.  The whole recipe for that slab (draw, boosted keys, QK-norm
+    row scales), so any slab can be regenerated alone.  boosted: the boosted
+    token indices when the caller already has them."""
+    seed = w.seed if seed is None else seed
+    x = torch.empty((w.N, w.D), dtype=torch.bfloat16)
+    _fill_slab(x, seed, tensor, bh, w)
+    if tensor == 1 and w.boost_frac > 0:
+        idx = boosted_tokens(w, seed) if boosted is None else boosted
+        x[idx, :] *= torch.tensor(w.boost, dtype=torch.bfloat16)  # x8: exact
+    if w.qk_norm and tensor in (0, 1):
+        gen = torch.Generator().manual_seed(slab_seed(seed, 4 + tensor, bh))
+        e = torch.randint(-4, 5, (w.N, 1), generator=gen).to(torch.float32)
+        x.mul_(torch.exp2(e).to(torch.bfloat16))  # powers of two: exact
+    return x
+
+
 def make_inputs(w: Workload, seed: int = None, threads: int = None):
     """Return (q, k, v): bf16 CPU tensors [B, H, N, D], contiguous."""
     seed = w.seed if seed is None else seed
@@ -180,23 +198,14 @@ def make_inputs(w: Workload, seed: int = None, threads: int = None):
     jobs = [(t, bh) for t in range(3) for bh in range(w.B * w.H)]
     if threads is None:
         threads = min(16, len(os.sched_getaffinity(0)))
+    boosted = boosted_tokens(w, seed)
 
     def run(job):
         t, bh = job
-        _fill_slab(out[t].view(w.B * w.H, w.N, w.D)[bh], seed, t, bh, w)
+        out[t].view(w.B * w.H, w.N, w.D)[bh].copy_(make_slab(w, t, bh, seed, boosted))
 
     with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
         list(ex.map(run, jobs))
-    idx = boosted_tokens(w, seed)
-    if idx.numel():
-        out[1][:, :, idx, :] *= torch.tensor(w.boost, dtype=torch.bfloat16)
-    if w.qk_norm:
-        for t in (0, 1):
-            x = out[t].view(w.B * w.H, w.N, w.D)
-            for bh in range(w.B * w.H):
-                gen = torch.Generator().manual_seed(slab_seed(seed, 4 + t, bh))
-                e = torch.randint(-4, 5, (w.N, 1), generator=gen).to(torch.float32)
-                x[bh].mul_(torch.exp2(e).to(torch.bfloat16))  # powers of two: exact
     return tuple(out)
 
 
@@ -212,11 +221,20 @@ def norm_weights(w: Workload, seed: int = None):
     return tuple(res)
 
 
-def make_ref_inputs(w: Workload, seed: int = None, threads: int = None):
-    """(k_ref, v_ref): the cached reference segment's keys and values, bf16
-    [B, H, n_ref, D], drawn like video rows (N(0,1) times the workload scale)."""
+def make_ref_slab(w: Workload, tensor: int, bh: int, seed: int = None):
+    """One slab of make_ref_inputs, bf16 [n_ref, D]: tensor 0 = k, 1 = v of the
+    cached reference segment, drawn like video rows (N(0,1) times the workload
+    scale) from stream 8 + tensor."""
     seed = w.seed if seed is None else seed
     rw = Workload("ref", w.index, w.B, w.H, *w.ref_grid, scale=w.scale, D=w.D)
+    x = torch.empty((w.n_ref, w.D), dtype=torch.bfloat16)
+    _fill_slab(x, seed, 8 + tensor, bh, rw)
+    return x
+
+
+def make_ref_inputs(w: Workload, seed: int = None, threads: int = None):
+    """(k_ref, v_ref): the cached reference segment's keys and values, bf16
+    [B, H, n_ref, D]."""
     out = [torch.empty((w.B, w.H, w.n_ref, w.D), dtype=torch.bfloat16) for _ in range(2)]
     jobs = [(t, bh) for t in range(2) for bh in range(w.B * w.H)]
     if threads is None:
@@ -224,7 +242,7 @@ def make_ref_inputs(w: Workload, seed: int = None, threads: int = None):
 
     def run(job):
         t, bh = job
-        _fill_slab(out[t].view(w.B * w.H, w.n_ref, w.D)[bh], seed, 8 + t, bh, rw)
+        out[t].view(w.B * w.H, w.n_ref, w.D)[bh].copy_(make_ref_slab(w, t, bh, seed))
 
     with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
         list(ex.map(run, jobs))
