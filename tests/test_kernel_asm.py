@@ -229,3 +229,41 @@ def test_first_pass_copy_count_waits_see_only_copies(asm_text):
                     assert not others, "%s: %r before a copy-count wait" % (name, others[:3])
                 since = []
         assert n_waits >= 2, name
+
+
+def _vregs(text):
+    """VGPR and AGPR names (v12, a3, ...) in an operand list."""
+    out = set()
+    for m in re.finditer(r"\b([va])(\d+)\b", text):
+        out.add(m.group(1) + m.group(2))
+    for m in re.finditer(r"\b([va])\[(\d+):(\d+)\]", text):
+        out.update(m.group(1) + str(r) for r in range(int(m.group(2)), int(m.group(3)) + 1))
+    return out
+
+
+def test_loaded_registers_read_after_their_vmcnt_wait(asm_text):
+    """A register that a vector-memory load writes is read only after a vmcnt
+    wait that retires the load, counting every vector-memory instruction
+    issued after it -- the inline-asm tile copies included, which the
+    compiler's own wait insertion does not see.  (The counter retires in
+    order, so a wait the compiler places for its own loads is at least as
+    strict as it needs; this checks that on the generated code, in program
+    order within each instance.)"""
+    for name, body in functions(asm_text, "attn_prepared_kernel"):
+        pending = []  # vector-memory instructions in issue order: (index, registers it loads)
+        for i, (t, _) in enumerate(instructions(body)):
+            op = t.split()[0]
+            ops = operands(t)
+            if op == "s_waitcnt":
+                m = re.search(r"vmcnt\((\d+)\)", t)
+                if m and len(pending) > int(m.group(1)):
+                    pending = pending[len(pending) - int(m.group(1)):]
+                continue
+            if ops:
+                reads = _vregs(",".join(ops if op.startswith(STORE_PREFIXES) else ops[1:]))
+                for j, dst in pending:
+                    assert not (dst & reads), "%s: %r reads a register loaded by instruction %d before its wait" % (
+                        name, t, j)
+            if op.startswith(("buffer_", "global_", "scratch_", "flat_")):
+                loads = "load" in op and not t.endswith(" lds")
+                pending.append((i, _vregs(ops[0]) if loads else set()))
