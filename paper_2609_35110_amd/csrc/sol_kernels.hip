@@ -752,9 +752,23 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int wave = tid >> 6;
   const int hh = lane >> 5;
   const int l32 = lane & 31;
-  const int wg = xcd_local_id(blockIdx.x, gridDim.x);
-  const int bh = wg / n_qtiles;
-  const int qt = wg - bh * n_qtiles;
+  int bh, qt;
+  if (kSparse) {
+    // Slab-synchronous order: XCD x takes query tiles [x c, x c + c) of every
+    // slab in turn (c = ceil(n_qtiles / 8); the grid holds 8 c workgroups per
+    // slab), so the eight XCDs work on about one slab at a time and the
+    // slab's K/V, which the sparse walks miss L2 on far more often than the
+    // dense walk, stays in the memory-side cache.  Tiles past the slab leave.
+    const int c = (n_qtiles + kXcds - 1) / kXcds;
+    const int x = blockIdx.x % kXcds, l = blockIdx.x / kXcds;
+    bh = l / c;
+    qt = x * c + (l - bh * c);
+    if (qt >= n_qtiles) return;  // the whole workgroup, before any barrier
+  } else {
+    const int wg = xcd_local_id(blockIdx.x, gridDim.x);
+    bh = wg / n_qtiles;
+    qt = wg - bh * n_qtiles;
+  }
   const int Nq = g.n;  // query rows of the slab (the grid describes them)
   const int N = n_keys;  // keys of the slab
   const size_t slab = (size_t)bh * Nq * D;
@@ -1490,8 +1504,10 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   uint16_t* out = static_cast<uint16_t*>(out_v);
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
-  const dim3 grid((unsigned)((int64_t)n_qtiles * BH));
   const bool sparse = blocks != nullptr;
+  // the block-sparse walk runs in slab-synchronous order: 8 ceil(n_qtiles / 8) per slab
+  const int64_t per_slab = sparse ? (int64_t)kXcds * ((n_qtiles + kXcds - 1) / kXcds) : n_qtiles;
+  const dim3 grid((unsigned)(per_slab * BH));
   // First pass, then the second over the row blocks whose probabilities left
   // the fp16 range.
   for (int pass = 0; pass < 2; ++pass) {
