@@ -4,7 +4,9 @@ A step is one pass of the whole path over one layer (every batch and head):
 by default the prepared path -- sol_prepare_kv_ex (k rotated, k and v
 converted to fp16 tiles, one pass) then sol_attn_fwd_prepared_ex (q rotated in
 its tile load, softmax(q^ k^T / sqrt(D)) v, bf16 out); --path fused times
-sol_attn_fwd (q and k rotated in every tile load).  The p720n workload adds
+sol_attn_fwd, the workspace-free signature (the prepared path chunk by
+chunk with its K and V in the out slabs not yet written, then the fused
+kernel -- q and k rotated in every tile load -- for the last slabs).  The p720n workload adds
 the QK normalization ahead of the rotation; ref720 attends to a cached
 reference segment prepared once, before the timed steps; --tau runs the
 block-sparse attention, --records the block-INT8 QKV wire records (encoded,
@@ -156,7 +158,8 @@ def main():
     ap.add_argument("--path", default="prepared", choices=["fused", "prepared"],
                     help="prepared: sol_prepare_kv (K rotated, V to fp16, one pass) then "
                          "sol_attn_fwd_prepared (q rotated in its tile load); fused: sol_attn_fwd "
-                         "(q and k rotated in every tile load)")
+                         "(no workspace: prepared chunks in the unwritten out slabs, the fused kernel "
+                         "for the last slabs)")
     ap.add_argument("--tau", type=float, default=None,
                     help="block-sparse attention with this threshold parameter (the paper's "
                          "refinement steps use 1.0, 1.25, 1.5); the step is then sol_prepare_kv_ex + "

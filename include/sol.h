@@ -21,7 +21,8 @@
  * rotation: the kernels turn each pair in fp64 with cos and sin to 48 bits
  * (the table's two planes) and round once, so they differ from the correctly
  * rounded value only where it lies within about 2^-47 |pair| of a rounding
- * midpoint.  (One exception, sol_attn_fwd's key tiles, is documented there.)
+ * midpoint.  (One exception, the fused kernel's key tiles, is documented at
+ * sol_attn_fwd.)
  *
  * Sequence packing follows Sec. 3.4 "Safety rails" (prefix before the target
  * video): of the N tokens, the first Nt = N - T*Hl*Wl form an unrotated
@@ -76,15 +77,16 @@ enum {
  * Range status (sol_range_status): bits the kernels set, per device and
  * sticky until cleared, when an input leaves the range the computation
  * supports or an output is not finite.  The prepared path (sol_prepare_kv*,
- * sol_attn_fwd_prepared*, sol_attn_fwd_ws, sol_attn_fwd_noalloc, the
- * block-sparse and records paths) multiplies in fp16 with fp32 accumulation:
+ * sol_attn_fwd_prepared*, sol_attn_fwd_ws, sol_attn_fwd_noalloc, the chunks
+ * of sol_attn_fwd, the block-sparse and records paths) multiplies in fp16
+ * with fp32 accumulation:
  *   SOL_RANGE_Q: a query value q^ log2(e)/sqrt(D) is not finite in fp16
  *     (|q^| >= about 513,000, or an inf/NaN input);
  *   SOL_RANGE_K: a key value k^ (normalised, rotated, bf16) is not finite in
  *     fp16 (|k^| >= 65520, or inf/NaN);
  *   SOL_RANGE_V: a value v is not finite in fp16 (|v| >= 65520, or inf/NaN);
  *   SOL_RANGE_OUT: an output element is inf or NaN (any attention entry
- *     point: the fused sol_attn_fwd also converts v to fp16 for the second
+ *     point: the fused kernel also converts v to fp16 for the second
  *     product, so |v| >= 65520 lands here; inf or NaN inputs too).
  * Such a call's outputs are not finite where the bad operand takes part --
  * never a finite wrong value -- and the bits say why.  fp16's subnormal range
@@ -163,24 +165,42 @@ int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T,
                       float eps, sol_stream_t stream);
 
 /*
- * out = softmax(q^ k^T / sqrt(D)) v with q^, k^ rotated and rounded to bf16
- * inside the kernel (fused into the tile loads): q^ as sol_rope3d, bit for
- * bit; k^, rotated again in every query tile's pass over the keys, in fp32
- * with the table's hi plane only (two operations an element against about
- * ten), which is within one bf16 ulp of sol_rope3d's and equal to it except
- * where the exact rotation lies within a few 2^-24 |pair| of a rounding
- * midpoint (about 1 element in 10^4).  fp32 logits, softmax
- * statistics and accumulators.  The second product takes the probabilities
- * rounded to fp16 and v converted to fp16 (exact for |v| < 65504; larger
- * values overflow to inf and raise SOL_RANGE_OUT), so the output error stays
- * at the bf16 rounding of out (round to nearest even).
+ * out = softmax(q^ k^T / sqrt(D)) v for every (b, h) slab, q^ and k^ rotated
+ * and rounded to bf16 as sol_rope3d (exact rotation).  The call allocates
+ * nothing and takes no workspace, so it uses the slabs of `out` it has not
+ * written yet as one: it walks the slabs front to back in chunks, and for a
+ * chunk of c slabs prepares their K and V (sol_prepare_kv, 2 c slabs' worth of
+ * fp16 tiles) in the out slabs after the chunk, then attends to them
+ * (sol_attn_fwd_prepared), writing the chunk's own out slabs; each chunk is as
+ * large as the room after it allows.  The last slabs, with no room left after
+ * them (sol_attn_fwd_plan tells how many slabs the chunks cover: 37 of 40 at
+ * 720p, none of 2), run the fused kernel instead, which rotates q and k in its tile
+ * loads -- q^ as sol_rope3d, bit for bit; k^, rotated again in every query
+ * tile's pass over the keys, in fp32 with the table's hi plane only, within
+ * one bf16 ulp of sol_rope3d's and equal to it except where the exact
+ * rotation lies within a few 2^-24 |pair| of a rounding midpoint (about 1
+ * element in 10^4) -- with bf16 score operands.  Either way: fp32 softmax
+ * statistics and accumulators, probabilities rounded to fp16 and v converted
+ * to fp16 for the second product, the output rounded to bf16 (nearest even);
+ * the chunks take the prepared path's operand ranges and status bits (below),
+ * the fused kernel needs |v| < 65504 (else SOL_RANGE_OUT).  A slab's result
+ * depends only on its data and on which of the two it ran through.
  * q, k, v, out: [B][H][N][D] bf16, 16-byte aligned; out must not overlap
- * q, k or v.  0 <= T*Hl*Wl <= N.  rope_tab_dev = NULL or T*Hl*Wl = 0 means
- * plain attention (nothing rotated); otherwise it is the device copy of
- * sol_rope3d_table(D, T, Hl, Wl), 16-byte aligned.
+ * q, k or v (its contents on entry are ignored).  0 <= T*Hl*Wl <= N.
+ * rope_tab_dev = NULL or T*Hl*Wl = 0 means plain attention (nothing rotated);
+ * otherwise it is the device copy of sol_rope3d_table(D, T, Hl, Wl), 16-byte
+ * aligned.
  */
 int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
                  int D, int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream);
+
+/*
+ * The number of leading (b, h) slabs, in [b][h] order, that sol_attn_fwd
+ * computes through the prepared path in place for this shape; the remaining
+ * B*H minus that run the fused kernel.  Host-only; negative status for
+ * invalid shapes.
+ */
+int sol_attn_fwd_plan(int B, int H, int N, int D);
 
 /*
  * The attention in two stages, for callers that keep prepared K/V (the
@@ -213,7 +233,7 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
  * score distribution: p480's 1 % of keys x8 runs at the rate of the dense
  * shapes).  out must not overlap q, k_prep or v_prep.
  *
- * The result differs from sol_attn_fwd's by rounding only (same contract and
+ * The result differs from the fused kernel's by rounding only (same contract and
  * error bound; the fp16 score operands and the reference max change the last
  * bits).
  */

@@ -220,6 +220,35 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
                            nullptr, 0.0f, stream);
 }
 
+// sol_attn_fwd's schedule: chunks of whole (b, h) slabs, front to back, each
+// through the prepared path with its prepared K and V held in the slabs of
+// `out` after the chunk (not yet written); a chunk takes as many slabs as
+// leave room for that, up to kMaxChunks chunks.  Returns the number of slabs
+// the chunks cover (the rest run the fused kernel) and their sizes in chunk[].
+constexpr int kMaxChunks = 64;
+static int attn_fwd_schedule(int B, int H, int N, int D, int (&chunk)[kMaxChunks]) {
+  const int64_t S = (int64_t)B * H;
+  const int64_t region = (int64_t)N * D * 2;                        // one slab of out
+  const int64_t kv = 2 * sol::prepared_tile_elems(N) * 2;           // one slab of K and V tiles
+  int64_t s = 0;
+  for (int n = 0; n < kMaxChunks && s < S; ++n) {
+    // the largest c with c * kv <= (S - s - c) * region
+    int64_t c = (S - s) * region / (kv + region);
+    while (c > 0 && c * kv > (S - s - c) * region) --c;
+    if (c == 0) break;
+    chunk[n] = (int)c;
+    s += c;
+  }
+  return (int)s;
+}
+
+int sol_attn_fwd_plan(int B, int H, int N, int D) {
+  int st = check_shape(B, H, N, D, 0, 0, 0);
+  if (st != SOL_OK) return st;
+  int chunk[kMaxChunks];
+  return attn_fwd_schedule(B, H, N, D, chunk);
+}
+
 int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int D,
                  int T, int Hl, int Wl, const float* rope_tab_dev, sol_stream_t stream) {
   if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v, out must not be NULL");
@@ -235,10 +264,34 @@ int sol_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, 
   const int64_t nv = (int64_t)T * Hl * Wl;
   const float2* tab = nv > 0 ? reinterpret_cast<const float2*>(rope_tab_dev) : nullptr;
   const sol::SeqGrid g = sol::make_grid(N, T, Hl, Wl);
-  hipError_t e = sol::launch_attn_fwd(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                                      static_cast<const uint16_t*>(v), static_cast<uint16_t*>(out), B * H,
-                                      g, tab, reinterpret_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+  const hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const size_t slab = (size_t)N * D;  // elements of one (b, h) slab
+  const uint16_t* qs = static_cast<const uint16_t*>(q);
+  const uint16_t* ks = static_cast<const uint16_t*>(k);
+  const uint16_t* vs = static_cast<const uint16_t*>(v);
+  uint16_t* os = static_cast<uint16_t*>(out);
+  const size_t kv_elems = (size_t)sol::prepared_tile_elems(N);  // per slab, K or V
+  int chunk[kMaxChunks];
+  const int covered = attn_fwd_schedule(B, H, N, D, chunk);
+  int s = 0;
+  for (int i = 0; s < covered; ++i) {
+    const int c = chunk[i];
+    // prepared K and V of slabs [s, s + c) in the out slabs from s + c on
+    uint16_t* kp = os + (size_t)(s + c) * slab;
+    uint16_t* vp = kp + (size_t)c * kv_elems;
+    hipError_t e = sol::launch_prepare_kv(ks + s * slab, vs + s * slab, kp, vp, c, g, tab, 0, N, nullptr,
+                                          0.0f, hs);
+    if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd (prepare) launch: %s", hipGetErrorString(e));
+    e = sol::launch_attn_fwd_prepared(qs + s * slab, kp, vp, os + s * slab, c, g, N, tab, nullptr, 0.0f,
+                                      SOL_OUT_BF16, nullptr, nullptr, 0, hs, nullptr, c);
+    if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd (attention) launch: %s", hipGetErrorString(e));
+    s += c;
+  }
+  if (s < B * H) {
+    hipError_t e = sol::launch_attn_fwd(qs + s * slab, ks + s * slab, vs + s * slab, os + s * slab,
+                                        B * H - s, g, tab, hs);
+    if (e != hipSuccess) return fail(SOL_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+  }
   return ok();
 }
 

@@ -61,6 +61,8 @@ def lib():
         L.sol_rope3d.restype = i32
         L.sol_attn_fwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_attn_fwd.restype = i32
+        L.sol_attn_fwd_plan.argtypes = [i32, i32, i32, i32]
+        L.sol_attn_fwd_plan.restype = i32
         L.sol_prepare_kv.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
         L.sol_prepare_kv.restype = i32
         L.sol_attn_fwd_prepared.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, i32, i32, P, P]
@@ -172,6 +174,10 @@ def sol_attn_fwd_sparse(q, k_prep, v_prep, out, B, H, N, D, T, Hl, Wl, dt, dh, d
 
 def sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream):
     return lib().sol_attn_fwd(q, k, v, out, B, H, N, D, T, Hl, Wl, rope_tab, stream)
+
+
+def sol_attn_fwd_plan(B, H, N, D):
+    return lib().sol_attn_fwd_plan(B, H, N, D)
 
 
 def sol_prepare_kv(k, v, k_prep, v_prep, B, H, N, D, T, Hl, Wl, rope_tab, stream):

@@ -513,3 +513,31 @@ def test_binding_rejects_a_table_of_another_grid():
     with pytest.raises(ValueError, match="need"):
         sol._table_ptr(part, dev, 128, 8, 30, 52)  # the default split needs twice as many floats
     assert sol._table_ptr(part, dev, 128, 8, 30, 52, split=(16, 24, 24)) is not None
+
+
+# ------------------------------------------------------- sol_attn_fwd's plan
+
+def _plan_rule(S, N, D=128):
+    """The schedule sol.h states, written out: chunks front to back, each the
+    largest c whose prepared K and V (2 ceil(N/32) 32 D fp16 values per slab)
+    fit in the S - s - c out slabs (N D bf16 each) after it."""
+    region = N * D * 2
+    kv = 2 * ((N + 31) // 32) * 32 * D * 2
+    s = 0
+    while s < S:
+        c = max([t for t in range(0, S - s + 1) if t * kv <= (S - s - t) * region])
+        if c == 0:
+            break
+        s += c
+    return s
+
+
+def test_attn_fwd_plan(L):
+    assert sol.sol_attn_fwd_plan(1, 40, 111600, 128) == 37  # 720p: three slabs run the fused kernel
+    assert sol.sol_attn_fwd_plan(1, 2, 192, 128) == 0       # two slabs: no room for any chunk
+    assert sol.sol_attn_fwd_plan(1, 3, 192, 128) == 1       # N a multiple of 32: K and V fill two slabs
+    assert sol.sol_attn_fwd_plan(1, 3, 193, 128) == 0       # padding to 224 keys: they do not
+    for B, H, N in [(2, 5, 112112), (1, 24, 12480), (3, 7, 466), (1, 1, 1), (4, 16, 1000), (1, 200, 64)]:
+        assert sol.sol_attn_fwd_plan(B, H, N, 128) == _plan_rule(B * H, N), (B, H, N)
+    assert sol.sol_attn_fwd_plan(1, 2, 0, 128) < 0
+    assert sol.sol_attn_fwd_plan(1, 2, 64, 64) < 0

@@ -376,15 +376,52 @@ def test_repeated_runs_are_bitwise_identical(path):
 
 @pytest.mark.parametrize("path", PATHS)
 def test_heads_and_batches_are_independent(path):
+    """A slab's result is a function of its own data (and, for sol_attn_fwd,
+    of which of its two routes it took): every slab of a batched call equals
+    the same slab computed alone by that route, bit for bit."""
     w = W.custom(2, 3, 3, 11, 13, n_text=5, seed_index=702)
     q, k, v = (t.to(DEV) for t in W.make_inputs(w))
     tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
     full = _attn(path, q, k, v, w, tab)
-    b, h = 1, 2
-    one = _attn(path, q[b:b + 1, h:h + 1].contiguous(), k[b:b + 1, h:h + 1].contiguous(),
-                v[b:b + 1, h:h + 1].contiguous(), w, tab)
+    chunked = sol.sol_attn_fwd_plan(w.B, w.H, w.N, w.D) if path == "fused" else 0
+    for b in range(w.B):
+        for h in range(w.H):
+            alone = [x[b:b + 1, h:h + 1].contiguous() for x in (q, k, v)]
+            # one slab alone: sol_attn_fwd has no room for a chunk and runs the fused kernel
+            route = "prepared" if b * w.H + h < chunked else path
+            one = _attn(route, *alone, w, tab)
+            torch.cuda.synchronize()
+            assert torch.equal(full[b:b + 1, h:h + 1], one), (b, h, route)
+
+
+def test_attn_fwd_runs_chunks_in_place_then_the_fused_kernel():
+    """sol_attn_fwd's schedule (prepared chunks whose K and V live in the out
+    slabs not yet written, then the fused kernel for the slabs left without
+    room): the chunked slabs equal the prepared path bit for bit, the rest
+    equal the fused kernel alone, the whole matches the oracle, and nothing is
+    written outside out (sentinels)."""
+    w = W.custom(2, 5, 3, 8, 9, n_text=19, seed_index=705)  # N = 235: ragged tiles
+    plan = sol.sol_attn_fwd_plan(w.B, w.H, w.N, w.D)
+    assert 0 < plan < w.B * w.H
+    q, k, v = (t.to(DEV) for t in W.make_inputs(w))
+    tab = sol.rope3d_table(w.T, w.Hl, w.Wl, device=DEV)
+    numel = q.numel()
+    buf = torch.full((numel + 4096,), 123.0, dtype=torch.bfloat16, device=DEV)
+    out = buf[:numel].view(q.shape)
+    sol.attn_fwd(q, k, v, w.T, w.Hl, w.Wl, tab, out=out)
+    prepared = sol.attn_fwd_ws(q, k, v, w.T, w.Hl, w.Wl, tab)
+    S = w.B * w.H
+    flat = lambda x: x.reshape(1, S, w.N, w.D)
+    tail = sol.attn_fwd(*(flat(x)[:, plan:].contiguous() for x in (q, k, v)), w.T, w.Hl, w.Wl, tab)
     torch.cuda.synchronize()
-    assert torch.equal(full[b:b + 1, h:h + 1], one)
+    assert (buf[numel:] == 123.0).all(), "write past the end of out"
+    assert torch.equal(flat(out)[:, :plan], flat(prepared)[:, :plan])
+    assert torch.equal(flat(out)[:, plan:], tail)
+    ref = oracle.attn_rows(_bits(q.cpu()), _bits(k.cpu()), _bits(v.cpu()), w.T, w.Hl, w.Wl)
+    R = S * w.N
+    st = compare(_bits(out.cpu()).reshape(R, w.D), ref.reshape(R, w.D), np.repeat(np.arange(S), w.N))
+    _log("attn_fwd chunks %d + fused %d: %s" % (plan, S - plan, st))
+    assert_parity(st, "attn_fwd schedule")
 
 
 def test_offsets_beyond_2_pow_31_elements():
