@@ -1079,6 +1079,11 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
         mfma_s_next(ns[1], kr[j], qf[1][j]);
       }
       __builtin_amdgcn_sched_barrier(0);
+      // First pass: the iteration's barrier, once its first two score MFMAs
+      // (register operands only) are on the matrix cores, which then keep
+      // working through the wait; every LDS read and copy of the iteration
+      // comes after it.
+      if (!kRobust && j == 0) dma_barrier<kInflight>();
       kr[j] = kfrag(i + 2, j);
       if (j == 2) { t01 = add_f16x2(p1[0], p1[1]); keep(t01); }
       if (j == 4) { t23 = add_f16x2(p1[2], p1[3]); keep(t23); }
@@ -1191,8 +1196,9 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // The copies the next iteration reads must have landed: those issued
     // kKAhead - 2 iterations ago (K) and kVAhead - 1 ago (V) -- so only the
     // copies of this and the kInflight - 1 previous iterations (4 each) may
-    // still be in flight.
-    dma_barrier<kInflight>();
+    // still be in flight.  (First pass: that barrier is the next iteration's,
+    // after its first two MFMAs.)
+    if (kRobust) dma_barrier<kInflight>();
     // Raise block 0's m while S(i+1) is still in registers (the block's next
     // scores are computed with the raised m).
     if (kRobust && __builtin_expect(ovf0 != 0, 0)) raise_max(0, ns[0], nullptr, p0_next, l0_next);
@@ -1322,6 +1328,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     if (lane == 0) atomicAdd(&n_gave_up, 1);
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt 0: the raise is done before the barrier
     for (; i < n_kv; ++i) {
+      dma_barrier<kInflight>();  // iteration i's barrier, as in the computing waves
+      if (__builtin_amdgcn_readfirstlane(n_gave_up) == kWaves2) break;
       const uint32_t pair = kSparse ? blist[min(i + kVAhead, n_kv - 1) >> 2] : 0u;
       int tile_k, tile_v;
       copy_tiles(i, pair, tile_k, tile_v);
@@ -1329,8 +1337,6 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
       dma_v(i + kVAhead, tile_v, 0);
       dma_k(i + kKAhead, tile_k, 1);
       dma_v(i + kVAhead, tile_v, 1);
-      dma_barrier<kInflight>();
-      if (__builtin_amdgcn_readfirstlane(n_gave_up) == kWaves2) break;
     }
   } else if (i < n_kv) {
     iteration(i, sa, sb, pA, pB, lA, lB);
