@@ -171,6 +171,8 @@ def main():
     ap.add_argument("--cpu-rows-per-thread", type=int, default=1536,
                     help="oracle rows per host thread for the CPU baseline (p720: about 14 s on 16 cores)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-path", action="store_true",
+                    help="skip timing the other dense path (profiling runs: one path per trace)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times), the "
                          "known-size reference for the FETCH_SIZE / WRITE_SIZE counters")
@@ -320,7 +322,7 @@ def main():
         % (args.steps, args.path, ms_step, main_kernel, ms_launch, ms_median, tflops))
     other = "fused" if args.path == "prepared" else "prepared"
     ms_other = None
-    if not special:
+    if not special and not args.no_other_path:
         ms_other, _ = timed(other, min(3, args.steps), 1)
         log("other path (%s): %.3f ms/step" % (other, ms_other))
 
