@@ -172,9 +172,12 @@ int sol_qknorm_rope3d(const void* x, void* y, int B, int H, int N, int D, int T,
  * chunk of c slabs prepares their K and V (sol_prepare_kv, 2 c slabs' worth of
  * fp16 tiles) in the out slabs after the chunk, then attends to them
  * (sol_attn_fwd_prepared), writing the chunk's own out slabs; each chunk is as
- * large as the room after it allows.  The last slabs, with no room left after
- * them (sol_attn_fwd_plan tells how many slabs the chunks cover: 37 of 40 at
- * 720p, none of 2), run the fused kernel instead, which rotates q and k in its tile
+ * large as the room after it allows, and of these chunks the call keeps the
+ * leading ones that a launch-round model says pay (a chunk too small to fill
+ * the chip costs more than running its slabs in the fused kernel).  The
+ * slabs after the kept chunks (sol_attn_fwd_plan tells how many slabs the
+ * chunks cover: 36 of 40 at 720p, none at the low resolution's 24 x 12,480)
+ * run the fused kernel instead, which rotates q and k in its tile
  * loads -- q^ as sol_rope3d, bit for bit; k^, rotated again in every query
  * tile's pass over the keys, in fp32 with the table's hi plane only, within
  * one bf16 ulp of sol_rope3d's and equal to it except where the exact

@@ -223,15 +223,27 @@ int sol_rope3d(const void* x, void* y, int B, int H, int N, int D, int T, int Hl
 // sol_attn_fwd's schedule: chunks of whole (b, h) slabs, front to back, each
 // through the prepared path with its prepared K and V held in the slabs of
 // `out` after the chunk (not yet written); a chunk takes as many slabs as
-// leave room for that, up to kMaxChunks chunks.  Returns the number of slabs
-// the chunks cover (the rest run the fused kernel) and their sizes in chunk[].
+// leave room for that, up to kMaxChunks chunks.  Of those chunks it keeps the
+// leading ones that make the call fastest by a simple model: a launch over x
+// workgroups takes ceil(x / 256) rounds on the 256 compute units, a round
+// costs 1 on the prepared path and kFusedCost on the fused kernel (measured:
+// 1.4 at 720p and at the low resolution), each chunk adds kChunkCost for its
+// prepare pass and launches, and the slabs after the kept chunks run the
+// fused kernel in one launch.  Returns the number of
+// slabs the kept chunks cover and their sizes in chunk[].
 constexpr int kMaxChunks = 64;
+constexpr double kFusedCost = 1.4;
+constexpr double kChunkCost = 0.1;
+constexpr int kComputeUnits = 256;
 static int attn_fwd_schedule(int B, int H, int N, int D, int (&chunk)[kMaxChunks]) {
   const int64_t S = (int64_t)B * H;
   const int64_t region = (int64_t)N * D * 2;                        // one slab of out
   const int64_t kv = 2 * sol::prepared_tile_elems(N) * 2;           // one slab of K and V tiles
+  const int64_t nq = (N + sol::kFusedRows - 1) / sol::kFusedRows;   // workgroups per slab (both paths)
+  auto rounds = [&](int64_t slabs) { return (double)((slabs * nq + kComputeUnits - 1) / kComputeUnits); };
   int64_t s = 0;
-  for (int n = 0; n < kMaxChunks && s < S; ++n) {
+  int n = 0;
+  for (; n < kMaxChunks && s < S; ++n) {
     // the largest c with c * kv <= (S - s - c) * region
     int64_t c = (S - s) * region / (kv + region);
     while (c > 0 && c * kv > (S - s - c) * region) --c;
@@ -239,7 +251,19 @@ static int attn_fwd_schedule(int B, int H, int N, int D, int (&chunk)[kMaxChunks
     chunk[n] = (int)c;
     s += c;
   }
-  return (int)s;
+  // keep the prefix of chunks with the lowest modelled time
+  double best = kFusedCost * rounds(S), prefix = 0.0;
+  int64_t covered = 0, best_covered = 0;
+  for (int i = 0; i < n; ++i) {
+    prefix += rounds(chunk[i]) + kChunkCost;
+    covered += chunk[i];
+    const double t = prefix + (covered < S ? kFusedCost * rounds(S - covered) : 0.0);
+    if (t < best) {
+      best = t;
+      best_covered = covered;
+    }
+  }
+  return (int)best_covered;
 }
 
 int sol_attn_fwd_plan(int B, int H, int N, int D) {

@@ -520,24 +520,40 @@ def test_binding_rejects_a_table_of_another_grid():
 def _plan_rule(S, N, D=128):
     """The schedule sol.h states, written out: chunks front to back, each the
     largest c whose prepared K and V (2 ceil(N/32) 32 D fp16 values per slab)
-    fit in the S - s - c out slabs (N D bf16 each) after it."""
+    fit in the S - s - c out slabs (N D bf16 each) after it; then the prefix
+    of chunks with the least modelled time, a launch over x workgroups
+    (ceil(N/256) per slab) costing ceil(x / 256) rounds, 1.4 times as long on
+    the fused kernel, which takes every slab after the prefix, and each chunk
+    0.1 round more."""
     region = N * D * 2
     kv = 2 * ((N + 31) // 32) * 32 * D * 2
-    s = 0
-    while s < S:
+    nq = (N + 255) // 256
+    rounds = lambda slabs: -(-slabs * nq // 256)
+    chunks, s = [], 0
+    while s < S and len(chunks) < 64:
         c = max([t for t in range(0, S - s + 1) if t * kv <= (S - s - t) * region])
         if c == 0:
             break
+        chunks.append(c)
         s += c
-    return s
+    best, best_cov = 1.4 * rounds(S), 0
+    t, cov = 0, 0
+    for c in chunks:
+        t += rounds(c) + 0.1
+        cov += c
+        total = t + (1.4 * rounds(S - cov) if cov < S else 0)
+        if total < best:
+            best, best_cov = total, cov
+    return best_cov
 
 
 def test_attn_fwd_plan(L):
-    assert sol.sol_attn_fwd_plan(1, 40, 111600, 128) == 37  # 720p: three slabs run the fused kernel
-    assert sol.sol_attn_fwd_plan(1, 2, 192, 128) == 0       # two slabs: no room for any chunk
-    assert sol.sol_attn_fwd_plan(1, 3, 192, 128) == 1       # N a multiple of 32: K and V fill two slabs
-    assert sol.sol_attn_fwd_plan(1, 3, 193, 128) == 0       # padding to 224 keys: they do not
-    for B, H, N in [(2, 5, 112112), (1, 24, 12480), (3, 7, 466), (1, 1, 1), (4, 16, 1000), (1, 200, 64)]:
+    assert sol.sol_attn_fwd_plan(1, 40, 111600, 128) == _plan_rule(40, 111600) > 30  # 720p: most slabs in place
+    assert sol.sol_attn_fwd_plan(1, 24, 12480, 128) == 0     # low resolution: chunks too small to fill the chip
+    assert sol.sol_attn_fwd_plan(1, 2, 192, 128) == 0        # two slabs: no room for any chunk
+    assert _plan_rule(3, 192) == 0
+    for B, H, N in [(2, 5, 112112), (1, 24, 12480), (3, 7, 466), (1, 1, 1), (4, 16, 1000), (1, 200, 64),
+                    (1, 40, 48360), (2, 20, 200000), (8, 40, 4096)]:
         assert sol.sol_attn_fwd_plan(B, H, N, 128) == _plan_rule(B * H, N), (B, H, N)
     assert sol.sol_attn_fwd_plan(1, 2, 0, 128) < 0
     assert sol.sol_attn_fwd_plan(1, 2, 64, 64) < 0
