@@ -344,7 +344,7 @@ def main():
     log("mfma probe: %.1f TFLOP/s (%.2f GHz equivalent); the step reaches %.1f %% of it"
         % (probe_tflops, 2.4 * probe_tflops / PEAK_BF16_TFLOPS, 100.0 * tflops / probe_tflops))
 
-    traffic = measured_traffic(w.name, main_kernel)
+    traffic = measured_traffic(w.name + ("@tau%g" % args.tau if sparse else ""), main_kernel)
     result = {
         "metric": METRIC,
         "value": tflops,
