@@ -207,7 +207,7 @@ def test_m0_used_only_by_tile_copies(asm_text):
 
 def test_first_pass_copy_count_waits_see_only_copies(asm_text):
     """The closing barrier's vmcnt(4) (a vmcnt(4) wait right before
-    s_barrier; vmcnt(8) in the block-sparse walk) assumes the last four (eight)
+    s_barrier; vmcnt(12) in the block-sparse walk) assumes the last four (twelve)
     vector-memory instructions of the wave are its tile copies: between the previous vmcnt wait and such a barrier wait
     the compiler must issue no load, store or spill of its own.  (Its own
     vmcnt waits for its own loads, e.g. in the prologue, wait for at least as
@@ -221,8 +221,8 @@ def test_first_pass_copy_count_waits_see_only_copies(asm_text):
             if t.startswith(("buffer_", "global_", "flat_")):
                 since.append((t, in_asm))
             if t.startswith("s_waitcnt") and "vmcnt" in t:
-                # the dense walk leaves its four copies in flight, the sparse walk eight
-                want = "vmcnt(8)" if template_args(name)[2] else "vmcnt(4)"
+                # the dense walk leaves its four copies in flight, the sparse walk twelve
+                want = "vmcnt(12)" if template_args(name)[2] else "vmcnt(4)"
                 if want in t and i + 1 < len(ins) and ins[i + 1][0] == "s_barrier":
                     n_waits += 1
                     others = [x for x, a in since if not (a and x.endswith(" lds"))]
