@@ -24,6 +24,7 @@ CASES = [
     "tests/test_gpu_attn.py::test_rising_scores_raise_the_reference_in_place",
     "tests/test_gpu_attn.py::test_workspace_path_is_the_two_prepared_calls",
     "tests/test_gpu_attn.py::test_no_out_of_bounds_reads_or_writes",
+    "tests/test_gpu_attn.py::test_attn_fwd_runs_chunks_in_place_then_the_fused_kernel",
     "tests/test_gpu_sparse.py::test_sparse_full_parity",
     "tests/test_gpu_sparse.py::test_sparse_with_qknorm",
     "tests/test_gpu_qknorm_refkv.py::test_key_segments_full_parity",
