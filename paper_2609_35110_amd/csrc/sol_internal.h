@@ -101,6 +101,17 @@ constexpr int kMaxSparseBlocks = 8064;  // key blocks per slab: N <= 1,032,192
 // Query rows per workgroup of the fused kernel (sol_attn_fwd).
 constexpr int kFusedRows = 256;
 
+// The block-sparse walk's order of a slab's query blocks: S query blocks to a
+// frame of hw tokens (hw / 256 rounded; 1 for frames under two blocks or
+// without a grid), R = ceil(nqb / S) rows of S, and order position o in
+// [0, R S) is block (o % R) S + o / R (none past the last block).  Consecutive
+// positions hold the same place in consecutive frames, where a video DiT's
+// attention keeps the same key blocks (that patch in every frame).
+__host__ __device__ inline int sparse_order_stride(int hw) {
+  return hw >= 2 * kSparseQueryBlock ? (hw + kSparseQueryBlock / 2) / kSparseQueryBlock : 1;
+}
+__host__ __device__ inline int sparse_order_len(int nqb, int stride) { return (nqb + stride - 1) / stride * stride; }
+
 // fp16 elements of one (b, h) slab of prepared K (or V).
 inline int64_t prepared_tile_elems(int N) {
   return (int64_t)((N + kPrepTile - 1) / kPrepTile) * kPrepTileElems;
@@ -134,9 +145,12 @@ hipError_t launch_sparse_route(const uint16_t* q, const uint16_t* k_prep, int BH
 hipError_t launch_mfma_probe(const uint16_t* operands, float* out, int workgroups, int iters,
                              hipStream_t stream);
 
-// Workgroups launch_attn_fwd would launch (the caller checks it fits a 1D grid).
+// At least the workgroups of any attention launch over BH slabs of N tokens
+// (the caller checks it fits a 1D grid).
 inline int64_t attn_max_workgroups(int N, int BH) {
-  return (int64_t)((N + kFusedRows - 1) / kFusedRows) * BH;
+  // the block-sparse grid's frame-strided order pads a slab to at most
+  // 2 nqb + 7 positions (its stride is at most nqb)
+  return (2 * (int64_t)((N + kFusedRows - 1) / kFusedRows) + 8) * BH;
 }
 
 // The current device's sticky range status (sol_range_status): waits for all

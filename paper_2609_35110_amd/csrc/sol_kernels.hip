@@ -755,16 +755,25 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
   const int l32 = lane & 31;
   int bh, qt;
   if (kSparse) {
-    // Slab-synchronous order: XCD x takes query tiles [x c, x c + c) of every
-    // slab in turn (c = ceil(n_qtiles / 8); the grid holds 8 c workgroups per
-    // slab), so the eight XCDs work on about one slab at a time and the
-    // slab's K/V, which the sparse walks miss L2 on far more often than the
-    // dense walk, stays in the memory-side cache.  Tiles past the slab leave.
-    const int c = (n_qtiles + kXcds - 1) / kXcds;
+    // Slab-synchronous, frame-strided order.  A slab's query tiles are taken
+    // in the order of sparse_order_stride (o = 0 .. R S - 1 is tile
+    // (o % R) S + o / R, S tiles to a frame: runs of one place in the frame,
+    // one tile per frame), and XCD x takes positions [x c, x c + c) of every
+    // slab in turn (c = ceil(R S / 8); the grid holds 8 c workgroups per
+    // slab).  The workgroups an XCD runs side by side then hold the same
+    // patch of different frames, whose kept key blocks -- that patch in every
+    // frame -- mostly agree, and walk them in the same order (below), so L2
+    // serves most of their copies; the eight XCDs work on about one slab at a
+    // time, whose K/V stays in the memory-side cache.  Positions past the
+    // slab's tiles leave.
+    const int S = sparse_order_stride(g.hw);
+    const int R = (n_qtiles + S - 1) / S;
+    const int c = (R * S + kXcds - 1) / kXcds;
     const int x = blockIdx.x % kXcds, l = blockIdx.x / kXcds;
     bh = l / c;
-    qt = x * c + (l - bh * c);
-    if (qt >= n_qtiles) return;  // the whole workgroup, before any barrier
+    const int o = x * c + (l - bh * c);
+    qt = (o % R) * S + o / R;
+    if (o >= R * S || qt >= n_qtiles) return;  // the whole workgroup, before any barrier
   } else {
     const int wg = xcd_local_id(blockIdx.x, gridDim.x);
     bh = wg / n_qtiles;
@@ -800,19 +809,10 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     const size_t qb = (size_t)bh * n_qtiles + qt;
     const int cnt = min(max(counts[qb], 1), min(nkb, kMaxSparseBlocks));
     auto listed = [&](int e) { return min((int)blocks[qb * nkb + e], nkb - 1); };
-    // Walk the ascending list from the first block at or past the rows' own
-    // keys (the diagonal), wrapping around: query blocks running side by side
-    // then fetch neighbouring key blocks at about the same time, so L2 serves
-    // more of them.  A full list keeps the plain order (the dense walk).
-    __shared__ int start_pos;
-    if (tid == 0) start_pos = 0;
-    __syncthreads();
-    const int diag = min((qt * BM + (N - Nq)) / kSparseKeyBlock, nkb - 1);
-    if (cnt < nkb)
-      for (int e = tid; e < cnt; e += 256)
-        if (listed(e) >= diag && (e == 0 || listed(e - 1) < diag)) start_pos = e;
-    __syncthreads();
-    const int pos0 = start_pos;
+    // Every workgroup walks its ascending list from the first entry: those
+    // running side by side, whose lists mostly agree, then fetch the same key
+    // blocks at about the same time.  (A full list is the dense walk.)
+    const int pos0 = 0;
     auto entry = [&](int e) { return (uint32_t)listed((pos0 + min(e, cnt - 1)) % cnt); };
     for (int e = tid; e < cnt; e += 256) blist[e] = entry(e) | entry(e + 1) << 16;
     n_kv = 4 * cnt;
@@ -1512,8 +1512,10 @@ hipError_t launch_attn_fwd_prepared(const uint16_t* q, const uint16_t* k_prep,
   const int n_qtiles = (g.n + BM - 1) / BM;
   const float c_log2 = (float)(1.4426950408889634 / 11.313708498984761);  // log2(e)/sqrt(128)
   const bool sparse = blocks != nullptr;
-  // the block-sparse walk runs in slab-synchronous order: 8 ceil(n_qtiles / 8) per slab
-  const int64_t per_slab = sparse ? (int64_t)kXcds * ((n_qtiles + kXcds - 1) / kXcds) : n_qtiles;
+  // the block-sparse walk runs in slab-synchronous, frame-strided order: 8 ceil(R S / 8) per slab
+  const int64_t per_slab =
+      sparse ? (int64_t)kXcds * ((sparse_order_len(n_qtiles, sparse_order_stride(g.hw)) + kXcds - 1) / kXcds)
+             : n_qtiles;
   const dim3 grid((unsigned)(per_slab * BH));
   // First pass, then the second over the row blocks whose probabilities left
   // the fp16 range.
