@@ -684,8 +684,8 @@ constexpr int kBufferDword3 = 0x00020000;
 // the next one of the walk (which starts at the diagonal block and wraps);
 // the loop walks the listed tiles in that order -- LDS ring slots follow the
 // walk, copies read the listed tile.  One LDS read per iteration,
-// issued at its start and made scalar a phase later, gives the tiles of both
-// copies (walk positions i + 3 and i + 4 lie in one block or two neighbours);
+// issued at its start and made scalar halfway through phase A, gives the tiles of both
+// copies (walk positions i + kVAhead and i + kKAhead lie in one block or two neighbours);
 // masks need no lookup, since only the last listed block can hold keys past
 // N and its walk position is known.
 static_assert(kSparseQueryBlock == BM, "a routing query block is one workgroup's rows");
@@ -1047,10 +1047,11 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // least two barriers after the last wave consumed the reads of the tile
     // it replaces.
     // Sparse walk: the list word of the tiles this iteration copies, read
-    // from LDS now and made scalar at the start of phase B.
+    // from LDS now and made scalar in phase A.
     uint32_t pair = 0;  // list word of walk position i + kVAhead (and the next entry)
     if (kSparse) pair = blist[min(i + kVAhead, n_kv - 1) >> 2];
     // ---- phase A
+    int tile_k = 0, tile_v = 0;
     uint32_t p1[8];
     float l1;
     uint32_t t01 = 0, t23 = 0, t03 = 0, t45 = 0;  // fp16 pair sums of the words
@@ -1071,6 +1072,11 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
         p1[j - 1] = pack_f16x2(pa, pb);
         keep(p1[j - 1]);
       }
+      // sparse walk: the slab tiles of phase B's copies (scalar work on the
+      // list word) in a slot with little VALU work (0.7 % faster there; the
+      // dense walk's trivial tiles stay at phase B's start, where moving
+      // them cost it 2 %)
+      if (kSparse && j == 3) copy_tiles(i, pair, tile_k, tile_v);
       __builtin_amdgcn_sched_barrier(0);
       // slot 2: S MFMA of block 1; fragment kk = j of K(i+2) into the register
       // just used; exponential of register 2j + 1; a step of the word-sum tree.
@@ -1146,8 +1152,7 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // ---- phase B
     pa = pb = 0.0f;
     t01 = t23 = t03 = t45 = 0;
-    int tile_k, tile_v;
-    copy_tiles(i, pair, tile_k, tile_v);
+    if (!kSparse) copy_tiles(i, pair, tile_k, tile_v);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int kst = j >> 2, db = j & 3;
