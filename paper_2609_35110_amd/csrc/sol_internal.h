@@ -111,6 +111,12 @@ __host__ __device__ inline int sparse_order_stride(int hw) {
   return hw >= 2 * kSparseQueryBlock ? (hw + kSparseQueryBlock / 2) / kSparseQueryBlock : 1;
 }
 __host__ __device__ inline int sparse_order_len(int nqb, int stride) { return (nqb + stride - 1) / stride * stride; }
+// The query block at order position o (o >= 0), or -1 when none.
+__host__ __device__ inline int sparse_order_block(int o, int nqb, int stride) {
+  const int rows = (nqb + stride - 1) / stride;
+  const int b = (o % rows) * stride + o / rows;
+  return o < rows * stride && b < nqb ? b : -1;
+}
 
 // fp16 elements of one (b, h) slab of prepared K (or V).
 inline int64_t prepared_tile_elems(int N) {

@@ -767,13 +767,11 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
     // time, whose K/V stays in the memory-side cache.  Positions past the
     // slab's tiles leave.
     const int S = sparse_order_stride(g.hw);
-    const int R = (n_qtiles + S - 1) / S;
-    const int c = (R * S + kXcds - 1) / kXcds;
+    const int c = (sparse_order_len(n_qtiles, S) + kXcds - 1) / kXcds;
     const int x = blockIdx.x % kXcds, l = blockIdx.x / kXcds;
     bh = l / c;
-    const int o = x * c + (l - bh * c);
-    qt = (o % R) * S + o / R;
-    if (o >= R * S || qt >= n_qtiles) return;  // the whole workgroup, before any barrier
+    qt = sparse_order_block(x * c + (l - bh * c), n_qtiles, S);
+    if (qt < 0) return;  // the whole workgroup, before any barrier
   } else {
     const int wg = xcd_local_id(blockIdx.x, gridDim.x);
     bh = wg / n_qtiles;
