@@ -681,7 +681,7 @@ constexpr int kBufferDword3 = 0x00020000;
 // to the key blocks (kSparseKeyBlock keys = 4 tiles each) listed for it in
 // blocks[(bh * n_qtiles + qt) * nkb ..] (ascending, counts[bh * n_qtiles + qt]
 // of them).  The list is staged into LDS once, each word holding an entry and
-// the next one of the walk (which starts at the diagonal block and wraps);
+// the next one of the walk (ascending from the first entry);
 // the loop walks the listed tiles in that order -- LDS ring slots follow the
 // walk, copies read the listed tile.  One LDS read per iteration,
 // issued at its start and made scalar halfway through phase A, gives the tiles of both
@@ -1164,7 +1164,8 @@ void attn_prepared_kernel(const uint16_t* __restrict__ q, const uint16_t* __rest
         p0_next[j - 1] = pack_f16x2(pa, pb);
         keep(p0_next[j - 1]);
       }
-      // over K(i + kKAhead - 8), read in iteration i - 6 at the latest; over
+      // over K(i + kKAhead - 8), read in iteration i + kKAhead - 10 at the
+      // latest (i - 6 in the dense walk, i - 4 in the sparse one); over
       // V(i + kVAhead - kVB), whose fragments every wave read two barriers ago
       if (j == 1) dma_k(i + kKAhead, tile_k, 0);
       if (j == 2) dma_v(i + kVAhead, tile_v, 0);
